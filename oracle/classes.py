@@ -1,0 +1,60 @@
+"""Code-point classes seen by the pre-tokenization patterns (oracle; test infrastructure).
+
+The patterns of both families test three Unicode properties: letters
+(``\\p{L}``), numbers (``\\p{N}``) and whitespace (``\\s``).  Every other
+code point is "other".  The paper pins these tables by probing the reference
+regex engine rather than trusting a library's Unicode version (Sec. 3.1,
+table pinning; Sec. 6.1, the Unicode table skew).  ``data/onig_classes.txt``
+holds that probe for Oniguruma inside HF tokenizers 0.22.2; it was written by
+``data/probe_onig.py``.
+
+Parity pins: the whole table is compared with a fresh probe of the engine
+(tests), and the 25 whitespace code points are checked against the Unicode
+White_Space list written out in the test.
+"""
+
+import os
+
+L, N, W, O = 1, 2, 3, 0
+NAMES = {L: "L", N: "N", W: "W", O: "O"}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+TABLE_PATH = os.path.join(_HERE, "data", "onig_classes.txt")
+
+
+def _load():
+    table = bytearray(0x110000)  # O everywhere by default
+    folds = {}
+    code = {"L": L, "N": N, "W": W}
+    with open(TABLE_PATH) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            parts = line.split()
+            if parts[0] == "FOLD":
+                folds[parts[1]] = frozenset(int(x, 16) for x in parts[2:])
+                continue
+            a, b, k = int(parts[0], 16), int(parts[1], 16), code[parts[2]]
+            for c in range(a, b + 1):
+                table[c] = k
+    return table, folds
+
+
+TABLE, FOLDS = _load()
+
+
+def char_class(cp: int) -> int:
+    """Class (L, N, W or O) of one Unicode scalar value."""
+    return TABLE[cp]
+
+
+def classes_of(text: str) -> list:
+    """Class of every character of ``text``."""
+    t = TABLE
+    return [t[ord(c)] for c in text]
+
+
+def folds_to(ch: str, letter: str) -> bool:
+    """True iff ``ch`` matches the ASCII ``letter`` case-insensitively in the engine."""
+    return ord(ch) in FOLDS[letter]

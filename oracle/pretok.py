@@ -1,0 +1,199 @@
+"""Leftmost-first regex pre-tokenization, written out by hand (oracle; test infrastructure).
+
+GPT-family pre-tokenizers are a leftmost-first alternation regex with
+backtracking; every match starts where the previous one ended (Sec. 1;
+Sec. 3.1, "Removing the sequential regex scan").  This module is that
+definition and nothing more: at the current position it tries the
+alternatives in their order, the first one that matches wins, its match is the
+next piece, and the scan continues at the match's end.  Each alternative is
+evaluated with the greedy-then-backtrack semantics of its regex operators.
+There is no run decomposition here; that reformulation is what the library
+implements and what these functions check.
+
+The paper names the pattern lineages but does not print the regexes.  The two
+families used here, transcribed from their lineage definitions:
+
+GPT-2 style, alternatives in order
+  G1  ``'`` followed by one of ``s t re ve m ll d`` (case-sensitive)
+  G2  optional U+0020, then one or more letters           `` ?\\p{L}+``
+  G3  optional U+0020, then one or more numbers           `` ?\\p{N}+``
+  G4  optional U+0020, then one or more "other" chars     `` ?[^\\s\\p{L}\\p{N}]+``
+  G5  whitespace not followed by a non-whitespace char    ``\\s+(?!\\S)``
+  G6  whitespace                                          ``\\s+``
+
+cl100k style, alternatives in order
+  C1  G1, case-insensitive                                ``(?i:'s|'t|'re|'ve|'m|'ll|'d)``
+  C2  one optional char that is not CR/LF, letter or number, then letters
+                                                          ``[^\\r\\n\\p{L}\\p{N}]?\\p{L}+``
+  C3  one to three numbers                                ``\\p{N}{1,3}``
+  C4  optional U+0020, "other" chars, then CR/LF chars    `` ?[^\\s\\p{L}\\p{N}]+[\\r\\n]*``
+  C5  whitespace ending in CR/LF                          ``\\s*[\\r\\n]+``
+  C6  = G5
+  C7  = G6
+
+Readings taken where the paper is silent: ``\\s`` is the engine's whitespace
+class (25 code points), "space" in the optional-space alternatives is U+0020
+only, case-insensitive contractions use the engine's case folding (which maps
+U+017F to ``s``), and only U+0027 is an apostrophe.
+"""
+
+from .classes import L, N, O, W, classes_of, folds_to
+
+GPT2 = "gpt2"
+CL100K = "cl100k"
+PATTERNS = (GPT2, CL100K)
+
+SUFFIXES = ("s", "t", "re", "ve", "m", "ll", "d")
+SP = " "
+NL = "\r\n"
+
+
+def _run(cl, i, k):
+    """First index >= i whose class is not k."""
+    n = len(cl)
+    while i < n and cl[i] == k:
+        i += 1
+    return i
+
+
+# -- alternatives: each returns the end of its match at p, or None ----------
+
+def _contraction(text, p, insensitive):
+    if text[p] != "'":
+        return None
+    for suf in SUFFIXES:
+        e = p + 1 + len(suf)
+        if e > len(text):
+            continue
+        seg = text[p + 1:e]
+        if insensitive:
+            ok = all(folds_to(ch, letter) for ch, letter in zip(seg, suf))
+        else:
+            ok = seg == suf
+        if ok:
+            return e
+    return None
+
+
+def _opt_space_then_run(text, cl, p, k):
+    """`` ?X+`` with X the class k: greedy optional space, backtracking to none."""
+    if text[p] == SP:
+        e = _run(cl, p + 1, k)
+        if e > p + 1:
+            return e
+    e = _run(cl, p, k)
+    return e if e > p else None
+
+
+def _ws_not_before_nonws(text, cl, p):
+    """``\\s+(?!\\S)``: the longest whitespace run, backtracked until the lookahead holds."""
+    n = len(text)
+    e = _run(cl, p, W)
+    for j in range(e, p, -1):
+        if j == n or cl[j] == W:
+            return j
+    return None
+
+
+def _ws(text, cl, p):
+    e = _run(cl, p, W)
+    return e if e > p else None
+
+
+def _gpt2_at(text, cl, p):
+    return (_contraction(text, p, False)
+            or _opt_space_then_run(text, cl, p, L)
+            or _opt_space_then_run(text, cl, p, N)
+            or _opt_space_then_run(text, cl, p, O)
+            or _ws_not_before_nonws(text, cl, p)
+            or _ws(text, cl, p))
+
+
+def _cl_prefixed_letters(text, cl, p):
+    """``[^\\r\\n\\p{L}\\p{N}]?\\p{L}+``"""
+    if text[p] not in NL and cl[p] not in (L, N):
+        e = _run(cl, p + 1, L)
+        if e > p + 1:
+            return e
+    e = _run(cl, p, L)
+    return e if e > p else None
+
+
+def _cl_numbers(text, cl, p):
+    """``\\p{N}{1,3}``"""
+    n = len(text)
+    e = p
+    while e < n and e - p < 3 and cl[e] == N:
+        e += 1
+    return e if e > p else None
+
+
+def _cl_other(text, cl, p):
+    """`` ?[^\\s\\p{L}\\p{N}]+[\\r\\n]*``"""
+    n = len(text)
+    starts = (p + 1, p) if text[p] == SP else (p,)
+    for s in starts:
+        e = _run(cl, s, O)
+        if e > s:
+            while e < n and text[e] in NL:
+                e += 1
+            return e
+    return None
+
+
+def _cl_ws_newlines(text, cl, p):
+    """``\\s*[\\r\\n]+``: greedy whitespace, backtracked until CR/LF can follow."""
+    n = len(text)
+    e = _run(cl, p, W)
+    for j in range(e, p - 1, -1):
+        if j < n and text[j] in NL:
+            k = j
+            while k < n and text[k] in NL:
+                k += 1
+            return k
+    return None
+
+
+def _cl100k_at(text, cl, p):
+    return (_contraction(text, p, True)
+            or _cl_prefixed_letters(text, cl, p)
+            or _cl_numbers(text, cl, p)
+            or _cl_other(text, cl, p)
+            or _cl_ws_newlines(text, cl, p)
+            or _ws_not_before_nonws(text, cl, p)
+            or _ws(text, cl, p))
+
+
+def pretokenize(text: str, pattern: str) -> list:
+    """Pieces of ``text`` as (start, end) character spans, in order, tiling the text."""
+    if pattern == GPT2:
+        step = _gpt2_at
+    elif pattern == CL100K:
+        step = _cl100k_at
+    else:
+        raise ValueError("unknown pattern %r" % (pattern,))
+    cl = classes_of(text)
+    spans = []
+    p = 0
+    n = len(text)
+    while p < n:
+        e = step(text, cl, p)
+        assert e is not None and e > p, "no alternative matched at %d" % p
+        spans.append((p, e))
+        p = e
+    return spans
+
+
+def pieces(text: str, pattern: str) -> list:
+    """Pieces of ``text`` as strings."""
+    return [text[a:b] for a, b in pretokenize(text, pattern)]
+
+
+def piece_byte_starts(text: str, pattern: str) -> list:
+    """UTF-8 byte offset of the first byte of every piece."""
+    starts = []
+    off = 0
+    for a, b in pretokenize(text, pattern):
+        starts.append(off)
+        off += len(text[a:b].encode("utf-8"))
+    return starts

@@ -1,0 +1,17 @@
+"""Exact GPU tokenization for AMD Instinct MI355X (gfx950).
+
+A HIP library (``libtoktier.so``, C ABI in ``include/toktier.h``) that computes
+the full-request tokenization path of TokTier: GPT-family pre-tokenization
+recast as run-local rules, then exact byte-level BPE and output compaction,
+with token IDs identical to full reference tokenization.  This package holds
+the library sources (``csrc/``), its build script and a thin ctypes binding.
+"""
+
+from .tokenizer import CL100K, GPT2, PATTERNS, Tokenizer, status_string  # noqa: F401
+from ._lib import TokTierError  # noqa: F401
+
+
+def build(verbose: bool = False) -> str:
+    from ._build import build as _b
+
+    return _b(verbose)

@@ -1,0 +1,74 @@
+"""ctypes declarations of the C ABI in ``include/toktier.h``.
+
+Loading fails loudly when ``libtoktier.so`` has not been built: there is no
+fallback implementation in this package.
+"""
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtoktier.so")
+
+TT_OK = 0
+TT_PATTERN_GPT2 = 0
+TT_PATTERN_CL100K = 1
+TT_MAX_BYTES = 1 << 30
+
+STATUS = {
+    0: "TT_OK",
+    -1: "TT_ERR_NULL_ARG",
+    -2: "TT_ERR_BAD_PATTERN",
+    -3: "TT_ERR_BAD_MERGES",
+    -4: "TT_ERR_BAD_VOCAB",
+    -5: "TT_ERR_INVALID_UTF8",
+    -6: "TT_ERR_TOO_LARGE",
+    -7: "TT_ERR_HIP",
+    -8: "TT_ERR_OOM",
+    -9: "TT_ERR_BAD_ARG",
+}
+
+# every symbol the header declares, with (restype, argtypes)
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+SIGNATURES = {
+    "tt_create": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _I32, ctypes.POINTER(_P)]),
+    "tt_destroy": (None, [_P]),
+    "tt_encode": (ctypes.c_int, [_P, _P, _I64, _P, ctypes.POINTER(_I64), _P]),
+    "tt_encode_device": (ctypes.c_int, [_P, _P, _I64, _P, _P, _P]),
+    "tt_encode_batch": (ctypes.c_int, [_P, _P, _P, _I32, _P, _P, _P]),
+    "tt_pretokenize": (ctypes.c_int, [_P, _P, _I64, _P, ctypes.POINTER(_I64), _P]),
+    "tt_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "tt_info": (ctypes.c_int, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32), ctypes.POINTER(_I32)]),
+}
+
+_lib = None
+
+
+class TokTierError(RuntimeError):
+    def __init__(self, status, what=""):
+        self.status = status
+        name = STATUS.get(status, str(status))
+        super().__init__("%s%s (%s)" % (what + ": " if what else "", name, status))
+
+
+def load():
+    """The loaded library; raises if it was not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libtoktier.so is not built: run __graft_entry__.build() "
+                              "or python -m paper_2607_29678_amd._build")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def check(status, what=""):
+    if status != TT_OK:
+        raise TokTierError(status, what)

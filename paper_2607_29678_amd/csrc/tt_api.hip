@@ -1,0 +1,410 @@
+// C ABI of the tokenizer: handle creation and validation, per-stream
+// workspaces, and the launch chain of one call.
+//
+// Chain of one request (all on the caller's stream, no host round trip
+// between kernels; Sec. 3.3 keeps piece counts, dispatch lists and the output
+// length on the device and sizes launches from buffer capacity):
+//   reset -> pre-tokenize -> BPE (thread / wave / block engines) -> compact
+// The host synchronises twice per blocking call: once for the output length,
+// once for the IDs.
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <unordered_map>
+#include <unordered_set>
+#include <vector>
+
+#include "tt_internal.h"
+
+using namespace tt;
+
+namespace {
+
+struct Workspace {
+  uint64_t cap = 0;           // bytes of request this workspace holds
+  int64_t doc_cap = 0;        // documents the batch buffers hold
+  void* dmem = nullptr;       // one device allocation for everything below
+  Work w{};                   // device pointers (text/out set per call)
+  uint8_t* d_in = nullptr;    // staged request bytes (host calls)
+  int32_t* d_out = nullptr;   // IDs (host calls)
+  int64_t* d_len = nullptr;   // output length (host calls)
+  int64_t* d_docs = nullptr;  // batch: document byte offsets
+  int64_t* d_out_docs = nullptr;
+  int64_t* h_len = nullptr;   // pinned readback word
+  uint32_t* h_ctrl = nullptr; // pinned readback of the control block
+};
+
+}  // namespace
+
+struct tt_tokenizer {
+  int pattern = 0;
+  int32_t n_merges = 0;
+  int32_t vocab_size = 0;
+  int device = 0;
+  MergeSlot* d_slots = nullptr;
+  uint32_t mask = 0;
+  int32_t* d_byte_id = nullptr;
+  std::mutex mu;
+  std::unordered_map<hipStream_t, Workspace*> ws;
+};
+
+namespace {
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+void free_ws(Workspace* s) {
+  if (!s) return;
+  if (s->dmem) (void)hipFree(s->dmem);
+  if (s->d_docs) (void)hipFree(s->d_docs);
+  if (s->h_len) (void)hipHostFree(s->h_len);
+  if (s->h_ctrl) (void)hipHostFree(s->h_ctrl);
+  delete s;
+}
+
+// (Re)allocate the device buffers of a workspace for requests up to `need` bytes.
+int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
+  if (need <= s->cap) return TT_OK;
+  // earlier asynchronous calls on this stream may still use the old buffers
+  if (s->dmem && hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  uint64_t cap = std::max<uint64_t>(need, std::max<uint64_t>(65536, s->cap * 2));
+  if (cap > (uint64_t)TT_MAX_BYTES) cap = std::max<uint64_t>(need, (uint64_t)TT_MAX_BYTES);
+  if (s->dmem) {
+    (void)hipFree(s->dmem);
+    s->dmem = nullptr;
+    s->cap = 0;
+  }
+  const uint64_t N = cap;
+  const uint64_t npt = pt_tiles((uint32_t)N) + 1, nct = ct_tiles_cap((uint32_t)N) + 1;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  size_t o_ctrl = take(sizeof(Ctrl));
+  size_t o_poff = take(4 * (N + 2));
+  size_t o_pcnt = take(4 * (N + 1));
+  size_t o_pout = take(4 * (N + 2));
+  size_t o_ids = take(4 * N);
+  size_t o_long = take(4 * (N + 1));
+  size_t o_big = take(4 * (N + 1));
+  size_t o_tst = take(8 * npt);
+  size_t o_tsum = take(4 * npt);
+  size_t o_cst = take(8 * nct);
+  size_t o_scr = take(4 * 6 * N + 8 * (N / 32 + 8));
+  size_t o_in = take(N + 64);
+  size_t o_out = take(4 * N);
+  size_t o_len = take(8);
+  void* mem = nullptr;
+  if (hipMalloc(&mem, off) != hipSuccess) return TT_ERR_OOM;
+  uint8_t* b = static_cast<uint8_t*>(mem);
+  s->dmem = mem;
+  s->cap = cap;
+  Work& w = s->w;
+  w.ctrl = reinterpret_cast<Ctrl*>(b + o_ctrl);
+  w.piece_off = reinterpret_cast<uint32_t*>(b + o_poff);
+  w.piece_cnt = reinterpret_cast<uint32_t*>(b + o_pcnt);
+  w.piece_out = reinterpret_cast<uint32_t*>(b + o_pout);
+  w.ids = reinterpret_cast<int32_t*>(b + o_ids);
+  w.long_list = reinterpret_cast<uint32_t*>(b + o_long);
+  w.big_list = reinterpret_cast<uint32_t*>(b + o_big);
+  w.tile_status = reinterpret_cast<uint64_t*>(b + o_tst);
+  w.tile_summary = reinterpret_cast<uint32_t*>(b + o_tsum);
+  w.ctile_status = reinterpret_cast<uint64_t*>(b + o_cst);
+  w.scratch32 = reinterpret_cast<uint32_t*>(b + o_scr);
+  s->d_in = b + o_in;
+  s->d_out = reinterpret_cast<int32_t*>(b + o_out);
+  s->d_len = reinterpret_cast<int64_t*>(b + o_len);
+  return TT_OK;
+}
+
+int ws_reserve_docs(Workspace* s, int64_t n_docs, hipStream_t st) {
+  if (n_docs + 1 <= s->doc_cap) return TT_OK;
+  if (s->d_docs && hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  if (s->d_docs) (void)hipFree(s->d_docs);
+  s->d_docs = nullptr;
+  s->doc_cap = 0;
+  int64_t cap = std::max<int64_t>(n_docs + 1, 64);
+  void* m = nullptr;
+  if (hipMalloc(&m, 2 * 8 * cap) != hipSuccess) return TT_ERR_OOM;
+  s->d_docs = static_cast<int64_t*>(m);
+  s->d_out_docs = s->d_docs + cap;
+  s->doc_cap = cap;
+  return TT_OK;
+}
+
+int get_ws(tt_tokenizer* h, hipStream_t stream, uint64_t need, Workspace** out) {
+  Workspace* s;
+  {
+    std::lock_guard<std::mutex> g(h->mu);
+    auto it = h->ws.find(stream);
+    if (it == h->ws.end()) {
+      s = new Workspace();
+      if (hipHostMalloc(reinterpret_cast<void**>(&s->h_len), 8, hipHostMallocDefault) != hipSuccess ||
+          hipHostMalloc(reinterpret_cast<void**>(&s->h_ctrl), sizeof(Ctrl), hipHostMallocDefault) !=
+              hipSuccess) {
+        free_ws(s);
+        return TT_ERR_OOM;
+      }
+      h->ws[stream] = s;
+    } else {
+      s = it->second;
+    }
+  }
+  int rc = ws_reserve(s, need, stream);
+  if (rc) return rc;
+  *out = s;
+  return TT_OK;
+}
+
+// Enqueue the whole chain for `n` bytes at device address `text`.
+int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, const int64_t* d_docs,
+              int32_t n_docs, int32_t* out_ids, int64_t* out_len, int64_t* out_docs, hipStream_t st,
+              bool pretok_only) {
+  Work w = s->w;
+  w.text = text;
+  w.n = n;
+  w.doc_off = d_docs;
+  w.n_docs = n_docs;
+  w.out_ids = out_ids;
+  w.out_len = out_len;
+  w.out_doc_off = out_docs;
+  DevTables tb{h->d_slots, h->mask, h->d_byte_id};
+  const uint32_t npt = pt_tiles(n), nct = ct_tiles_cap(n);
+  if (launch_reset(w, npt, nct, st) != hipSuccess) return TT_ERR_HIP;
+  if (launch_pretok(w, h->pattern, npt, st) != hipSuccess) return TT_ERR_HIP;
+  if (pretok_only) return TT_OK;
+  if (launch_bpe(w, tb, st) != hipSuccess) return TT_ERR_HIP;
+  if (launch_compact(w, nct, st) != hipSuccess) return TT_ERR_HIP;
+  if (d_docs && launch_doc_offsets(w, st) != hipSuccess) return TT_ERR_HIP;
+  return TT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tt_status_string(int status) {
+  switch (status) {
+    case TT_OK: return "ok";
+    case TT_ERR_NULL_ARG: return "a required pointer is NULL";
+    case TT_ERR_BAD_PATTERN: return "unknown pattern id";
+    case TT_ERR_BAD_MERGES: return "merge table out of range, duplicated or not proper";
+    case TT_ERR_BAD_VOCAB: return "vocabulary inconsistent with the merges";
+    case TT_ERR_INVALID_UTF8: return "input is not valid UTF-8";
+    case TT_ERR_TOO_LARGE: return "request larger than TT_MAX_BYTES";
+    case TT_ERR_HIP: return "HIP runtime error";
+    case TT_ERR_OOM: return "out of memory";
+    case TT_ERR_BAD_ARG: return "inconsistent size or offset argument";
+    default: return "unknown status";
+  }
+}
+
+int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_bytes,
+              const int64_t* vocab_offsets, int32_t vocab_size, int32_t pattern_id, tt_tokenizer** out) {
+  if (!out || !vocab_offsets || (n_merges > 0 && !merges)) return TT_ERR_NULL_ARG;
+  *out = nullptr;
+  if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K) return TT_ERR_BAD_PATTERN;
+  if (n_merges < 0 || vocab_size < 256 || n_merges >= (int32_t)0x7FFFFFF0) return TT_ERR_BAD_ARG;
+  if (vocab_offsets[0] != 0) return TT_ERR_BAD_VOCAB;
+  for (int32_t i = 0; i < vocab_size; ++i)
+    if (vocab_offsets[i + 1] < vocab_offsets[i]) return TT_ERR_BAD_VOCAB;
+  if (vocab_offsets[vocab_size] > 0 && !vocab_bytes) return TT_ERR_NULL_ARG;
+  auto vlen = [&](int32_t id) { return vocab_offsets[id + 1] - vocab_offsets[id]; };
+  auto vptr = [&](int32_t id) { return vocab_bytes + vocab_offsets[id]; };
+
+  // base IDs: lowest ID spelling each single byte
+  std::vector<int32_t> byte_id(256, -1);
+  for (int32_t i = 0; i < vocab_size; ++i)
+    if (vlen(i) == 1 && byte_id[vptr(i)[0]] < 0) byte_id[vptr(i)[0]] = i;
+  for (int b = 0; b < 256; ++b)
+    if (byte_id[b] < 0) return TT_ERR_BAD_VOCAB;
+
+  // properness: operands available before use, results fresh and unique
+  std::vector<uint8_t> avail(vocab_size, 0);
+  for (int b = 0; b < 256; ++b) avail[byte_id[b]] = 1;
+  std::unordered_set<uint64_t> pairs;
+  pairs.reserve((size_t)n_merges * 2 + 16);
+  for (int32_t r = 0; r < n_merges; ++r) {
+    const tt_merge& m = merges[r];
+    if (m.left < 0 || m.right < 0 || m.result < 0 || m.left >= vocab_size || m.right >= vocab_size ||
+        m.result >= vocab_size)
+      return TT_ERR_BAD_MERGES;
+    uint64_t key = ((uint64_t)(uint32_t)m.left << 32) | (uint32_t)m.right;
+    if (!pairs.insert(key).second) return TT_ERR_BAD_MERGES;
+    if (!avail[m.left] || !avail[m.right] || avail[m.result]) return TT_ERR_BAD_MERGES;
+    int64_t la = vlen(m.left), lb = vlen(m.right);
+    if (vlen(m.result) != la + lb || std::memcmp(vptr(m.result), vptr(m.left), la) != 0 ||
+        std::memcmp(vptr(m.result) + la, vptr(m.right), lb) != 0)
+      return TT_ERR_BAD_VOCAB;
+    avail[m.result] = 1;
+  }
+
+  // open-addressing table, load factor <= 1/2
+  uint32_t cap = 16;
+  while (cap < 2u * (uint32_t)n_merges) cap <<= 1;
+  std::vector<MergeSlot> slots(cap, MergeSlot{EMPTY, EMPTY, RANK_INF, 0});
+  for (int32_t r = 0; r < n_merges; ++r) {
+    uint32_t a = (uint32_t)merges[r].left, b = (uint32_t)merges[r].right;
+    uint32_t i = pair_hash(a, b) & (cap - 1);
+    while (slots[i].left != EMPTY) i = (i + 1) & (cap - 1);
+    slots[i] = MergeSlot{a, b, (uint32_t)r, (uint32_t)merges[r].result};
+  }
+
+  tt_tokenizer* h = new tt_tokenizer();
+  h->pattern = pattern_id;
+  h->n_merges = n_merges;
+  h->vocab_size = vocab_size;
+  h->mask = cap - 1;
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    delete h;
+    return TT_ERR_HIP;
+  }
+  if (hipMalloc(reinterpret_cast<void**>(&h->d_slots), sizeof(MergeSlot) * cap) != hipSuccess ||
+      hipMalloc(reinterpret_cast<void**>(&h->d_byte_id), sizeof(int32_t) * 256) != hipSuccess) {
+    tt_destroy(h);
+    return TT_ERR_OOM;
+  }
+  if (hipMemcpy(h->d_slots, slots.data(), sizeof(MergeSlot) * cap, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(h->d_byte_id, byte_id.data(), sizeof(int32_t) * 256, hipMemcpyHostToDevice) != hipSuccess) {
+    tt_destroy(h);
+    return TT_ERR_HIP;
+  }
+  *out = h;
+  return TT_OK;
+}
+
+void tt_destroy(tt_tokenizer* h) {
+  if (!h) return;
+  (void)hipSetDevice(h->device);
+  (void)hipDeviceSynchronize();
+  for (auto& kv : h->ws) free_ws(kv.second);
+  if (h->d_slots) (void)hipFree(h->d_slots);
+  if (h->d_byte_id) (void)hipFree(h->d_byte_id);
+  delete h;
+}
+
+int tt_info(const tt_tokenizer* h, int32_t* n_merges, int32_t* vocab_size, int32_t* pattern_id) {
+  if (!h) return TT_ERR_NULL_ARG;
+  if (n_merges) *n_merges = h->n_merges;
+  if (vocab_size) *vocab_size = h->vocab_size;
+  if (pattern_id) *pattern_id = h->pattern;
+  return TT_OK;
+}
+
+int tt_encode_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_t* d_out_ids,
+                     int64_t* d_out_len, void* stream) {
+  if (!h || !d_out_len || (len > 0 && (!d_utf8 || !d_out_ids))) return TT_ERR_NULL_ARG;
+  if (len < 0) return TT_ERR_BAD_ARG;
+  if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  if (len == 0) {
+    static const int64_t zero = 0;
+    return hipMemcpyAsync(d_out_len, &zero, 8, hipMemcpyHostToDevice, st) == hipSuccess ? TT_OK : TT_ERR_HIP;
+  }
+  Workspace* s = nullptr;
+  int rc = get_ws(h, st, (uint64_t)len, &s);
+  if (rc) return rc;
+  return run_chain(h, s, d_utf8, (uint32_t)len, nullptr, 0, d_out_ids, d_out_len, nullptr, st, false);
+}
+
+int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_ids, int64_t* out_len,
+              void* stream) {
+  if (!h || !out_len || (len > 0 && (!utf8 || !out_ids))) return TT_ERR_NULL_ARG;
+  if (len < 0) return TT_ERR_BAD_ARG;
+  if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
+  *out_len = 0;
+  if (len == 0) return TT_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  Workspace* s = nullptr;
+  int rc = get_ws(h, st, (uint64_t)len, &s);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->d_in, utf8, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, false);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->h_len, s->d_len, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return TT_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  int64_t T = *s->h_len;
+  if (T < 0) return (int)T;
+  if (T > 0) {
+    if (hipMemcpyAsync(out_ids, s->d_out, (size_t)T * 4, hipMemcpyDeviceToHost, st) != hipSuccess)
+      return TT_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  }
+  *out_len = T;
+  return TT_OK;
+}
+
+int tt_encode_batch(tt_tokenizer* h, const uint8_t* concat, const int64_t* doc_offsets, int32_t n_docs,
+                    int32_t* out_ids, int64_t* out_doc_offsets, void* stream) {
+  if (!h || !doc_offsets || !out_doc_offsets) return TT_ERR_NULL_ARG;
+  if (n_docs < 0 || doc_offsets[0] != 0) return TT_ERR_BAD_ARG;
+  for (int32_t j = 0; j < n_docs; ++j)
+    if (doc_offsets[j + 1] < doc_offsets[j]) return TT_ERR_BAD_ARG;
+  const int64_t len = doc_offsets[n_docs];
+  if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
+  if (len > 0 && (!concat || !out_ids)) return TT_ERR_NULL_ARG;
+  if (len == 0) {
+    for (int32_t j = 0; j <= n_docs; ++j) out_doc_offsets[j] = 0;
+    return TT_OK;
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  Workspace* s = nullptr;
+  int rc = get_ws(h, st, (uint64_t)len, &s);
+  if (rc) return rc;
+  rc = ws_reserve_docs(s, n_docs, st);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->d_in, concat, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
+  if (hipMemcpyAsync(s->d_docs, doc_offsets, 8 * ((size_t)n_docs + 1), hipMemcpyHostToDevice, st) != hipSuccess)
+    return TT_ERR_HIP;
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, s->d_docs, n_docs, s->d_out, s->d_len, s->d_out_docs, st, false);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->h_len, s->d_len, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return TT_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  int64_t T = *s->h_len;
+  if (T < 0) return (int)T;
+  if (hipMemcpyAsync(out_ids, s->d_out, (size_t)T * 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(out_doc_offsets, s->d_out_docs, 8 * ((size_t)n_docs + 1), hipMemcpyDeviceToHost, st) !=
+          hipSuccess)
+    return TT_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  return TT_OK;
+}
+
+int tt_pretokenize(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int64_t* out_piece_starts, int64_t* out_n,
+                   void* stream) {
+  if (!h || !out_n || (len > 0 && (!utf8 || !out_piece_starts))) return TT_ERR_NULL_ARG;
+  if (len < 0) return TT_ERR_BAD_ARG;
+  if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
+  *out_n = 0;
+  if (len == 0) return TT_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  Workspace* s = nullptr;
+  int rc = get_ws(h, st, (uint64_t)len, &s);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->d_in, utf8, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, true);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->h_ctrl, s->w.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st) != hipSuccess)
+    return TT_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  const Ctrl* c = reinterpret_cast<const Ctrl*>(s->h_ctrl);
+  if (c->error) return -(int)c->error;
+  const uint32_t P = c->n_pieces;
+  std::vector<uint32_t> tmp(P);
+  if (P > 0) {
+    if (hipMemcpyAsync(tmp.data(), s->w.piece_off, 4 * (size_t)P, hipMemcpyDeviceToHost, st) != hipSuccess)
+      return TT_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  }
+  for (uint32_t i = 0; i < P; ++i) out_piece_starts[i] = tmp[i];
+  *out_n = P;
+  return TT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,373 @@
+// Exact byte-level BPE over the pieces, on the GPU.
+//
+// Each piece is encoded on its own: start from the IDs of its bytes and
+// repeatedly merge the adjacent pair with the lowest merge rank, leftmost
+// first (the model stage of the front-end/model factorisation, Appendix,
+// Definition d:frontend and Lemma l:homo).  Two facts license a parallel
+// schedule (Sec. 3.2, "GPU BPE"): the minimum rank of a round names one pair,
+// and merging all leftmost non-overlapping occurrences of that pair at once
+// equals merging them one by one; and after a merge only the two pairs next
+// to it need a new rank lookup.  Work is dispatched by piece length so each
+// piece gets the smallest execution unit that holds it (Sec. 3.2).
+//
+// MI355X design (wave64, LDS, one HBM-resident hash table):
+//   - pieces of at most 16 bytes: one thread per piece, the sequence in
+//     registers; ranks come from the open-addressing merge table;
+//   - 17..512 bytes: one 64-lane wave per piece, the sequence in LDS laid out
+//     as rows of 64 tokens; a round is a wave min-reduction, one ballot per
+//     row, a closed-form leftmost non-overlapping selection on the 64-bit
+//     mask, a popcount compaction and the neighbour re-probes;
+//   - longer pieces: the same rounds with 16 waves per piece and the rows in
+//     global memory; pieces reach this engine through a device work queue.
+// Pieces go to the wave and block engines through device-side queues, so no
+// count is read back by the host.
+#include "tt_internal.h"
+
+namespace tt {
+
+namespace {
+
+constexpr uint32_t RANK_DIRTY = 0xFFFFFFFEu;  // pair changed; rank to be probed again
+
+__device__ __forceinline__ uint32_t wave_min(uint32_t v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v = min(v, (uint32_t)__shfl_xor(v, d, 64));
+  return v;
+}
+
+// Leftmost non-overlapping choice among the set bits of m, where bit j stands
+// for the pair (token j, token j+1).  Within every run of consecutive set bits
+// the greedy left-to-right choice takes the run's first bit and every second
+// bit after it.  Runs that start on an even bit are isolated with one carry
+// propagation: adding their start bits clears exactly those runs.
+__device__ __forceinline__ uint64_t leftmost_nonoverlapping(uint64_t m) {
+  const uint64_t EVEN = 0x5555555555555555ull;
+  uint64_t starts = m & ~(m << 1);
+  uint64_t even_runs = ((m + (starts & EVEN)) ^ m) & m;
+  return (even_runs & EVEN) | (m & ~even_runs & ~EVEN);
+}
+
+__device__ __forceinline__ uint64_t lanemask_lt(int lane) {
+  return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Short pieces: one thread per piece, sequence in registers.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void bpe_small_kernel(Work w, DevTables tb) {
+  __shared__ int32_t s_bid[256];
+  s_bid[threadIdx.x] = tb.byte_id[threadIdx.x];
+  __syncthreads();
+  const uint32_t P = w.ctrl->n_pieces;
+  const uint32_t stride = gridDim.x * blockDim.x;
+  for (uint32_t p = blockIdx.x * blockDim.x + threadIdx.x; p < P; p += stride) {
+    const uint32_t a = w.piece_off[p];
+    const uint32_t L = w.piece_off[p + 1] - a;
+    if (L > (uint32_t)SMALL_MAX) {
+      uint32_t k = atomicAdd(&w.ctrl->n_long, 1u);
+      w.long_list[k] = p;
+      continue;
+    }
+    uint32_t ids[SMALL_MAX], rk[SMALL_MAX], rs[SMALL_MAX];
+#pragma unroll
+    for (int j = 0; j < SMALL_MAX; ++j) ids[j] = (uint32_t)j < L ? (uint32_t)s_bid[w.text[a + j]] : 0u;
+#pragma unroll
+    for (int j = 0; j < SMALL_MAX; ++j) {
+      uint2 r = make_uint2(RANK_INF, 0u);
+      if ((uint32_t)(j + 1) < L) r = probe_pair(tb.slots, tb.mask, ids[j], ids[j + 1]);
+      rk[j] = r.x;
+      rs[j] = r.y;
+    }
+    uint32_t n = L;
+    for (;;) {
+      uint32_t best = RANK_INF;
+      int bi = 0;
+#pragma unroll
+      for (int j = 0; j < SMALL_MAX - 1; ++j)
+        if (rk[j] < best) {
+          best = rk[j];
+          bi = j;
+        }
+      if (best == RANK_INF) break;
+      uint32_t nid = 0;
+#pragma unroll
+      for (int j = 0; j < SMALL_MAX; ++j)
+        if (j == bi) nid = rs[j];
+      // token bi becomes nid, token bi+1 leaves: shift the tail left by one
+#pragma unroll
+      for (int j = 0; j < SMALL_MAX - 1; ++j) {
+        if (j > bi) {
+          ids[j] = ids[j + 1];
+          rk[j] = rk[j + 1];
+          rs[j] = rs[j + 1];
+        } else if (j == bi) {
+          ids[j] = nid;
+        }
+      }
+      rk[SMALL_MAX - 1] = RANK_INF;
+      --n;
+      // the two pairs that touch the new token
+      uint32_t left = 0, right = 0;
+#pragma unroll
+      for (int j = 0; j < SMALL_MAX; ++j) {
+        if (j == bi - 1) left = ids[j];
+        if (j == bi + 1) right = ids[j];
+      }
+      uint2 rl = make_uint2(RANK_INF, 0u), rr = make_uint2(RANK_INF, 0u);
+      if (bi > 0) rl = probe_pair(tb.slots, tb.mask, left, nid);
+      if ((uint32_t)(bi + 1) < n) rr = probe_pair(tb.slots, tb.mask, nid, right);
+#pragma unroll
+      for (int j = 0; j < SMALL_MAX; ++j) {
+        if (j == bi - 1) {
+          rk[j] = rl.x;
+          rs[j] = rl.y;
+        }
+        if (j == bi) {
+          rk[j] = rr.x;
+          rs[j] = rr.y;
+        }
+      }
+    }
+    int32_t* out = w.ids + a;
+#pragma unroll
+    for (int j = 0; j < SMALL_MAX; ++j)
+      if ((uint32_t)j < n) out[j] = (int32_t)ids[j];
+    w.piece_cnt[p] = n;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Round engine over rows of 64 tokens, shared by the wave engine (NW = 1,
+// rows in LDS) and the block engine (NW = 16, rows in global memory).
+// ---------------------------------------------------------------------------
+template <int NW>
+struct RoundShared {
+  uint32_t wmin[NW];
+  uint32_t f0[NW], f1[NW], cin[NW];
+  uint32_t wsum[NW], wbase[NW];
+  uint32_t n_next;
+};
+
+template <int NW>
+__device__ void bpe_rounds(uint32_t* ids0, uint32_t* ids1, uint32_t* rk0, uint32_t* rk1, uint32_t* rs0,
+                           uint32_t* rs1, uint64_t* sel, const uint8_t* bytes, uint32_t L,
+                           const int32_t* bid, const DevTables& tb, int32_t* out, uint32_t* out_cnt,
+                           RoundShared<NW>& sm) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  constexpr int NT = NW * 64;
+  uint32_t* ids[2] = {ids0, ids1};
+  uint32_t* rk[2] = {rk0, rk1};
+  uint32_t* rs[2] = {rs0, rs1};
+  int cur = 0;
+  uint32_t n = L;
+
+  for (uint32_t i = tid; i < n; i += NT) ids[0][i] = (uint32_t)bid[bytes[i]];
+  __syncthreads();
+  for (uint32_t i = tid; i < n; i += NT) {
+    uint2 r = make_uint2(RANK_INF, 0u);
+    if (i + 1 < n) r = probe_pair(tb.slots, tb.mask, ids[0][i], ids[0][i + 1]);
+    rk[0][i] = r.x;
+    rs[0][i] = r.y;
+  }
+  __syncthreads();
+
+  for (;;) {
+    const uint32_t* I = ids[cur];
+    const uint32_t* R = rk[cur];
+    const uint32_t* S = rs[cur];
+    uint32_t* I2 = ids[cur ^ 1];
+    uint32_t* R2 = rk[cur ^ 1];
+    uint32_t* S2 = rs[cur ^ 1];
+
+    // 1. lowest rank in the piece
+    uint32_t m = RANK_INF;
+    for (uint32_t i = tid; i < n; i += NT) m = min(m, R[i]);
+    m = wave_min(m);
+    if (NW > 1) {
+      if (lane == 0) sm.wmin[wave] = m;
+      __syncthreads();
+      m = RANK_INF;
+      for (int v = 0; v < NW; ++v) m = min(m, sm.wmin[v]);
+    }
+    if (m == RANK_INF) break;
+
+    // 2. leftmost non-overlapping occurrences, row by row.  A row's choice
+    // depends on whether the last pair of the previous row was chosen; with
+    // several waves each wave first evaluates its rows for both carries.
+    const uint32_t rows = (n + 63) / 64;
+    const uint32_t rpw = (rows + NW - 1) / NW;
+    const uint32_t r_lo = min(rows, (uint32_t)wave * rpw);
+    const uint32_t r_hi = min(rows, r_lo + rpw);
+    uint32_t carry = 0;
+    if (NW > 1) {
+      uint32_t c0 = 0, c1 = 1;
+      for (uint32_t r = r_lo; r < r_hi; ++r) {
+        uint32_t i = r * 64 + lane;
+        uint64_t occ = __ballot(i < n && R[i] == m);
+        c0 = (uint32_t)(leftmost_nonoverlapping(occ & ~(uint64_t)c0) >> 63);
+        c1 = (uint32_t)(leftmost_nonoverlapping(occ & ~(uint64_t)c1) >> 63);
+      }
+      if (lane == 0) {
+        sm.f0[wave] = c0;
+        sm.f1[wave] = c1;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t c = 0;
+        for (int v = 0; v < NW; ++v) {
+          sm.cin[v] = c;
+          c = c ? sm.f1[v] : sm.f0[v];
+        }
+      }
+      __syncthreads();
+      carry = sm.cin[wave];
+    }
+    uint32_t keep_total = 0;
+    for (uint32_t r = r_lo; r < r_hi; ++r) {
+      uint32_t i = r * 64 + lane;
+      uint64_t occ = __ballot(i < n && R[i] == m);
+      uint64_t s = leftmost_nonoverlapping(occ & ~(uint64_t)carry);
+      if (lane == 0) sel[r] = s;
+      uint64_t valid = (n - r * 64 >= 64) ? ~0ull : ((1ull << (n - r * 64)) - 1ull);
+      uint64_t keep = valid & ~((s << 1) | (uint64_t)carry);
+      keep_total += __popcll(keep);
+      carry = (uint32_t)(s >> 63);
+    }
+    if (lane == 0) sel[rows] = 0;  // sentinel row (only bit 0 is ever read)
+    // 3. compaction offsets
+    if (NW > 1) {
+      if (lane == 0) sm.wsum[wave] = keep_total;
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t b = 0;
+        for (int v = 0; v < NW; ++v) {
+          sm.wbase[v] = b;
+          b += sm.wsum[v];
+        }
+        sm.n_next = b;
+      }
+      __syncthreads();
+    } else {
+      __syncthreads();
+    }
+    uint32_t base = NW > 1 ? sm.wbase[wave] : 0u;
+    const uint32_t n2 = NW > 1 ? sm.n_next : keep_total;
+    uint32_t prevbit = (NW > 1 && r_lo > 0) ? (uint32_t)(sel[r_lo - 1] >> 63) : 0u;
+    for (uint32_t r = r_lo; r < r_hi; ++r) {
+      uint32_t i = r * 64 + lane;
+      uint64_t s = sel[r];
+      uint64_t valid = (n - r * 64 >= 64) ? ~0ull : ((1ull << (n - r * 64)) - 1ull);
+      uint64_t keep = valid & ~((s << 1) | (uint64_t)prevbit);
+      if ((keep >> lane) & 1ull) {
+        uint32_t k = base + __popcll(keep & lanemask_lt(lane));
+        uint32_t my = (uint32_t)(s >> lane) & 1u;
+        uint32_t nx = lane < 63 ? (uint32_t)(s >> (lane + 1)) & 1u : (uint32_t)(sel[r + 1] & 1ull);
+        I2[k] = my ? S[i] : I[i];
+        R2[k] = (my | nx) ? RANK_DIRTY : R[i];
+        S2[k] = S[i];
+      }
+      base += __popcll(keep);
+      prevbit = (uint32_t)(s >> 63);
+    }
+    __syncthreads();
+    n = n2;
+    // 4. ranks of the pairs next to the merges
+    for (uint32_t i = tid; i < n; i += NT) {
+      if (R2[i] == RANK_DIRTY) {
+        uint2 r = make_uint2(RANK_INF, 0u);
+        if (i + 1 < n) r = probe_pair(tb.slots, tb.mask, I2[i], I2[i + 1]);
+        R2[i] = r.x;
+        S2[i] = r.y;
+      }
+    }
+    __syncthreads();
+    cur ^= 1;
+  }
+  const uint32_t* I = ids[cur];
+  for (uint32_t i = tid; i < n; i += NT) out[i] = (int32_t)I[i];
+  if (tid == 0) *out_cnt = n;
+}
+
+// ---------------------------------------------------------------------------
+// Wave engine: one 64-thread block pulls pieces from the queue.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void bpe_wave_kernel(Work w, DevTables tb) {
+  __shared__ uint32_t s_ids[2][WAVE_MAX], s_rk[2][WAVE_MAX], s_rs[2][WAVE_MAX];
+  __shared__ uint64_t s_sel[WAVE_MAX / 64 + 1];
+  __shared__ int32_t s_bid[256];
+  __shared__ RoundShared<1> sm;
+  for (int i = threadIdx.x; i < 256; i += 64) s_bid[i] = tb.byte_id[i];
+  __syncthreads();
+  const uint32_t n_long = w.ctrl->n_long;
+  for (;;) {
+    uint32_t k = 0;
+    if (threadIdx.x == 0) k = atomicAdd(&w.ctrl->long_ticket, 1u);
+    k = __shfl(k, 0, 64);
+    if (k >= n_long) break;
+    const uint32_t p = w.long_list[k];
+    const uint32_t a = w.piece_off[p];
+    const uint32_t L = w.piece_off[p + 1] - a;
+    if (L > (uint32_t)WAVE_MAX) {
+      if (threadIdx.x == 0) {
+        uint32_t z = atomicAdd(&w.ctrl->n_big, 1u);
+        w.big_list[z] = p;
+      }
+      continue;
+    }
+    bpe_rounds<1>(s_ids[0], s_ids[1], s_rk[0], s_rk[1], s_rs[0], s_rs[1], s_sel, w.text + a, L, s_bid, tb,
+                  w.ids + a, w.piece_cnt + p, sm);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Block engine: 16 waves per piece, rows in global scratch.
+// ---------------------------------------------------------------------------
+constexpr int BIG_WAVES = 16;
+
+__global__ __launch_bounds__(BIG_WAVES * 64) void bpe_big_kernel(Work w, DevTables tb) {
+  __shared__ int32_t s_bid[256];
+  __shared__ RoundShared<BIG_WAVES> sm;
+  __shared__ uint32_t s_k;
+  for (int i = threadIdx.x; i < 256; i += blockDim.x) s_bid[i] = tb.byte_id[i];
+  __syncthreads();
+  const uint32_t n_big = w.ctrl->n_big;
+  const uint32_t n = w.n;
+  for (;;) {
+    if (threadIdx.x == 0) s_k = atomicAdd(&w.ctrl->big_ticket, 1u);
+    __syncthreads();
+    const uint32_t k = s_k;
+    __syncthreads();
+    if (k >= n_big) break;
+    const uint32_t p = w.big_list[k];
+    const uint32_t a = w.piece_off[p];
+    const uint32_t L = w.piece_off[p + 1] - a;
+    uint32_t* sc = w.scratch32;
+    uint64_t* sel = reinterpret_cast<uint64_t*>(sc + 6ull * n) + a / 32;
+    bpe_rounds<BIG_WAVES>(sc + a, sc + n + a, sc + 2ull * n + a, sc + 3ull * n + a, sc + 4ull * n + a,
+                          sc + 5ull * n + a, sel, w.text + a, L, s_bid, tb, w.ids + a, w.piece_cnt + p, sm);
+    __syncthreads();
+  }
+}
+
+hipError_t launch_bpe(const Work& w, const DevTables& t, hipStream_t s) {
+  // Geometry depends only on the request size, never on counts the host
+  // would have to read back: kernels read P and the queue lengths on device.
+  uint32_t est = w.n / 4 + 1;  // generous bound on pieces per thread slot
+  uint32_t small_blocks = (est + 255) / 256;
+  if (small_blocks > 8192) small_blocks = 8192;
+  hipLaunchKernelGGL(bpe_small_kernel, dim3(small_blocks), dim3(256), 0, s, w, t);
+  uint32_t wave_blocks = w.n / 64 + 1;
+  if (wave_blocks > 4096) wave_blocks = 4096;
+  hipLaunchKernelGGL(bpe_wave_kernel, dim3(wave_blocks), dim3(64), 0, s, w, t);
+  uint32_t big_blocks = w.n / 4096 + 1;
+  if (big_blocks > 256) big_blocks = 256;
+  hipLaunchKernelGGL(bpe_big_kernel, dim3(big_blocks), dim3(BIG_WAVES * 64), 0, s, w, t);
+  return hipGetLastError();
+}
+
+}  // namespace tt

@@ -1,0 +1,655 @@
+// Pre-tokenization on the GPU: UTF-8 decode, character classes, run-local
+// piece-start rules and the piece-numbering scan, in one pass over the bytes.
+//
+// The paper replaces the sequential leftmost-first regex scan by an equivalent
+// per-character predicate: classify every character into letter / number /
+// whitespace / other, form maximal same-class runs, and decide whether a
+// character starts a piece from its offset in its run, at most four
+// characters of lookback and a few per-run aggregates (Sec. 3.1, "Removing
+// the sequential regex scan"; the pipeline of Sec. 3.2 is decode, classify,
+// runs, predicate, two prefix scans).
+//
+// MI355X design.  One 256-thread block owns 1,984 bytes and stages a 2,048
+// byte window (32 bytes of context on each side) in LDS; every thread decodes
+// and classifies 8 bytes.  Runs that reach past the window are resolved
+// without a second pass:
+//   - backwards (cl100k: a number run's length mod 3, the class before a
+//     CR/LF stretch) from run summaries that earlier blocks publish before
+//     they wait on anything;
+//   - forwards (cl100k: whether a whitespace stretch after CR/LF is the last
+//     stretch of its run) by reading the bytes after the window, which only a
+//     whitespace stretch longer than the window needs.
+// Piece numbers come from a block scan plus a decoupled look-back over the
+// per-block counts, so piece offsets are written in one pass with no host
+// round trip.  Block order is taken from an atomic ticket, so a block only
+// ever waits on blocks that started before it.
+#include "class_table.inc"
+#include "tt_internal.h"
+
+namespace tt {
+
+namespace {
+
+constexpr uint32_t ST_AGG = 1u, ST_INC = 2u;  // look-back flags (bits 32..33)
+constexpr uint32_t SUM_READY = 0x80000000u, SUM_RUNALL = 1u;
+
+__device__ __forceinline__ uint64_t ld_acquire(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_acquire(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_release(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_release(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// 2-bit class of a non-ASCII code point from the probed table.
+__device__ __forceinline__ uint32_t table_class(uint32_t cp) {
+  uint32_t blk = TT_CLS_L1[cp >> 8];
+  uint32_t b = TT_CLS_L2[blk * 64u + ((cp & 255u) >> 2)];
+  return (b >> ((cp & 3u) * 2u)) & 3u;
+}
+
+__device__ __forceinline__ uint32_t letter_ident(uint32_t lower) {
+  switch (lower) {
+    case 's': return I_S;
+    case 't': return I_T;
+    case 'r': return I_R;
+    case 'e': return I_E;
+    case 'v': return I_V;
+    case 'm': return I_M;
+    case 'l': return I_L;
+    case 'd': return I_D;
+    default: return I_NONE;
+  }
+}
+
+// Class and identity code of one code point.  Contraction letters are
+// case-sensitive for GPT-2 and folded for cl100k, where the engine also folds
+// U+017F (long s) to 's'.
+template <int PAT>
+__device__ __forceinline__ uint32_t char_code(uint32_t cp) {
+  uint32_t cls, id = I_NONE;
+  if (cp < 128u) {
+    if (((cp | 32u) - 'a') < 26u) cls = C_L;
+    else if ((cp - '0') < 10u) cls = C_N;
+    else if (cp == 10u || cp == 13u) cls = C_NL;
+    else if (cp == 32u || (cp - 9u) < 5u) cls = C_WS;
+    else cls = C_O;
+    if (cp == 32u) id = I_SP;
+    else if (cp == 39u) id = I_APO;
+    else if (cls == C_L && (PAT == TT_PATTERN_CL100K || cp >= 'a')) id = letter_ident(cp | 32u);
+  } else {
+    uint32_t c2 = table_class(cp);
+    cls = c2 == 1u ? C_L : c2 == 2u ? C_N : c2 == 3u ? C_WS : C_O;
+    if (PAT == TT_PATTERN_CL100K && cp == 0x17Fu) id = I_S;
+  }
+  return cls | (id << 3);
+}
+
+// Expected sequence length of a lead byte (0 for bytes that cannot lead).
+__device__ __forceinline__ int lead_len(uint32_t b) {
+  if (b < 0x80u) return 1;
+  if (b < 0xC2u) return 0;
+  if (b < 0xE0u) return 2;
+  if (b < 0xF0u) return 3;
+  if (b < 0xF5u) return 4;
+  return 0;
+}
+
+// Strict UTF-8 decode of the sequence starting at s[0]; `avail` bytes may be
+// read (bounded by the text end and the next document start).  Returns the
+// length, or 0 if the sequence is invalid.
+__device__ __forceinline__ int decode(const uint8_t* s, int avail, uint32_t& cp) {
+  uint32_t b0 = s[0];
+  int len = lead_len(b0);
+  if (len == 0 || len > avail) return 0;
+  if (len == 1) {
+    cp = b0;
+    return 1;
+  }
+  uint32_t b1 = s[1];
+  uint32_t lo = 0x80u, hi = 0xBFu;
+  if (b0 == 0xE0u) lo = 0xA0u;
+  else if (b0 == 0xEDu) hi = 0x9Fu;
+  else if (b0 == 0xF0u) lo = 0x90u;
+  else if (b0 == 0xF4u) hi = 0x8Fu;
+  if (b1 < lo || b1 > hi) return 0;
+  if (len == 2) {
+    cp = ((b0 & 0x1Fu) << 6) | (b1 & 0x3Fu);
+    return 2;
+  }
+  uint32_t b2 = s[2];
+  if ((b2 & 0xC0u) != 0x80u) return 0;
+  if (len == 3) {
+    cp = ((b0 & 0x0Fu) << 12) | ((b1 & 0x3Fu) << 6) | (b2 & 0x3Fu);
+    return 3;
+  }
+  uint32_t b3 = s[3];
+  if ((b3 & 0xC0u) != 0x80u) return 0;
+  cp = ((b0 & 0x07u) << 18) | ((b1 & 0x3Fu) << 12) | ((b2 & 0x3Fu) << 6) | (b3 & 0x3Fu);
+  return 4;
+}
+
+// Segmented char-count scan state for cl100k: has-head (bit 31), window index
+// of the latest run head (bits 16..27), characters since that head (bits 0..15;
+// or since the tile start when there is no head yet).
+__device__ __forceinline__ uint32_t seg_combine(uint32_t a, uint32_t b) {
+  return (b & 0x80000000u) ? b : ((a & 0xFFFF0000u) | ((a + b) & 0xFFFFu));
+}
+__device__ __forceinline__ bool seg_has(uint32_t s) { return (s & 0x80000000u) != 0; }
+__device__ __forceinline__ int seg_head(uint32_t s) { return (int)((s >> 16) & 0x0FFFu); }
+__device__ __forceinline__ uint32_t seg_cnt(uint32_t s) { return s & 0xFFFFu; }
+
+template <typename F>
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane, F comb) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint32_t o = __shfl_up(v, d, 64);
+    if (lane >= d) v = comb(o, v);
+  }
+  return v;
+}
+
+struct PtShared {
+  uint8_t buf[PT_WIN + 8];    // window bytes
+  uint8_t code[PT_WIN + 8];   // per-byte class/identity/doc-start codes
+  uint8_t dstart[PT_WIN + 8]; // 1 where a document starts
+  int16_t run_end[PT_WIN];    // cl100k: window index of the head after a run's head
+  uint32_t wave_tot[PT_THREADS / 64];
+  uint32_t tile;
+  uint32_t prefix;
+  uint32_t carry_n;           // cl100k: number-run chars before the tile, mod 3
+  uint32_t carry_nlpre;       // cl100k: class before a CR/LF stretch entering the tile
+  int64_t doc_lo_idx;         // batch: first document start index touching the window
+  int last_own;               // cl100k: window index of the tile's last own character
+};
+
+}  // namespace
+
+template <int PAT, bool BATCH>
+__global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_tiles) {
+  __shared__ PtShared sh;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t n = w.n;
+
+  if (tid == 0) sh.tile = atomicAdd(&w.ctrl->tile_ticket, 1u);
+  __syncthreads();
+  const uint32_t t = sh.tile;
+  if (t >= n_tiles) return;
+  const int64_t t0 = (int64_t)t * PT_OWN;
+  const int64_t w0 = t0 - PT_HALO;
+
+  auto inside = [&](int q) -> bool {
+    int64_t p = w0 + q;
+    return p >= 0 && p < n;
+  };
+
+  // ---- stage the window ----------------------------------------------------
+  for (int q = tid; q < PT_WIN + 8; q += PT_THREADS) {
+    int64_t p = w0 + q;
+    bool in = p >= 0 && p < n;
+    sh.buf[q] = in ? w.text[p] : 0;
+    sh.dstart[q] = (in && p == 0) ? 1 : 0;
+  }
+  if (BATCH) {
+    if (tid == 0) {
+      // first document start >= w0
+      int lo = 0, hi = w.n_docs;  // search in doc_off[0..n_docs)
+      while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        if (w.doc_off[mid] < w0) lo = mid + 1;
+        else hi = mid;
+      }
+      sh.doc_lo_idx = lo;
+    }
+  }
+  __syncthreads();
+  if (BATCH) {
+    for (int64_t j = sh.doc_lo_idx + tid; j < w.n_docs; j += PT_THREADS) {
+      int64_t d = w.doc_off[j];
+      if (d >= w0 + PT_WIN + 8) break;
+      if (d >= n) continue;
+      sh.dstart[d - w0] = 1;  // several empty documents may start here; all store the same value
+    }
+    __syncthreads();
+  }
+
+  // ---- decode, validate, classify ------------------------------------------
+  bool bad = false;
+  for (int q = tid; q < PT_WIN + 8; q += PT_THREADS) {
+    uint32_t ds = sh.dstart[q] ? CODE_DOCSTART : 0u;
+    uint32_t code = C_NONE;
+    bool own = q >= PT_HALO && q < PT_HALO + PT_OWN && inside(q);
+    if (inside(q)) {
+      uint32_t b = sh.buf[q];
+      if ((b & 0xC0u) == 0x80u) {
+        if (own) {
+          // a continuation byte must lie inside the sequence of a lead byte at
+          // most three bytes earlier, with no document start in between
+          bool claimed = false;
+          if (!ds) {
+            for (int k = 1; k <= 3; ++k) {
+              int r = q - k;
+              if (!inside(r)) break;
+              uint32_t br = sh.buf[r];
+              if ((br & 0xC0u) == 0x80u) {
+                if (sh.dstart[r]) break;
+                continue;
+              }
+              claimed = lead_len(br) > k;
+              break;
+            }
+          }
+          bad |= !claimed;
+        }
+      } else {
+        int avail = 1;
+        while (avail < 4 && q + avail < PT_WIN + 8 && inside(q + avail) && !sh.dstart[q + avail])
+          ++avail;
+        uint32_t cp = 0;
+        int len = decode(&sh.buf[q], avail, cp);
+        if (len == 0) {
+          bad |= own;
+          code = C_O;
+        } else {
+          code = char_code<PAT>(cp);
+        }
+      }
+    }
+    sh.code[q] = (uint8_t)(code | ds);
+  }
+  if (bad) __hip_atomic_store(&w.ctrl->error, (uint32_t)(-TT_ERR_INVALID_UTF8), __ATOMIC_RELAXED,
+                              __HIP_MEMORY_SCOPE_AGENT);
+  for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.run_end[q] = -1;
+  __syncthreads();
+
+  // ---- neighbour helpers (window indices; -1 = none) ----------------------
+  auto cls = [&](int q) -> uint32_t { return code_cls(sh.code[q]); };
+  auto ident = [&](int q) -> uint32_t { return code_id(sh.code[q]); };
+  auto prev = [&](int q) -> int {
+    if (sh.code[q] & CODE_DOCSTART) return -1;
+    for (int r = q - 1; r >= 0; --r) {
+      if (!inside(r)) return -1;
+      if (code_cls(sh.code[r]) != C_NONE) return r;
+    }
+    return -1;
+  };
+  auto next = [&](int q) -> int {
+    for (int r = q + 1; r < PT_WIN + 8; ++r) {
+      if (!inside(r)) return -1;
+      uint8_t c = sh.code[r];
+      if (c & CODE_DOCSTART) return -1;
+      if (code_cls(c) != C_NONE) return r;
+    }
+    return -1;
+  };
+  auto is_char = [&](int q) -> bool { return inside(q) && code_cls(sh.code[q]) != C_NONE; };
+  auto is_w = [](uint32_t c) -> bool { return c == C_WS || c == C_NL; };
+
+  // Suffix of a contraction starting at letter q: 1 or 2 letters, or 0.
+  auto suffix_len = [&](int q) -> int {
+    uint32_t a = ident(q);
+    if (a == I_S || a == I_T || a == I_M || a == I_D) return 1;
+    if (a == I_R || a == I_V || a == I_L) {
+      int q1 = next(q);
+      if (q1 >= 0) {
+        uint32_t b = ident(q1);
+        if ((a == I_R && b == I_E) || (a == I_V && b == I_E) || (a == I_L && b == I_L)) return 2;
+      }
+    }
+    return 0;
+  };
+  // Letter q starts a contraction suffix: the apostrophe before it begins a
+  // match, i.e. it is a one-character "other" run not preceded by U+0020.
+  auto contraction_len_at = [&](int q) -> int {
+    int p1 = prev(q);
+    if (p1 < 0 || ident(p1) != I_APO) return 0;
+    int p2 = prev(p1);
+    if (p2 >= 0 && (cls(p2) == C_O || ident(p2) == I_SP)) return 0;
+    return suffix_len(q);
+  };
+  // Letter q (inside a letter run) is the first letter after a contraction.
+  auto contraction_ends_here = [&](int q) -> bool {
+    int p1 = prev(q);
+    if (contraction_len_at(p1) == 1) return true;
+    int p2 = prev(p1);
+    return p2 >= 0 && cls(p2) == C_L && contraction_len_at(p2) == 2;
+  };
+
+  // ---- cl100k: run scan, run ends, summaries, carries ----------------------
+  uint32_t excl[PT_BPT];
+  const int qb = tid * PT_BPT;
+  if (PAT == TT_PATTERN_CL100K) {
+    // elements over window indices [HALO, WIN)
+    uint32_t elem[PT_BPT];
+    uint32_t agg = 0;
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) {
+      int q = qb + j;
+      uint32_t e = 0;
+      if (q >= PT_HALO && is_char(q)) {
+        int p = prev(q);
+        bool head = p < 0 || cls(p) != cls(q);
+        e = head ? (0x80000000u | ((uint32_t)q << 16) | 1u) : 1u;
+      }
+      elem[j] = e;
+      agg = seg_combine(agg, e);
+    }
+    uint32_t inc = wave_incl_scan(agg, lane, seg_combine);
+    if (lane == 63) sh.wave_tot[wave] = inc;
+    uint32_t lex = __shfl_up(inc, 1, 64);
+    if (lane == 0) lex = 0;
+    __syncthreads();
+    uint32_t wpre = 0;
+    for (int v = 0; v < wave; ++v) wpre = seg_combine(wpre, sh.wave_tot[v]);
+    uint32_t s = seg_combine(wpre, lex);
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) {
+      excl[j] = s;
+      uint32_t e = elem[j];
+      if ((e & 0x80000000u) && seg_has(s)) sh.run_end[seg_head(s)] = (int16_t)(qb + j);
+      s = seg_combine(s, e);
+    }
+    // summary of the tile's trailing run (own range), published before waiting
+    // on any other block
+    const int own_end = (int)(n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN);
+    int last_q = -1;
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) {
+      int q = qb + j;
+      if (q >= PT_HALO && q < own_end && is_char(q)) last_q = q;
+    }
+    // the thread holding the last own character publishes
+    if (tid == 0) sh.last_own = -1;
+    __syncthreads();
+    if (last_q >= 0) atomicMax(&sh.last_own, last_q);
+    __syncthreads();
+    const int s_last = sh.last_own;
+    if (s_last < 0) {
+      if (tid == 0) st_release(&w.tile_summary[t], SUM_READY | SUM_RUNALL);
+    } else if (s_last >= qb && s_last < qb + PT_BPT) {
+      int j = s_last - qb;
+      uint32_t st = 0;
+#pragma unroll
+      for (int k = 0; k < PT_BPT; ++k)
+        if (k == j) st = seg_combine(excl[k], elem[k]);
+      uint32_t sum = SUM_READY | ((seg_cnt(st) % 3u) << 1);
+      if (seg_has(st)) {
+        int hp = prev(seg_head(st));
+        sum |= (hp >= 0 ? cls(hp) : (uint32_t)C_NONE) << 3;
+      } else {
+        sum |= SUM_RUNALL;
+      }
+      st_release(&w.tile_summary[t], sum);
+    }
+    // carries for a run entering the tile from the left
+    if (tid == 0) {
+      sh.carry_n = 0;
+      sh.carry_nlpre = C_NONE;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      int f = -1;  // first own character
+      for (int q = PT_HALO; q < PT_HALO + PT_OWN; ++q)
+        if (is_char(q)) {
+          f = q;
+          break;
+        }
+      // a number run continuing into the tile needs its length so far; a
+      // CR/LF stretch ending at or after the tile start needs the class
+      // before it (the first own character may be the whitespace after it)
+      bool need = false;
+      if (f >= 0 && t > 0) {
+        int p = prev(f);
+        need = p >= 0 && ((cls(p) == C_N && cls(f) == C_N) || cls(p) == C_NL);
+      }
+      if (need) {
+        uint32_t acc = 0, pre = C_NONE;
+        for (int64_t base = (int64_t)t - 1; base >= 0; base -= 64) {
+          int64_t j = base - lane;
+          uint32_t v = 0;
+          if (j >= 0) {
+            do {
+              v = ld_acquire(&w.tile_summary[j]);
+            } while (!(v & SUM_READY));
+          }
+          bool stop = j >= 0 && !(v & SUM_RUNALL);
+          uint64_t m = __ballot(stop);
+          int first = m ? (__ffsll((unsigned long long)m) - 1) : 64;
+          uint32_t c = (j >= 0 && lane <= first) ? ((v >> 1) & 3u) : 0u;
+#pragma unroll
+          for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
+          acc += c;
+          if (m) {
+            pre = (__shfl(v, first, 64) >> 3) & 7u;
+            break;
+          }
+        }
+        if (lane == 0) {
+          sh.carry_n = acc % 3u;
+          sh.carry_nlpre = pre;
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // rule 2 of cl100k: is the whitespace stretch starting at q (after CR/LF)
+  // the last stretch of its whitespace run?
+  auto ws_stretch_is_last = [&](int q) -> bool {
+    int e = sh.run_end[q];
+    if (e >= 0) return (sh.code[e] & CODE_DOCSTART) || cls(e) != C_NL;
+    if (w0 + PT_WIN >= n) return true;  // the run reaches the end of the text
+    // the stretch continues past the window: read on in global memory
+    int64_t pos = w0 + PT_WIN;
+    int64_t lim = n;
+    if (BATCH) {
+      int lo = 0, hi = w.n_docs;
+      while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        if (w.doc_off[mid] < pos) lo = mid + 1;
+        else hi = mid;
+      }
+      if (lo < w.n_docs && w.doc_off[lo] < lim) lim = w.doc_off[lo];
+    }
+    while (pos < lim && (w.text[pos] & 0xC0u) == 0x80u) ++pos;
+    while (pos < lim) {
+      uint8_t tmp[4] = {0, 0, 0, 0};
+      int avail = 0;
+      while (avail < 4 && pos + avail < lim) {
+        tmp[avail] = w.text[pos + avail];
+        ++avail;
+      }
+      uint32_t cp = 0;
+      int len = decode(tmp, avail, cp);
+      if (len == 0) return true;  // invalid input; reported elsewhere
+      uint32_t c = code_cls(char_code<PAT>(cp));
+      if (c == C_NL) return false;
+      if (c != C_WS) return true;
+      pos += len;
+    }
+    return true;
+  };
+
+  // ---- piece-start predicate ----------------------------------------------
+  uint32_t flags = 0;
+#pragma unroll
+  for (int j = 0; j < PT_BPT; ++j) {
+    const int q = qb + j;
+    if (q < PT_HALO || q >= PT_HALO + PT_OWN || !is_char(q)) continue;
+    const uint32_t c0 = cls(q);
+    const int p1 = prev(q);
+    bool start;
+    if (p1 < 0) {
+      start = true;
+    } else {
+      const uint32_t c1 = cls(p1);
+      if (PAT == TT_PATTERN_GPT2) {
+        if (is_w(c0)) {
+          if (!is_w(c1)) {
+            start = true;  // whitespace run head
+          } else {
+            int n1 = next(q);  // last char of a run of >= 2, followed by non-space
+            start = n1 >= 0 && !is_w(cls(n1));
+          }
+        } else if (c1 == c0) {
+          start = c0 == C_L && contraction_ends_here(q);
+        } else if (ident(p1) == I_SP) {
+          start = false;  // the space before the run opens the piece
+        } else if (c0 == C_L && contraction_len_at(q) > 0) {
+          start = false;
+        } else {
+          start = true;
+        }
+      } else {
+        uint32_t ex = 0;
+#pragma unroll
+        for (int k = 0; k < PT_BPT; ++k)
+          if (k == j) ex = excl[k];
+        if (is_w(c0)) {
+          if (!is_w(c1)) {
+            // head of a whitespace run; after "other", leading CR/LF joins the symbol piece
+            start = !(c1 == C_O && c0 == C_NL);
+          } else if (c0 == C_NL) {
+            start = false;
+          } else if (c1 == C_NL) {
+            // first whitespace after a CR/LF stretch
+            uint32_t pre;
+            if (seg_has(ex)) {
+              int hp = prev(seg_head(ex));
+              pre = hp >= 0 ? cls(hp) : (uint32_t)C_NONE;
+            } else {
+              pre = sh.carry_nlpre;
+            }
+            start = (pre == C_O) || ws_stretch_is_last(q);
+          } else {
+            int n1 = next(q);
+            start = n1 >= 0 && !is_w(cls(n1));
+          }
+        } else if (c0 == C_N) {
+          if (c1 != C_N) {
+            start = true;
+          } else {
+            uint32_t off = seg_cnt(ex) + (seg_has(ex) ? 0u : sh.carry_n);
+            start = off % 3u == 0u;
+          }
+        } else if (c0 == C_O) {
+          start = c1 != C_O && ident(p1) != I_SP;
+        } else {  // letter
+          if (c1 == C_L) {
+            start = contraction_ends_here(q);
+          } else if (contraction_len_at(q) > 0) {
+            start = false;
+          } else if (c1 == C_WS) {
+            start = false;  // one whitespace char is the prefix
+          } else if (c1 == C_O) {
+            int p2 = prev(p1);
+            start = !(p2 < 0 || (cls(p2) != C_O && ident(p2) != I_SP));
+          } else {
+            start = true;
+          }
+        }
+      }
+    }
+    if (start) flags |= 1u << j;
+  }
+
+  // ---- number the pieces: block scan + decoupled look-back ------------------
+  const uint32_t cnt = __popc(flags);
+  uint32_t inc = wave_incl_scan(cnt, lane, [](uint32_t a, uint32_t b) { return a + b; });
+  __syncthreads();
+  if (lane == 63) sh.wave_tot[wave] = inc;
+  __syncthreads();
+  uint32_t wpre = 0, total = 0;
+  for (int v = 0; v < PT_THREADS / 64; ++v) {
+    if (v < wave) wpre += sh.wave_tot[v];
+    total += sh.wave_tot[v];
+  }
+  const uint32_t texcl = wpre + inc - cnt;
+
+  if (wave == 0) {
+    if (lane == 0) st_release(&w.tile_status[t], ((uint64_t)ST_AGG << 32) | total);
+    uint32_t prefix = 0;
+    for (int64_t base = (int64_t)t - 1; base >= 0; base -= 64) {
+      int64_t j = base - lane;
+      uint64_t v = 0;
+      if (j >= 0) {
+        do {
+          v = ld_acquire(&w.tile_status[j]);
+        } while ((v >> 32) == 0);
+      }
+      bool incl = j < 0 || (v >> 32) == ST_INC;
+      uint64_t m = __ballot(incl);
+      int first = m ? (__ffsll((unsigned long long)m) - 1) : 64;
+      uint32_t c = (j >= 0 && lane <= first) ? (uint32_t)v : 0u;
+#pragma unroll
+      for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
+      prefix += c;
+      if (m) break;
+    }
+    if (lane == 0) {
+      st_release(&w.tile_status[t], ((uint64_t)ST_INC << 32) | (prefix + total));
+      sh.prefix = prefix;
+    }
+  }
+  __syncthreads();
+  const uint32_t base = sh.prefix + texcl;
+  uint32_t k = 0;
+#pragma unroll
+  for (int j = 0; j < PT_BPT; ++j) {
+    if (flags & (1u << j)) {
+      w.piece_off[base + k] = (uint32_t)(w0 + qb + j);
+      ++k;
+    }
+  }
+  if (t == n_tiles - 1 && tid == 0) {
+    uint32_t P = sh.prefix + total;
+    w.ctrl->n_pieces = P;
+    w.piece_off[P] = (uint32_t)n;
+  }
+}
+
+hipError_t launch_pretok(const Work& w, int pattern, uint32_t n_tiles, hipStream_t s) {
+  dim3 grid(n_tiles), block(PT_THREADS);
+  bool batch = w.doc_off != nullptr;
+  if (pattern == TT_PATTERN_GPT2) {
+    if (batch) hipLaunchKernelGGL((pretok_kernel<TT_PATTERN_GPT2, true>), grid, block, 0, s, w, n_tiles);
+    else hipLaunchKernelGGL((pretok_kernel<TT_PATTERN_GPT2, false>), grid, block, 0, s, w, n_tiles);
+  } else {
+    if (batch) hipLaunchKernelGGL((pretok_kernel<TT_PATTERN_CL100K, true>), grid, block, 0, s, w, n_tiles);
+    else hipLaunchKernelGGL((pretok_kernel<TT_PATTERN_CL100K, false>), grid, block, 0, s, w, n_tiles);
+  }
+  return hipGetLastError();
+}
+
+// Zero the control block and the look-back words of one call.
+__global__ void reset_kernel(Work w, uint32_t n_pt, uint32_t n_ct) {
+  uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  uint32_t stride = gridDim.x * blockDim.x;
+  if (i == 0) {
+    Ctrl z = {};
+    *w.ctrl = z;
+  }
+  for (uint32_t k = i; k < n_pt; k += stride) {
+    w.tile_status[k] = 0;
+    w.tile_summary[k] = 0;
+  }
+  for (uint32_t k = i; k < n_ct; k += stride) w.ctile_status[k] = 0;
+}
+
+hipError_t launch_reset(const Work& w, uint32_t n_pt, uint32_t n_ct, hipStream_t s) {
+  uint32_t m = n_pt > n_ct ? n_pt : n_ct;
+  uint32_t blocks = (m + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(reset_kernel, dim3(blocks), dim3(256), 0, s, w, n_pt, n_ct);
+  return hipGetLastError();
+}
+
+}  // namespace tt

@@ -1,0 +1,121 @@
+"""The C ABI without a GPU: the library loads, exports what the header declares,
+and rejects invalid handles and tables before touching the device."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_29678_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "toktier.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tt_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    assert _declared() == sorted(["tt_create", "tt_destroy", "tt_encode", "tt_encode_device", "tt_encode_batch",
+                                  "tt_pretokenize", "tt_status_string", "tt_info"])
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib.load()
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_lib.SIGNATURES) == set(_declared())
+
+
+def test_status_strings():
+    lib = _lib.load()
+    for code in _lib.STATUS:
+        assert lib.tt_status_string(code)
+    assert lib.tt_status_string(-5).decode() == "input is not valid UTF-8"
+
+
+def _base_vocab():
+    vb = np.arange(256, dtype=np.uint8)
+    vo = np.arange(257, dtype=np.int64)
+    return vb, vo
+
+
+def _create(merges, vb, vo, pattern=0):
+    lib = _lib.load()
+    m = np.ascontiguousarray(np.asarray(merges, dtype=np.int32).reshape(-1, 3))
+    h = ctypes.c_void_p()
+    st = lib.tt_create(m.ctypes.data_as(ctypes.c_void_p) if len(m) else None, len(m),
+                       vb.ctypes.data_as(ctypes.c_void_p), vo.ctypes.data_as(ctypes.c_void_p), len(vo) - 1,
+                       pattern, ctypes.byref(h))
+    return st, h
+
+
+def _vocab_with(extra):
+    toks = [bytes([i]) for i in range(256)] + extra
+    vb = np.frombuffer(b"".join(toks), dtype=np.uint8).copy()
+    vo = np.zeros(len(toks) + 1, dtype=np.int64)
+    np.cumsum([len(t) for t in toks], out=vo[1:])
+    return vb, vo
+
+
+def test_create_rejects_bad_pattern():
+    vb, vo = _base_vocab()
+    assert _create([], vb, vo, pattern=7)[0] == -2
+
+
+def test_create_rejects_out_of_range():
+    vb, vo = _vocab_with([b"ab"])
+    assert _create([(97, 98, 300)], vb, vo)[0] == -3
+    assert _create([(-1, 98, 256)], vb, vo)[0] == -3
+
+
+def test_create_rejects_duplicate_pair():
+    vb, vo = _vocab_with([b"ab", b"ab"])
+    assert _create([(97, 98, 256), (97, 98, 257)], vb, vo)[0] == -3
+
+
+def test_create_rejects_non_proper_operand():
+    vb, vo = _vocab_with([b"abc", b"ab"])
+    # merge 0 uses 257 ("ab") before any merge produced it
+    assert _create([(257, 99, 256), (97, 98, 257)], vb, vo)[0] == -3
+
+
+def test_create_rejects_repeated_result():
+    vb, vo = _vocab_with([b"ab", b"abc", b"bc"])
+    assert _create([(97, 98, 256), (98, 99, 258), (97, 258, 256)], vb, vo)[0] == -3
+
+
+def test_create_rejects_vocab_mismatch():
+    vb, vo = _vocab_with([b"ba"])
+    assert _create([(97, 98, 256)], vb, vo)[0] == -4
+
+
+def test_create_rejects_missing_byte():
+    toks = [bytes([i]) for i in range(255)] + [b"xy"]
+    vb = np.frombuffer(b"".join(toks), dtype=np.uint8).copy()
+    vo = np.zeros(len(toks) + 1, dtype=np.int64)
+    np.cumsum([len(t) for t in toks], out=vo[1:])
+    assert _create([], vb, vo)[0] == -4
+
+
+def test_null_arguments():
+    lib = _lib.load()
+    n = ctypes.c_int64(0)
+    assert lib.tt_encode(None, None, 0, None, ctypes.byref(n), None) == -1
+    assert lib.tt_pretokenize(None, None, 0, None, ctypes.byref(n), None) == -1
+    assert lib.tt_encode_device(None, None, 0, None, None, None) == -1
+    assert lib.tt_encode_batch(None, None, None, 0, None, None, None) == -1
+    assert lib.tt_create(None, 0, None, None, 256, 0, None) == -1
+    lib.tt_destroy(None)
+
+
+def test_binding_fails_loudly_without_library(monkeypatch):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", "/nonexistent/libtoktier.so")
+    with pytest.raises(ImportError):
+        _lib.load()
