@@ -1,0 +1,207 @@
+"""Benchmark: exact tokenization of 1M-character requests on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3|4] [--no-cpu]
+
+A step is one full-request tokenization (pre-tokenization, BPE, compaction)
+of one distinct seeded 1,000,000-character sample whose bytes are already in
+HBM; the IDs stay in HBM.  W warm-up requests use separate samples.  The K
+timed requests run back to back between two stream synchronisations:
+value = K * 1e6 chars / elapsed.  Per-request latencies (enqueue to
+completion, input in HBM) give P50/P90/P99; a second pass over the same
+samples records HIP events between the library's stages (same stream) for the
+per-kernel times and the roofline of the dominant kernel.  The host-to-host
+latency through ``tt_encode`` (PCIe copies included) is reported separately.
+The CPU oracle is timed on one sample, single-threaded, as a baseline.
+
+Prints one JSON line.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def percentile(xs, q):
+    xs = sorted(xs)
+    if not xs:
+        return None
+    k = (len(xs) - 1) * q / 100.0
+    lo = int(k)
+    hi = min(lo + 1, len(xs) - 1)
+    return xs[lo] + (xs[hi] - xs[lo]) * (k - lo)
+
+
+def stage_bytes(stage, B, P, T):
+    """Algorithmic HBM bytes of one stage (what the method must move)."""
+    if stage == "pretokenize":   # read the text, write piece offsets
+        return B + 4 * (P + 1)
+    if stage == "bpe_short":     # read text + offsets, write IDs + counts
+        return B + 4 * (P + 1) + 4 * T + 4 * P
+    if stage == "compact":       # read counts + per-piece IDs, write dense IDs
+        return 4 * P + 4 * T + 4 * T
+    return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3, choices=(3, 4))
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build runs the tokenizer on a single MI355X "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_29678_amd import Tokenizer
+    from workloads import textgen
+    from workloads.tables import load_table
+
+    k = args.config
+    cfg = textgen.CONFIGS[k]
+    merges, vb, vo = load_table(k)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    sid = stream.cuda_stream
+    tok = Tokenizer(merges, vb, vo, cfg["pattern"])
+
+    # seeded samples: warm-up samples are distinct from the timed ones
+    n_total = args.warmup + args.steps
+    texts = [textgen.latency_sample(k, s % 32).encode("utf-8") for s in range(n_total)]
+    d_in = [torch.from_numpy(np.frombuffer(t, dtype=np.uint8).copy()).to(dev) for t in texts]
+    cap = max(len(t) for t in texts)
+    d_out = torch.empty(cap, dtype=torch.int32, device=dev)
+    d_len = torch.zeros(len(texts), dtype=torch.int64, device=dev)
+    n_chars = [len(t.decode("utf-8")) for t in texts]
+    torch.cuda.synchronize()
+
+    def run(i):
+        tok.encode_device(d_in[i], len(texts[i]), d_out, d_len[i:i + 1], sid)
+
+    for i in range(args.warmup):
+        run(i)
+    torch.cuda.synchronize()
+
+    # --- timed region: K requests back to back -----------------------------
+    timed = list(range(args.warmup, n_total))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in timed:
+        run(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    chars = sum(n_chars[i] for i in timed)
+    value = chars / elapsed
+    lens = d_len.cpu().numpy()
+    if (lens[timed] <= 0).any():
+        raise SystemExit("tokenizer reported an error: %s" % lens[timed])
+
+    # --- per-request latency (enqueue to completion, input in HBM) -----------
+    lat = []
+    for i in timed:
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        run(i)
+        stream.synchronize()
+        lat.append((time.perf_counter() - a) * 1e3)
+
+    # --- stage times from library events on the same stream -------------------
+    tok.set_profiling(True)
+    stage = {}
+    for i in timed:
+        run(i)
+        for name, ms in tok.stage_times(sid).items():
+            stage.setdefault(name, []).append(ms)
+    tok.set_profiling(False)
+    stage_avg = {s: sum(v) / len(v) for s, v in stage.items()}
+
+    # sizes for algorithmic bytes: P from the split-level export, T from the output
+    P_avg = sum(len(tok.pretokenize(texts[i])) for i in timed[:4]) / min(4, len(timed))
+    B_avg = sum(len(texts[i]) for i in timed) / len(timed)
+    T_avg = float(np.mean(lens[timed]))
+    rl = {}
+    for s, ms in stage_avg.items():
+        b = stage_bytes(s, B_avg, P_avg, T_avg)
+        if b is not None and ms > 0:
+            rl[s] = {"ms": round(ms, 4), "bytes": int(b), "GBs": round(b / (ms * 1e-3) / 1e9, 1),
+                     "frac": round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 5)}
+    dominant = max((s for s in rl), key=lambda s: rl[s]["ms"]) if rl else None
+
+    # --- host-to-host latency through tt_encode (PCIe copies included) --------
+    host_lat = []
+    for i in timed[: min(10, len(timed))]:
+        a = time.perf_counter()
+        tok.encode(texts[i], sid)
+        host_lat.append((time.perf_counter() - a) * 1e3)
+
+    # --- CPU oracle baseline on one sample --------------------------------------
+    cpu = None
+    if not args.no_cpu:
+        from oracle.bpe import MergeTable
+        from oracle.tokenizer import encode as oracle_encode
+        from workloads.tables import vocab_list
+
+        table = MergeTable(merges.tolist(), vocab_list(vb, vo))
+        sample = texts[timed[0]]
+        a = time.perf_counter()
+        ids = oracle_encode(sample, table, cfg["pattern"])
+        dt = time.perf_counter() - a
+        got = d_out[: int(lens[timed[-1]])]  # last run used the last timed sample
+        run(timed[0])
+        torch.cuda.synchronize()
+        same = d_out[: int(d_len[timed[0]].item())].cpu().numpy().tolist() == ids
+        cpu = {"value": round(n_chars[timed[0]] / dt, 1), "unit": "chars/s", "cores": 1, "kind": "oracle",
+               "sample": "one full %d-char sample of the timed workload, single thread, pure Python"
+                         % n_chars[timed[0]],
+               "seconds": round(dt, 2), "ids_identical_to_gpu": bool(same)}
+        del got
+
+    out = {
+        "metric": "exact-tokenization chars/sec and P50 latency for a 1M-char request, 1 MI355X",
+        "value": round(value, 1),
+        "unit": "chars/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed * 1e3 / len(timed), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": "%s: 1,000,000-char seeded %s request, %s-style pattern, %d merges"
+                               % (cfg["name"].upper(), "agent-transcript" if k == 3 else
+                                  "multilingual agent-transcript", cfg["pattern"], cfg["merges"]),
+                   "chars": 1_000_000, "bytes_avg": int(B_avg), "tokens_avg": int(T_avg),
+                   "pieces_avg": int(P_avg), "samples": len(timed)},
+        "p50_ms": round(percentile(lat, 50), 4),
+        "p90_ms": round(percentile(lat, 90), 4),
+        "p99_ms": round(percentile(lat, 99), 4),
+        "host_to_host_p50_ms": round(percentile(host_lat, 50), 4),
+        "stage_ms": {s: round(v, 4) for s, v in stage_avg.items()},
+        "roofline": None,
+        "cpu_baseline": cpu,
+        "context": {"paper_p50_ms_1M_chars": 0.87, "paper_hardware": "RTX PRO 6000 Blackwell (Qwen3 real text)"},
+    }
+    if dominant:
+        r = rl[dominant]
+        out["roofline"] = {"kernel": dominant, "bound": "hbm", "achieved": r["GBs"], "peak": HBM_PEAK_GBS,
+                           "unit": "GB/s", "frac": r["frac"], "traffic": None, "per_stage": rl}
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

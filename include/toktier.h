@@ -4,8 +4,8 @@
  * The library computes, on one GPU, the full-request tokenization path of
  * "TokTier: Exact Stateful CPU+GPU Tokenization for Agentic LLM Serving":
  * exact GPT-family regex pre-tokenization recast as run-local rules
- * (Sec. 3.1, "Removing the sequential regex scan"), then exact byte-level BPE
- * (Sec. 3.2, "GPU BPE"), with output compaction.  The output contract is the
+ * (Sec. 4.1, "Removing the sequential regex scan"), then exact byte-level BPE
+ * (Sec. 4.2, "GPU BPE"), with output compaction.  The output contract is the
  * paper's (Sec. 1; Sec. 3 problem statement): the emitted token IDs are
  * identical to full reference tokenization of the whole request, i.e. to
  * leftmost-first pre-tokenization followed by per-piece greedy lowest-rank
@@ -22,7 +22,7 @@
  *    nothing is written to caller buffers except where stated.
  *  - Byte-level BPE emits at most one ID per input byte, so an output buffer
  *    of `len` IDs (or the total byte count for a batch) is always enough.
- *  - A handle is immutable after tt_create (Sec. 3.5: registry entries are
+ *  - A handle is immutable after tt_create (Sec. 4.5: registry entries are
  *    immutable after registration).  Calls on one handle from several host
  *    threads are allowed if each thread uses its own stream; the handle keeps
  *    one workspace per stream.
@@ -55,14 +55,14 @@ enum {
 #define TT_MAX_BYTES ((int64_t)1 << 30)
 
 /* ---- pattern families ------------------------------------------------ */
-/* Pre-tokenization pattern, each a leftmost-first alternation (Sec. 3.1):
+/* Pre-tokenization pattern, each a leftmost-first alternation (Sec. 4.1):
  *  TT_PATTERN_GPT2:   's 't 're 've 'm 'll 'd | ?\p{L}+ | ?\p{N}+ |
  *                      ?[^\s\p{L}\p{N}]+ | \s+(?!\S) | \s+
  *  TT_PATTERN_CL100K: (?i:'s|'t|'re|'ve|'m|'ll|'d) | [^\r\n\p{L}\p{N}]?\p{L}+ |
  *                     \p{N}{1,3} | ?[^\s\p{L}\p{N}]+[\r\n]* | \s*[\r\n]+ |
  *                     \s+(?!\S) | \s+
  * Character classes are those of the Oniguruma engine of HF tokenizers 0.22.2
- * (the paper pins class tables probed from the reference engine, Sec. 3.1). */
+ * (the paper pins class tables probed from the reference engine, Sec. 4.1). */
 enum { TT_PATTERN_GPT2 = 0, TT_PATTERN_CL100K = 1 };
 
 typedef struct tt_tokenizer tt_tokenizer; /* opaque */
@@ -86,7 +86,7 @@ typedef struct {
  * The base ID of byte b is the lowest ID whose vocabulary entry is the single
  * byte b; all 256 must exist.  The merge list must be *proper*, which is what
  * makes one round of merging all leftmost non-overlapping occurrences of the
- * lowest-ranked pair equal to merging them one at a time (Sec. 3.2):
+ * lowest-ranked pair equal to merging them one at a time (Sec. 4.2):
  *   - left, right, result lie in [0, vocab_size); no pair occurs twice;
  *   - each operand of merge r is a base ID or the result of a merge of rank < r;
  *   - results are pairwise distinct and none is a base ID;
@@ -125,7 +125,7 @@ int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_id
 int tt_encode_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_t* d_out_ids,
                      int64_t* d_out_len, void* stream);
 
-/* Tokenize a batch of independent documents in one call (Sec. 3.2: documents
+/* Tokenize a batch of independent documents in one call (Sec. 4.2: documents
  * are concatenated and runs are cut at document boundaries; no piece or token
  * crosses a document boundary).
  *  concat         all documents back to back (host), doc_offsets[n_docs] bytes.
@@ -140,7 +140,7 @@ int tt_encode_batch(tt_tokenizer* h, const uint8_t* concat, const int64_t* doc_o
 
 /* ---- split-level export (tests) ---------------------------------------- */
 /* Pre-tokenization only: the UTF-8 byte offset of the first byte of every
- * piece, in order (Sec. 3.1: differential testing compares piece boundaries as
+ * piece, in order (Sec. 4.1: differential testing compares piece boundaries as
  * well as IDs, because an ID-level check can hide a split fault).
  *  utf8[len]          host bytes.
  *  out_piece_starts   host buffer of at least max(len, 1) entries.
@@ -155,6 +155,19 @@ const char* tt_status_string(int status);
 
 /* Number of merges and vocabulary size of a handle (for bindings). */
 int tt_info(const tt_tokenizer* h, int32_t* n_merges, int32_t* vocab_size, int32_t* pattern_id);
+
+/* ---- measurement ------------------------------------------------------- */
+/* Record HIP events between the stages of every later call on this handle
+ * (enable != 0) or stop recording (enable == 0).  For measurement only: the
+ * events add a few microseconds per call. */
+int tt_set_profiling(tt_tokenizer* h, int enable);
+
+/* Elapsed milliseconds of the stages of the most recent call on `stream`, in
+ * launch order: reset, pre-tokenization, short-piece BPE, wave BPE, block BPE,
+ * compaction.  Waits for that call to finish.  out_ms holds `cap` entries;
+ * *n_out receives how many were written (0 if profiling was off or the last
+ * call on the stream stopped after pre-tokenization earlier than BPE). */
+int tt_stage_times(tt_tokenizer* h, void* stream, double* out_ms, int32_t cap, int32_t* n_out);
 
 #ifdef __cplusplus
 }

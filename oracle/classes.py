@@ -3,8 +3,8 @@
 The patterns of both families test three Unicode properties: letters
 (``\\p{L}``), numbers (``\\p{N}``) and whitespace (``\\s``).  Every other
 code point is "other".  The paper pins these tables by probing the reference
-regex engine rather than trusting a library's Unicode version (Sec. 3.1,
-table pinning; Sec. 6.1, the Unicode table skew).  ``data/onig_classes.txt``
+regex engine rather than trusting a library's Unicode version (Sec. 4.1,
+table pinning; Sec. 5.2, the Unicode table skew).  ``data/onig_classes.txt``
 holds that probe for Oniguruma inside HF tokenizers 0.22.2; it was written by
 ``data/probe_onig.py``.
 

@@ -2,8 +2,8 @@
 
 The paper pins its Unicode class tables by probing them out of the reference
 engine instead of taking them from a library's Unicode data, because two
-Unicode versions disagreed on thousands of code points (Sec. 3.1 on table
-pinning; Sec. 6.1 on the table skew it found).  The reference engine here is
+Unicode versions disagreed on thousands of code points (Sec. 4.1 on table
+pinning; Sec. 5.2 on the table skew it found).  The reference engine here is
 the Oniguruma build inside HF ``tokenizers`` 0.22.2, the version the paper
 pins.  This script asks that engine, for every Unicode scalar value, whether it
 matches ``\\p{L}``, ``\\p{N}`` and ``\\s``, and which code points match each

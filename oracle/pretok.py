@@ -2,7 +2,7 @@
 
 GPT-family pre-tokenizers are a leftmost-first alternation regex with
 backtracking; every match starts where the previous one ended (Sec. 1;
-Sec. 3.1, "Removing the sequential regex scan").  This module is that
+Sec. 4.1, "Removing the sequential regex scan").  This module is that
 definition and nothing more: at the current position it tries the
 alternatives in their order, the first one that matches wins, its match is the
 next piece, and the scan continues at the match's end.  Each alternative is

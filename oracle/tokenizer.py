@@ -1,11 +1,11 @@
 """Full-request tokenization, the definition the library must reproduce (oracle; test infrastructure).
 
-The output contract (Sec. 1; Sec. 3 problem statement; Sec. 3.4 scope) is that
+The output contract (Sec. 1; Sec. 3 problem statement; Sec. 4.4 scope) is that
 the IDs equal those of full reference tokenization of the whole request.  For
 the tokenizers here that is: strict UTF-8 decoding, leftmost-first
 pre-tokenization, per-piece BPE, concatenation (Appendix, Definition
 d:frontend and Lemma l:homo).  A batch encodes each document on its own; no
-piece or token crosses a document boundary (Sec. 3.2, multi-document batches).
+piece or token crosses a document boundary (Sec. 4.2, multi-document batches).
 """
 
 from .bpe import MergeTable, bpe

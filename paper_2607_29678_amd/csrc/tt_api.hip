@@ -2,7 +2,7 @@
 // workspaces, and the launch chain of one call.
 //
 // Chain of one request (all on the caller's stream, no host round trip
-// between kernels; Sec. 3.3 keeps piece counts, dispatch lists and the output
+// between kernels; Sec. 4.3 keeps piece counts, dispatch lists and the output
 // length on the device and sizes launches from buffer capacity):
 //   reset -> pre-tokenize -> BPE (thread / wave / block engines) -> compact
 // The host synchronises twice per blocking call: once for the output length,
@@ -21,6 +21,9 @@ using namespace tt;
 
 namespace {
 
+// Stages of one call, in launch order (profiling names them in this order).
+enum { ST_RESET, ST_PRETOK, ST_BPE_SMALL, ST_BPE_WAVE, ST_BPE_BLOCK, ST_COMPACT, N_STAGES };
+
 struct Workspace {
   uint64_t cap = 0;           // bytes of request this workspace holds
   int64_t doc_cap = 0;        // documents the batch buffers hold
@@ -33,6 +36,8 @@ struct Workspace {
   int64_t* d_out_docs = nullptr;
   int64_t* h_len = nullptr;   // pinned readback word
   uint32_t* h_ctrl = nullptr; // pinned readback of the control block
+  hipEvent_t ev[N_STAGES + 1] = {};  // stage boundaries of the last call (profiling)
+  int n_ev = 0;                      // events recorded by the last call
 };
 
 }  // namespace
@@ -42,6 +47,7 @@ struct tt_tokenizer {
   int32_t n_merges = 0;
   int32_t vocab_size = 0;
   int device = 0;
+  int profile = 0;  // record stage events on every call
   MergeSlot* d_slots = nullptr;
   uint32_t mask = 0;
   int32_t* d_byte_id = nullptr;
@@ -59,6 +65,8 @@ void free_ws(Workspace* s) {
   if (s->d_docs) (void)hipFree(s->d_docs);
   if (s->h_len) (void)hipHostFree(s->h_len);
   if (s->h_ctrl) (void)hipHostFree(s->h_ctrl);
+  for (auto& e : s->ev)
+    if (e) (void)hipEventDestroy(e);
   delete s;
 }
 
@@ -172,11 +180,21 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_doc_off = out_docs;
   DevTables tb{h->d_slots, h->mask, h->d_byte_id};
   const uint32_t npt = pt_tiles(n), nct = ct_tiles_cap(n);
-  if (launch_reset(w, npt, nct, st) != hipSuccess) return TT_ERR_HIP;
-  if (launch_pretok(w, h->pattern, npt, st) != hipSuccess) return TT_ERR_HIP;
+  const bool prof = h->profile != 0;
+  s->n_ev = 0;
+  auto mark = [&]() -> bool {
+    if (!prof) return true;
+    if (!s->ev[s->n_ev] && hipEventCreate(&s->ev[s->n_ev]) != hipSuccess) return false;
+    return hipEventRecord(s->ev[s->n_ev++], st) == hipSuccess;
+  };
+  if (!mark()) return TT_ERR_HIP;
+  if (launch_reset(w, npt, nct, st) != hipSuccess || !mark()) return TT_ERR_HIP;
+  if (launch_pretok(w, h->pattern, npt, st) != hipSuccess || !mark()) return TT_ERR_HIP;
   if (pretok_only) return TT_OK;
-  if (launch_bpe(w, tb, st) != hipSuccess) return TT_ERR_HIP;
-  if (launch_compact(w, nct, st) != hipSuccess) return TT_ERR_HIP;
+  if (launch_bpe_small(w, tb, st) != hipSuccess || !mark()) return TT_ERR_HIP;
+  if (launch_bpe_wave(w, tb, st) != hipSuccess || !mark()) return TT_ERR_HIP;
+  if (launch_bpe_block(w, tb, st) != hipSuccess || !mark()) return TT_ERR_HIP;
+  if (launch_compact(w, nct, st) != hipSuccess || !mark()) return TT_ERR_HIP;
   if (d_docs && launch_doc_offsets(w, st) != hipSuccess) return TT_ERR_HIP;
   return TT_OK;
 }
@@ -404,6 +422,36 @@ int tt_pretokenize(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int64_t* o
   }
   for (uint32_t i = 0; i < P; ++i) out_piece_starts[i] = tmp[i];
   *out_n = P;
+  return TT_OK;
+}
+
+int tt_set_profiling(tt_tokenizer* h, int enable) {
+  if (!h) return TT_ERR_NULL_ARG;
+  h->profile = enable ? 1 : 0;
+  return TT_OK;
+}
+
+int tt_stage_times(tt_tokenizer* h, void* stream, double* out_ms, int32_t cap, int32_t* n_out) {
+  if (!h || !n_out || (cap > 0 && !out_ms)) return TT_ERR_NULL_ARG;
+  *n_out = 0;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Workspace* s = nullptr;
+  {
+    std::lock_guard<std::mutex> g(h->mu);
+    auto it = h->ws.find(st);
+    if (it == h->ws.end()) return TT_OK;
+    s = it->second;
+  }
+  if (s->n_ev < 2) return TT_OK;
+  if (hipSetDevice(h->device) != hipSuccess || hipEventSynchronize(s->ev[s->n_ev - 1]) != hipSuccess)
+    return TT_ERR_HIP;
+  int k = 0;
+  for (int i = 0; i + 1 < s->n_ev && k < cap; ++i, ++k) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, s->ev[i], s->ev[i + 1]) != hipSuccess) return TT_ERR_HIP;
+    out_ms[k] = ms;
+  }
+  *n_out = k;
   return TT_OK;
 }
 

@@ -4,11 +4,11 @@
 // repeatedly merge the adjacent pair with the lowest merge rank, leftmost
 // first (the model stage of the front-end/model factorisation, Appendix,
 // Definition d:frontend and Lemma l:homo).  Two facts license a parallel
-// schedule (Sec. 3.2, "GPU BPE"): the minimum rank of a round names one pair,
+// schedule (Sec. 4.2, "GPU BPE"): the minimum rank of a round names one pair,
 // and merging all leftmost non-overlapping occurrences of that pair at once
 // equals merging them one by one; and after a merge only the two pairs next
 // to it need a new rank lookup.  Work is dispatched by piece length so each
-// piece gets the smallest execution unit that holds it (Sec. 3.2).
+// piece gets the smallest execution unit that holds it (Sec. 4.2).
 //
 // MI355X design (wave64, LDS, one HBM-resident hash table):
 //   - pieces of at most 16 bytes: one thread per piece, the sequence in
@@ -354,19 +354,27 @@ __global__ __launch_bounds__(BIG_WAVES * 64) void bpe_big_kernel(Work w, DevTabl
   }
 }
 
-hipError_t launch_bpe(const Work& w, const DevTables& t, hipStream_t s) {
-  // Geometry depends only on the request size, never on counts the host
-  // would have to read back: kernels read P and the queue lengths on device.
-  uint32_t est = w.n / 4 + 1;  // generous bound on pieces per thread slot
-  uint32_t small_blocks = (est + 255) / 256;
-  if (small_blocks > 8192) small_blocks = 8192;
-  hipLaunchKernelGGL(bpe_small_kernel, dim3(small_blocks), dim3(256), 0, s, w, t);
-  uint32_t wave_blocks = w.n / 64 + 1;
-  if (wave_blocks > 4096) wave_blocks = 4096;
-  hipLaunchKernelGGL(bpe_wave_kernel, dim3(wave_blocks), dim3(64), 0, s, w, t);
-  uint32_t big_blocks = w.n / 4096 + 1;
-  if (big_blocks > 256) big_blocks = 256;
-  hipLaunchKernelGGL(bpe_big_kernel, dim3(big_blocks), dim3(BIG_WAVES * 64), 0, s, w, t);
+// Geometry depends only on the request size, never on counts the host would
+// have to read back: the kernels read P and the queue lengths on the device.
+hipError_t launch_bpe_small(const Work& w, const DevTables& t, hipStream_t s) {
+  uint32_t est = w.n / 4 + 1;  // one thread per piece slot (P <= n), grid-stride beyond
+  uint32_t blocks = (est + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(bpe_small_kernel, dim3(blocks), dim3(256), 0, s, w, t);
+  return hipGetLastError();
+}
+
+hipError_t launch_bpe_wave(const Work& w, const DevTables& t, hipStream_t s) {
+  uint32_t blocks = w.n / 64 + 1;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(bpe_wave_kernel, dim3(blocks), dim3(64), 0, s, w, t);
+  return hipGetLastError();
+}
+
+hipError_t launch_bpe_block(const Work& w, const DevTables& t, hipStream_t s) {
+  uint32_t blocks = w.n / 4096 + 1;
+  if (blocks > 256) blocks = 256;
+  hipLaunchKernelGGL(bpe_big_kernel, dim3(blocks), dim3(BIG_WAVES * 64), 0, s, w, t);
   return hipGetLastError();
 }
 

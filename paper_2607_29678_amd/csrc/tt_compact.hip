@@ -2,10 +2,10 @@
 //
 // The BPE engines leave piece p's IDs at its byte offset and its token count
 // in piece_cnt[p].  An exclusive scan of the counts gives every piece its
-// output offset; the IDs are then copied (Sec. 3.2: the complete path is
+// output offset; the IDs are then copied (Sec. 4.2: the complete path is
 // pre-tokenization, BPE and output compaction).  One pass: a block scan plus
 // a decoupled look-back over the per-block totals.  The output length stays
-// in device memory (Sec. 3.3: piece counts, dispatch lists and output length
+// in device memory (Sec. 4.3: piece counts, dispatch lists and output length
 // stay on the device).
 #include "tt_internal.h"
 

@@ -128,7 +128,9 @@ inline uint32_t ct_tiles_cap(uint32_t n) { return (n + CT_TILE - 1) / CT_TILE + 
 // Launchers (defined in the .hip files) -------------------------------------
 hipError_t launch_reset(const Work& w, uint32_t n_pt_tiles, uint32_t n_ct_tiles, hipStream_t s);
 hipError_t launch_pretok(const Work& w, int pattern, uint32_t n_pt_tiles, hipStream_t s);
-hipError_t launch_bpe(const Work& w, const DevTables& t, hipStream_t s);
+hipError_t launch_bpe_small(const Work& w, const DevTables& t, hipStream_t s);
+hipError_t launch_bpe_wave(const Work& w, const DevTables& t, hipStream_t s);
+hipError_t launch_bpe_block(const Work& w, const DevTables& t, hipStream_t s);
 hipError_t launch_compact(const Work& w, uint32_t n_ct_tiles, hipStream_t s);
 hipError_t launch_doc_offsets(const Work& w, hipStream_t s);
 

@@ -5,8 +5,8 @@
 // per-character predicate: classify every character into letter / number /
 // whitespace / other, form maximal same-class runs, and decide whether a
 // character starts a piece from its offset in its run, at most four
-// characters of lookback and a few per-run aggregates (Sec. 3.1, "Removing
-// the sequential regex scan"; the pipeline of Sec. 3.2 is decode, classify,
+// characters of lookback and a few per-run aggregates (Sec. 4.1, "Removing
+// the sequential regex scan"; the pipeline of Sec. 4.2 is decode, classify,
 // runs, predicate, two prefix scans).
 //
 // MI355X design.  One 256-thread block owns 1,984 bytes and stages a 2,048

@@ -117,5 +117,19 @@ class Tokenizer:
         _lib.check(st, "tt_encode_device")
 
 
+    # -- measurement -------------------------------------------------------
+    def set_profiling(self, enable=True):
+        """``tt_set_profiling``: record stage events on later calls."""
+        _lib.check(self._lib.tt_set_profiling(self._h, 1 if enable else 0), "tt_set_profiling")
+
+    def stage_times(self, stream=None) -> dict:
+        """``tt_stage_times``: {stage name: ms} of the last call on ``stream``."""
+        out = np.zeros(16, dtype=np.float64)
+        n = ctypes.c_int32(0)
+        _lib.check(self._lib.tt_stage_times(self._h, _stream(stream), _ptr(out), 16, ctypes.byref(n)),
+                   "tt_stage_times")
+        return {_lib.STAGES[i]: float(out[i]) for i in range(n.value)}
+
+
 def status_string(status: int) -> str:
     return _lib.load().tt_status_string(status).decode()

@@ -1,7 +1,7 @@
 """GPU parity: the HIP library against the CPU oracle, split level and ID level.
 
 The paper checks its GPU path at two levels, piece boundaries and final IDs,
-because an ID-level comparison can hide a wrong split (Sec. 3.1).  Both are
+because an ID-level comparison can hide a wrong split (Sec. 4.1).  Both are
 compared element by element here on the seeded configurations, at their full
 sizes, through the C ABI.
 """

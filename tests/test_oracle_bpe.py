@@ -6,7 +6,7 @@
   * the HF tokenizers BPE model with the same merges agrees (library routine);
   * invariants: the IDs spell the input, no adjacent pair inside a piece still
     has a rank, at most one ID per byte;
-  * the parallel round schedule the GPU uses (Sec. 3.2: merge every leftmost
+  * the parallel round schedule the GPU uses (Sec. 4.2: merge every leftmost
     non-overlapping occurrence of the round's lowest-ranked pair) equals the
     greedy definition.
 """

@@ -1,7 +1,7 @@
 """Seeded synthetic text in the shapes of the paper's workloads.
 
 The paper measures on real agent transcripts and web text that are not
-available here (Sec. 6, Table tab:coldhead; the workload study in Sec. 2).
+available here (Sec. 5.4, Table tab:coldhead; the workload study in Sec. 2).
 These generators stand in for them: prose built from a synthetic lexicon,
 code-like lines, JSON tool outputs, log lines with timestamps and hex IDs,
 and, for the multilingual configuration, accented Latin, Cyrillic, CJK runs
