@@ -347,6 +347,7 @@ int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_id
   if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
   int64_t T = *s->h_len;
   if (T < 0) return (int)T;
+  if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
   if (T > 0) {
     if (hipMemcpyAsync(out_ids, s->d_out, (size_t)T * 4, hipMemcpyDeviceToHost, st) != hipSuccess)
       return TT_ERR_HIP;
@@ -385,6 +386,7 @@ int tt_encode_batch(tt_tokenizer* h, const uint8_t* concat, const int64_t* doc_o
   if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
   int64_t T = *s->h_len;
   if (T < 0) return (int)T;
+  if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
   if (hipMemcpyAsync(out_ids, s->d_out, (size_t)T * 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
       hipMemcpyAsync(out_doc_offsets, s->d_out_docs, 8 * ((size_t)n_docs + 1), hipMemcpyDeviceToHost, st) !=
           hipSuccess)

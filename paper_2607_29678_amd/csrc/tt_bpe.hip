@@ -54,15 +54,30 @@ __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
 }  // namespace
 
 // ---------------------------------------------------------------------------
-// Short pieces: one thread per piece, sequence in registers.
+// Short pieces: one thread per piece.
+//
+// A piece of at most 16 bytes lives in 16 token slots.  Pair ranks stay in
+// registers; token IDs and merge results live in LDS as [slot][thread], so the
+// bank of an access depends only on the thread and per-thread slot indices
+// never conflict.  A merge clears the right token's bit in an alive mask
+// instead of shifting the tail; neighbours are found with bit scans.  The
+// per-piece chain is one probe round trip for the initial pairs (issued four
+// at a time) plus one per merge (its two re-probes overlap).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void bpe_small_kernel(Work w, DevTables tb) {
+constexpr int SP_THREADS = 256;
+
+__global__ __launch_bounds__(SP_THREADS) void bpe_small_kernel(Work w, DevTables tb) {
   __shared__ int32_t s_bid[256];
-  s_bid[threadIdx.x] = tb.byte_id[threadIdx.x];
+  __shared__ uint32_t s_ids[SMALL_MAX][SP_THREADS];
+  __shared__ uint32_t s_res[SMALL_MAX][SP_THREADS];
+  const int tid = threadIdx.x;
+  s_bid[tid] = tb.byte_id[tid];
   __syncthreads();
   const uint32_t P = w.ctrl->n_pieces;
   const uint32_t stride = gridDim.x * blockDim.x;
-  for (uint32_t p = blockIdx.x * blockDim.x + threadIdx.x; p < P; p += stride) {
+  const MergeSlot* __restrict__ tab = tb.slots;
+  const uint32_t mask = tb.mask;
+  for (uint32_t p = blockIdx.x * blockDim.x + tid; p < P; p += stride) {
     const uint32_t a = w.piece_off[p];
     const uint32_t L = w.piece_off[p + 1] - a;
     if (L > (uint32_t)SMALL_MAX) {
@@ -70,71 +85,84 @@ __global__ __launch_bounds__(256) void bpe_small_kernel(Work w, DevTables tb) {
       w.long_list[k] = p;
       continue;
     }
-    uint32_t ids[SMALL_MAX], rk[SMALL_MAX], rs[SMALL_MAX];
-#pragma unroll
-    for (int j = 0; j < SMALL_MAX; ++j) ids[j] = (uint32_t)j < L ? (uint32_t)s_bid[w.text[a + j]] : 0u;
+    uint32_t id0[SMALL_MAX];
 #pragma unroll
     for (int j = 0; j < SMALL_MAX; ++j) {
-      uint2 r = make_uint2(RANK_INF, 0u);
-      if ((uint32_t)(j + 1) < L) r = probe_pair(tb.slots, tb.mask, ids[j], ids[j + 1]);
-      rk[j] = r.x;
-      rs[j] = r.y;
+      id0[j] = (uint32_t)j < L ? (uint32_t)s_bid[w.text[a + j]] : 0u;
+      s_ids[j][tid] = id0[j];
     }
-    uint32_t n = L;
+    uint32_t rk[SMALL_MAX];
+#pragma unroll
+    for (int g = 0; g < SMALL_MAX; g += 4) {
+      uint32_t si[4];
+      uint4 sv[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int j = g + k;
+        if (j + 1 < SMALL_MAX && (uint32_t)(j + 1) < L) {
+          si[k] = probe_start(mask, id0[j], id0[j + 1]);
+          sv[k] = load_slot(tab, si[k]);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int j = g + k;
+        uint2 r = make_uint2(RANK_INF, 0u);
+        if (j + 1 < SMALL_MAX && (uint32_t)(j + 1) < L) r = probe_finish(tab, mask, si[k], sv[k], id0[j], id0[j + 1]);
+        rk[j] = r.x;
+        s_res[j][tid] = r.y;
+      }
+    }
+    uint32_t alive = L >= 32 ? 0xFFFFFFFFu : ((1u << L) - 1u);
     for (;;) {
       uint32_t best = RANK_INF;
-      int bi = 0;
+      int k = 0;
 #pragma unroll
       for (int j = 0; j < SMALL_MAX - 1; ++j)
         if (rk[j] < best) {
           best = rk[j];
-          bi = j;
+          k = j;
         }
       if (best == RANK_INF) break;
-      uint32_t nid = 0;
-#pragma unroll
-      for (int j = 0; j < SMALL_MAX; ++j)
-        if (j == bi) nid = rs[j];
-      // token bi becomes nid, token bi+1 leaves: shift the tail left by one
-#pragma unroll
-      for (int j = 0; j < SMALL_MAX - 1; ++j) {
-        if (j > bi) {
-          ids[j] = ids[j + 1];
-          rk[j] = rk[j + 1];
-          rs[j] = rs[j + 1];
-        } else if (j == bi) {
-          ids[j] = nid;
-        }
+      // token k absorbs the next live token m
+      const uint32_t above_k = alive & ~((2u << k) - 1u);
+      const int m = __builtin_ctz(above_k);
+      alive &= ~(1u << m);
+      const uint32_t above_m = alive & ~((2u << m) - 1u);
+      const uint32_t below_k = alive & ((1u << k) - 1u);
+      const uint32_t nid = s_res[k][tid];
+      s_ids[k][tid] = nid;
+      const bool hr = above_m != 0, hl = below_k != 0;
+      const int r_i = hr ? __builtin_ctz(above_m) : 0;
+      const int l_i = hl ? 31 - __builtin_clz(below_k) : 0;
+      const uint32_t right = s_ids[r_i][tid];
+      const uint32_t left = s_ids[l_i][tid];
+      uint32_t il = 0, ir = 0;
+      uint4 sl = make_uint4(EMPTY, 0, 0, 0), sr = make_uint4(EMPTY, 0, 0, 0);
+      if (hr) {
+        ir = probe_start(mask, nid, right);
+        sr = load_slot(tab, ir);
       }
-      rk[SMALL_MAX - 1] = RANK_INF;
-      --n;
-      // the two pairs that touch the new token
-      uint32_t left = 0, right = 0;
+      if (hl) {
+        il = probe_start(mask, left, nid);
+        sl = load_slot(tab, il);
+      }
+      uint2 rr = make_uint2(RANK_INF, 0u), rl = make_uint2(RANK_INF, 0u);
+      if (hr) rr = probe_finish(tab, mask, ir, sr, nid, right);
+      if (hl) rl = probe_finish(tab, mask, il, sl, left, nid);
+      s_res[k][tid] = rr.y;
+      if (hl) s_res[l_i][tid] = rl.y;
 #pragma unroll
       for (int j = 0; j < SMALL_MAX; ++j) {
-        if (j == bi - 1) left = ids[j];
-        if (j == bi + 1) right = ids[j];
-      }
-      uint2 rl = make_uint2(RANK_INF, 0u), rr = make_uint2(RANK_INF, 0u);
-      if (bi > 0) rl = probe_pair(tb.slots, tb.mask, left, nid);
-      if ((uint32_t)(bi + 1) < n) rr = probe_pair(tb.slots, tb.mask, nid, right);
-#pragma unroll
-      for (int j = 0; j < SMALL_MAX; ++j) {
-        if (j == bi - 1) {
-          rk[j] = rl.x;
-          rs[j] = rl.y;
-        }
-        if (j == bi) {
-          rk[j] = rr.x;
-          rs[j] = rr.y;
-        }
+        if (j == m) rk[j] = RANK_INF;
+        if (j == k) rk[j] = rr.x;
+        if (hl && j == l_i) rk[j] = rl.x;
       }
     }
     int32_t* out = w.ids + a;
-#pragma unroll
-    for (int j = 0; j < SMALL_MAX; ++j)
-      if ((uint32_t)j < n) out[j] = (int32_t)ids[j];
-    w.piece_cnt[p] = n;
+    uint32_t c = 0;
+    for (uint32_t al = alive; al; al &= al - 1u) out[c++] = (int32_t)s_ids[__builtin_ctz(al)][tid];
+    w.piece_cnt[p] = c;
   }
 }
 

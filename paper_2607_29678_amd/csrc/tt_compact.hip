@@ -29,6 +29,17 @@ __global__ __launch_bounds__(CT_THREADS) void compact_kernel(Work w) {
   }
   __syncthreads();
   const uint32_t t = s_tile;
+  if (P == 0) {
+    // no character at all (only possible for invalid input): still report
+    if (t == 0 && tid == 0) {
+      w.piece_out[0] = 0;
+      uint32_t err = __hip_atomic_load(&w.ctrl->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      int64_t len = err ? -(int64_t)err : 0;
+      w.ctrl->out_len = len;
+      if (w.out_len) *w.out_len = len;
+    }
+    return;
+  }
   if (t >= n_tiles) return;
   const uint32_t p0 = t * CT_TILE + tid * CT_PPT;
   uint32_t c[CT_PPT];

@@ -68,16 +68,33 @@ __host__ __device__ inline uint32_t pair_hash(uint32_t a, uint32_t b) {
   return h;
 }
 
-// Rank and result of the pair (a, b), or RANK_INF if the pair has no merge.
-__device__ inline uint2 probe_pair(const MergeSlot* __restrict__ tab, uint32_t mask, uint32_t a,
-                                   uint32_t b) {
-  uint32_t i = pair_hash(a, b) & mask;
-  for (;;) {
-    uint4 s = *reinterpret_cast<const uint4*>(tab + i);
-    if (s.x == a && s.y == b) return make_uint2(s.z, s.w);
-    if (s.x == EMPTY) return make_uint2(RANK_INF, 0u);
+// Slot index where the search for the pair (a, b) starts.
+__device__ __forceinline__ uint32_t probe_start(uint32_t mask, uint32_t a, uint32_t b) {
+  return pair_hash(a, b) & mask;
+}
+
+// One 16-byte slot, fetched with a single 128-bit load.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_slot(const MergeSlot* __restrict__ tab, uint32_t i) {
+  u32x4 v = reinterpret_cast<const u32x4*>(tab)[i];
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Finish a probe whose first slot `s` (at index i) is already loaded: rank
+// and result of the pair (a, b), or RANK_INF if the pair has no merge.
+__device__ __forceinline__ uint2 probe_finish(const MergeSlot* __restrict__ tab, uint32_t mask, uint32_t i,
+                                              uint4 s, uint32_t a, uint32_t b) {
+  while (!((s.x == a) & (s.y == b)) && s.x != EMPTY) {
     i = (i + 1) & mask;
+    s = load_slot(tab, i);
   }
+  return (s.x == a) & (s.y == b) ? make_uint2(s.z, s.w) : make_uint2(RANK_INF, 0u);
+}
+
+__device__ __forceinline__ uint2 probe_pair(const MergeSlot* __restrict__ tab, uint32_t mask, uint32_t a,
+                                           uint32_t b) {
+  uint32_t i = probe_start(mask, a, b);
+  return probe_finish(tab, mask, i, load_slot(tab, i), a, b);
 }
 
 // Everything a kernel needs to know about a tokenizer handle.
