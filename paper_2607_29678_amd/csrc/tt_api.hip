@@ -51,6 +51,8 @@ struct tt_tokenizer {
   MergeSlot* d_slots = nullptr;
   uint32_t mask = 0;
   int32_t* d_byte_id = nullptr;
+  uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
+                               // byte x to a token starting with byte y
   std::mutex mu;
   std::unordered_map<hipStream_t, Workspace*> ws;
 };
@@ -189,7 +191,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   };
   if (!mark()) return TT_ERR_HIP;
   if (launch_reset(w, npt, nct, st) != hipSuccess || !mark()) return TT_ERR_HIP;
-  if (launch_pretok(w, h->pattern, npt, st) != hipSuccess || !mark()) return TT_ERR_HIP;
+  if (launch_pretok(w, h->pattern, npt, h->d_join, !pretok_only, st) != hipSuccess || !mark()) return TT_ERR_HIP;
   if (pretok_only) return TT_OK;
   if (launch_bpe_small(w, tb, st) != hipSuccess || !mark()) return TT_ERR_HIP;
   if (launch_bpe_wave(w, tb, st) != hipSuccess || !mark()) return TT_ERR_HIP;
@@ -270,6 +272,18 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
     slots[i] = MergeSlot{a, b, (uint32_t)r, (uint32_t)merges[r].result};
   }
 
+  // junction byte pairs: the first merge that ever joins across a byte
+  // boundary has its junction exactly there, so a boundary whose byte pair is
+  // no merge's junction is never crossed
+  std::vector<uint32_t> join(2048, 0u);
+  for (int32_t r = 0; r < n_merges; ++r) {
+    if (vlen(merges[r].left) == 0 || vlen(merges[r].right) == 0) continue;
+    uint32_t x = vptr(merges[r].left)[vlen(merges[r].left) - 1];
+    uint32_t y = vptr(merges[r].right)[0];
+    uint32_t key = (x << 8) | y;
+    join[key >> 5] |= 1u << (key & 31u);
+  }
+
   tt_tokenizer* h = new tt_tokenizer();
   h->pattern = pattern_id;
   h->n_merges = n_merges;
@@ -280,12 +294,14 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
     return TT_ERR_HIP;
   }
   if (hipMalloc(reinterpret_cast<void**>(&h->d_slots), sizeof(MergeSlot) * cap) != hipSuccess ||
-      hipMalloc(reinterpret_cast<void**>(&h->d_byte_id), sizeof(int32_t) * 256) != hipSuccess) {
+      hipMalloc(reinterpret_cast<void**>(&h->d_byte_id), sizeof(int32_t) * 256) != hipSuccess ||
+      hipMalloc(reinterpret_cast<void**>(&h->d_join), sizeof(uint32_t) * 2048) != hipSuccess) {
     tt_destroy(h);
     return TT_ERR_OOM;
   }
   if (hipMemcpy(h->d_slots, slots.data(), sizeof(MergeSlot) * cap, hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemcpy(h->d_byte_id, byte_id.data(), sizeof(int32_t) * 256, hipMemcpyHostToDevice) != hipSuccess) {
+      hipMemcpy(h->d_byte_id, byte_id.data(), sizeof(int32_t) * 256, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(h->d_join, join.data(), sizeof(uint32_t) * 2048, hipMemcpyHostToDevice) != hipSuccess) {
     tt_destroy(h);
     return TT_ERR_HIP;
   }
@@ -300,6 +316,7 @@ void tt_destroy(tt_tokenizer* h) {
   for (auto& kv : h->ws) free_ws(kv.second);
   if (h->d_slots) (void)hipFree(h->d_slots);
   if (h->d_byte_id) (void)hipFree(h->d_byte_id);
+  if (h->d_join) (void)hipFree(h->d_join);
   delete h;
 }
 

@@ -111,9 +111,11 @@ struct Work {
   const int64_t* doc_off;   // batch: n_docs+1 byte offsets, else nullptr
   int32_t n_docs;
   Ctrl* ctrl;
-  uint32_t* piece_off;      // [P+1] byte offset of each piece start, then n
-  uint32_t* piece_cnt;      // [P] tokens per piece
-  uint32_t* piece_out;      // [P+1] output offset of each piece
+  // "pieces" below are the units of the call: pre-tokenization pieces for the
+  // split-level export, BPE segments of pieces for encoding
+  uint32_t* piece_off;      // [P+1] byte offset of each unit start, then n
+  uint32_t* piece_cnt;      // [P] tokens per unit
+  uint32_t* piece_out;      // [P+1] output offset of each unit
   int32_t* ids;             // [n] per-piece IDs stored at the piece's byte offset
   uint32_t* long_list;      // [P] pieces for the wave engine
   uint32_t* big_list;       // [P] pieces for the block engine
@@ -144,7 +146,8 @@ inline uint32_t ct_tiles_cap(uint32_t n) { return (n + CT_TILE - 1) / CT_TILE + 
 
 // Launchers (defined in the .hip files) -------------------------------------
 hipError_t launch_reset(const Work& w, uint32_t n_pt_tiles, uint32_t n_ct_tiles, hipStream_t s);
-hipError_t launch_pretok(const Work& w, int pattern, uint32_t n_pt_tiles, hipStream_t s);
+hipError_t launch_pretok(const Work& w, int pattern, uint32_t n_pt_tiles, const uint32_t* join_bits, bool seg,
+                         hipStream_t s);
 hipError_t launch_bpe_small(const Work& w, const DevTables& t, hipStream_t s);
 hipError_t launch_bpe_wave(const Work& w, const DevTables& t, hipStream_t s);
 hipError_t launch_bpe_block(const Work& w, const DevTables& t, hipStream_t s);

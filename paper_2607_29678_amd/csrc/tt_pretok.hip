@@ -170,8 +170,13 @@ struct PtShared {
 
 }  // namespace
 
-template <int PAT, bool BATCH>
-__global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_tiles) {
+// SEG = false: units are the pieces (split-level export).
+// SEG = true:  units are the BPE segments of the pieces: a piece is also cut
+//              at every byte position q whose byte pair (b[q-1], b[q]) is the
+//              junction of no merge; no merge can ever join across such a
+//              position, so each segment is an independent BPE problem.
+template <int PAT, bool BATCH, bool SEG>
+__global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_tiles, const uint32_t* join_bits) {
   __shared__ PtShared sh;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -559,6 +564,18 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
     }
     if (start) flags |= 1u << j;
   }
+  if (SEG) {
+    // BPE segments: add the byte positions inside pieces that no merge spans
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) {
+      const int q = qb + j;
+      if (q < PT_HALO || q >= PT_HALO + PT_OWN || !inside(q) || (flags & (1u << j))) continue;
+      if (sh.dstart[q] || !inside(q - 1)) continue;  // piece starts are already flagged
+      // q is not a piece start, so q - 1 lies in the same piece
+      const uint32_t key = ((uint32_t)sh.buf[q - 1] << 8) | sh.buf[q];
+      if (!((join_bits[key >> 5] >> (key & 31u)) & 1u)) flags |= 1u << j;
+    }
+  }
 
   // ---- number the pieces: block scan + decoupled look-back ------------------
   const uint32_t cnt = __popc(flags);
@@ -615,15 +632,23 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
   }
 }
 
-hipError_t launch_pretok(const Work& w, int pattern, uint32_t n_tiles, hipStream_t s) {
+hipError_t launch_pretok(const Work& w, int pattern, uint32_t n_tiles, const uint32_t* join_bits, bool seg,
+                         hipStream_t s) {
   dim3 grid(n_tiles), block(PT_THREADS);
-  bool batch = w.doc_off != nullptr;
-  if (pattern == TT_PATTERN_GPT2) {
-    if (batch) hipLaunchKernelGGL((pretok_kernel<TT_PATTERN_GPT2, true>), grid, block, 0, s, w, n_tiles);
-    else hipLaunchKernelGGL((pretok_kernel<TT_PATTERN_GPT2, false>), grid, block, 0, s, w, n_tiles);
-  } else {
-    if (batch) hipLaunchKernelGGL((pretok_kernel<TT_PATTERN_CL100K, true>), grid, block, 0, s, w, n_tiles);
-    else hipLaunchKernelGGL((pretok_kernel<TT_PATTERN_CL100K, false>), grid, block, 0, s, w, n_tiles);
+  const bool batch = w.doc_off != nullptr;
+  const int variant = (pattern == TT_PATTERN_GPT2 ? 0 : 4) + (batch ? 2 : 0) + (seg ? 1 : 0);
+  switch (variant) {
+#define TT_PRETOK_CASE(V, P, B, S) \
+  case V: hipLaunchKernelGGL((pretok_kernel<P, B, S>), grid, block, 0, s, w, n_tiles, join_bits); break;
+    TT_PRETOK_CASE(0, TT_PATTERN_GPT2, false, false)
+    TT_PRETOK_CASE(1, TT_PATTERN_GPT2, false, true)
+    TT_PRETOK_CASE(2, TT_PATTERN_GPT2, true, false)
+    TT_PRETOK_CASE(3, TT_PATTERN_GPT2, true, true)
+    TT_PRETOK_CASE(4, TT_PATTERN_CL100K, false, false)
+    TT_PRETOK_CASE(5, TT_PATTERN_CL100K, false, true)
+    TT_PRETOK_CASE(6, TT_PATTERN_CL100K, true, false)
+    TT_PRETOK_CASE(7, TT_PATTERN_CL100K, true, true)
+#undef TT_PRETOK_CASE
   }
   return hipGetLastError();
 }

@@ -188,3 +188,55 @@ def test_against_hf_bpe(k):
         p = bytes(rng.choice(alphabet) for _ in range(rng.randint(1, 40)))
         hf = [tok.id for tok in model.tokenize("".join(b2u[x] for x in p))]
         assert hf == bpe(p, t), p
+
+
+def _junctions(t):
+    return {(t.vocab[a][-1], t.vocab[b][0]) for a, b, _ in t.merges}
+
+
+def _segments(piece, junctions):
+    out, prev = [], 0
+    for i in range(1, len(piece)):
+        if (piece[i - 1], piece[i]) not in junctions:
+            out.append(piece[prev:i])
+            prev = i
+    out.append(piece[prev:])
+    return out
+
+
+@pytest.mark.parametrize("k", [1, 3, 4])
+def test_junction_barrier_segments_encode_independently(k):
+    """A byte boundary whose byte pair is the junction of no merge is never crossed by any merge,
+    so BPE of the piece equals BPE of the segments between such boundaries, concatenated (the
+    library cuts pieces there before BPE)."""
+    from conftest import config_bytes, pattern_of
+    from oracle.pretok import pretokenize
+
+    t = oracle_table(k)
+    jn = _junctions(t)
+    text = config_bytes(k).decode("utf-8")
+    spans = pretokenize(text, pattern_of(k))
+    rng = random.Random(k)
+    for a, b in rng.sample(spans, min(5000, len(spans))):
+        p = text[a:b].encode("utf-8")
+        assert sum((bpe(s, t) for s in _segments(p, jn)), []) == bpe(p, t)
+
+
+def test_junction_barriers_on_random_tables():
+    rng = random.Random(5)
+    for trial in range(30):
+        alphabet = b"abcd"
+        vocab = [bytes([i]) for i in range(256)]
+        merges = []
+        for r in range(rng.randint(1, 12)):
+            a = rng.choice(list(alphabet) + list(range(256, len(vocab))))
+            b = rng.choice(list(alphabet) + list(range(256, len(vocab))))
+            if any(m[0] == a and m[1] == b for m in merges):
+                continue
+            merges.append((a, b, len(vocab)))
+            vocab.append(vocab[a] + vocab[b])
+        t = MergeTable(merges, vocab)
+        jn = _junctions(t)
+        for _ in range(300):
+            p = bytes(rng.choice(alphabet) for _ in range(rng.randint(1, 30)))
+            assert sum((bpe(s, t) for s in _segments(p, jn)), []) == bpe(p, t), (merges, p)
