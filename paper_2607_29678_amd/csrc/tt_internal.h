@@ -129,8 +129,8 @@ struct Work {
 };
 
 // Tiles and geometry --------------------------------------------------------
-constexpr int PT_THREADS = 256;                   // pre-tokenization block
-constexpr int PT_BPT = 8;                          // bytes per thread
+constexpr int PT_THREADS = 1024;                  // pre-tokenization block
+constexpr int PT_BPT = 2;                          // bytes per thread
 constexpr int PT_WIN = PT_THREADS * PT_BPT;        // window bytes in LDS
 constexpr int PT_HALO = 32;                        // context bytes each side
 constexpr int PT_OWN = PT_WIN - 2 * PT_HALO;       // bytes a tile decides

@@ -154,10 +154,13 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane, F comb)
   return v;
 }
 
+constexpr int PT_PAD = 8;  // LDS arrays also hold window positions [-8, 0) and [PT_WIN, PT_WIN + 16)
+
 struct PtShared {
-  uint8_t buf[PT_WIN + 8];    // window bytes
-  uint8_t code[PT_WIN + 8];   // per-byte class/identity/doc-start codes
-  uint8_t dstart[PT_WIN + 8]; // 1 where a document starts
+  uint8_t buf[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));     // window bytes
+  uint8_t code[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));    // class/identity/doc-start codes
+  uint8_t dstart[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));  // 1 where a document starts
+  uint32_t join[2048];        // segments: junction byte pairs of the merges
   int16_t run_end[PT_WIN];    // cl100k: window index of the head after a run's head
   uint32_t wave_tot[PT_THREADS / 64];
   uint32_t tile;
@@ -195,20 +198,53 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
     return p >= 0 && p < n;
   };
 
-  // ---- stage the window ----------------------------------------------------
-  for (int q = tid; q < PT_WIN + 8; q += PT_THREADS) {
-    int64_t p = w0 + q;
-    bool in = p >= 0 && p < n;
-    sh.buf[q] = in ? w.text[p] : 0;
-    sh.dstart[q] = (in && p == 0) ? 1 : 0;
+  // ---- stage the window: 8 bytes per thread, one 64-bit load when possible --
+  // LDS index of window position q is q + PT_PAD, for q in [-PT_PAD, PT_WIN + 16)
+  auto stage_chunk = [&](int c) {  // window bytes [8c, 8c + 8)
+    const int q0 = 8 * c;
+    const int64_t p0 = w0 + q0;
+    uint2 v = make_uint2(0u, 0u);
+    if (p0 >= 0 && p0 + 8 <= n && ((reinterpret_cast<uintptr_t>(w.text + p0) & 7u) == 0)) {
+      v = *reinterpret_cast<const uint2*>(w.text + p0);
+    } else {
+      uint32_t lo = 0, hi = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        int64_t p = p0 + k;
+        uint32_t b = (p >= 0 && p < n) ? w.text[p] : 0u;
+        if (k < 4) lo |= b << (8 * k);
+        else hi |= b << (8 * (k - 4));
+      }
+      v = make_uint2(lo, hi);
+    }
+    *reinterpret_cast<uint2*>(&sh.buf[PT_PAD + q0]) = v;
+    uint2 d = make_uint2(0u, 0u);
+    if (p0 <= 0 && p0 + 8 > 0) d.x = (p0 == 0) ? 1u : 0u;  // the text start is a document start
+    if (p0 < 0 && p0 + 8 > 0) {
+      int k = (int)(-p0);
+      if (k < 4) d.x = 1u << (8 * k);
+      else d.y = 1u << (8 * (k - 4));
+    }
+    *reinterpret_cast<uint2*>(&sh.dstart[PT_PAD + q0]) = d;
+  };
+  {
+    constexpr int NCH = PT_WIN / 8;  // chunks of the window proper
+    if (tid < NCH) stage_chunk(tid);
+    else if (tid < NCH + 3) stage_chunk(tid == NCH ? -1 : tid - 1);  // [-8, 0) and [PT_WIN, PT_WIN + 16)
+  }
+  if (SEG) {
+    // the junction bitmap (8 KB) is read once per block
+    const uint4* src = reinterpret_cast<const uint4*>(join_bits);
+    uint4* dst = reinterpret_cast<uint4*>(sh.join);
+    for (int i = tid; i < 512; i += PT_THREADS) dst[i] = src[i];
   }
   if (BATCH) {
     if (tid == 0) {
-      // first document start >= w0
+      // first document start >= w0 - PT_PAD
       int lo = 0, hi = w.n_docs;  // search in doc_off[0..n_docs)
       while (lo < hi) {
         int mid = (lo + hi) >> 1;
-        if (w.doc_off[mid] < w0) lo = mid + 1;
+        if (w.doc_off[mid] < w0 - PT_PAD) lo = mid + 1;
         else hi = mid;
       }
       sh.doc_lo_idx = lo;
@@ -218,56 +254,66 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
   if (BATCH) {
     for (int64_t j = sh.doc_lo_idx + tid; j < w.n_docs; j += PT_THREADS) {
       int64_t d = w.doc_off[j];
-      if (d >= w0 + PT_WIN + 8) break;
+      if (d >= w0 + PT_WIN + 16) break;
       if (d >= n) continue;
-      sh.dstart[d - w0] = 1;  // several empty documents may start here; all store the same value
+      sh.dstart[PT_PAD + (d - w0)] = 1;  // several empty documents may start here; all store the same value
     }
     __syncthreads();
   }
 
-  // ---- decode, validate, classify ------------------------------------------
+  // ---- decode, validate, classify: 8 positions per thread ----------------
+  // (rolled loops keep the kernel small enough for the instruction cache)
   bool bad = false;
-  for (int q = tid; q < PT_WIN + 8; q += PT_THREADS) {
-    uint32_t ds = sh.dstart[q] ? CODE_DOCSTART : 0u;
-    uint32_t code = C_NONE;
-    bool own = q >= PT_HALO && q < PT_HALO + PT_OWN && inside(q);
-    if (inside(q)) {
-      uint32_t b = sh.buf[q];
-      if ((b & 0xC0u) == 0x80u) {
-        if (own) {
-          // a continuation byte must lie inside the sequence of a lead byte at
-          // most three bytes earlier, with no document start in between
-          bool claimed = false;
-          if (!ds) {
-            for (int k = 1; k <= 3; ++k) {
-              int r = q - k;
-              if (!inside(r)) break;
-              uint32_t br = sh.buf[r];
-              if ((br & 0xC0u) == 0x80u) {
-                if (sh.dstart[r]) break;
-                continue;
+  {
+    const int qb0 = tid * PT_BPT;
+    auto B = [&](int q) -> uint32_t { return sh.buf[PT_PAD + q]; };
+    auto D = [&](int q) -> bool { return sh.dstart[PT_PAD + q] != 0; };
+#pragma unroll 1
+    for (int j = 0; j < PT_BPT; ++j) {
+      const int q = qb0 + j;
+      const uint32_t ds = D(q) ? CODE_DOCSTART : 0u;
+      uint32_t code = C_NONE;
+      const bool own = q >= PT_HALO && q < PT_HALO + PT_OWN && inside(q);
+      if (inside(q)) {
+        const uint32_t b = B(q);
+        if ((b & 0xC0u) == 0x80u) {
+          if (own) {
+            // a continuation byte must lie inside the sequence of a lead byte at
+            // most three bytes earlier, with no document start in between
+            bool claimed = false;
+            if (!ds) {
+              for (int k = 1; k <= 3; ++k) {
+                if (!inside(q - k)) break;
+                const uint32_t br = B(q - k);
+                if ((br & 0xC0u) == 0x80u) {
+                  if (D(q - k)) break;
+                  continue;
+                }
+                claimed = lead_len(br) > k;
+                break;
               }
-              claimed = lead_len(br) > k;
-              break;
             }
+            bad |= !claimed;
           }
-          bad |= !claimed;
-        }
-      } else {
-        int avail = 1;
-        while (avail < 4 && q + avail < PT_WIN + 8 && inside(q + avail) && !sh.dstart[q + avail])
-          ++avail;
-        uint32_t cp = 0;
-        int len = decode(&sh.buf[q], avail, cp);
-        if (len == 0) {
-          bad |= own;
-          code = C_O;
         } else {
-          code = char_code<PAT>(cp);
+          int avail = 1;
+          while (avail < 4 && inside(q + avail) && !D(q + avail)) ++avail;
+          uint32_t cp = 0;
+          const int len = decode(&sh.buf[PT_PAD + q], avail, cp);
+          if (len == 0) {
+            bad |= own;
+            code = C_O;
+          } else {
+            code = char_code<PAT>(cp);
+          }
         }
       }
+      sh.code[PT_PAD + q] = (uint8_t)(code | ds);
     }
-    sh.code[q] = (uint8_t)(code | ds);
+    if (tid < 3) {  // positions outside [0, PT_WIN) carry no character for the rules
+      const int q0 = tid == 0 ? -8 : PT_WIN + 8 * (tid - 1);
+      *reinterpret_cast<uint2*>(&sh.code[PT_PAD + q0]) = make_uint2(0x07070707u, 0x07070707u);
+    }
   }
   if (bad) __hip_atomic_store(&w.ctrl->error, (uint32_t)(-TT_ERR_INVALID_UTF8), __ATOMIC_RELAXED,
                               __HIP_MEMORY_SCOPE_AGENT);
@@ -275,26 +321,27 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
   __syncthreads();
 
   // ---- neighbour helpers (window indices; -1 = none) ----------------------
-  auto cls = [&](int q) -> uint32_t { return code_cls(sh.code[q]); };
-  auto ident = [&](int q) -> uint32_t { return code_id(sh.code[q]); };
+  auto code_at = [&](int q) -> uint32_t { return sh.code[PT_PAD + q]; };
+  auto cls = [&](int q) -> uint32_t { return code_cls(code_at(q)); };
+  auto ident = [&](int q) -> uint32_t { return code_id(code_at(q)); };
   auto prev = [&](int q) -> int {
-    if (sh.code[q] & CODE_DOCSTART) return -1;
+    if (code_at(q) & CODE_DOCSTART) return -1;
     for (int r = q - 1; r >= 0; --r) {
       if (!inside(r)) return -1;
-      if (code_cls(sh.code[r]) != C_NONE) return r;
+      if (code_cls(code_at(r)) != C_NONE) return r;
     }
     return -1;
   };
   auto next = [&](int q) -> int {
     for (int r = q + 1; r < PT_WIN + 8; ++r) {
       if (!inside(r)) return -1;
-      uint8_t c = sh.code[r];
+      const uint32_t c = code_at(r);
       if (c & CODE_DOCSTART) return -1;
       if (code_cls(c) != C_NONE) return r;
     }
     return -1;
   };
-  auto is_char = [&](int q) -> bool { return inside(q) && code_cls(sh.code[q]) != C_NONE; };
+  auto is_char = [&](int q) -> bool { return inside(q) && code_cls(code_at(q)) != C_NONE; };
   auto is_w = [](uint32_t c) -> bool { return c == C_WS || c == C_NL; };
 
   // Suffix of a contraction starting at letter q: 1 or 2 letters, or 0.
@@ -328,24 +375,20 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
   };
 
   // ---- cl100k: run scan, run ends, summaries, carries ----------------------
-  uint32_t excl[PT_BPT];
   const int qb = tid * PT_BPT;
+  // scan element of window position q: a run head restarts the char count
+  auto elem_at = [&](int q) -> uint32_t {
+    if (q < PT_HALO || !is_char(q)) return 0u;
+    const int p = prev(q);
+    const bool head = p < 0 || cls(p) != cls(q);
+    return head ? (0x80000000u | ((uint32_t)q << 16) | 1u) : 1u;
+  };
+  uint32_t s0 = 0;  // scan state before the thread's first position
   if (PAT == TT_PATTERN_CL100K) {
     // elements over window indices [HALO, WIN)
-    uint32_t elem[PT_BPT];
     uint32_t agg = 0;
-#pragma unroll
-    for (int j = 0; j < PT_BPT; ++j) {
-      int q = qb + j;
-      uint32_t e = 0;
-      if (q >= PT_HALO && is_char(q)) {
-        int p = prev(q);
-        bool head = p < 0 || cls(p) != cls(q);
-        e = head ? (0x80000000u | ((uint32_t)q << 16) | 1u) : 1u;
-      }
-      elem[j] = e;
-      agg = seg_combine(agg, e);
-    }
+#pragma unroll 1
+    for (int j = 0; j < PT_BPT; ++j) agg = seg_combine(agg, elem_at(qb + j));
     uint32_t inc = wave_incl_scan(agg, lane, seg_combine);
     if (lane == 63) sh.wave_tot[wave] = inc;
     uint32_t lex = __shfl_up(inc, 1, 64);
@@ -353,24 +396,27 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
     __syncthreads();
     uint32_t wpre = 0;
     for (int v = 0; v < wave; ++v) wpre = seg_combine(wpre, sh.wave_tot[v]);
-    uint32_t s = seg_combine(wpre, lex);
-#pragma unroll
-    for (int j = 0; j < PT_BPT; ++j) {
-      excl[j] = s;
-      uint32_t e = elem[j];
-      if ((e & 0x80000000u) && seg_has(s)) sh.run_end[seg_head(s)] = (int16_t)(qb + j);
-      s = seg_combine(s, e);
-    }
-    // summary of the tile's trailing run (own range), published before waiting
-    // on any other block
+    s0 = seg_combine(wpre, lex);
+    // each run head records itself as the end of the previous run
     const int own_end = (int)(n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN);
     int last_q = -1;
-#pragma unroll
-    for (int j = 0; j < PT_BPT; ++j) {
-      int q = qb + j;
-      if (q >= PT_HALO && q < own_end && is_char(q)) last_q = q;
+    uint32_t last_st = 0;
+    {
+      uint32_t st = s0;
+#pragma unroll 1
+      for (int j = 0; j < PT_BPT; ++j) {
+        const int q = qb + j;
+        const uint32_t e = elem_at(q);
+        if ((e & 0x80000000u) && seg_has(st)) sh.run_end[seg_head(st)] = (int16_t)q;
+        st = seg_combine(st, e);
+        if (q >= PT_HALO && q < own_end && e != 0u) {
+          last_q = q;
+          last_st = st;
+        }
+      }
     }
-    // the thread holding the last own character publishes
+    // summary of the tile's trailing run (own range), published before waiting
+    // on any other block; the thread holding the last own character publishes
     if (tid == 0) sh.last_own = -1;
     __syncthreads();
     if (last_q >= 0) atomicMax(&sh.last_own, last_q);
@@ -378,15 +424,10 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
     const int s_last = sh.last_own;
     if (s_last < 0) {
       if (tid == 0) st_release(&w.tile_summary[t], SUM_READY | SUM_RUNALL);
-    } else if (s_last >= qb && s_last < qb + PT_BPT) {
-      int j = s_last - qb;
-      uint32_t st = 0;
-#pragma unroll
-      for (int k = 0; k < PT_BPT; ++k)
-        if (k == j) st = seg_combine(excl[k], elem[k]);
-      uint32_t sum = SUM_READY | ((seg_cnt(st) % 3u) << 1);
-      if (seg_has(st)) {
-        int hp = prev(seg_head(st));
+    } else if (s_last == last_q) {
+      uint32_t sum = SUM_READY | ((seg_cnt(last_st) % 3u) << 1);
+      if (seg_has(last_st)) {
+        int hp = prev(seg_head(last_st));
         sum |= (hp >= 0 ? cls(hp) : (uint32_t)C_NONE) << 3;
       } else {
         sum |= SUM_RUNALL;
@@ -449,7 +490,7 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
   // the last stretch of its whitespace run?
   auto ws_stretch_is_last = [&](int q) -> bool {
     int e = sh.run_end[q];
-    if (e >= 0) return (sh.code[e] & CODE_DOCSTART) || cls(e) != C_NL;
+    if (e >= 0) return (code_at(e) & CODE_DOCSTART) || cls(e) != C_NL;
     if (w0 + PT_WIN >= n) return true;  // the run reaches the end of the text
     // the stretch continues past the window: read on in global memory
     int64_t pos = w0 + PT_WIN;
@@ -484,9 +525,12 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
 
   // ---- piece-start predicate ----------------------------------------------
   uint32_t flags = 0;
-#pragma unroll
+  uint32_t scan_st = s0;  // cl100k: scan state before position q
+#pragma unroll 1
   for (int j = 0; j < PT_BPT; ++j) {
     const int q = qb + j;
+    const uint32_t ex = scan_st;
+    if (PAT == TT_PATTERN_CL100K) scan_st = seg_combine(scan_st, elem_at(q));
     if (q < PT_HALO || q >= PT_HALO + PT_OWN || !is_char(q)) continue;
     const uint32_t c0 = cls(q);
     const int p1 = prev(q);
@@ -513,10 +557,6 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
           start = true;
         }
       } else {
-        uint32_t ex = 0;
-#pragma unroll
-        for (int k = 0; k < PT_BPT; ++k)
-          if (k == j) ex = excl[k];
         if (is_w(c0)) {
           if (!is_w(c1)) {
             // head of a whitespace run; after "other", leading CR/LF joins the symbol piece
@@ -566,14 +606,14 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
   }
   if (SEG) {
     // BPE segments: add the byte positions inside pieces that no merge spans
-#pragma unroll
+#pragma unroll 1
     for (int j = 0; j < PT_BPT; ++j) {
       const int q = qb + j;
       if (q < PT_HALO || q >= PT_HALO + PT_OWN || !inside(q) || (flags & (1u << j))) continue;
-      if (sh.dstart[q] || !inside(q - 1)) continue;  // piece starts are already flagged
+      if (sh.dstart[PT_PAD + q] || !inside(q - 1)) continue;  // piece starts are already flagged
       // q is not a piece start, so q - 1 lies in the same piece
-      const uint32_t key = ((uint32_t)sh.buf[q - 1] << 8) | sh.buf[q];
-      if (!((join_bits[key >> 5] >> (key & 31u)) & 1u)) flags |= 1u << j;
+      const uint32_t key = ((uint32_t)sh.buf[PT_PAD + q - 1] << 8) | sh.buf[PT_PAD + q];
+      if (!((sh.join[key >> 5] >> (key & 31u)) & 1u)) flags |= 1u << j;
     }
   }
 
@@ -618,7 +658,7 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
   __syncthreads();
   const uint32_t base = sh.prefix + texcl;
   uint32_t k = 0;
-#pragma unroll
+#pragma unroll 1
   for (int j = 0; j < PT_BPT; ++j) {
     if (flags & (1u << j)) {
       w.piece_off[base + k] = (uint32_t)(w0 + qb + j);
