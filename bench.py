@@ -40,12 +40,10 @@ def percentile(xs, q):
 
 def stage_bytes(stage, B, P, T):
     """Algorithmic HBM bytes of one stage (what the method must move)."""
-    if stage == "pretokenize":   # read the text, write piece offsets
-        return B + 4 * (P + 1)
-    if stage == "bpe_short":     # read text + offsets, write IDs + counts
-        return B + 4 * (P + 1) + 4 * T + 4 * P
-    if stage == "compact":       # read counts + per-piece IDs, write dense IDs
-        return 4 * P + 4 * T + 4 * T
+    if stage == "tile":   # read the text, write the tile-compacted IDs
+        return B + 4 * T
+    if stage == "emit":   # read the staged IDs, write the dense output
+        return 4 * T + 4 * T
     return None
 
 

@@ -45,7 +45,7 @@ SIGNATURES = {
     "tt_stage_times": (ctypes.c_int, [_P, _P, _P, _I32, ctypes.POINTER(_I32)]),
 }
 
-STAGES = ["reset", "pretokenize", "bpe_short", "bpe_wave", "bpe_block", "compact"]
+STAGES = ["tile", "emit"]
 
 _lib = None
 

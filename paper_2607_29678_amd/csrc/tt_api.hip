@@ -4,7 +4,7 @@
 // Chain of one request (all on the caller's stream, no host round trip
 // between kernels; Sec. 4.3 keeps piece counts, dispatch lists and the output
 // length on the device and sizes launches from buffer capacity):
-//   reset -> pre-tokenize -> BPE (thread / wave / block engines) -> compact
+//   tile (pre-tokenize + BPE + tile compaction) -> emit [-> document offsets]
 // The host synchronises twice per blocking call: once for the output length,
 // once for the IDs.
 #include <algorithm>
@@ -22,20 +22,22 @@ using namespace tt;
 namespace {
 
 // Stages of one call, in launch order (profiling names them in this order).
-enum { ST_RESET, ST_PRETOK, ST_BPE_SMALL, ST_BPE_WAVE, ST_BPE_BLOCK, ST_COMPACT, N_STAGES };
+enum { ST_TILE, ST_EMIT, N_STAGES };
 
 struct Workspace {
   uint64_t cap = 0;           // bytes of request this workspace holds
   int64_t doc_cap = 0;        // documents the batch buffers hold
   void* dmem = nullptr;       // one device allocation for everything below
   Work w{};                   // device pointers (text/out set per call)
+  uint32_t epoch = 0;         // epoch of the latest call
+  uint32_t ticket_base = 0;   // first tile ticket of the next call
+  size_t ctl_bytes = 0;       // control block and tile words, cleared when allocated
   uint8_t* d_in = nullptr;    // staged request bytes (host calls)
   int32_t* d_out = nullptr;   // IDs (host calls)
   int64_t* d_len = nullptr;   // output length (host calls)
   int64_t* d_docs = nullptr;  // batch: document byte offsets
   int64_t* d_out_docs = nullptr;
   int64_t* h_len = nullptr;   // pinned readback word
-  uint32_t* h_ctrl = nullptr; // pinned readback of the control block
   hipEvent_t ev[N_STAGES + 1] = {};  // stage boundaries of the last call (profiling)
   int n_ev = 0;                      // events recorded by the last call
 };
@@ -48,9 +50,10 @@ struct tt_tokenizer {
   int32_t vocab_size = 0;
   int device = 0;
   int profile = 0;  // record stage events on every call
-  MergeSlot* d_slots = nullptr;
+  uint64_t* d_slots = nullptr;
   uint32_t mask = 0;
-  int32_t* d_byte_id = nullptr;
+  int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
+  uint32_t n_ids = 0;
   uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
                                // byte x to a token starting with byte y
   std::mutex mu;
@@ -66,7 +69,6 @@ void free_ws(Workspace* s) {
   if (s->dmem) (void)hipFree(s->dmem);
   if (s->d_docs) (void)hipFree(s->d_docs);
   if (s->h_len) (void)hipHostFree(s->h_len);
-  if (s->h_ctrl) (void)hipHostFree(s->h_ctrl);
   for (auto& e : s->ev)
     if (e) (void)hipEventDestroy(e);
   delete s;
@@ -85,44 +87,51 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
     s->cap = 0;
   }
   const uint64_t N = cap;
-  const uint64_t npt = pt_tiles((uint32_t)N) + 1, nct = ct_tiles_cap((uint32_t)N) + 1;
+  const uint64_t NT = n_tiles_for((uint32_t)N) + 1;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
     off = align_up(off + bytes, 256);
     return o;
   };
+  // words that carry epochs or the ticket come first: they are cleared once here
   size_t o_ctrl = take(sizeof(Ctrl));
-  size_t o_poff = take(4 * (N + 2));
-  size_t o_pcnt = take(4 * (N + 1));
-  size_t o_pout = take(4 * (N + 2));
-  size_t o_ids = take(4 * N);
-  size_t o_long = take(4 * (N + 1));
-  size_t o_big = take(4 * (N + 1));
-  size_t o_tst = take(8 * npt);
-  size_t o_tsum = take(4 * npt);
-  size_t o_cst = take(8 * nct);
-  size_t o_scr = take(4 * 6 * N + 8 * (N / 32 + 8));
+  size_t o_tsum = take(8 * NT);
+  size_t o_tlast = take(8 * NT);
+  const size_t ctl_bytes = off;
+  size_t o_tcnt = take(4 * NT);
+  size_t o_tbase = take(4 * NT);
+  size_t o_tpre = take(4 * NT);
+  size_t o_stage = take(4 * N);
+  size_t o_utile = take(4 * N);
+  size_t o_upos = take(4 * N);
+  size_t o_scr = take(4 * 4 * N + 8 * (N / 32 + 8));
   size_t o_in = take(N + 64);
   size_t o_out = take(4 * N);
   size_t o_len = take(8);
   void* mem = nullptr;
   if (hipMalloc(&mem, off) != hipSuccess) return TT_ERR_OOM;
+  if (hipMemsetAsync(mem, 0, ctl_bytes, st) != hipSuccess) {
+    (void)hipFree(mem);
+    return TT_ERR_HIP;
+  }
   uint8_t* b = static_cast<uint8_t*>(mem);
   s->dmem = mem;
   s->cap = cap;
+  s->ctl_bytes = ctl_bytes;
+  s->epoch = 0;
+  s->ticket_base = 0;
   Work& w = s->w;
   w.ctrl = reinterpret_cast<Ctrl*>(b + o_ctrl);
-  w.piece_off = reinterpret_cast<uint32_t*>(b + o_poff);
-  w.piece_cnt = reinterpret_cast<uint32_t*>(b + o_pcnt);
-  w.piece_out = reinterpret_cast<uint32_t*>(b + o_pout);
-  w.ids = reinterpret_cast<int32_t*>(b + o_ids);
-  w.long_list = reinterpret_cast<uint32_t*>(b + o_long);
-  w.big_list = reinterpret_cast<uint32_t*>(b + o_big);
-  w.tile_status = reinterpret_cast<uint64_t*>(b + o_tst);
-  w.tile_summary = reinterpret_cast<uint32_t*>(b + o_tsum);
-  w.ctile_status = reinterpret_cast<uint64_t*>(b + o_cst);
-  w.scratch32 = reinterpret_cast<uint32_t*>(b + o_scr);
+  w.tile_sum = reinterpret_cast<uint64_t*>(b + o_tsum);
+  w.tile_last = reinterpret_cast<uint64_t*>(b + o_tlast);
+  w.tile_cnt = reinterpret_cast<uint32_t*>(b + o_tcnt);
+  w.tile_base = reinterpret_cast<uint32_t*>(b + o_tbase);
+  w.tile_pre = reinterpret_cast<uint32_t*>(b + o_tpre);
+  w.stage = reinterpret_cast<uint32_t*>(b + o_stage);
+  w.unit_tile = reinterpret_cast<uint32_t*>(b + o_utile);
+  w.unit_pos = reinterpret_cast<uint32_t*>(b + o_upos);
+  w.scratch = reinterpret_cast<uint32_t*>(b + o_scr);
   s->d_in = b + o_in;
   s->d_out = reinterpret_cast<int32_t*>(b + o_out);
   s->d_len = reinterpret_cast<int64_t*>(b + o_len);
@@ -151,9 +160,7 @@ int get_ws(tt_tokenizer* h, hipStream_t stream, uint64_t need, Workspace** out) 
     auto it = h->ws.find(stream);
     if (it == h->ws.end()) {
       s = new Workspace();
-      if (hipHostMalloc(reinterpret_cast<void**>(&s->h_len), 8, hipHostMallocDefault) != hipSuccess ||
-          hipHostMalloc(reinterpret_cast<void**>(&s->h_ctrl), sizeof(Ctrl), hipHostMallocDefault) !=
-              hipSuccess) {
+      if (hipHostMalloc(reinterpret_cast<void**>(&s->h_len), 8, hipHostMallocDefault) != hipSuccess) {
         free_ws(s);
         return TT_ERR_OOM;
       }
@@ -169,19 +176,27 @@ int get_ws(tt_tokenizer* h, hipStream_t stream, uint64_t need, Workspace** out) 
 }
 
 // Enqueue the whole chain for `n` bytes at device address `text`.
+// mode 0: split export (out_ids receives piece offsets); mode 1: encode.
 int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, const int64_t* d_docs,
-              int32_t n_docs, int32_t* out_ids, int64_t* out_len, int64_t* out_docs, hipStream_t st,
-              bool pretok_only) {
+              int32_t n_docs, int32_t* out_ids, int64_t* out_len, int64_t* out_docs, hipStream_t st, int mode) {
+  if (s->epoch == 0xFFFFFFFFu) {
+    // epochs wrapped: clear the words that carry them and start again
+    if (hipMemsetAsync(s->dmem, 0, s->ctl_bytes, st) != hipSuccess) return TT_ERR_HIP;
+    s->epoch = 0;
+    s->ticket_base = 0;
+  }
   Work w = s->w;
   w.text = text;
   w.n = n;
   w.doc_off = d_docs;
   w.n_docs = n_docs;
+  w.epoch = ++s->epoch;
+  w.ticket_base = s->ticket_base;
+  w.n_tiles = n_tiles_for(n);
   w.out_ids = out_ids;
   w.out_len = out_len;
   w.out_doc_off = out_docs;
-  DevTables tb{h->d_slots, h->mask, h->d_byte_id};
-  const uint32_t npt = pt_tiles(n), nct = ct_tiles_cap(n);
+  DevTables tb{h->d_slots, h->mask, h->d_join, h->d_ext, h->n_ids};
   const bool prof = h->profile != 0;
   s->n_ev = 0;
   auto mark = [&]() -> bool {
@@ -190,14 +205,13 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
     return hipEventRecord(s->ev[s->n_ev++], st) == hipSuccess;
   };
   if (!mark()) return TT_ERR_HIP;
-  if (launch_reset(w, npt, nct, st) != hipSuccess || !mark()) return TT_ERR_HIP;
-  if (launch_pretok(w, h->pattern, npt, h->d_join, !pretok_only, st) != hipSuccess || !mark()) return TT_ERR_HIP;
-  if (pretok_only) return TT_OK;
-  if (launch_bpe_small(w, tb, st) != hipSuccess || !mark()) return TT_ERR_HIP;
-  if (launch_bpe_wave(w, tb, st) != hipSuccess || !mark()) return TT_ERR_HIP;
-  if (launch_bpe_block(w, tb, st) != hipSuccess || !mark()) return TT_ERR_HIP;
-  if (launch_compact(w, nct, st) != hipSuccess || !mark()) return TT_ERR_HIP;
+  if (launch_tile(w, tb, h->pattern, mode, st) != hipSuccess) return TT_ERR_HIP;
+  s->ticket_base += w.n_tiles;  // the tiles took their tickets
+  if (!mark()) return TT_ERR_HIP;
+  if (w.n_tiles > EMIT_DIRECT_TILES && launch_tile_scan(w, st) != hipSuccess) return TT_ERR_HIP;
+  if (launch_emit(w, tb, mode, st) != hipSuccess) return TT_ERR_HIP;
   if (d_docs && launch_doc_offsets(w, st) != hipSuccess) return TT_ERR_HIP;
+  if (!mark()) return TT_ERR_HIP;
   return TT_OK;
 }
 
@@ -226,7 +240,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   if (!out || !vocab_offsets || (n_merges > 0 && !merges)) return TT_ERR_NULL_ARG;
   *out = nullptr;
   if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K) return TT_ERR_BAD_PATTERN;
-  if (n_merges < 0 || vocab_size < 256 || n_merges >= (int32_t)0x7FFFFFF0) return TT_ERR_BAD_ARG;
+  if (n_merges < 0 || vocab_size < 256 || (uint32_t)n_merges > MAX_MERGES) return TT_ERR_BAD_ARG;
   if (vocab_offsets[0] != 0) return TT_ERR_BAD_VOCAB;
   for (int32_t i = 0; i < vocab_size; ++i)
     if (vocab_offsets[i + 1] < vocab_offsets[i]) return TT_ERR_BAD_VOCAB;
@@ -241,9 +255,11 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   for (int b = 0; b < 256; ++b)
     if (byte_id[b] < 0) return TT_ERR_BAD_VOCAB;
 
-  // properness: operands available before use, results fresh and unique
-  std::vector<uint8_t> avail(vocab_size, 0);
-  for (int b = 0; b < 256; ++b) avail[byte_id[b]] = 1;
+  // properness: operands available before use, results fresh and unique.
+  // internal[] gives the library's ID of every available vocabulary ID: byte b
+  // is b, the result of merge r is 256 + r
+  std::vector<int32_t> internal(vocab_size, -1);
+  for (int b = 0; b < 256; ++b) internal[byte_id[b]] = b;
   std::unordered_set<uint64_t> pairs;
   pairs.reserve((size_t)n_merges * 2 + 16);
   for (int32_t r = 0; r < n_merges; ++r) {
@@ -253,23 +269,27 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       return TT_ERR_BAD_MERGES;
     uint64_t key = ((uint64_t)(uint32_t)m.left << 32) | (uint32_t)m.right;
     if (!pairs.insert(key).second) return TT_ERR_BAD_MERGES;
-    if (!avail[m.left] || !avail[m.right] || avail[m.result]) return TT_ERR_BAD_MERGES;
+    if (internal[m.left] < 0 || internal[m.right] < 0 || internal[m.result] >= 0) return TT_ERR_BAD_MERGES;
     int64_t la = vlen(m.left), lb = vlen(m.right);
     if (vlen(m.result) != la + lb || std::memcmp(vptr(m.result), vptr(m.left), la) != 0 ||
         std::memcmp(vptr(m.result) + la, vptr(m.right), lb) != 0)
       return TT_ERR_BAD_VOCAB;
-    avail[m.result] = 1;
+    internal[m.result] = 256 + r;
   }
+  const uint32_t n_ids = 256u + (uint32_t)n_merges;
+  std::vector<int32_t> ext(n_ids);
+  for (int b = 0; b < 256; ++b) ext[b] = byte_id[b];
+  for (int32_t r = 0; r < n_merges; ++r) ext[256 + r] = merges[r].result;
 
   // open-addressing table, load factor <= 1/2
   uint32_t cap = 16;
   while (cap < 2u * (uint32_t)n_merges) cap <<= 1;
-  std::vector<MergeSlot> slots(cap, MergeSlot{EMPTY, EMPTY, RANK_INF, 0});
+  std::vector<uint64_t> slots(cap, SLOT_EMPTY);
   for (int32_t r = 0; r < n_merges; ++r) {
-    uint32_t a = (uint32_t)merges[r].left, b = (uint32_t)merges[r].right;
+    const uint32_t a = (uint32_t)internal[merges[r].left], b = (uint32_t)internal[merges[r].right];
     uint32_t i = pair_hash(a, b) & (cap - 1);
-    while (slots[i].left != EMPTY) i = (i + 1) & (cap - 1);
-    slots[i] = MergeSlot{a, b, (uint32_t)r, (uint32_t)merges[r].result};
+    while (slots[i] != SLOT_EMPTY) i = (i + 1) & (cap - 1);
+    slots[i] = slot_key(a, b) | ((uint64_t)r << (2 * ID_BITS));
   }
 
   // junction byte pairs: the first merge that ever joins across a byte
@@ -289,18 +309,19 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   h->n_merges = n_merges;
   h->vocab_size = vocab_size;
   h->mask = cap - 1;
+  h->n_ids = n_ids;
   if (hipGetDevice(&h->device) != hipSuccess) {
     delete h;
     return TT_ERR_HIP;
   }
-  if (hipMalloc(reinterpret_cast<void**>(&h->d_slots), sizeof(MergeSlot) * cap) != hipSuccess ||
-      hipMalloc(reinterpret_cast<void**>(&h->d_byte_id), sizeof(int32_t) * 256) != hipSuccess ||
+  if (hipMalloc(reinterpret_cast<void**>(&h->d_slots), sizeof(uint64_t) * cap) != hipSuccess ||
+      hipMalloc(reinterpret_cast<void**>(&h->d_ext), sizeof(int32_t) * n_ids) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_join), sizeof(uint32_t) * 2048) != hipSuccess) {
     tt_destroy(h);
     return TT_ERR_OOM;
   }
-  if (hipMemcpy(h->d_slots, slots.data(), sizeof(MergeSlot) * cap, hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemcpy(h->d_byte_id, byte_id.data(), sizeof(int32_t) * 256, hipMemcpyHostToDevice) != hipSuccess ||
+  if (hipMemcpy(h->d_slots, slots.data(), sizeof(uint64_t) * cap, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(h->d_ext, ext.data(), sizeof(int32_t) * n_ids, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_join, join.data(), sizeof(uint32_t) * 2048, hipMemcpyHostToDevice) != hipSuccess) {
     tt_destroy(h);
     return TT_ERR_HIP;
@@ -315,7 +336,7 @@ void tt_destroy(tt_tokenizer* h) {
   (void)hipDeviceSynchronize();
   for (auto& kv : h->ws) free_ws(kv.second);
   if (h->d_slots) (void)hipFree(h->d_slots);
-  if (h->d_byte_id) (void)hipFree(h->d_byte_id);
+  if (h->d_ext) (void)hipFree(h->d_ext);
   if (h->d_join) (void)hipFree(h->d_join);
   delete h;
 }
@@ -342,7 +363,7 @@ int tt_encode_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_
   Workspace* s = nullptr;
   int rc = get_ws(h, st, (uint64_t)len, &s);
   if (rc) return rc;
-  return run_chain(h, s, d_utf8, (uint32_t)len, nullptr, 0, d_out_ids, d_out_len, nullptr, st, false);
+  return run_chain(h, s, d_utf8, (uint32_t)len, nullptr, 0, d_out_ids, d_out_len, nullptr, st, 1);
 }
 
 int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_ids, int64_t* out_len,
@@ -358,7 +379,7 @@ int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_id
   int rc = get_ws(h, st, (uint64_t)len, &s);
   if (rc) return rc;
   if (hipMemcpyAsync(s->d_in, utf8, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
-  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, false);
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, 1);
   if (rc) return rc;
   if (hipMemcpyAsync(s->h_len, s->d_len, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return TT_ERR_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
@@ -397,7 +418,7 @@ int tt_encode_batch(tt_tokenizer* h, const uint8_t* concat, const int64_t* doc_o
   if (hipMemcpyAsync(s->d_in, concat, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
   if (hipMemcpyAsync(s->d_docs, doc_offsets, 8 * ((size_t)n_docs + 1), hipMemcpyHostToDevice, st) != hipSuccess)
     return TT_ERR_HIP;
-  rc = run_chain(h, s, s->d_in, (uint32_t)len, s->d_docs, n_docs, s->d_out, s->d_len, s->d_out_docs, st, false);
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, s->d_docs, n_docs, s->d_out, s->d_len, s->d_out_docs, st, 1);
   if (rc) return rc;
   if (hipMemcpyAsync(s->h_len, s->d_len, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return TT_ERR_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
@@ -425,21 +446,20 @@ int tt_pretokenize(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int64_t* o
   int rc = get_ws(h, st, (uint64_t)len, &s);
   if (rc) return rc;
   if (hipMemcpyAsync(s->d_in, utf8, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
-  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, true);
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, 0);
   if (rc) return rc;
-  if (hipMemcpyAsync(s->h_ctrl, s->w.ctrl, sizeof(Ctrl), hipMemcpyDeviceToHost, st) != hipSuccess)
-    return TT_ERR_HIP;
+  if (hipMemcpyAsync(s->h_len, s->d_len, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return TT_ERR_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
-  const Ctrl* c = reinterpret_cast<const Ctrl*>(s->h_ctrl);
-  if (c->error) return -(int)c->error;
-  const uint32_t P = c->n_pieces;
-  std::vector<uint32_t> tmp(P);
+  const int64_t P = *s->h_len;
+  if (P < 0) return (int)P;
+  if (P > len) return TT_ERR_HIP;  // cannot happen: at most one piece per byte
+  std::vector<uint32_t> tmp((size_t)P);
   if (P > 0) {
-    if (hipMemcpyAsync(tmp.data(), s->w.piece_off, 4 * (size_t)P, hipMemcpyDeviceToHost, st) != hipSuccess)
+    if (hipMemcpyAsync(tmp.data(), s->d_out, 4 * (size_t)P, hipMemcpyDeviceToHost, st) != hipSuccess)
       return TT_ERR_HIP;
     if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
   }
-  for (uint32_t i = 0; i < P; ++i) out_piece_starts[i] = tmp[i];
+  for (int64_t i = 0; i < P; ++i) out_piece_starts[i] = tmp[(size_t)i];
   *out_n = P;
   return TT_OK;
 }

@@ -1,0 +1,329 @@
+// Exact byte-level BPE of one unit (a piece, or a segment of a piece that no
+// merge can cross), on the GPU.
+//
+// A unit starts as the IDs of its bytes; the adjacent pair with the lowest
+// merge rank is merged, leftmost first, until no pair has a rank (the model
+// stage of the front-end/model factorisation, Appendix, Definition
+// d:frontend and Lemma l:homo).  Two facts license the parallel schedules
+// below (Sec. 4.2, "GPU BPE"): with a proper merge list, merging all leftmost
+// non-overlapping occurrences of the round's lowest-ranked pair at once equals
+// merging them one by one, and after a merge only the pairs that touch the new
+// token need a new rank lookup.  The unit length picks the execution unit
+// (Sec. 4.2 dispatches by piece length):
+//   bpe_thread  <= 16 bytes: one thread, the unit in registers;
+//   bpe_wave    <= 64 bytes: one wave64, one token per lane;
+//   bpe_rows    longer:      NW waves over rows of 64 tokens in LDS or global
+//                            memory.
+// IDs are internal: byte b is b, the result of merge r is 256 + r.
+#pragma once
+
+#include "tt_internal.h"
+
+namespace tt {
+
+constexpr uint32_t RANK_DIRTY = 0xFFFFFFFEu;  // pair changed; its rank must be looked up again
+
+// Leftmost non-overlapping choice among the set bits of m, where bit j stands
+// for the pair (token j, token j+1).  Two chosen pairs may not share a token,
+// so within every run of consecutive set bits the left-to-right greedy choice
+// takes the run's first bit and every second bit after it.  Runs that start on
+// an even bit are isolated with one carry propagation: adding their start bits
+// clears exactly those runs.
+__device__ __forceinline__ uint64_t leftmost_nonoverlapping(uint64_t m) {
+  const uint64_t EVEN = 0x5555555555555555ull;
+  const uint64_t starts = m & ~(m << 1);
+  const uint64_t even_runs = ((m + (starts & EVEN)) ^ m) & m;
+  return (even_runs & EVEN) | (m & ~even_runs & ~EVEN);
+}
+
+// Number of set bits of m below the calling lane.
+__device__ __forceinline__ uint32_t bits_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Minimum over the 64 lanes of a wave, in every lane (DPP row steps, then
+// the row broadcasts; the full result ends in lane 63).
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+  int x = (int)v;
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));  // row_mirror
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x142, 0xA, 0xF, false));  // row_bcast15
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x143, 0xC, 0xF, false));  // row_bcast31
+  return (uint32_t)__builtin_amdgcn_readlane(x, 63);
+}
+
+// ---------------------------------------------------------------------------
+// One thread, at most 16 bytes.  Token IDs and pair ranks stay in registers
+// (all indexing is unrolled); a merge clears the right token's bit in an alive
+// mask instead of shifting the tail.  A pair's rank is kept as
+// (rank << 4) | position so that one unsigned minimum finds the lowest rank
+// and, among equal ranks (the same pair), the leftmost occurrence.  The chain
+// is two probe round trips for the initial pairs and one per merge (its two
+// neighbour probes overlap).
+//   byte(j)      byte j of the unit, j < L
+//   out(j, id)   stores output token j
+// Returns the number of tokens.
+// ---------------------------------------------------------------------------
+template <class ByteF, class OutF>
+__device__ __forceinline__ uint32_t bpe_thread(uint32_t L, ByteF byte, const DevTables& tb, OutF out) {
+  constexpr int S = SMALL_MAX;
+  const uint64_t* __restrict__ tab = tb.slots;
+  const uint32_t mask = tb.mask;
+  uint32_t id[S], rk[S];
+#pragma unroll
+  for (int j = 0; j < S; ++j) id[j] = (uint32_t)j < L ? byte(j) : 0u;
+#pragma unroll
+  for (int g = 0; g < S; g += 8) {
+    uint32_t si[8];
+    uint64_t sv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int j = g + k;
+      si[k] = 0;
+      sv[k] = SLOT_EMPTY;
+      if (j + 1 < S && (uint32_t)(j + 1) < L) {
+        si[k] = probe_start(mask, id[j], id[j + 1]);
+        sv[k] = tab[si[k]];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int j = g + k;
+      uint32_t r = RANK_INF;
+      if (j + 1 < S && (uint32_t)(j + 1) < L) r = probe_finish(tab, mask, si[k], sv[k], id[j], id[j + 1]);
+      rk[j] = r == RANK_INF ? RANK_INF : ((r << 4) | (uint32_t)j);
+    }
+  }
+  uint32_t alive = (1u << L) - 1u;  // L <= 16
+  for (;;) {
+    uint32_t best = RANK_INF;
+#pragma unroll
+    for (int j = 0; j < S - 1; ++j) best = min(best, rk[j]);
+    if (best == RANK_INF) break;
+    const int k = (int)(best & 15u);
+    const uint32_t nid = 256u + (best >> 4);
+    // token k absorbs the next live token m
+    const int m = __builtin_ctz(alive & ~((2u << k) - 1u));
+    alive &= ~(1u << m);
+    const uint32_t above_m = alive & ~((2u << m) - 1u);
+    const uint32_t below_k = alive & ((1u << k) - 1u);
+    const bool hr = above_m != 0u, hl = below_k != 0u;
+    const int r_i = hr ? __builtin_ctz(above_m) : 0;
+    const int l_i = hl ? 31 - __builtin_clz(below_k) : 0;
+    uint32_t right = 0, left = 0;
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      right = j == r_i ? id[j] : right;
+      left = j == l_i ? id[j] : left;
+    }
+    uint32_t ir = 0, il = 0;
+    uint64_t sr = SLOT_EMPTY, sl = SLOT_EMPTY;
+    if (hr) {
+      ir = probe_start(mask, nid, right);
+      sr = tab[ir];
+    }
+    if (hl) {
+      il = probe_start(mask, left, nid);
+      sl = tab[il];
+    }
+    const uint32_t rr = hr ? probe_finish(tab, mask, ir, sr, nid, right) : RANK_INF;
+    const uint32_t rl = hl ? probe_finish(tab, mask, il, sl, left, nid) : RANK_INF;
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      if (j == k) {
+        id[j] = nid;
+        rk[j] = rr == RANK_INF ? RANK_INF : ((rr << 4) | (uint32_t)j);
+      }
+      if (j == m) rk[j] = RANK_INF;
+      if (hl && j == l_i) rk[j] = rl == RANK_INF ? RANK_INF : ((rl << 4) | (uint32_t)j);
+    }
+  }
+  uint32_t c = 0;
+#pragma unroll
+  for (int j = 0; j < S; ++j)
+    if ((alive >> j) & 1u) out(c++, id[j]);
+  return c;
+}
+
+// ---------------------------------------------------------------------------
+// One wave64, at most 64 bytes: lane i holds token i and the rank of the pair
+// (i, i+1).  A round is a wave minimum, one ballot, the closed-form leftmost
+// non-overlapping choice, a push permute that compacts the survivors, and the
+// rank lookups of the changed pairs (one probe round trip).  Every lane of the
+// wave calls it with the same arguments.
+// ---------------------------------------------------------------------------
+template <class ByteF, class OutF>
+__device__ __forceinline__ uint32_t bpe_wave(uint32_t L, ByteF byte, const DevTables& tb, OutF out) {
+  const int lane = (int)(threadIdx.x & 63u);
+  uint32_t n = L;  // <= 64
+  uint32_t id = (uint32_t)lane < n ? byte(lane) : 0u;
+  uint32_t idn = (uint32_t)__shfl_down((int)id, 1, 64);
+  uint32_t rk = (uint32_t)lane + 1u < n ? probe_rank(tb.slots, tb.mask, id, idn) : RANK_INF;
+  for (;;) {
+    const uint32_t m = wave_min_u32(rk);
+    if (m == RANK_INF) break;
+    const uint64_t sel = leftmost_nonoverlapping(__ballot(rk == m));
+    const uint64_t valid = n >= 64u ? ~0ull : ((1ull << n) - 1ull);
+    const uint64_t keep = valid & ~(sel << 1);
+    const bool me_sel = (sel >> lane) & 1ull;
+    const bool nx_sel = lane < 63 && ((sel >> (lane + 1)) & 1ull);
+    const uint32_t nid = me_sel ? 256u + m : id;
+    const uint32_t r = (me_sel || nx_sel) ? RANK_DIRTY : rk;
+    // at least one pair merged, so at most 63 tokens survive and lane 63 is
+    // free to take the values of the lanes that do not survive
+    const int dest = ((keep >> lane) & 1ull) ? (int)bits_below(keep) : 63;
+    id = (uint32_t)__builtin_amdgcn_ds_permute(dest << 2, (int)nid);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_ds_permute(dest << 2, (int)r);
+    n = (uint32_t)__popcll(keep);
+    idn = (uint32_t)__shfl_down((int)id, 1, 64);
+    rk = RANK_INF;
+    if ((uint32_t)lane < n) {
+      rk = r2;
+      if (r2 == RANK_DIRTY) rk = (uint32_t)lane + 1u < n ? probe_rank(tb.slots, tb.mask, id, idn) : RANK_INF;
+    }
+  }
+  if ((uint32_t)lane < n) out(lane, id);
+  return n;
+}
+
+// ---------------------------------------------------------------------------
+// NW waves over rows of 64 tokens.  I0/I1 (IDs) and R0/R1 (pair ranks) are
+// double buffers of at least L words, `sel` holds rows(L) + 1 selection masks;
+// they may live in LDS or in global memory (visible to the whole block).
+// Every thread of the block calls it with the same arguments.
+// ---------------------------------------------------------------------------
+template <int NW>
+struct RowsShared {
+  uint32_t wmin[NW];
+  uint32_t f0[NW], f1[NW], cin[NW];
+  uint32_t wsum[NW], wbase[NW];
+  uint32_t n_next;
+};
+
+template <int NW, class ByteF, class OutF>
+__device__ uint32_t bpe_rows(uint32_t L, ByteF byte, const DevTables& tb, uint32_t* I0, uint32_t* I1, uint32_t* R0,
+                             uint32_t* R1, uint64_t* sel, RowsShared<NW>& sm, OutF out) {
+  const int tid = (int)threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  constexpr int NT = NW * 64;
+  uint32_t* ids[2] = {I0, I1};
+  uint32_t* rk[2] = {R0, R1};
+  int cur = 0;
+  uint32_t n = L;
+
+  for (uint32_t i = tid; i < n; i += NT) I0[i] = byte(i);
+  __syncthreads();
+  for (uint32_t i = tid; i < n; i += NT) R0[i] = i + 1 < n ? probe_rank(tb.slots, tb.mask, I0[i], I0[i + 1]) : RANK_INF;
+  __syncthreads();
+
+  for (;;) {
+    const uint32_t* I = ids[cur];
+    const uint32_t* R = rk[cur];
+    uint32_t* I2 = ids[cur ^ 1];
+    uint32_t* R2 = rk[cur ^ 1];
+
+    // 1. lowest rank in the unit
+    uint32_t m = RANK_INF;
+    for (uint32_t i = tid; i < n; i += NT) m = min(m, R[i]);
+    m = wave_min_u32(m);
+    if (NW > 1) {
+      if (lane == 0) sm.wmin[wave] = m;
+      __syncthreads();
+      m = RANK_INF;
+      for (int v = 0; v < NW; ++v) m = min(m, sm.wmin[v]);
+    }
+    if (m == RANK_INF) break;
+
+    // 2. leftmost non-overlapping occurrences, row by row.  A row's choice
+    // depends on whether the last pair of the previous row was chosen; with
+    // several waves each wave first evaluates its rows for both carries.
+    const uint32_t rows = (n + 63) / 64;
+    const uint32_t rpw = (rows + NW - 1) / NW;
+    const uint32_t r_lo = min(rows, (uint32_t)wave * rpw);
+    const uint32_t r_hi = min(rows, r_lo + rpw);
+    uint32_t carry = 0;
+    if (NW > 1) {
+      uint32_t c0 = 0, c1 = 1;
+      for (uint32_t r = r_lo; r < r_hi; ++r) {
+        const uint32_t i = r * 64 + lane;
+        const uint64_t occ = __ballot(i < n && R[i] == m);
+        c0 = (uint32_t)(leftmost_nonoverlapping(occ & ~(uint64_t)c0) >> 63);
+        c1 = (uint32_t)(leftmost_nonoverlapping(occ & ~(uint64_t)c1) >> 63);
+      }
+      if (lane == 0) {
+        sm.f0[wave] = c0;
+        sm.f1[wave] = c1;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t c = 0;
+        for (int v = 0; v < NW; ++v) {
+          sm.cin[v] = c;
+          c = c ? sm.f1[v] : sm.f0[v];
+        }
+      }
+      __syncthreads();
+      carry = sm.cin[wave];
+    }
+    uint32_t keep_total = 0;
+    for (uint32_t r = r_lo; r < r_hi; ++r) {
+      const uint32_t i = r * 64 + lane;
+      const uint64_t occ = __ballot(i < n && R[i] == m);
+      const uint64_t s = leftmost_nonoverlapping(occ & ~(uint64_t)carry);
+      if (lane == 0) sel[r] = s;
+      const uint64_t valid = (n - r * 64 >= 64) ? ~0ull : ((1ull << (n - r * 64)) - 1ull);
+      const uint64_t keep = valid & ~((s << 1) | (uint64_t)carry);
+      keep_total += (uint32_t)__popcll(keep);
+      carry = (uint32_t)(s >> 63);
+    }
+    if (tid == 0) sel[rows] = 0;  // sentinel row (only bit 0 is ever read)
+    // 3. compaction
+    if (NW > 1) {
+      if (lane == 0) sm.wsum[wave] = keep_total;
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t b = 0;
+        for (int v = 0; v < NW; ++v) {
+          sm.wbase[v] = b;
+          b += sm.wsum[v];
+        }
+        sm.n_next = b;
+      }
+    }
+    __syncthreads();
+    uint32_t base = NW > 1 ? sm.wbase[wave] : 0u;
+    const uint32_t n2 = NW > 1 ? sm.n_next : keep_total;
+    uint32_t prevbit = (NW > 1 && r_lo > 0) ? (uint32_t)(sel[r_lo - 1] >> 63) : 0u;
+    for (uint32_t r = r_lo; r < r_hi; ++r) {
+      const uint32_t i = r * 64 + lane;
+      const uint64_t s = sel[r];
+      const uint64_t valid = (n - r * 64 >= 64) ? ~0ull : ((1ull << (n - r * 64)) - 1ull);
+      const uint64_t keep = valid & ~((s << 1) | (uint64_t)prevbit);
+      if ((keep >> lane) & 1ull) {
+        const uint32_t k = base + bits_below(keep);
+        const uint32_t my = (uint32_t)(s >> lane) & 1u;
+        const uint32_t nx = lane < 63 ? (uint32_t)(s >> (lane + 1)) & 1u : (uint32_t)(sel[r + 1] & 1ull);
+        I2[k] = my ? 256u + m : I[i];
+        R2[k] = (my | nx) ? RANK_DIRTY : R[i];
+      }
+      base += (uint32_t)__popcll(keep);
+      prevbit = (uint32_t)(s >> 63);
+    }
+    __syncthreads();
+    n = n2;
+    // 4. ranks of the pairs next to the merges
+    for (uint32_t i = tid; i < n; i += NT) {
+      if (R2[i] == RANK_DIRTY) R2[i] = i + 1 < n ? probe_rank(tb.slots, tb.mask, I2[i], I2[i + 1]) : RANK_INF;
+    }
+    __syncthreads();
+    cur ^= 1;
+  }
+  const uint32_t* I = ids[cur];
+  for (uint32_t i = tid; i < n; i += NT) out(i, I[i]);
+  return n;
+}
+
+}  // namespace tt

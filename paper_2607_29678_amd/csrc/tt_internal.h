@@ -9,7 +9,7 @@
 namespace tt {
 
 // ---------------------------------------------------------------------------
-// Character codes kept per byte in LDS by the pre-tokenization kernel.
+// Character codes kept per byte in LDS by the tile kernel.
 //   bits 0..2  class of the character whose first byte is here:
 //              O other, L letter, N number, WS whitespace except CR/LF,
 //              NL CR or LF, NONE for continuation bytes and positions
@@ -35,28 +35,24 @@ constexpr uint32_t CODE_DOCSTART = 0x80u;
 __host__ __device__ inline uint32_t code_cls(uint32_t c) { return c & 7u; }
 __host__ __device__ inline uint32_t code_id(uint32_t c) { return (c >> 3) & 15u; }
 
-// Device control block of one call.  Zeroed by the first kernel of the chain.
-struct Ctrl {
-  uint32_t tile_ticket;   // pre-tokenization tiles taken
-  uint32_t n_pieces;      // P, written by the last pre-tokenization tile
-  uint32_t error;         // 0, or the magnitude of a TT_ERR_* code
-  uint32_t n_long;        // pieces queued for the wave engine
-  uint32_t long_ticket;   // wave-engine queue head
-  uint32_t n_big;         // pieces queued for the block engine
-  uint32_t big_ticket;    // block-engine queue head
-  uint32_t ctile_ticket;  // compaction tiles taken
-  uint32_t small_done;    // (unused; keeps the struct 8-byte aligned)
-  uint32_t pad;
-  int64_t out_len;        // T, written by the last compaction tile
-};
-
-// One slot of the open-addressing merge table: key (left, right), value
-// (rank, result).  Empty slots have left == EMPTY.
-struct MergeSlot {
-  uint32_t left, right, rank, result;
-};
-constexpr uint32_t EMPTY = 0xFFFFFFFFu;
+// ---------------------------------------------------------------------------
+// Token IDs inside the library.  Byte b is ID b and the result of the merge
+// of rank r is ID 256 + r; the output stage maps them to the caller's IDs.
+// A proper merge list makes this a bijection onto the IDs BPE can produce
+// (every operand is a byte or an earlier result, and results are unique), and
+// it lets a merge table slot hold the key and the rank in 64 bits: the result
+// of a merge is implied by its rank.
+// ---------------------------------------------------------------------------
+constexpr uint32_t ID_BITS = 21;
+constexpr uint32_t ID_LIMIT = (1u << ID_BITS) - 1u;       // internal IDs are < ID_LIMIT
+constexpr uint32_t MAX_MERGES = ID_LIMIT - 256u;          // 2,096,895
+constexpr uint64_t KEY_MASK = (1ull << (2 * ID_BITS)) - 1ull;
+constexpr uint64_t SLOT_EMPTY = ~0ull;                    // its key is (ID_LIMIT, ID_LIMIT)
 constexpr uint32_t RANK_INF = 0xFFFFFFFFu;
+
+__host__ __device__ inline uint64_t slot_key(uint32_t a, uint32_t b) {
+  return (uint64_t)a | ((uint64_t)b << ID_BITS);
+}
 
 __host__ __device__ inline uint32_t pair_hash(uint32_t a, uint32_t b) {
   uint32_t h = a * 0x9E3779B1u ^ (b + 0x7F4A7C15u) * 0x85EBCA77u;
@@ -68,90 +64,95 @@ __host__ __device__ inline uint32_t pair_hash(uint32_t a, uint32_t b) {
   return h;
 }
 
-// Slot index where the search for the pair (a, b) starts.
+// Open-addressing lookup in two halves so that several first loads can be in
+// flight before any comparison: probe_start gives the first slot index,
+// probe_finish walks on from the loaded slot (linear probing; load <= 1/2).
 __device__ __forceinline__ uint32_t probe_start(uint32_t mask, uint32_t a, uint32_t b) {
   return pair_hash(a, b) & mask;
 }
-
-// One 16-byte slot, fetched with a single 128-bit load.
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint4 load_slot(const MergeSlot* __restrict__ tab, uint32_t i) {
-  u32x4 v = reinterpret_cast<const u32x4*>(tab)[i];
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-// Finish a probe whose first slot `s` (at index i) is already loaded: rank
-// and result of the pair (a, b), or RANK_INF if the pair has no merge.
-__device__ __forceinline__ uint2 probe_finish(const MergeSlot* __restrict__ tab, uint32_t mask, uint32_t i,
-                                              uint4 s, uint32_t a, uint32_t b) {
-  while (!((s.x == a) & (s.y == b)) && s.x != EMPTY) {
-    i = (i + 1) & mask;
-    s = load_slot(tab, i);
+__device__ __forceinline__ uint32_t probe_finish(const uint64_t* __restrict__ tab, uint32_t mask, uint32_t i,
+                                                 uint64_t s, uint32_t a, uint32_t b) {
+  const uint64_t key = slot_key(a, b);
+  while ((s & KEY_MASK) != key && s != SLOT_EMPTY) {
+    i = (i + 1u) & mask;
+    s = tab[i];
   }
-  return (s.x == a) & (s.y == b) ? make_uint2(s.z, s.w) : make_uint2(RANK_INF, 0u);
+  return (s & KEY_MASK) == key ? (uint32_t)(s >> (2 * ID_BITS)) : RANK_INF;
 }
-
-__device__ __forceinline__ uint2 probe_pair(const MergeSlot* __restrict__ tab, uint32_t mask, uint32_t a,
-                                           uint32_t b) {
-  uint32_t i = probe_start(mask, a, b);
-  return probe_finish(tab, mask, i, load_slot(tab, i), a, b);
+// Rank of the pair (a, b), or RANK_INF if no merge joins it.
+__device__ __forceinline__ uint32_t probe_rank(const uint64_t* __restrict__ tab, uint32_t mask, uint32_t a,
+                                               uint32_t b) {
+  const uint32_t i = probe_start(mask, a, b);
+  return probe_finish(tab, mask, i, tab[i], a, b);
 }
 
 // Everything a kernel needs to know about a tokenizer handle.
 struct DevTables {
-  const MergeSlot* slots;  // open-addressing merge table
-  uint32_t mask;           // slot count - 1
-  const int32_t* byte_id;  // [256] base ID of each byte
+  const uint64_t* slots;    // merge table: key (left | right << 21), rank in bits 42..63
+  uint32_t mask;            // slot count - 1
+  const uint32_t* join;     // [2048] bit (x << 8 | y): some merge joins a token ending
+                            // in byte x to a token starting with byte y
+  const int32_t* ext_id;    // [n_ids] caller's ID of every internal ID
+  uint32_t n_ids;           // 256 + M
 };
 
-// Buffers of one call (all device memory).
+// ---------------------------------------------------------------------------
+// Control words of a workspace.  Nothing is cleared between calls: every call
+// has an epoch (1, 2, ...), words that later blocks wait on carry the epoch of
+// the call that wrote them, and the tile ticket only ever grows (a call's
+// tiles are tickets [ticket_base, ticket_base + n_tiles)).
+// ---------------------------------------------------------------------------
+struct Ctrl {
+  uint32_t tile_ticket;
+  uint32_t pad;
+  uint64_t err;             // (epoch << 32) | error magnitude of the latest failing call
+};
+
+constexpr uint32_t NO_START = 0xFFFFFFFFu;  // tile_last: no unit starts in the tile
+
+// Buffers and parameters of one call (all device memory).
 struct Work {
   const uint8_t* text;      // request bytes (caller's or staged)
   uint32_t n;               // bytes
   const int64_t* doc_off;   // batch: n_docs+1 byte offsets, else nullptr
   int32_t n_docs;
   Ctrl* ctrl;
-  // "pieces" below are the units of the call: pre-tokenization pieces for the
-  // split-level export, BPE segments of pieces for encoding
-  uint32_t* piece_off;      // [P+1] byte offset of each unit start, then n
-  uint32_t* piece_cnt;      // [P] tokens per unit
-  uint32_t* piece_out;      // [P+1] output offset of each unit
-  int32_t* ids;             // [n] per-piece IDs stored at the piece's byte offset
-  uint32_t* long_list;      // [P] pieces for the wave engine
-  uint32_t* big_list;       // [P] pieces for the block engine
-  uint64_t* tile_status;    // pre-tokenization look-back words
-  uint32_t* tile_summary;   // pre-tokenization run summaries (cl100k carries)
-  uint64_t* ctile_status;   // compaction look-back words
-  uint32_t* scratch32;      // [6 * n] block-engine double buffers
-  int32_t* out_ids;         // output IDs
-  int64_t* out_len;         // output length (or -error)
+  uint32_t epoch;           // this call's epoch
+  uint32_t ticket_base;     // first tile ticket of this call
+  uint32_t n_tiles;
+  uint64_t* tile_sum;       // [tiles] (epoch << 32) | trailing-run summary (cl100k carries)
+  uint64_t* tile_last;      // [tiles] (epoch << 32) | last unit start in the tile, or NO_START
+  uint32_t* tile_cnt;       // [tiles] outputs staged by the tile
+  uint32_t* tile_base;      // [tiles] where they are staged
+  uint32_t* tile_pre;       // [tiles] exclusive prefix of tile_cnt (large requests, batches)
+  uint32_t* stage;          // [n] staged outputs: tile t's at stage[tile_base[t] ..]
+  uint32_t* unit_tile;      // batch: [n] processing tile of the unit starting at a byte
+  uint32_t* unit_pos;       // batch: [n] its first output within that tile's outputs
+  uint32_t* scratch;        // rows of units longer than a tile window: 4 * n words + selection masks
+  int32_t* out_ids;         // output (caller IDs, or piece offsets for the split export)
+  int64_t* out_len;         // output length, or -error
   int64_t* out_doc_off;     // batch: n_docs+1 output offsets (device)
 };
 
 // Tiles and geometry --------------------------------------------------------
-constexpr int PT_THREADS = 1024;                  // pre-tokenization block
+constexpr int PT_THREADS = 1024;                  // tile block
 constexpr int PT_BPT = 2;                          // bytes per thread
 constexpr int PT_WIN = PT_THREADS * PT_BPT;        // window bytes in LDS
 constexpr int PT_HALO = 32;                        // context bytes each side
 constexpr int PT_OWN = PT_WIN - 2 * PT_HALO;       // bytes a tile decides
 
-constexpr int SMALL_MAX = 16;                      // thread-per-piece limit (bytes)
-constexpr int WAVE_MAX = 512;                      // wave engine limit (bytes)
-constexpr int CT_THREADS = 256;                    // compaction block
-constexpr int CT_PPT = 8;                          // pieces per thread
-constexpr int CT_TILE = CT_THREADS * CT_PPT;
+constexpr int SMALL_MAX = 16;                      // thread-per-unit limit (bytes)
+constexpr int WAVE_MAX = 64;                       // wave-per-unit limit (bytes)
+constexpr uint32_t EMIT_THREADS = 256;
+constexpr uint32_t EMIT_DIRECT_TILES = 4096;       // above this, a scan kernel makes tile_pre
 
-inline uint32_t pt_tiles(uint32_t n) { return (n + PT_OWN - 1) / PT_OWN; }
-inline uint32_t ct_tiles_cap(uint32_t n) { return (n + CT_TILE - 1) / CT_TILE + 1; }
+inline uint32_t n_tiles_for(uint32_t n) { return (n + PT_OWN - 1) / PT_OWN; }
 
 // Launchers (defined in the .hip files) -------------------------------------
-hipError_t launch_reset(const Work& w, uint32_t n_pt_tiles, uint32_t n_ct_tiles, hipStream_t s);
-hipError_t launch_pretok(const Work& w, int pattern, uint32_t n_pt_tiles, const uint32_t* join_bits, bool seg,
-                         hipStream_t s);
-hipError_t launch_bpe_small(const Work& w, const DevTables& t, hipStream_t s);
-hipError_t launch_bpe_wave(const Work& w, const DevTables& t, hipStream_t s);
-hipError_t launch_bpe_block(const Work& w, const DevTables& t, hipStream_t s);
-hipError_t launch_compact(const Work& w, uint32_t n_ct_tiles, hipStream_t s);
+// mode 0: split export (outputs are piece byte offsets); mode 1: encode
+hipError_t launch_tile(const Work& w, const DevTables& t, int pattern, int mode, hipStream_t s);
+hipError_t launch_tile_scan(const Work& w, hipStream_t s);
+hipError_t launch_emit(const Work& w, const DevTables& t, int mode, hipStream_t s);
 hipError_t launch_doc_offsets(const Work& w, hipStream_t s);
 
 }  // namespace tt

@@ -1,48 +1,60 @@
-// Pre-tokenization on the GPU: UTF-8 decode, character classes, run-local
-// piece-start rules and the piece-numbering scan, in one pass over the bytes.
+// The tile kernel: one block decides the pieces of 1,984 bytes of the request
+// and encodes them, with no host round trip and no kernel boundary between
+// pre-tokenization and BPE.
 //
-// The paper replaces the sequential leftmost-first regex scan by an equivalent
-// per-character predicate: classify every character into letter / number /
-// whitespace / other, form maximal same-class runs, and decide whether a
-// character starts a piece from its offset in its run, at most four
-// characters of lookback and a few per-run aggregates (Sec. 4.1, "Removing
-// the sequential regex scan"; the pipeline of Sec. 4.2 is decode, classify,
-// runs, predicate, two prefix scans).
-//
-// MI355X design.  One 256-thread block owns 1,984 bytes and stages a 2,048
-// byte window (32 bytes of context on each side) in LDS; every thread decodes
-// and classifies 8 bytes.  Runs that reach past the window are resolved
-// without a second pass:
+// Pre-tokenization.  The paper replaces the sequential leftmost-first regex
+// scan by an equivalent per-character predicate: classify every character
+// into letter / number / whitespace / other, form maximal same-class runs,
+// and decide whether a character starts a piece from its offset in its run,
+// at most four characters of lookback and a few per-run aggregates (Sec. 4.1,
+// "Removing the sequential regex scan"; Sec. 4.2 lists the stages: decode,
+// classify, runs, predicate, scans).  A block stages a 2,048-byte window (32
+// bytes of context on each side of the bytes it owns) in LDS and every thread
+// decodes and classifies two positions.  Runs that reach past the window are
+// resolved without a second pass:
 //   - backwards (cl100k: a number run's length mod 3, the class before a
 //     CR/LF stretch) from run summaries that earlier blocks publish before
 //     they wait on anything;
 //   - forwards (cl100k: whether a whitespace stretch after CR/LF is the last
 //     stretch of its run) by reading the bytes after the window, which only a
 //     whitespace stretch longer than the window needs.
-// Piece numbers come from a block scan plus a decoupled look-back over the
-// per-block counts, so piece offsets are written in one pass with no host
-// round trip.  Block order is taken from an atomic ticket, so a block only
-// ever waits on blocks that started before it.
+//
+// Units.  For encoding, a piece is also cut at every byte position whose byte
+// pair (b[q-1], b[q]) is the junction of no merge: the first merge that joins
+// across a position has its left operand ending in b[q-1] and its right one
+// starting with b[q], so no merge ever crosses such a position and the two
+// sides are independent BPE problems.  The resulting units are numbered by a
+// block scan.
+//
+// BPE (Sec. 4.2, "GPU BPE").  The block encodes every unit that starts in its
+// bytes except its last one, whose end lies in a later tile: that unit is the
+// "incoming" unit of the next tile that has a unit start, which learns its
+// start from the position the earlier tiles publish right after their scan.
+// Units go to the smallest execution unit that holds them (thread, wave, or
+// the whole block over rows in LDS or, past the window size, global memory).
+// Tokens are compacted in the tile and staged in global memory where the
+// tile's bytes begin, so a tile's outputs never overlap another's; the emit
+// kernel only has to place each tile's block of outputs.
+//
+// Block order is taken from an atomic ticket, so a block only ever waits on
+// blocks that started before it, and every block publishes what later blocks
+// wait for before it waits on anything itself.
 #include "class_table.inc"
+#include "tt_bpe.h"
 #include "tt_internal.h"
 
 namespace tt {
 
 namespace {
 
-constexpr uint32_t ST_AGG = 1u, ST_INC = 2u;  // look-back flags (bits 32..33)
-constexpr uint32_t SUM_READY = 0x80000000u, SUM_RUNALL = 1u;
+// trailing-run summary of a tile (cl100k): bit 0 the run spans the whole tile,
+// bits 1..2 its character count mod 3, bits 3..5 the class before it
+constexpr uint32_t SUM_RUNALL = 1u;
 
 __device__ __forceinline__ uint64_t ld_acquire(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint32_t ld_acquire(const uint32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-}
 __device__ __forceinline__ void st_release(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_release(uint32_t* p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -156,15 +168,30 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane, F comb)
 
 constexpr int PT_PAD = 8;  // LDS arrays also hold window positions [-8, 0) and [PT_WIN, PT_WIN + 16)
 
+constexpr int MED_CAP = PT_WIN / (SMALL_MAX + 1) + 2;  // units of 17..64 bytes in a tile
+constexpr int BIG_CAP = PT_WIN / (WAVE_MAX + 1) + 2;   // longer units in a tile
+constexpr uint16_t U_INCOMING = 0xFFFFu;               // list entry for the incoming unit
+
 struct PtShared {
   uint8_t buf[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));     // window bytes
   uint8_t code[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));    // class/identity/doc-start codes
   uint8_t dstart[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));  // 1 where a document starts
-  uint32_t join[2048];        // segments: junction byte pairs of the merges
+  uint32_t join[2048];        // junction byte pairs of the merges
   int16_t run_end[PT_WIN];    // cl100k: window index of the head after a run's head
+  uint16_t ustart[PT_OWN + 2];  // window index of every unit start in the owned bytes
+  uint16_t ucnt[PT_OWN + 2];    // tokens of each unit
+  uint16_t uoff[PT_WIN];      // first output of each unit within the tile
+  uint32_t tok[PT_WIN];       // tokens of unit k at tok[ustart[k] ..]
+  uint32_t rI0[PT_WIN], rI1[PT_WIN], rR0[PT_WIN], rR1[PT_WIN];  // rows engine (long units)
+  uint64_t rsel[PT_WIN / 64 + 1];
+  RowsShared<PT_THREADS / 64> rows;
+  uint16_t med[MED_CAP];
+  uint16_t big[BIG_CAP];
+  uint32_t n_med, n_big;
   uint32_t wave_tot[PT_THREADS / 64];
   uint32_t tile;
-  uint32_t prefix;
+  uint32_t s_prev;            // start of the incoming unit
+  uint32_t inc_cnt;           // its tokens
   uint32_t carry_n;           // cl100k: number-run chars before the tile, mod 3
   uint32_t carry_nlpre;       // cl100k: class before a CR/LF stretch entering the tile
   int64_t doc_lo_idx;         // batch: first document start index touching the window
@@ -173,22 +200,26 @@ struct PtShared {
 
 }  // namespace
 
-// SEG = false: units are the pieces (split-level export).
-// SEG = true:  units are the BPE segments of the pieces: a piece is also cut
-//              at every byte position q whose byte pair (b[q-1], b[q]) is the
-//              junction of no merge; no merge can ever join across such a
-//              position, so each segment is an independent BPE problem.
-template <int PAT, bool BATCH, bool SEG>
-__global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_tiles, const uint32_t* join_bits) {
+// MODE 0: split-level export; the outputs are the byte offsets of the pieces.
+// MODE 1: encoding; the outputs are the (internal) IDs of the units' tokens.
+template <int PAT, bool BATCH, int MODE>
+__global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) {
+  constexpr bool SEG = MODE == 1;
   __shared__ PtShared sh;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int64_t n = w.n;
 
-  if (tid == 0) sh.tile = atomicAdd(&w.ctrl->tile_ticket, 1u);
+  if (tid == 0) {
+    sh.tile = atomicAdd(&w.ctrl->tile_ticket, 1u) - w.ticket_base;
+    sh.n_med = 0;
+    sh.n_big = 0;
+    sh.inc_cnt = 0;
+  }
   __syncthreads();
   const uint32_t t = sh.tile;
+  const uint32_t n_tiles = w.n_tiles;
   if (t >= n_tiles) return;
   const int64_t t0 = (int64_t)t * PT_OWN;
   const int64_t w0 = t0 - PT_HALO;
@@ -234,7 +265,7 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
   }
   if (SEG) {
     // the junction bitmap (8 KB) is read once per block
-    const uint4* src = reinterpret_cast<const uint4*>(join_bits);
+    const uint4* src = reinterpret_cast<const uint4*>(tb.join);
     uint4* dst = reinterpret_cast<uint4*>(sh.join);
     for (int i = tid; i < 512; i += PT_THREADS) dst[i] = src[i];
   }
@@ -315,7 +346,7 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
       *reinterpret_cast<uint2*>(&sh.code[PT_PAD + q0]) = make_uint2(0x07070707u, 0x07070707u);
     }
   }
-  if (bad) __hip_atomic_store(&w.ctrl->error, (uint32_t)(-TT_ERR_INVALID_UTF8), __ATOMIC_RELAXED,
+  if (bad) __hip_atomic_store(&w.ctrl->err, ((uint64_t)w.epoch << 32) | (uint32_t)(-TT_ERR_INVALID_UTF8), __ATOMIC_RELAXED,
                               __HIP_MEMORY_SCOPE_AGENT);
   for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.run_end[q] = -1;
   __syncthreads();
@@ -423,16 +454,16 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
     __syncthreads();
     const int s_last = sh.last_own;
     if (s_last < 0) {
-      if (tid == 0) st_release(&w.tile_summary[t], SUM_READY | SUM_RUNALL);
+      if (tid == 0) st_release(&w.tile_sum[t], ((uint64_t)w.epoch << 32) | SUM_RUNALL);
     } else if (s_last == last_q) {
-      uint32_t sum = SUM_READY | ((seg_cnt(last_st) % 3u) << 1);
+      uint32_t sum = (seg_cnt(last_st) % 3u) << 1;
       if (seg_has(last_st)) {
         int hp = prev(seg_head(last_st));
         sum |= (hp >= 0 ? cls(hp) : (uint32_t)C_NONE) << 3;
       } else {
         sum |= SUM_RUNALL;
       }
-      st_release(&w.tile_summary[t], sum);
+      st_release(&w.tile_sum[t], ((uint64_t)w.epoch << 32) | sum);
     }
     // carries for a run entering the tile from the left
     if (tid == 0) {
@@ -461,9 +492,11 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
           int64_t j = base - lane;
           uint32_t v = 0;
           if (j >= 0) {
+            uint64_t x;
             do {
-              v = ld_acquire(&w.tile_summary[j]);
-            } while (!(v & SUM_READY));
+              x = ld_acquire(&w.tile_sum[j]);
+            } while ((uint32_t)(x >> 32) != w.epoch);
+            v = (uint32_t)x;
           }
           bool stop = j >= 0 && !(v & SUM_RUNALL);
           uint64_t m = __ballot(stop);
@@ -617,103 +650,239 @@ __global__ __launch_bounds__(PT_THREADS) void pretok_kernel(Work w, uint32_t n_t
     }
   }
 
-  // ---- number the pieces: block scan + decoupled look-back ------------------
+  // ---- units: block scan of the start flags --------------------------------
   const uint32_t cnt = __popc(flags);
-  uint32_t inc = wave_incl_scan(cnt, lane, [](uint32_t a, uint32_t b) { return a + b; });
+  const uint32_t inc = wave_incl_scan(cnt, lane, [](uint32_t a, uint32_t b) { return a + b; });
   __syncthreads();
   if (lane == 63) sh.wave_tot[wave] = inc;
   __syncthreads();
-  uint32_t wpre = 0, total = 0;
+  uint32_t wpre = 0, m = 0;
   for (int v = 0; v < PT_THREADS / 64; ++v) {
     if (v < wave) wpre += sh.wave_tot[v];
-    total += sh.wave_tot[v];
+    m += sh.wave_tot[v];
   }
-  const uint32_t texcl = wpre + inc - cnt;
+  const uint32_t texcl = wpre + inc - cnt;  // unit starts before this thread's positions
+  const bool last = t == n_tiles - 1;
 
-  if (wave == 0) {
-    if (lane == 0) st_release(&w.tile_status[t], ((uint64_t)ST_AGG << 32) | total);
-    uint32_t prefix = 0;
-    for (int64_t base = (int64_t)t - 1; base >= 0; base -= 64) {
-      int64_t j = base - lane;
-      uint64_t v = 0;
-      if (j >= 0) {
-        do {
-          v = ld_acquire(&w.tile_status[j]);
-        } while ((v >> 32) == 0);
-      }
-      bool incl = j < 0 || (v >> 32) == ST_INC;
-      uint64_t m = __ballot(incl);
-      int first = m ? (__ffsll((unsigned long long)m) - 1) : 64;
-      uint32_t c = (j >= 0 && lane <= first) ? (uint32_t)v : 0u;
-#pragma unroll
-      for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
-      prefix += c;
-      if (m) break;
+  if (MODE == 0) {
+    // split export: the tile's piece offsets, staged where its bytes begin
+    uint32_t k = texcl;
+#pragma unroll 1
+    for (int j = 0; j < PT_BPT; ++j)
+      if ((flags >> j) & 1u) w.stage[t0 + k++] = (uint32_t)(w0 + qb + j);
+    if (tid == 0) {
+      w.tile_cnt[t] = m;
+      w.tile_base[t] = (uint32_t)t0;
     }
-    if (lane == 0) {
-      st_release(&w.tile_status[t], ((uint64_t)ST_INC << 32) | (prefix + total));
-      sh.prefix = prefix;
+    return;
+  }
+
+  // the tile's last unit start, published before this block waits on anything
+  if (m == 0) {
+    if (tid == 0) st_release(&w.tile_last[t], ((uint64_t)w.epoch << 32) | NO_START);
+  } else if (cnt != 0u && texcl + cnt == m) {
+    st_release(&w.tile_last[t], ((uint64_t)w.epoch << 32) | (uint32_t)(w0 + qb + 31 - __builtin_clz(flags)));
+  }
+  {
+    uint32_t k = texcl;
+#pragma unroll 1
+    for (int j = 0; j < PT_BPT; ++j)
+      if ((flags >> j) & 1u) sh.ustart[k++] = (uint16_t)(qb + j);
+  }
+  if (tid == 0) sh.ustart[m] = (uint16_t)(last ? n - w0 : 0);
+
+  // The units this tile encodes: its own units but the last (whose end lies
+  // in a later tile), all of them in the last tile, and the incoming unit
+  // that ends at its first unit start.
+  const bool has_inc = t > 0 && (m > 0 || last);
+  const uint32_t m_proc = last ? m : (m > 0 ? m - 1 : 0);
+  if (wave == 0 && has_inc) {
+    // the incoming unit starts at the last unit start of the nearest earlier
+    // tile that has one
+    uint32_t found = NO_START;
+    for (int64_t base = (int64_t)t - 1; base >= 0; base -= 64) {
+      const int64_t j = base - lane;
+      uint32_t v = NO_START;
+      if (j >= 0) {
+        uint64_t x;
+        do {
+          x = ld_acquire(&w.tile_last[j]);
+        } while ((uint32_t)(x >> 32) != w.epoch);
+        v = (uint32_t)x;
+      }
+      const uint64_t hit = __ballot(v != NO_START);
+      if (hit) {
+        found = (uint32_t)__shfl((int)v, __ffsll((unsigned long long)hit) - 1, 64);
+        break;
+      }
+    }
+    if (lane == 0) sh.s_prev = found;
+  }
+  __syncthreads();
+  // (only invalid input, whose text starts with a continuation byte, leaves
+  // no unit start before the tile; its output is discarded)
+  const uint32_t s_prev = has_inc && sh.s_prev != NO_START ? sh.s_prev : 0u;
+  const uint32_t e_inc = m > 0 ? (uint32_t)(w0 + sh.ustart[0]) : (uint32_t)n;
+  const uint32_t L_inc = has_inc ? e_inc - s_prev : 0u;
+  auto byte_abs = [&](uint32_t p) -> uint32_t {
+    const int64_t q = (int64_t)p - w0;
+    return (q >= -PT_PAD && q < PT_WIN + 16) ? (uint32_t)sh.buf[PT_PAD + q] : (uint32_t)w.text[p];
+  };
+  auto inc_byte = [&](uint32_t j) -> uint32_t { return byte_abs(s_prev + j); };
+  auto inc_out = [&](uint32_t j, uint32_t id) { w.stage[s_prev + j] = id; };
+
+  // ---- BPE, thread per unit of at most 16 bytes; longer ones are listed ------
+  const uint32_t U = m_proc + (has_inc ? 1u : 0u);
+#pragma unroll 1
+  for (uint32_t u = tid; u < U; u += PT_THREADS) {
+    if (u < m_proc) {
+      const uint32_t a = sh.ustart[u];
+      const uint32_t L = sh.ustart[u + 1] - a;
+      if (L <= (uint32_t)SMALL_MAX) {
+        const uint32_t c = bpe_thread(
+            L, [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb,
+            [&](uint32_t j, uint32_t id) { sh.tok[a + j] = id; });
+        sh.ucnt[u] = (uint16_t)c;
+      } else if (L <= (uint32_t)WAVE_MAX) {
+        sh.med[atomicAdd(&sh.n_med, 1u)] = (uint16_t)u;
+      } else {
+        sh.big[atomicAdd(&sh.n_big, 1u)] = (uint16_t)u;
+      }
+    } else if (L_inc <= (uint32_t)SMALL_MAX) {
+      sh.inc_cnt = bpe_thread(
+          L_inc, [&](int j) -> uint32_t { return inc_byte((uint32_t)j); }, tb, inc_out);
+    } else if (L_inc <= (uint32_t)WAVE_MAX) {
+      sh.med[atomicAdd(&sh.n_med, 1u)] = U_INCOMING;
+    } else {
+      sh.big[atomicAdd(&sh.n_big, 1u)] = U_INCOMING;
     }
   }
   __syncthreads();
-  const uint32_t base = sh.prefix + texcl;
-  uint32_t k = 0;
+
+  // ---- BPE, wave per unit of 17..64 bytes -----------------------------------
+  const uint32_t n_med = sh.n_med;
 #pragma unroll 1
-  for (int j = 0; j < PT_BPT; ++j) {
-    if (flags & (1u << j)) {
-      w.piece_off[base + k] = (uint32_t)(w0 + qb + j);
-      ++k;
+  for (uint32_t i = wave; i < n_med; i += PT_THREADS / 64) {
+    const uint32_t u = sh.med[i];
+    if (u == U_INCOMING) {
+      const uint32_t c = bpe_wave(
+          L_inc, [&](int j) -> uint32_t { return inc_byte((uint32_t)j); }, tb,
+          [&](int j, uint32_t id) { inc_out((uint32_t)j, id); });
+      if (lane == 0) sh.inc_cnt = c;
+    } else {
+      const uint32_t a = sh.ustart[u];
+      const uint32_t L = sh.ustart[u + 1] - a;
+      const uint32_t c = bpe_wave(
+          L, [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb,
+          [&](int j, uint32_t id) { sh.tok[a + j] = id; });
+      if (lane == 0) sh.ucnt[u] = (uint16_t)c;
     }
   }
-  if (t == n_tiles - 1 && tid == 0) {
-    uint32_t P = sh.prefix + total;
-    w.ctrl->n_pieces = P;
-    w.piece_off[P] = (uint32_t)n;
+  __syncthreads();
+
+  // ---- BPE, whole block per longer unit ------------------------------------
+  const uint32_t n_big = sh.n_big;
+#pragma unroll 1
+  for (uint32_t i = 0; i < n_big; ++i) {
+    const uint32_t u = sh.big[i];
+    if (u == U_INCOMING) {
+      uint32_t c;
+      if (L_inc <= (uint32_t)PT_WIN) {
+        c = bpe_rows<PT_THREADS / 64>(L_inc, inc_byte, tb, sh.rI0, sh.rI1, sh.rR0, sh.rR1, sh.rsel, sh.rows,
+                                      inc_out);
+      } else {
+        // longer than a window: rows in global memory at the unit's byte offset
+        uint32_t* sc = w.scratch;
+        const uint64_t nn = (uint64_t)n;
+        c = bpe_rows<PT_THREADS / 64>(L_inc, inc_byte, tb, sc + s_prev, sc + nn + s_prev, sc + 2 * nn + s_prev,
+                                      sc + 3 * nn + s_prev, reinterpret_cast<uint64_t*>(sc + 4 * nn) + s_prev / 32,
+                                      sh.rows, inc_out);
+      }
+      if (tid == 0) sh.inc_cnt = c;
+    } else {
+      const uint32_t a = sh.ustart[u];
+      const uint32_t L = sh.ustart[u + 1] - a;
+      const uint32_t c = bpe_rows<PT_THREADS / 64>(
+          L, [&](uint32_t j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb, sh.rI0, sh.rI1, sh.rR0, sh.rR1,
+          sh.rsel, sh.rows, [&](uint32_t j, uint32_t id) { sh.tok[a + j] = id; });
+      if (tid == 0) sh.ucnt[u] = (uint16_t)c;
+    }
+    __syncthreads();
+  }
+
+  // ---- compaction: the tile's tokens, in order, where its bytes begin -------
+  // (the incoming unit's tokens are already first there)
+  uint32_t csum = 0;
+#pragma unroll 1
+  for (int j = 0; j < PT_BPT; ++j) {
+    const uint32_t k = (uint32_t)(tid * PT_BPT + j);
+    csum += k < m_proc ? sh.ucnt[k] : 0u;
+  }
+  const uint32_t cinc = wave_incl_scan(csum, lane, [](uint32_t a, uint32_t b) { return a + b; });
+  if (lane == 63) sh.wave_tot[wave] = cinc;
+  __syncthreads();
+  uint32_t cpre = 0, ctot = 0;
+  for (int v = 0; v < PT_THREADS / 64; ++v) {
+    if (v < wave) cpre += sh.wave_tot[v];
+    ctot += sh.wave_tot[v];
+  }
+  {
+    uint32_t o = cpre + cinc - csum;
+#pragma unroll 1
+    for (int j = 0; j < PT_BPT; ++j) {
+      const uint32_t k = (uint32_t)(tid * PT_BPT + j);
+      if (k < m_proc) {
+        sh.uoff[k] = (uint16_t)o;
+        o += sh.ucnt[k];
+      }
+    }
+  }
+  __syncthreads();
+  const uint32_t inc_cnt = has_inc ? sh.inc_cnt : 0u;
+  const uint32_t base = has_inc ? s_prev : (m > 0 ? (uint32_t)(w0 + sh.ustart[0]) : 0u);
+  uint32_t* dst = w.stage + base + inc_cnt;
+  uint32_t before = texcl;  // unit starts at or before position q
+#pragma unroll 1
+  for (int j = 0; j < PT_BPT; ++j) {
+    const int q = qb + j;
+    const bool st = (flags >> j) & 1u;
+    before += st ? 1u : 0u;
+    if (before == 0u || before - 1u >= m_proc) continue;
+    const uint32_t k = before - 1u;
+    const uint32_t o = (uint32_t)q - sh.ustart[k];
+    if (o < sh.ucnt[k]) dst[sh.uoff[k] + o] = sh.tok[q];
+    if (BATCH && st && sh.dstart[PT_PAD + q]) {
+      w.unit_tile[w0 + q] = t;
+      w.unit_pos[w0 + q] = inc_cnt + sh.uoff[k];
+    }
+  }
+  if (tid == 0) {
+    if (BATCH && has_inc) {
+      w.unit_tile[s_prev] = t;
+      w.unit_pos[s_prev] = 0;
+    }
+    w.tile_cnt[t] = inc_cnt + ctot;
+    w.tile_base[t] = base;
   }
 }
 
-hipError_t launch_pretok(const Work& w, int pattern, uint32_t n_tiles, const uint32_t* join_bits, bool seg,
-                         hipStream_t s) {
-  dim3 grid(n_tiles), block(PT_THREADS);
+hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode, hipStream_t s) {
+  dim3 grid(w.n_tiles), block(PT_THREADS);
   const bool batch = w.doc_off != nullptr;
-  const int variant = (pattern == TT_PATTERN_GPT2 ? 0 : 4) + (batch ? 2 : 0) + (seg ? 1 : 0);
+  const int variant = (pattern == TT_PATTERN_GPT2 ? 0 : 4) + (batch ? 2 : 0) + (mode ? 1 : 0);
   switch (variant) {
-#define TT_PRETOK_CASE(V, P, B, S) \
-  case V: hipLaunchKernelGGL((pretok_kernel<P, B, S>), grid, block, 0, s, w, n_tiles, join_bits); break;
-    TT_PRETOK_CASE(0, TT_PATTERN_GPT2, false, false)
-    TT_PRETOK_CASE(1, TT_PATTERN_GPT2, false, true)
-    TT_PRETOK_CASE(2, TT_PATTERN_GPT2, true, false)
-    TT_PRETOK_CASE(3, TT_PATTERN_GPT2, true, true)
-    TT_PRETOK_CASE(4, TT_PATTERN_CL100K, false, false)
-    TT_PRETOK_CASE(5, TT_PATTERN_CL100K, false, true)
-    TT_PRETOK_CASE(6, TT_PATTERN_CL100K, true, false)
-    TT_PRETOK_CASE(7, TT_PATTERN_CL100K, true, true)
-#undef TT_PRETOK_CASE
+#define TT_TILE_CASE(V, P, B, M) \
+  case V: hipLaunchKernelGGL((tile_kernel<P, B, M>), grid, block, 0, s, w, tb); break;
+    TT_TILE_CASE(0, TT_PATTERN_GPT2, false, 0)
+    TT_TILE_CASE(1, TT_PATTERN_GPT2, false, 1)
+    TT_TILE_CASE(2, TT_PATTERN_GPT2, true, 0)
+    TT_TILE_CASE(3, TT_PATTERN_GPT2, true, 1)
+    TT_TILE_CASE(4, TT_PATTERN_CL100K, false, 0)
+    TT_TILE_CASE(5, TT_PATTERN_CL100K, false, 1)
+    TT_TILE_CASE(6, TT_PATTERN_CL100K, true, 0)
+    TT_TILE_CASE(7, TT_PATTERN_CL100K, true, 1)
+#undef TT_TILE_CASE
   }
-  return hipGetLastError();
-}
-
-// Zero the control block and the look-back words of one call.
-__global__ void reset_kernel(Work w, uint32_t n_pt, uint32_t n_ct) {
-  uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  uint32_t stride = gridDim.x * blockDim.x;
-  if (i == 0) {
-    Ctrl z = {};
-    *w.ctrl = z;
-  }
-  for (uint32_t k = i; k < n_pt; k += stride) {
-    w.tile_status[k] = 0;
-    w.tile_summary[k] = 0;
-  }
-  for (uint32_t k = i; k < n_ct; k += stride) w.ctile_status[k] = 0;
-}
-
-hipError_t launch_reset(const Work& w, uint32_t n_pt, uint32_t n_ct, hipStream_t s) {
-  uint32_t m = n_pt > n_ct ? n_pt : n_ct;
-  uint32_t blocks = (m + 255) / 256;
-  if (blocks < 1) blocks = 1;
-  if (blocks > 1024) blocks = 1024;
-  hipLaunchKernelGGL(reset_kernel, dim3(blocks), dim3(256), 0, s, w, n_pt, n_ct);
   return hipGetLastError();
 }
 
