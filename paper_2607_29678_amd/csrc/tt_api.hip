@@ -8,6 +8,7 @@
 // The host synchronises twice per blocking call: once for the output length,
 // once for the IDs.
 #include <algorithm>
+#include <cstdint>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -50,8 +51,9 @@ struct tt_tokenizer {
   int32_t vocab_size = 0;
   int device = 0;
   int profile = 0;  // record stage events on every call
-  uint64_t* d_slots = nullptr;
-  uint32_t mask = 0;
+  u64x2* d_slots = nullptr;    // cuckoo buckets
+  uint32_t shift = 0;          // 32 - log2(bucket count)
+  uint32_t* d_pair0 = nullptr;  // [65536] byte-pair ranks
   int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
   uint32_t n_ids = 0;
   uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
@@ -105,7 +107,7 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
   size_t o_stage = take(4 * N);
   size_t o_utile = take(4 * N);
   size_t o_upos = take(4 * N);
-  size_t o_scr = take(4 * 4 * N + 8 * (N / 32 + 8));
+  size_t o_scr = take(4 * 4 * N + 8 * (N / 16 + 8));
   size_t o_in = take(N + 64);
   size_t o_out = take(4 * N);
   size_t o_len = take(8);
@@ -196,7 +198,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_ids = out_ids;
   w.out_len = out_len;
   w.out_doc_off = out_docs;
-  DevTables tb{h->d_slots, h->mask, h->d_join, h->d_ext, h->n_ids};
+  DevTables tb{h->d_slots, h->shift, h->d_pair0, h->d_join, h->d_ext, h->n_ids};
   const bool prof = h->profile != 0;
   s->n_ev = 0;
   auto mark = [&]() -> bool {
@@ -281,15 +283,52 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   for (int b = 0; b < 256; ++b) ext[b] = byte_id[b];
   for (int32_t r = 0; r < n_merges; ++r) ext[256 + r] = merges[r].result;
 
-  // open-addressing table, load factor <= 1/2
-  uint32_t cap = 16;
-  while (cap < 2u * (uint32_t)n_merges) cap <<= 1;
-  std::vector<uint64_t> slots(cap, SLOT_EMPTY);
+  // byte-pair ranks, and the two-choice cuckoo table of all pairs (two slots
+  // per bucket, load <= 1/2; the table doubles if an insertion cannot be placed)
+  std::vector<uint32_t> pair0(65536, RANK_INF);
   for (int32_t r = 0; r < n_merges; ++r) {
-    const uint32_t a = (uint32_t)internal[merges[r].left], b = (uint32_t)internal[merges[r].right];
-    uint32_t i = pair_hash(a, b) & (cap - 1);
-    while (slots[i] != SLOT_EMPTY) i = (i + 1) & (cap - 1);
-    slots[i] = slot_key(a, b) | ((uint64_t)r << (2 * ID_BITS));
+    const int32_t a = internal[merges[r].left], b = internal[merges[r].right];
+    if (a < 256 && b < 256) pair0[((uint32_t)a << 8) | (uint32_t)b] = (uint32_t)r;
+  }
+  uint32_t nb = 16, bits = 4;
+  while (nb < (uint32_t)n_merges) {
+    nb <<= 1;
+    ++bits;
+  }
+  std::vector<uint64_t> slots;
+  for (;;) {
+    slots.assign(2 * (size_t)nb, SLOT_EMPTY);
+    uint64_t rng = 0x9E3779B97F4A7C15ull;
+    bool ok = true;
+    for (int32_t r = 0; r < n_merges && ok; ++r) {
+      uint64_t item = slot_key((uint32_t)internal[merges[r].left], (uint32_t)internal[merges[r].right]) |
+                      ((uint64_t)r << (2 * ID_BITS));
+      ok = false;
+      for (int kick = 0; kick < 1000; ++kick) {
+        const uint32_t a = (uint32_t)(item & ID_LIMIT), b = (uint32_t)((item >> ID_BITS) & ID_LIMIT);
+        const uint32_t b1 = pair_hash(a, b, 32 - bits), b2 = pair_hash2(a, b, 32 - bits);
+        size_t free_at = SIZE_MAX;
+        for (size_t c : {2 * (size_t)b1, 2 * (size_t)b1 + 1, 2 * (size_t)b2, 2 * (size_t)b2 + 1})
+          if (slots[c] == SLOT_EMPTY) {
+            free_at = c;
+            break;
+          }
+        if (free_at != SIZE_MAX) {
+          slots[free_at] = item;
+          ok = true;
+          break;
+        }
+        rng ^= rng << 13;
+        rng ^= rng >> 7;
+        rng ^= rng << 17;
+        const size_t victim = 2 * (size_t)((rng & 2) ? b1 : b2) + (rng & 1);
+        std::swap(item, slots[victim]);
+      }
+    }
+    if (ok) break;
+    nb <<= 1;
+    ++bits;
+    if (nb > (1u << 28)) return TT_ERR_OOM;
   }
 
   // junction byte pairs: the first merge that ever joins across a byte
@@ -308,19 +347,21 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   h->pattern = pattern_id;
   h->n_merges = n_merges;
   h->vocab_size = vocab_size;
-  h->mask = cap - 1;
+  h->shift = 32 - bits;
   h->n_ids = n_ids;
   if (hipGetDevice(&h->device) != hipSuccess) {
     delete h;
     return TT_ERR_HIP;
   }
-  if (hipMalloc(reinterpret_cast<void**>(&h->d_slots), sizeof(uint64_t) * cap) != hipSuccess ||
+  if (hipMalloc(reinterpret_cast<void**>(&h->d_slots), 16 * (size_t)nb) != hipSuccess ||
+      hipMalloc(reinterpret_cast<void**>(&h->d_pair0), sizeof(uint32_t) * 65536) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_ext), sizeof(int32_t) * n_ids) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_join), sizeof(uint32_t) * 2048) != hipSuccess) {
     tt_destroy(h);
     return TT_ERR_OOM;
   }
-  if (hipMemcpy(h->d_slots, slots.data(), sizeof(uint64_t) * cap, hipMemcpyHostToDevice) != hipSuccess ||
+  if (hipMemcpy(h->d_slots, slots.data(), 16 * (size_t)nb, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(h->d_pair0, pair0.data(), sizeof(uint32_t) * 65536, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_ext, ext.data(), sizeof(int32_t) * n_ids, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_join, join.data(), sizeof(uint32_t) * 2048, hipMemcpyHostToDevice) != hipSuccess) {
     tt_destroy(h);
@@ -337,6 +378,7 @@ void tt_destroy(tt_tokenizer* h) {
   for (auto& kv : h->ws) free_ws(kv.second);
   if (h->d_slots) (void)hipFree(h->d_slots);
   if (h->d_ext) (void)hipFree(h->d_ext);
+  if (h->d_pair0) (void)hipFree(h->d_pair0);
   if (h->d_join) (void)hipFree(h->d_join);
   delete h;
 }

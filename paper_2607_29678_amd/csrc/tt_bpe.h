@@ -60,42 +60,28 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
 // mask instead of shifting the tail.  A pair's rank is kept as
 // (rank << 4) | position so that one unsigned minimum finds the lowest rank
 // and, among equal ranks (the same pair), the leftmost occurrence.  The chain
-// is two probe round trips for the initial pairs and one per merge (its two
-// neighbour probes overlap).
-//   byte(j)      byte j of the unit, j < L
+// is one round trip for the initial byte pairs (all loads in flight at once)
+// and one per merge (its two neighbour lookups overlap).
+//   byte(j)      byte j of the unit for j < L; called for every j < 16 and
+//                must be safe to call there (the value is then ignored)
 //   out(j, id)   stores output token j
 // Returns the number of tokens.
 // ---------------------------------------------------------------------------
 template <class ByteF, class OutF>
 __device__ __forceinline__ uint32_t bpe_thread(uint32_t L, ByteF byte, const DevTables& tb, OutF out) {
   constexpr int S = SMALL_MAX;
-  const uint64_t* __restrict__ tab = tb.slots;
-  const uint32_t mask = tb.mask;
+  const u64x2* __restrict__ tab = tb.slots;
+  const uint32_t shift = tb.shift;
   uint32_t id[S], rk[S];
 #pragma unroll
-  for (int j = 0; j < S; ++j) id[j] = (uint32_t)j < L ? byte(j) : 0u;
+  for (int j = 0; j < S; ++j) id[j] = byte(j);  // bytes past the unit are read but not used
+  // every initial rank load is issued before any is used (no branches)
 #pragma unroll
-  for (int g = 0; g < S; g += 8) {
-    uint32_t si[8];
-    uint64_t sv[8];
+  for (int j = 0; j < S - 1; ++j) rk[j] = tb.pair0[((id[j] & 255u) << 8) | (id[j + 1] & 255u)];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int j = g + k;
-      si[k] = 0;
-      sv[k] = SLOT_EMPTY;
-      if (j + 1 < S && (uint32_t)(j + 1) < L) {
-        si[k] = probe_start(mask, id[j], id[j + 1]);
-        sv[k] = tab[si[k]];
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int j = g + k;
-      uint32_t r = RANK_INF;
-      if (j + 1 < S && (uint32_t)(j + 1) < L) r = probe_finish(tab, mask, si[k], sv[k], id[j], id[j + 1]);
-      rk[j] = r == RANK_INF ? RANK_INF : ((r << 4) | (uint32_t)j);
-    }
-  }
+  for (int j = 0; j < S - 1; ++j)
+    rk[j] = ((uint32_t)(j + 1) < L && rk[j] != RANK_INF) ? ((rk[j] << 4) | (uint32_t)j) : RANK_INF;
+  rk[S - 1] = RANK_INF;
   uint32_t alive = (1u << L) - 1u;  // L <= 16
   for (;;) {
     uint32_t best = RANK_INF;
@@ -118,18 +104,12 @@ __device__ __forceinline__ uint32_t bpe_thread(uint32_t L, ByteF byte, const Dev
       right = j == r_i ? id[j] : right;
       left = j == l_i ? id[j] : left;
     }
-    uint32_t ir = 0, il = 0;
-    uint64_t sr = SLOT_EMPTY, sl = SLOT_EMPTY;
-    if (hr) {
-      ir = probe_start(mask, nid, right);
-      sr = tab[ir];
-    }
-    if (hl) {
-      il = probe_start(mask, left, nid);
-      sl = tab[il];
-    }
-    const uint32_t rr = hr ? probe_finish(tab, mask, ir, sr, nid, right) : RANK_INF;
-    const uint32_t rl = hl ? probe_finish(tab, mask, il, sl, left, nid) : RANK_INF;
+    // both lookups are issued unconditionally (a missing neighbour looks up a
+    // harmless pair) so that their four loads are in flight together
+    const ProbeIssued pr = probe_issue(tab, shift, nid, right);
+    const ProbeIssued pl = probe_issue(tab, shift, left, nid);
+    const uint32_t rr = hr ? probe_finish(pr, nid, right) : RANK_INF;
+    const uint32_t rl = hl ? probe_finish(pl, left, nid) : RANK_INF;
 #pragma unroll
     for (int j = 0; j < S; ++j) {
       if (j == k) {
@@ -160,7 +140,7 @@ __device__ __forceinline__ uint32_t bpe_wave(uint32_t L, ByteF byte, const DevTa
   uint32_t n = L;  // <= 64
   uint32_t id = (uint32_t)lane < n ? byte(lane) : 0u;
   uint32_t idn = (uint32_t)__shfl_down((int)id, 1, 64);
-  uint32_t rk = (uint32_t)lane + 1u < n ? probe_rank(tb.slots, tb.mask, id, idn) : RANK_INF;
+  uint32_t rk = (uint32_t)lane + 1u < n ? tb.pair0[(id << 8) | idn] : RANK_INF;
   for (;;) {
     const uint32_t m = wave_min_u32(rk);
     if (m == RANK_INF) break;
@@ -181,7 +161,7 @@ __device__ __forceinline__ uint32_t bpe_wave(uint32_t L, ByteF byte, const DevTa
     rk = RANK_INF;
     if ((uint32_t)lane < n) {
       rk = r2;
-      if (r2 == RANK_DIRTY) rk = (uint32_t)lane + 1u < n ? probe_rank(tb.slots, tb.mask, id, idn) : RANK_INF;
+      if (r2 == RANK_DIRTY) rk = (uint32_t)lane + 1u < n ? probe_rank(tb.slots, tb.shift, id, idn) : RANK_INF;
     }
   }
   if ((uint32_t)lane < n) out(lane, id);
@@ -216,7 +196,7 @@ __device__ uint32_t bpe_rows(uint32_t L, ByteF byte, const DevTables& tb, uint32
 
   for (uint32_t i = tid; i < n; i += NT) I0[i] = byte(i);
   __syncthreads();
-  for (uint32_t i = tid; i < n; i += NT) R0[i] = i + 1 < n ? probe_rank(tb.slots, tb.mask, I0[i], I0[i + 1]) : RANK_INF;
+  for (uint32_t i = tid; i < n; i += NT) R0[i] = i + 1 < n ? tb.pair0[(I0[i] << 8) | I0[i + 1]] : RANK_INF;
   __syncthreads();
 
   for (;;) {
@@ -316,7 +296,7 @@ __device__ uint32_t bpe_rows(uint32_t L, ByteF byte, const DevTables& tb, uint32
     n = n2;
     // 4. ranks of the pairs next to the merges
     for (uint32_t i = tid; i < n; i += NT) {
-      if (R2[i] == RANK_DIRTY) R2[i] = i + 1 < n ? probe_rank(tb.slots, tb.mask, I2[i], I2[i + 1]) : RANK_INF;
+      if (R2[i] == RANK_DIRTY) R2[i] = i + 1 < n ? probe_rank(tb.slots, tb.shift, I2[i], I2[i + 1]) : RANK_INF;
     }
     __syncthreads();
     cur ^= 1;

@@ -54,42 +54,48 @@ __host__ __device__ inline uint64_t slot_key(uint32_t a, uint32_t b) {
   return (uint64_t)a | ((uint64_t)b << ID_BITS);
 }
 
-__host__ __device__ inline uint32_t pair_hash(uint32_t a, uint32_t b) {
-  uint32_t h = a * 0x9E3779B1u ^ (b + 0x7F4A7C15u) * 0x85EBCA77u;
-  h ^= h >> 15;
-  h *= 0x2C1B3C6Du;
-  h ^= h >> 12;
-  h *= 0x297A2D39u;
-  h ^= h >> 15;
-  return h;
+// Two bucket hashes of a pair (multiply-shift; `shift` = 32 - log2(buckets)).
+__host__ __device__ inline uint32_t pair_hash(uint32_t a, uint32_t b, uint32_t shift) {
+  return ((a * 0x9E3779B1u + b) * 0x85EBCA77u) >> shift;
+}
+__host__ __device__ inline uint32_t pair_hash2(uint32_t a, uint32_t b, uint32_t shift) {
+  return (((b * 0xC2B2AE3Du) ^ (a + 0x165667B1u)) * 0x27D4EB2Fu) >> shift;
 }
 
-// Open-addressing lookup in two halves so that several first loads can be in
-// flight before any comparison: probe_start gives the first slot index,
-// probe_finish walks on from the loaded slot (linear probing; load <= 1/2).
-__device__ __forceinline__ uint32_t probe_start(uint32_t mask, uint32_t a, uint32_t b) {
-  return pair_hash(a, b) & mask;
+// The merge table is a two-choice cuckoo table of 16-byte buckets holding
+// two slots each: a pair lives in one of the two buckets its hashes name, so
+// every lookup is exactly two independent 16-byte loads (one memory round
+// trip, no probe chain).  Pairs of two bytes, the only pairs before any
+// merge, also have a direct 64 K-entry rank table.
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+
+struct ProbeIssued {
+  u64x2 x, y;
+};
+__device__ __forceinline__ ProbeIssued probe_issue(const u64x2* __restrict__ tab, uint32_t shift, uint32_t a,
+                                                   uint32_t b) {
+  return ProbeIssued{tab[pair_hash(a, b, shift)], tab[pair_hash2(a, b, shift)]};
 }
-__device__ __forceinline__ uint32_t probe_finish(const uint64_t* __restrict__ tab, uint32_t mask, uint32_t i,
-                                                 uint64_t s, uint32_t a, uint32_t b) {
+__device__ __forceinline__ uint32_t probe_finish(const ProbeIssued& p, uint32_t a, uint32_t b) {
   const uint64_t key = slot_key(a, b);
-  while ((s & KEY_MASK) != key && s != SLOT_EMPTY) {
-    i = (i + 1u) & mask;
-    s = tab[i];
-  }
-  return (s & KEY_MASK) == key ? (uint32_t)(s >> (2 * ID_BITS)) : RANK_INF;
+  uint64_t hit = SLOT_EMPTY;
+  hit = (p.x.x & KEY_MASK) == key ? p.x.x : hit;
+  hit = (p.x.y & KEY_MASK) == key ? p.x.y : hit;
+  hit = (p.y.x & KEY_MASK) == key ? p.y.x : hit;
+  hit = (p.y.y & KEY_MASK) == key ? p.y.y : hit;
+  return hit == SLOT_EMPTY ? RANK_INF : (uint32_t)(hit >> (2 * ID_BITS));
 }
 // Rank of the pair (a, b), or RANK_INF if no merge joins it.
-__device__ __forceinline__ uint32_t probe_rank(const uint64_t* __restrict__ tab, uint32_t mask, uint32_t a,
+__device__ __forceinline__ uint32_t probe_rank(const u64x2* __restrict__ tab, uint32_t shift, uint32_t a,
                                                uint32_t b) {
-  const uint32_t i = probe_start(mask, a, b);
-  return probe_finish(tab, mask, i, tab[i], a, b);
+  return probe_finish(probe_issue(tab, shift, a, b), a, b);
 }
 
 // Everything a kernel needs to know about a tokenizer handle.
 struct DevTables {
-  const uint64_t* slots;    // merge table: key (left | right << 21), rank in bits 42..63
-  uint32_t mask;            // slot count - 1
+  const u64x2* slots;       // cuckoo buckets of two slots: key (left | right << 21), rank in bits 42..63
+  uint32_t shift;           // 32 - log2(bucket count)
+  const uint32_t* pair0;    // [65536] rank of the byte pair (x << 8 | y), or RANK_INF
   const uint32_t* join;     // [2048] bit (x << 8 | y): some merge joins a token ending
                             // in byte x to a token starting with byte y
   const int32_t* ext_id;    // [n_ids] caller's ID of every internal ID
@@ -128,15 +134,15 @@ struct Work {
   uint32_t* stage;          // [n] staged outputs: tile t's at stage[tile_base[t] ..]
   uint32_t* unit_tile;      // batch: [n] processing tile of the unit starting at a byte
   uint32_t* unit_pos;       // batch: [n] its first output within that tile's outputs
-  uint32_t* scratch;        // rows of units longer than a tile window: 4 * n words + selection masks
+  uint32_t* scratch;        // rows of units longer than 64 bytes: 4 * n words, then n / 16 + 8 masks
   int32_t* out_ids;         // output (caller IDs, or piece offsets for the split export)
   int64_t* out_len;         // output length, or -error
   int64_t* out_doc_off;     // batch: n_docs+1 output offsets (device)
 };
 
 // Tiles and geometry --------------------------------------------------------
-constexpr int PT_THREADS = 1024;                  // tile block
-constexpr int PT_BPT = 2;                          // bytes per thread
+constexpr int PT_THREADS = 512;                   // tile block
+constexpr int PT_BPT = 4;                          // bytes per thread
 constexpr int PT_WIN = PT_THREADS * PT_BPT;        // window bytes in LDS
 constexpr int PT_HALO = 32;                        // context bytes each side
 constexpr int PT_OWN = PT_WIN - 2 * PT_HALO;       // bytes a tile decides

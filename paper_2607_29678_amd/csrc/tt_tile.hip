@@ -51,11 +51,14 @@ namespace {
 // bits 1..2 its character count mod 3, bits 3..5 the class before it
 constexpr uint32_t SUM_RUNALL = 1u;
 
-__device__ __forceinline__ uint64_t ld_acquire(const uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+// Words published for later blocks are self-contained values (the consumer
+// reads nothing else the producer wrote), so relaxed device-scope atomics are
+// enough: they are coherent across the chip without ordering other accesses.
+__device__ __forceinline__ uint64_t ld_word(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_release(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void st_word(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // 2-bit class of a non-ASCII code point from the probed table.
@@ -172,22 +175,33 @@ constexpr int MED_CAP = PT_WIN / (SMALL_MAX + 1) + 2;  // units of 17..64 bytes 
 constexpr int BIG_CAP = PT_WIN / (WAVE_MAX + 1) + 2;   // longer units in a tile
 constexpr uint16_t U_INCOMING = 0xFFFFu;               // list entry for the incoming unit
 
+// LDS of the classification phase and of the BPE phase share one region:
+// nothing of the first is read after the unit scan, nothing of the second is
+// written before it.
+union PhaseMem {
+  struct {
+    uint32_t join[2048];      // junction byte pairs of the merges
+    uint8_t code[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));  // class/identity/doc-start codes
+    int16_t run_end[PT_WIN];  // cl100k: window index of the head after a run's head
+  } a;
+  struct {
+    uint32_t tok[PT_WIN];     // tokens of unit k at tok[ustart[k] ..]
+    uint16_t uoff[PT_WIN];    // first output of each unit within the tile
+    uint16_t small[PT_OWN + 2];  // units of 3..16 bytes, sorted by length
+  } b;
+};
+
 struct PtShared {
   uint8_t buf[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));     // window bytes
-  uint8_t code[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));    // class/identity/doc-start codes
   uint8_t dstart[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));  // 1 where a document starts
-  uint32_t join[2048];        // junction byte pairs of the merges
-  int16_t run_end[PT_WIN];    // cl100k: window index of the head after a run's head
+  PhaseMem ph;
   uint16_t ustart[PT_OWN + 2];  // window index of every unit start in the owned bytes
   uint16_t ucnt[PT_OWN + 2];    // tokens of each unit
-  uint16_t uoff[PT_WIN];      // first output of each unit within the tile
-  uint32_t tok[PT_WIN];       // tokens of unit k at tok[ustart[k] ..]
-  uint32_t rI0[PT_WIN], rI1[PT_WIN], rR0[PT_WIN], rR1[PT_WIN];  // rows engine (long units)
-  uint64_t rsel[PT_WIN / 64 + 1];
   RowsShared<PT_THREADS / 64> rows;
   uint16_t med[MED_CAP];
   uint16_t big[BIG_CAP];
-  uint32_t n_med, n_big;
+  uint32_t hist[SMALL_MAX + 1];  // small units per length, then where each length starts
+  uint32_t n_small, n_med, n_big;
   uint32_t wave_tot[PT_THREADS / 64];
   uint32_t tile;
   uint32_t s_prev;            // start of the incoming unit
@@ -203,7 +217,7 @@ struct PtShared {
 // MODE 0: split-level export; the outputs are the byte offsets of the pieces.
 // MODE 1: encoding; the outputs are the (internal) IDs of the units' tokens.
 template <int PAT, bool BATCH, int MODE>
-__global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) {
+__global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void tile_kernel(Work w, DevTables tb) {
   constexpr bool SEG = MODE == 1;
   __shared__ PtShared sh;
   const int tid = threadIdx.x;
@@ -211,6 +225,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
   const int wave = tid >> 6;
   const int64_t n = w.n;
 
+  if (tid <= SMALL_MAX) sh.hist[tid] = 0;
   if (tid == 0) {
     sh.tile = atomicAdd(&w.ctrl->tile_ticket, 1u) - w.ticket_base;
     sh.n_med = 0;
@@ -266,7 +281,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
   if (SEG) {
     // the junction bitmap (8 KB) is read once per block
     const uint4* src = reinterpret_cast<const uint4*>(tb.join);
-    uint4* dst = reinterpret_cast<uint4*>(sh.join);
+    uint4* dst = reinterpret_cast<uint4*>(sh.ph.a.join);
     for (int i = tid; i < 512; i += PT_THREADS) dst[i] = src[i];
   }
   if (BATCH) {
@@ -339,20 +354,20 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
           }
         }
       }
-      sh.code[PT_PAD + q] = (uint8_t)(code | ds);
+      sh.ph.a.code[PT_PAD + q] = (uint8_t)(code | ds);
     }
     if (tid < 3) {  // positions outside [0, PT_WIN) carry no character for the rules
       const int q0 = tid == 0 ? -8 : PT_WIN + 8 * (tid - 1);
-      *reinterpret_cast<uint2*>(&sh.code[PT_PAD + q0]) = make_uint2(0x07070707u, 0x07070707u);
+      *reinterpret_cast<uint2*>(&sh.ph.a.code[PT_PAD + q0]) = make_uint2(0x07070707u, 0x07070707u);
     }
   }
   if (bad) __hip_atomic_store(&w.ctrl->err, ((uint64_t)w.epoch << 32) | (uint32_t)(-TT_ERR_INVALID_UTF8), __ATOMIC_RELAXED,
                               __HIP_MEMORY_SCOPE_AGENT);
-  for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.run_end[q] = -1;
+  for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.ph.a.run_end[q] = -1;
   __syncthreads();
 
   // ---- neighbour helpers (window indices; -1 = none) ----------------------
-  auto code_at = [&](int q) -> uint32_t { return sh.code[PT_PAD + q]; };
+  auto code_at = [&](int q) -> uint32_t { return sh.ph.a.code[PT_PAD + q]; };
   auto cls = [&](int q) -> uint32_t { return code_cls(code_at(q)); };
   auto ident = [&](int q) -> uint32_t { return code_id(code_at(q)); };
   auto prev = [&](int q) -> int {
@@ -438,7 +453,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
       for (int j = 0; j < PT_BPT; ++j) {
         const int q = qb + j;
         const uint32_t e = elem_at(q);
-        if ((e & 0x80000000u) && seg_has(st)) sh.run_end[seg_head(st)] = (int16_t)q;
+        if ((e & 0x80000000u) && seg_has(st)) sh.ph.a.run_end[seg_head(st)] = (int16_t)q;
         st = seg_combine(st, e);
         if (q >= PT_HALO && q < own_end && e != 0u) {
           last_q = q;
@@ -454,7 +469,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
     __syncthreads();
     const int s_last = sh.last_own;
     if (s_last < 0) {
-      if (tid == 0) st_release(&w.tile_sum[t], ((uint64_t)w.epoch << 32) | SUM_RUNALL);
+      if (tid == 0) st_word(&w.tile_sum[t], ((uint64_t)w.epoch << 32) | SUM_RUNALL);
     } else if (s_last == last_q) {
       uint32_t sum = (seg_cnt(last_st) % 3u) << 1;
       if (seg_has(last_st)) {
@@ -463,7 +478,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
       } else {
         sum |= SUM_RUNALL;
       }
-      st_release(&w.tile_sum[t], ((uint64_t)w.epoch << 32) | sum);
+      st_word(&w.tile_sum[t], ((uint64_t)w.epoch << 32) | sum);
     }
     // carries for a run entering the tile from the left
     if (tid == 0) {
@@ -494,7 +509,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
           if (j >= 0) {
             uint64_t x;
             do {
-              x = ld_acquire(&w.tile_sum[j]);
+              x = ld_word(&w.tile_sum[j]);
             } while ((uint32_t)(x >> 32) != w.epoch);
             v = (uint32_t)x;
           }
@@ -522,7 +537,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
   // rule 2 of cl100k: is the whitespace stretch starting at q (after CR/LF)
   // the last stretch of its whitespace run?
   auto ws_stretch_is_last = [&](int q) -> bool {
-    int e = sh.run_end[q];
+    int e = sh.ph.a.run_end[q];
     if (e >= 0) return (code_at(e) & CODE_DOCSTART) || cls(e) != C_NL;
     if (w0 + PT_WIN >= n) return true;  // the run reaches the end of the text
     // the stretch continues past the window: read on in global memory
@@ -646,7 +661,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
       if (sh.dstart[PT_PAD + q] || !inside(q - 1)) continue;  // piece starts are already flagged
       // q is not a piece start, so q - 1 lies in the same piece
       const uint32_t key = ((uint32_t)sh.buf[PT_PAD + q - 1] << 8) | sh.buf[PT_PAD + q];
-      if (!((sh.join[key >> 5] >> (key & 31u)) & 1u)) flags |= 1u << j;
+      if (!((sh.ph.a.join[key >> 5] >> (key & 31u)) & 1u)) flags |= 1u << j;
     }
   }
 
@@ -679,9 +694,9 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
 
   // the tile's last unit start, published before this block waits on anything
   if (m == 0) {
-    if (tid == 0) st_release(&w.tile_last[t], ((uint64_t)w.epoch << 32) | NO_START);
+    if (tid == 0) st_word(&w.tile_last[t], ((uint64_t)w.epoch << 32) | NO_START);
   } else if (cnt != 0u && texcl + cnt == m) {
-    st_release(&w.tile_last[t], ((uint64_t)w.epoch << 32) | (uint32_t)(w0 + qb + 31 - __builtin_clz(flags)));
+    st_word(&w.tile_last[t], ((uint64_t)w.epoch << 32) | (uint32_t)(w0 + qb + 31 - __builtin_clz(flags)));
   }
   {
     uint32_t k = texcl;
@@ -706,7 +721,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
       if (j >= 0) {
         uint64_t x;
         do {
-          x = ld_acquire(&w.tile_last[j]);
+          x = ld_word(&w.tile_last[j]);
         } while ((uint32_t)(x >> 32) != w.epoch);
         v = (uint32_t)x;
       }
@@ -731,81 +746,146 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
   auto inc_byte = [&](uint32_t j) -> uint32_t { return byte_abs(s_prev + j); };
   auto inc_out = [&](uint32_t j, uint32_t id) { w.stage[s_prev + j] = id; };
 
-  // ---- BPE, thread per unit of at most 16 bytes; longer ones are listed ------
+  // ---- BPE dispatch ---------------------------------------------------------
+  // Units of one or two bytes are finished here.  Units of 3..16 bytes go to
+  // one thread each, counting-sorted by length, so that the threads of a wave
+  // hold units of similar length (a wave runs as long as its longest unit).
+  // Units of 17..64 bytes go to one wave each, first to the waves that have no
+  // thread work, with no block barrier between the two, and longer units to
+  // the whole block.  The incoming unit is listed last.
+  constexpr int UPT = (PT_OWN + 1 + PT_THREADS - 1) / PT_THREADS;  // units per thread
   const uint32_t U = m_proc + (has_inc ? 1u : 0u);
-#pragma unroll 1
-  for (uint32_t u = tid; u < U; u += PT_THREADS) {
-    if (u < m_proc) {
-      const uint32_t a = sh.ustart[u];
-      const uint32_t L = sh.ustart[u + 1] - a;
-      if (L <= (uint32_t)SMALL_MAX) {
-        const uint32_t c = bpe_thread(
-            L, [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb,
-            [&](uint32_t j, uint32_t id) { sh.tok[a + j] = id; });
-        sh.ucnt[u] = (uint16_t)c;
-      } else if (L <= (uint32_t)WAVE_MAX) {
-        sh.med[atomicAdd(&sh.n_med, 1u)] = (uint16_t)u;
-      } else {
-        sh.big[atomicAdd(&sh.n_big, 1u)] = (uint16_t)u;
+  uint32_t my_slot[UPT], my_len[UPT];
+#pragma unroll
+  for (int r = 0; r < UPT; ++r) {
+    my_len[r] = 0;
+    my_slot[r] = 0;
+    const uint32_t u = (uint32_t)(tid + r * PT_THREADS);
+    if (u >= U) continue;
+    const bool inc_u = u == m_proc;
+    const uint32_t a = inc_u ? 0u : sh.ustart[u];
+    const uint32_t L = inc_u ? L_inc : sh.ustart[u + 1] - a;
+    if (L <= 2u) {
+      const uint32_t b0 = inc_u ? inc_byte(0) : sh.buf[PT_PAD + a];
+      uint32_t c = 1, t0 = b0, t1 = 0;
+      if (L == 2u) {
+        const uint32_t b1 = inc_u ? inc_byte(1) : sh.buf[PT_PAD + a + 1];
+        const uint32_t r2 = tb.pair0[(b0 << 8) | b1];
+        if (r2 != RANK_INF) {
+          t0 = 256u + r2;
+        } else {
+          c = 2;
+          t1 = b1;
+        }
       }
-    } else if (L_inc <= (uint32_t)SMALL_MAX) {
-      sh.inc_cnt = bpe_thread(
-          L_inc, [&](int j) -> uint32_t { return inc_byte((uint32_t)j); }, tb, inc_out);
-    } else if (L_inc <= (uint32_t)WAVE_MAX) {
-      sh.med[atomicAdd(&sh.n_med, 1u)] = U_INCOMING;
+      if (inc_u) {
+        inc_out(0, t0);
+        if (c == 2) inc_out(1, t1);
+        sh.inc_cnt = c;
+      } else {
+        sh.ph.b.tok[a] = t0;
+        if (c == 2) sh.ph.b.tok[a + 1] = t1;
+        sh.ucnt[u] = (uint16_t)c;
+      }
+    } else if (L <= (uint32_t)SMALL_MAX) {
+      my_len[r] = L;
+      my_slot[r] = atomicAdd(&sh.hist[L], 1u);
+    } else if (L <= (uint32_t)WAVE_MAX) {
+      sh.med[atomicAdd(&sh.n_med, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
     } else {
-      sh.big[atomicAdd(&sh.n_big, 1u)] = U_INCOMING;
+      sh.big[atomicAdd(&sh.n_big, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
     }
   }
   __syncthreads();
+  if (tid == 0) {
+    uint32_t acc = 0;
+    for (int L = 3; L <= SMALL_MAX; ++L) {
+      const uint32_t c = sh.hist[L];
+      sh.hist[L] = acc;
+      acc += c;
+    }
+    sh.n_small = acc;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < UPT; ++r) {
+    if (my_len[r] == 0) continue;
+    const uint32_t u = (uint32_t)(tid + r * PT_THREADS);
+    sh.ph.b.small[sh.hist[my_len[r]] + my_slot[r]] = u == m_proc ? U_INCOMING : (uint16_t)u;
+  }
+  __syncthreads();
+  const uint32_t n_small = sh.n_small, n_med = sh.n_med;
 
-  // ---- BPE, wave per unit of 17..64 bytes -----------------------------------
-  const uint32_t n_med = sh.n_med;
+  // thread per unit
 #pragma unroll 1
-  for (uint32_t i = wave; i < n_med; i += PT_THREADS / 64) {
-    const uint32_t u = sh.med[i];
+  for (uint32_t i = tid; i < n_small; i += PT_THREADS) {
+    const uint32_t u = sh.ph.b.small[i];
     if (u == U_INCOMING) {
-      const uint32_t c = bpe_wave(
-          L_inc, [&](int j) -> uint32_t { return inc_byte((uint32_t)j); }, tb,
-          [&](int j, uint32_t id) { inc_out((uint32_t)j, id); });
-      if (lane == 0) sh.inc_cnt = c;
+      sh.inc_cnt = bpe_thread(
+          L_inc, [&](int j) -> uint32_t { return (uint32_t)j < L_inc ? inc_byte((uint32_t)j) : 0u; }, tb,
+          inc_out);
     } else {
       const uint32_t a = sh.ustart[u];
       const uint32_t L = sh.ustart[u + 1] - a;
-      const uint32_t c = bpe_wave(
+      sh.ucnt[u] = (uint16_t)bpe_thread(
           L, [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb,
-          [&](int j, uint32_t id) { sh.tok[a + j] = id; });
-      if (lane == 0) sh.ucnt[u] = (uint16_t)c;
+          [&](uint32_t j, uint32_t id) { sh.ph.b.tok[a + j] = id; });
+    }
+  }
+
+  // wave per unit: unit i runs on wave (first + i) mod 16, where the waves
+  // from `first` on have no thread work
+  {
+    constexpr uint32_t NWV = PT_THREADS / 64;
+    const uint32_t busy = n_small >= (uint32_t)PT_THREADS ? NWV : (n_small + 63) / 64;
+    const uint32_t first = busy % NWV;
+#pragma unroll 1
+    for (uint32_t i = ((uint32_t)wave + NWV - first) % NWV; i < n_med; i += NWV) {
+      const uint32_t u = sh.med[i];
+      if (u == U_INCOMING) {
+        const uint32_t c = bpe_wave(
+            L_inc, [&](int j) -> uint32_t { return inc_byte((uint32_t)j); }, tb,
+            [&](int j, uint32_t id) { inc_out((uint32_t)j, id); });
+        if (lane == 0) sh.inc_cnt = c;
+      } else {
+        const uint32_t a = sh.ustart[u];
+        const uint32_t L = sh.ustart[u + 1] - a;
+        const uint32_t c = bpe_wave(
+            L, [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb,
+            [&](int j, uint32_t id) { sh.ph.b.tok[a + j] = id; });
+        if (lane == 0) sh.ucnt[u] = (uint16_t)c;
+      }
     }
   }
   __syncthreads();
 
   // ---- BPE, whole block per longer unit ------------------------------------
+  // (rare in text: rows in global scratch at the unit's byte offset; the
+  // selection masks of a unit of L > 64 bytes at byte s take words
+  // [s/16, s/16 + L/64 + 2), which never reach the next unit's)
   const uint32_t n_big = sh.n_big;
 #pragma unroll 1
   for (uint32_t i = 0; i < n_big; ++i) {
     const uint32_t u = sh.big[i];
-    if (u == U_INCOMING) {
-      uint32_t c;
-      if (L_inc <= (uint32_t)PT_WIN) {
-        c = bpe_rows<PT_THREADS / 64>(L_inc, inc_byte, tb, sh.rI0, sh.rI1, sh.rR0, sh.rR1, sh.rsel, sh.rows,
-                                      inc_out);
-      } else {
-        // longer than a window: rows in global memory at the unit's byte offset
-        uint32_t* sc = w.scratch;
-        const uint64_t nn = (uint64_t)n;
-        c = bpe_rows<PT_THREADS / 64>(L_inc, inc_byte, tb, sc + s_prev, sc + nn + s_prev, sc + 2 * nn + s_prev,
-                                      sc + 3 * nn + s_prev, reinterpret_cast<uint64_t*>(sc + 4 * nn) + s_prev / 32,
-                                      sh.rows, inc_out);
-      }
-      if (tid == 0) sh.inc_cnt = c;
+    const bool inc_u = u == U_INCOMING;
+    const uint32_t a = inc_u ? 0u : sh.ustart[u];
+    const uint32_t L = inc_u ? L_inc : sh.ustart[u + 1] - a;
+    const uint64_t s0 = inc_u ? (uint64_t)s_prev : (uint64_t)(w0 + a);
+    uint32_t* sc = w.scratch;
+    const uint64_t nn = (uint64_t)n;
+    uint64_t* sel = reinterpret_cast<uint64_t*>(sc + 4 * nn) + s0 / 16;
+    uint32_t c;
+    if (inc_u) {
+      c = bpe_rows<PT_THREADS / 64>(L, inc_byte, tb, sc + s0, sc + nn + s0, sc + 2 * nn + s0, sc + 3 * nn + s0, sel,
+                                    sh.rows, inc_out);
     } else {
-      const uint32_t a = sh.ustart[u];
-      const uint32_t L = sh.ustart[u + 1] - a;
-      const uint32_t c = bpe_rows<PT_THREADS / 64>(
-          L, [&](uint32_t j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb, sh.rI0, sh.rI1, sh.rR0, sh.rR1,
-          sh.rsel, sh.rows, [&](uint32_t j, uint32_t id) { sh.tok[a + j] = id; });
-      if (tid == 0) sh.ucnt[u] = (uint16_t)c;
+      c = bpe_rows<PT_THREADS / 64>(
+          L, [&](uint32_t j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb, sc + s0, sc + nn + s0,
+          sc + 2 * nn + s0, sc + 3 * nn + s0, sel, sh.rows, [&](uint32_t j, uint32_t id) { sh.ph.b.tok[a + j] = id; });
+    }
+    if (tid == 0) {
+      if (inc_u) sh.inc_cnt = c;
+      else sh.ucnt[u] = (uint16_t)c;
     }
     __syncthreads();
   }
@@ -832,7 +912,7 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
     for (int j = 0; j < PT_BPT; ++j) {
       const uint32_t k = (uint32_t)(tid * PT_BPT + j);
       if (k < m_proc) {
-        sh.uoff[k] = (uint16_t)o;
+        sh.ph.b.uoff[k] = (uint16_t)o;
         o += sh.ucnt[k];
       }
     }
@@ -850,10 +930,10 @@ __global__ __launch_bounds__(PT_THREADS) void tile_kernel(Work w, DevTables tb) 
     if (before == 0u || before - 1u >= m_proc) continue;
     const uint32_t k = before - 1u;
     const uint32_t o = (uint32_t)q - sh.ustart[k];
-    if (o < sh.ucnt[k]) dst[sh.uoff[k] + o] = sh.tok[q];
+    if (o < sh.ucnt[k]) dst[sh.ph.b.uoff[k] + o] = sh.ph.b.tok[q];
     if (BATCH && st && sh.dstart[PT_PAD + q]) {
       w.unit_tile[w0 + q] = t;
-      w.unit_pos[w0 + q] = inc_cnt + sh.uoff[k];
+      w.unit_pos[w0 + q] = inc_cnt + sh.ph.b.uoff[k];
     }
   }
   if (tid == 0) {
