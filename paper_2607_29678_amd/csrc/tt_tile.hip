@@ -61,10 +61,18 @@ __device__ __forceinline__ void st_word(uint64_t* p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+constexpr int CLS_L1_BYTES = 4352, CLS_L2_BYTES = TT_CLS_NBLOCKS * 64;
+
+// The probed class table, staged in LDS by every block.
+struct ClassLds {
+  uint8_t l1[CLS_L1_BYTES] __attribute__((aligned(16)));
+  uint8_t l2[CLS_L2_BYTES] __attribute__((aligned(16)));
+};
+
 // 2-bit class of a non-ASCII code point from the probed table.
-__device__ __forceinline__ uint32_t table_class(uint32_t cp) {
-  uint32_t blk = TT_CLS_L1[cp >> 8];
-  uint32_t b = TT_CLS_L2[blk * 64u + ((cp & 255u) >> 2)];
+__device__ __forceinline__ uint32_t table_class(const ClassLds& ct, uint32_t cp) {
+  const uint32_t blk = ct.l1[cp >> 8];
+  const uint32_t b = ct.l2[blk * 64u + ((cp & 255u) >> 2)];
   return (b >> ((cp & 3u) * 2u)) & 3u;
 }
 
@@ -86,7 +94,7 @@ __device__ __forceinline__ uint32_t letter_ident(uint32_t lower) {
 // case-sensitive for GPT-2 and folded for cl100k, where the engine also folds
 // U+017F (long s) to 's'.
 template <int PAT>
-__device__ __forceinline__ uint32_t char_code(uint32_t cp) {
+__device__ __forceinline__ uint32_t char_code(const ClassLds& ct, uint32_t cp) {
   uint32_t cls, id = I_NONE;
   if (cp < 128u) {
     if (((cp | 32u) - 'a') < 26u) cls = C_L;
@@ -98,7 +106,7 @@ __device__ __forceinline__ uint32_t char_code(uint32_t cp) {
     else if (cp == 39u) id = I_APO;
     else if (cls == C_L && (PAT == TT_PATTERN_CL100K || cp >= 'a')) id = letter_ident(cp | 32u);
   } else {
-    uint32_t c2 = table_class(cp);
+    uint32_t c2 = table_class(ct, cp);
     cls = c2 == 1u ? C_L : c2 == 2u ? C_N : c2 == 3u ? C_WS : C_O;
     if (PAT == TT_PATTERN_CL100K && cp == 0x17Fu) id = I_S;
   }
@@ -180,6 +188,7 @@ constexpr uint16_t U_INCOMING = 0xFFFFu;               // list entry for the inc
 // written before it.
 union PhaseMem {
   struct {
+    ClassLds cls;             // character classes
     uint32_t join[2048];      // junction byte pairs of the merges
     uint8_t code[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));  // class/identity/doc-start codes
     int16_t run_end[PT_WIN];  // cl100k: window index of the head after a run's head
@@ -278,6 +287,19 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (tid < NCH) stage_chunk(tid);
     else if (tid < NCH + 3) stage_chunk(tid == NCH ? -1 : tid - 1);  // [-8, 0) and [PT_WIN, PT_WIN + 16)
   }
+  {
+    // the class table (12.9 KB) is read once per block
+    static_assert(CLS_L1_BYTES % 16 == 0 && CLS_L2_BYTES % 16 == 0, "class table staging uses 16-byte words");
+    constexpr int N1 = CLS_L1_BYTES / 16, N2 = CLS_L2_BYTES / 16;
+    const uint4* s1 = reinterpret_cast<const uint4*>(TT_CLS_L1);
+    const uint4* s2 = reinterpret_cast<const uint4*>(TT_CLS_L2);
+    uint4* d1 = reinterpret_cast<uint4*>(sh.ph.a.cls.l1);
+    uint4* d2 = reinterpret_cast<uint4*>(sh.ph.a.cls.l2);
+    for (int i = tid; i < N1 + N2; i += PT_THREADS) {
+      if (i < N1) d1[i] = s1[i];
+      else d2[i - N1] = s2[i - N1];
+    }
+  }
   if (SEG) {
     // the junction bitmap (8 KB) is read once per block
     const uint4* src = reinterpret_cast<const uint4*>(tb.join);
@@ -350,7 +372,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
             bad |= own;
             code = C_O;
           } else {
-            code = char_code<PAT>(cp);
+            code = char_code<PAT>(sh.ph.a.cls, cp);
           }
         }
       }
@@ -501,34 +523,24 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         int p = prev(f);
         need = p >= 0 && ((cls(p) == C_N && cls(f) == C_N) || cls(p) == C_NL);
       }
-      if (need) {
+      // walk back tile by tile (usually one step) until a tile whose trailing
+      // run does not span it
+      if (need && lane == 0) {
         uint32_t acc = 0, pre = C_NONE;
-        for (int64_t base = (int64_t)t - 1; base >= 0; base -= 64) {
-          int64_t j = base - lane;
-          uint32_t v = 0;
-          if (j >= 0) {
-            uint64_t x;
-            do {
-              x = ld_word(&w.tile_sum[j]);
-            } while ((uint32_t)(x >> 32) != w.epoch);
-            v = (uint32_t)x;
-          }
-          bool stop = j >= 0 && !(v & SUM_RUNALL);
-          uint64_t m = __ballot(stop);
-          int first = m ? (__ffsll((unsigned long long)m) - 1) : 64;
-          uint32_t c = (j >= 0 && lane <= first) ? ((v >> 1) & 3u) : 0u;
-#pragma unroll
-          for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
-          acc += c;
-          if (m) {
-            pre = (__shfl(v, first, 64) >> 3) & 7u;
+        for (int64_t j = (int64_t)t - 1; j >= 0; --j) {
+          uint64_t x;
+          do {
+            x = ld_word(&w.tile_sum[j]);
+          } while ((uint32_t)(x >> 32) != w.epoch);
+          const uint32_t v = (uint32_t)x;
+          acc += (v >> 1) & 3u;
+          if (!(v & SUM_RUNALL)) {
+            pre = (v >> 3) & 7u;
             break;
           }
         }
-        if (lane == 0) {
-          sh.carry_n = acc % 3u;
-          sh.carry_nlpre = pre;
-        }
+        sh.carry_n = acc % 3u;
+        sh.carry_nlpre = pre;
       }
     }
     __syncthreads();
@@ -563,7 +575,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       uint32_t cp = 0;
       int len = decode(tmp, avail, cp);
       if (len == 0) return true;  // invalid input; reported elsewhere
-      uint32_t c = code_cls(char_code<PAT>(cp));
+      uint32_t c = code_cls(char_code<PAT>(sh.ph.a.cls, cp));
       if (c == C_NL) return false;
       if (c != C_WS) return true;
       pos += len;
@@ -711,27 +723,21 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // that ends at its first unit start.
   const bool has_inc = t > 0 && (m > 0 || last);
   const uint32_t m_proc = last ? m : (m > 0 ? m - 1 : 0);
-  if (wave == 0 && has_inc) {
+  if (tid == 0 && has_inc) {
     // the incoming unit starts at the last unit start of the nearest earlier
-    // tile that has one
+    // tile that has one (usually the previous tile)
     uint32_t found = NO_START;
-    for (int64_t base = (int64_t)t - 1; base >= 0; base -= 64) {
-      const int64_t j = base - lane;
-      uint32_t v = NO_START;
-      if (j >= 0) {
-        uint64_t x;
-        do {
-          x = ld_word(&w.tile_last[j]);
-        } while ((uint32_t)(x >> 32) != w.epoch);
-        v = (uint32_t)x;
-      }
-      const uint64_t hit = __ballot(v != NO_START);
-      if (hit) {
-        found = (uint32_t)__shfl((int)v, __ffsll((unsigned long long)hit) - 1, 64);
+    for (int64_t j = (int64_t)t - 1; j >= 0; --j) {
+      uint64_t x;
+      do {
+        x = ld_word(&w.tile_last[j]);
+      } while ((uint32_t)(x >> 32) != w.epoch);
+      if ((uint32_t)x != NO_START) {
+        found = (uint32_t)x;
         break;
       }
     }
-    if (lane == 0) sh.s_prev = found;
+    sh.s_prev = found;
   }
   __syncthreads();
   // (only invalid input, whose text starts with a continuation byte, leaves
