@@ -1,22 +1,28 @@
 """Benchmark: exact tokenization of 1M-character requests on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3|4] [--no-cpu]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3|4] [--no-cpu] [--calibrate-copy]
 
 A step is one full-request tokenization (pre-tokenization, BPE, compaction)
 of one distinct seeded 1,000,000-character sample whose bytes are already in
-HBM; the IDs stay in HBM.  W warm-up requests use separate samples.  The K
-timed requests run back to back between two stream synchronisations:
-value = K * 1e6 chars / elapsed.  Per-request latencies (enqueue to
-completion, input in HBM) give P50/P90/P99; a second pass over the same
-samples records HIP events between the library's stages (same stream) for the
-per-kernel times and the roofline of the dominant kernel.  The host-to-host
-latency through ``tt_encode`` (PCIe copies included) is reported separately.
-The CPU oracle is timed on one sample, single-threaded, as a baseline.
+HBM; the IDs stay in HBM.  W warm-up requests use other samples.  The K timed
+requests run back to back between two stream synchronisations:
+value = K * 1e6 chars / elapsed.  During the timed region the library records
+HIP events between its stages on the same stream; their average gives the
+duration of the dominant kernel (the tile kernel) for the roofline.
+Per-request latencies (enqueue to completion, input in HBM) give P50/P90/P99
+in a second pass; the host-to-host latency through ``tt_encode`` (PCIe copies
+included) is reported separately.  The CPU oracle is timed on the same timed
+samples, single-threaded, and its IDs are compared with the GPU's.
+
+``--calibrate-copy`` first runs a plain int32 copy kernel of 64 MiB read +
+64 MiB written, so that a hardware-counter profile of this command can scale
+the tile kernel's FETCH_SIZE / WRITE_SIZE to bytes.
 
 Prints one JSON line.
 """
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -26,6 +32,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tile_kernel_traffic.json")
+CSRC = os.path.join(ROOT, "paper_2607_29678_amd", "csrc")
 
 
 def percentile(xs, q):
@@ -38,13 +46,26 @@ def percentile(xs, q):
     return xs[lo] + (xs[hi] - xs[lo]) * (k - lo)
 
 
-def stage_bytes(stage, B, P, T):
-    """Algorithmic HBM bytes of one stage (what the method must move)."""
-    if stage == "tile":   # read the text, write the tile-compacted IDs
-        return B + 4 * T
-    if stage == "emit":   # read the staged IDs, write the dense output
-        return 4 * T + 4 * T
-    return None
+def kernel_source_sha():
+    """SHA-256 over the library sources (the counters are void once these change)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h", ".inc")):
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(config):
+    """HBM bytes per tile-kernel launch from the committed counter profile, if still valid."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != kernel_source_sha() or rec.get("config") != config:
+        return None
+    return rec.get("traffic_bytes_per_launch")
 
 
 def main():
@@ -54,9 +75,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=(3, 4))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--calibrate-copy", action="store_true", help="run the counter-calibration copy kernel first")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build runs the tokenizer on a single MI355X "
+        print("bench.py measures one GPU only: the tokenizer runs on a single MI355X "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
@@ -76,36 +98,47 @@ def main():
     sid = stream.cuda_stream
     tok = Tokenizer(merges, vb, vo, cfg["pattern"])
 
+    if args.calibrate_copy:
+        src = torch.arange(16 << 20, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        torch.add(src, 0, out=dst)  # reads 64 MiB, writes 64 MiB
+        torch.cuda.synchronize()
+        del src, dst
+
     # seeded samples: warm-up samples are distinct from the timed ones
     n_total = args.warmup + args.steps
     texts = [textgen.latency_sample(k, s % 32).encode("utf-8") for s in range(n_total)]
     d_in = [torch.from_numpy(np.frombuffer(t, dtype=np.uint8).copy()).to(dev) for t in texts]
     cap = max(len(t) for t in texts)
-    d_out = torch.empty(cap, dtype=torch.int32, device=dev)
+    d_out = torch.empty((len(texts), cap), dtype=torch.int32, device=dev)
     d_len = torch.zeros(len(texts), dtype=torch.int64, device=dev)
     n_chars = [len(t.decode("utf-8")) for t in texts]
     torch.cuda.synchronize()
 
     def run(i):
-        tok.encode_device(d_in[i], len(texts[i]), d_out, d_len[i:i + 1], sid)
+        tok.encode_device(d_in[i], len(texts[i]), d_out[i], d_len[i:i + 1], sid)
 
     for i in range(args.warmup):
         run(i)
     torch.cuda.synchronize()
 
-    # --- timed region: K requests back to back -----------------------------
+    # --- timed region: K requests back to back, stage events recorded -------
     timed = list(range(args.warmup, n_total))
+    tok.set_profiling(len(timed))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in timed:
         run(i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    stage_calls = tok.stage_times(sid)
+    tok.set_profiling(0)
     chars = sum(n_chars[i] for i in timed)
     value = chars / elapsed
     lens = d_len.cpu().numpy()
     if (lens[timed] <= 0).any():
         raise SystemExit("tokenizer reported an error: %s" % lens[timed])
+    stage_avg = {s: sum(c[s] for c in stage_calls) / len(stage_calls) for s in stage_calls[0]}
 
     # --- per-request latency (enqueue to completion, input in HBM) -----------
     lat = []
@@ -116,28 +149,6 @@ def main():
         stream.synchronize()
         lat.append((time.perf_counter() - a) * 1e3)
 
-    # --- stage times from library events on the same stream -------------------
-    tok.set_profiling(True)
-    stage = {}
-    for i in timed:
-        run(i)
-        for name, ms in tok.stage_times(sid).items():
-            stage.setdefault(name, []).append(ms)
-    tok.set_profiling(False)
-    stage_avg = {s: sum(v) / len(v) for s, v in stage.items()}
-
-    # sizes for algorithmic bytes: P from the split-level export, T from the output
-    P_avg = sum(len(tok.pretokenize(texts[i])) for i in timed[:4]) / min(4, len(timed))
-    B_avg = sum(len(texts[i]) for i in timed) / len(timed)
-    T_avg = float(np.mean(lens[timed]))
-    rl = {}
-    for s, ms in stage_avg.items():
-        b = stage_bytes(s, B_avg, P_avg, T_avg)
-        if b is not None and ms > 0:
-            rl[s] = {"ms": round(ms, 4), "bytes": int(b), "GBs": round(b / (ms * 1e-3) / 1e9, 1),
-                     "frac": round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 5)}
-    dominant = max((s for s in rl), key=lambda s: rl[s]["ms"]) if rl else None
-
     # --- host-to-host latency through tt_encode (PCIe copies included) --------
     host_lat = []
     for i in timed[: min(10, len(timed))]:
@@ -145,7 +156,21 @@ def main():
         tok.encode(texts[i], sid)
         host_lat.append((time.perf_counter() - a) * 1e3)
 
-    # --- CPU oracle baseline on one sample --------------------------------------
+    # --- roofline of the dominant kernel -------------------------------------
+    # algorithmic bytes of one tile-kernel launch: the request's bytes are
+    # read once and its token IDs written once (merge-table probes are L2
+    # traffic, not HBM traffic, for tables of a few MB)
+    B_avg = sum(len(texts[i]) for i in timed) / len(timed)
+    T_avg = float(np.mean(lens[timed]))
+    tile_ms = stage_avg["tile"]
+    alg = B_avg + 4.0 * T_avg
+    achieved = alg / (tile_ms * 1e-3) / 1e9
+    roofline = {"kernel": "tile_kernel", "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
+                "traffic": measured_traffic(k), "algorithmic_bytes": int(alg),
+                "kernel_ms": round(tile_ms, 4)}
+
+    # --- CPU oracle baseline on the timed samples --------------------------------
     cpu = None
     if not args.no_cpu:
         from oracle.bpe import MergeTable
@@ -153,19 +178,19 @@ def main():
         from workloads.tables import vocab_list
 
         table = MergeTable(merges.tolist(), vocab_list(vb, vo))
-        sample = texts[timed[0]]
-        a = time.perf_counter()
-        ids = oracle_encode(sample, table, cfg["pattern"])
-        dt = time.perf_counter() - a
-        got = d_out[: int(lens[timed[-1]])]  # last run used the last timed sample
-        run(timed[0])
-        torch.cuda.synchronize()
-        same = d_out[: int(d_len[timed[0]].item())].cpu().numpy().tolist() == ids
-        cpu = {"value": round(n_chars[timed[0]] / dt, 1), "unit": "chars/s", "cores": 1, "kind": "oracle",
-               "sample": "one full %d-char sample of the timed workload, single thread, pure Python"
-                         % n_chars[timed[0]],
+        host_ids = d_out.cpu().numpy()
+        same = True
+        dt = 0.0
+        for i in timed:
+            a = time.perf_counter()
+            ids = oracle_encode(texts[i], table, cfg["pattern"])
+            dt += time.perf_counter() - a
+            same &= host_ids[i, : int(lens[i])].tolist() == ids
+        cpu = {"value": round(sum(n_chars[i] for i in timed) / dt, 1), "unit": "chars/s", "cores": 1,
+               "kind": "oracle",
+               "sample": "the %d timed 1,000,000-char samples, one after another, single thread, pure Python"
+                         % len(timed),
                "seconds": round(dt, 2), "ids_identical_to_gpu": bool(same)}
-        del got
 
     out = {
         "metric": "exact-tokenization chars/sec and P50 latency for a 1M-char request, 1 MI355X",
@@ -180,24 +205,19 @@ def main():
         "vs_baseline": None,
         "dtype": "int32",
         "data": "synthetic",
-        "config": {"workload": "%s: 1,000,000-char seeded %s request, %s-style pattern, %d merges"
-                               % (cfg["name"].upper(), "agent-transcript" if k == 3 else
-                                  "multilingual agent-transcript", cfg["pattern"], cfg["merges"]),
-                   "chars": 1_000_000, "bytes_avg": int(B_avg), "tokens_avg": int(T_avg),
-                   "pieces_avg": int(P_avg), "samples": len(timed)},
+        "config": {"workload": "C%d: 1,000,000-char seeded %s request, %s-style pattern, %d merges"
+                               % (k, "agent-transcript" if k == 3 else "multilingual agent-transcript",
+                                  cfg["pattern"], cfg["merges"]),
+                   "chars": 1_000_000, "bytes_avg": int(B_avg), "tokens_avg": int(T_avg), "samples": len(timed)},
         "p50_ms": round(percentile(lat, 50), 4),
         "p90_ms": round(percentile(lat, 90), 4),
         "p99_ms": round(percentile(lat, 99), 4),
         "host_to_host_p50_ms": round(percentile(host_lat, 50), 4),
         "stage_ms": {s: round(v, 4) for s, v in stage_avg.items()},
-        "roofline": None,
+        "roofline": roofline,
         "cpu_baseline": cpu,
         "context": {"paper_p50_ms_1M_chars": 0.87, "paper_hardware": "RTX PRO 6000 Blackwell (Qwen3 real text)"},
     }
-    if dominant:
-        r = rl[dominant]
-        out["roofline"] = {"kernel": dominant, "bound": "hbm", "achieved": r["GBs"], "peak": HBM_PEAK_GBS,
-                           "unit": "GB/s", "frac": r["frac"], "traffic": None, "per_stage": rl}
     print(json.dumps(out))
 
 

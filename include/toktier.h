@@ -157,16 +157,22 @@ const char* tt_status_string(int status);
 int tt_info(const tt_tokenizer* h, int32_t* n_merges, int32_t* vocab_size, int32_t* pattern_id);
 
 /* ---- measurement ------------------------------------------------------- */
-/* Record HIP events between the stages of every later call on this handle
- * (enable != 0) or stop recording (enable == 0).  For measurement only: the
- * events add a few microseconds per call. */
-int tt_set_profiling(tt_tokenizer* h, int enable);
+/* Stages of a call, in launch order: the tile kernel (pre-tokenization, BPE
+ * and per-tile compaction of every tile, Sec. 4.1-4.2) and the emit stage
+ * (placement of every tile's outputs in the dense output, the output length,
+ * and for batches the per-document offsets). */
+#define TT_N_STAGES 2
 
-/* Elapsed milliseconds of the stages of the most recent call on `stream`, in
- * launch order: reset, pre-tokenization, short-piece BPE, wave BPE, block BPE,
- * compaction.  Waits for that call to finish.  out_ms holds `cap` entries;
- * *n_out receives how many were written (0 if profiling was off or the last
- * call on the stream stopped after pre-tokenization earlier than BPE). */
+/* Record HIP events between the stages of every later call on this handle and
+ * keep those of the most recent `n_calls` calls of each stream (0 stops
+ * recording; at most 65,536).  For measurement only: each call then records
+ * TT_N_STAGES + 1 events on its stream. */
+int tt_set_profiling(tt_tokenizer* h, int32_t n_calls);
+
+/* Elapsed milliseconds of the stages of the recorded calls on `stream`, oldest
+ * call first, TT_N_STAGES entries per call.  Waits for those calls to finish.
+ * out_ms holds `cap` entries; *n_out receives how many were written (whole
+ * calls only; 0 if nothing was recorded). */
 int tt_stage_times(tt_tokenizer* h, void* stream, double* out_ms, int32_t cap, int32_t* n_out);
 
 #ifdef __cplusplus

@@ -41,11 +41,11 @@ SIGNATURES = {
     "tt_pretokenize": (ctypes.c_int, [_P, _P, _I64, _P, ctypes.POINTER(_I64), _P]),
     "tt_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "tt_info": (ctypes.c_int, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32), ctypes.POINTER(_I32)]),
-    "tt_set_profiling": (ctypes.c_int, [_P, ctypes.c_int]),
+    "tt_set_profiling": (ctypes.c_int, [_P, _I32]),
     "tt_stage_times": (ctypes.c_int, [_P, _P, _P, _I32, ctypes.POINTER(_I32)]),
 }
 
-STAGES = ["tile", "emit"]
+STAGES = ["tile", "emit"]  # TT_N_STAGES stages per call, in launch order
 
 _lib = None
 

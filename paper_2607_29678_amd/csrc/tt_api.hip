@@ -39,8 +39,11 @@ struct Workspace {
   int64_t* d_docs = nullptr;  // batch: document byte offsets
   int64_t* d_out_docs = nullptr;
   int64_t* h_len = nullptr;   // pinned readback word
-  hipEvent_t ev[N_STAGES + 1] = {};  // stage boundaries of the last call (profiling)
-  int n_ev = 0;                      // events recorded by the last call
+  // profiling: stage boundaries of the most recent calls, a ring of
+  // `ring` calls with N_STAGES + 1 events each
+  std::vector<hipEvent_t> ev;
+  int ring = 0;          // calls the ring holds
+  int64_t n_calls = 0;   // calls recorded since profiling was enabled
 };
 
 }  // namespace
@@ -50,7 +53,7 @@ struct tt_tokenizer {
   int32_t n_merges = 0;
   int32_t vocab_size = 0;
   int device = 0;
-  int profile = 0;  // record stage events on every call
+  int profile = 0;  // calls whose stage events are kept (0: no events)
   u64x2* d_slots = nullptr;    // cuckoo buckets
   uint32_t shift = 0;          // 32 - log2(bucket count)
   uint32_t* d_pair0 = nullptr;  // [65536] byte-pair ranks
@@ -71,7 +74,7 @@ void free_ws(Workspace* s) {
   if (s->dmem) (void)hipFree(s->dmem);
   if (s->d_docs) (void)hipFree(s->d_docs);
   if (s->h_len) (void)hipHostFree(s->h_len);
-  for (auto& e : s->ev)
+  for (auto e : s->ev)
     if (e) (void)hipEventDestroy(e);
   delete s;
 }
@@ -199,12 +202,21 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_len = out_len;
   w.out_doc_off = out_docs;
   DevTables tb{h->d_slots, h->shift, h->d_pair0, h->d_join, h->d_ext, h->n_ids};
-  const bool prof = h->profile != 0;
-  s->n_ev = 0;
+  const int ring = h->profile;
+  if (ring != s->ring) {  // (re)size the event ring
+    for (auto e : s->ev)
+      if (e) (void)hipEventDestroy(e);
+    s->ev.assign((size_t)ring * (N_STAGES + 1), nullptr);
+    s->ring = ring;
+    s->n_calls = 0;
+  }
+  hipEvent_t* evs = ring ? &s->ev[(size_t)(s->n_calls % ring) * (N_STAGES + 1)] : nullptr;
+  int n_mark = 0;
   auto mark = [&]() -> bool {
-    if (!prof) return true;
-    if (!s->ev[s->n_ev] && hipEventCreate(&s->ev[s->n_ev]) != hipSuccess) return false;
-    return hipEventRecord(s->ev[s->n_ev++], st) == hipSuccess;
+    if (!ring) return true;
+    hipEvent_t& e = evs[n_mark++];
+    if (!e && hipEventCreate(&e) != hipSuccess) return false;
+    return hipEventRecord(e, st) == hipSuccess;
   };
   if (!mark()) return TT_ERR_HIP;
   if (launch_tile(w, tb, h->pattern, mode, st) != hipSuccess) return TT_ERR_HIP;
@@ -214,6 +226,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   if (launch_emit(w, tb, mode, st) != hipSuccess) return TT_ERR_HIP;
   if (d_docs && launch_doc_offsets(w, st) != hipSuccess) return TT_ERR_HIP;
   if (!mark()) return TT_ERR_HIP;
+  if (ring) ++s->n_calls;
   return TT_OK;
 }
 
@@ -506,9 +519,11 @@ int tt_pretokenize(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int64_t* o
   return TT_OK;
 }
 
-int tt_set_profiling(tt_tokenizer* h, int enable) {
+int tt_set_profiling(tt_tokenizer* h, int32_t n_calls) {
   if (!h) return TT_ERR_NULL_ARG;
-  h->profile = enable ? 1 : 0;
+  if (n_calls < 0 || n_calls > 65536) return TT_ERR_BAD_ARG;
+  std::lock_guard<std::mutex> g(h->mu);
+  h->profile = n_calls;
   return TT_OK;
 }
 
@@ -523,14 +538,18 @@ int tt_stage_times(tt_tokenizer* h, void* stream, double* out_ms, int32_t cap, i
     if (it == h->ws.end()) return TT_OK;
     s = it->second;
   }
-  if (s->n_ev < 2) return TT_OK;
-  if (hipSetDevice(h->device) != hipSuccess || hipEventSynchronize(s->ev[s->n_ev - 1]) != hipSuccess)
-    return TT_ERR_HIP;
+  if (s->ring == 0 || s->n_calls == 0) return TT_OK;
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  const int64_t kept = s->n_calls < s->ring ? s->n_calls : s->ring;
   int k = 0;
-  for (int i = 0; i + 1 < s->n_ev && k < cap; ++i, ++k) {
-    float ms = 0.f;
-    if (hipEventElapsedTime(&ms, s->ev[i], s->ev[i + 1]) != hipSuccess) return TT_ERR_HIP;
-    out_ms[k] = ms;
+  for (int64_t c = s->n_calls - kept; c < s->n_calls && k + N_STAGES <= cap; ++c) {
+    hipEvent_t* e = &s->ev[(size_t)(c % s->ring) * (N_STAGES + 1)];
+    if (hipEventSynchronize(e[N_STAGES]) != hipSuccess) return TT_ERR_HIP;
+    for (int i = 0; i < N_STAGES; ++i) {
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, e[i], e[i + 1]) != hipSuccess) return TT_ERR_HIP;
+      out_ms[k++] = ms;
+    }
   }
   *n_out = k;
   return TT_OK;

@@ -118,17 +118,18 @@ class Tokenizer:
 
 
     # -- measurement -------------------------------------------------------
-    def set_profiling(self, enable=True):
-        """``tt_set_profiling``: record stage events on later calls."""
-        _lib.check(self._lib.tt_set_profiling(self._h, 1 if enable else 0), "tt_set_profiling")
+    def set_profiling(self, n_calls=1):
+        """``tt_set_profiling``: keep the stage events of the last ``n_calls`` calls (0 = off)."""
+        _lib.check(self._lib.tt_set_profiling(self._h, int(n_calls)), "tt_set_profiling")
 
-    def stage_times(self, stream=None) -> dict:
-        """``tt_stage_times``: {stage name: ms} of the last call on ``stream``."""
-        out = np.zeros(16, dtype=np.float64)
+    def stage_times(self, stream=None, max_calls=4096) -> list:
+        """``tt_stage_times``: one {stage name: ms} dict per recorded call on ``stream``, oldest first."""
+        ns = len(_lib.STAGES)
+        out = np.zeros(ns * max_calls, dtype=np.float64)
         n = ctypes.c_int32(0)
-        _lib.check(self._lib.tt_stage_times(self._h, _stream(stream), _ptr(out), 16, ctypes.byref(n)),
+        _lib.check(self._lib.tt_stage_times(self._h, _stream(stream), _ptr(out), out.size, ctypes.byref(n)),
                    "tt_stage_times")
-        return {_lib.STAGES[i]: float(out[i]) for i in range(n.value)}
+        return [{_lib.STAGES[i]: float(out[c * ns + i]) for i in range(ns)} for c in range(n.value // ns)]
 
 
 def status_string(status: int) -> str:

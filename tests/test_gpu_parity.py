@@ -153,3 +153,19 @@ def test_device_entry_matches_host(gpu):
     stream.synchronize()
     T = int(d_len.item())
     assert d_out[:T].cpu().numpy().tolist() == _oracle_config_ids(k)
+
+
+def test_stage_times_ring(gpu):
+    """Stage events of the most recent calls are kept, oldest first, one entry per stage."""
+    tok = lib_tokenizer(1)
+    data = config_bytes(1)
+    tok.set_profiling(3)
+    try:
+        for _ in range(5):
+            tok.encode(data)
+        calls = tok.stage_times()
+    finally:
+        tok.set_profiling(0)
+    assert len(calls) == 3
+    for c in calls:
+        assert set(c) == {"tile", "emit"} and all(v > 0 for v in c.values())
