@@ -54,30 +54,44 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane(x, 63);
 }
 
+// Inclusive sum over the lanes of a wave (DPP: shifts within rows of 16
+// lanes, then the row broadcasts carry row totals forward).
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) {
+  int x = (int)v;
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false); // row_bcast:15 into rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false); // row_bcast:31 into rows 2, 3
+  return (uint32_t)x;
+}
+
 // ---------------------------------------------------------------------------
-// One thread, at most 16 bytes.  Token IDs and pair ranks stay in registers
-// (all indexing is unrolled); a merge clears the right token's bit in an alive
-// mask instead of shifting the tail.  A pair's rank is kept as
+// One thread, at most 16 bytes.  The unit's tokens live in its own LDS words
+// ids[0..L) (the caller puts the bytes there; merged tokens overwrite their
+// left operand in place, and the tokens end compacted in ids[0..count)); the
+// pair ranks stay in registers.  A merge clears the right token's bit in an
+// alive mask instead of shifting the tail.  A pair's rank is kept as
 // (rank << 4) | position so that one unsigned minimum finds the lowest rank
 // and, among equal ranks (the same pair), the leftmost occurrence.  The chain
 // is one round trip for the initial byte pairs (all loads in flight at once)
-// and one per merge (its two neighbour lookups overlap).
-//   byte(j)      byte j of the unit for j < L; called for every j < 16 and
-//                must be safe to call there (the value is then ignored)
-//   out(j, id)   stores output token j
-// Returns the number of tokens.
+// and one per merge (its two neighbour lookups overlap).  Returns the number
+// of tokens.
 // ---------------------------------------------------------------------------
-template <class ByteF, class OutF>
-__device__ __forceinline__ uint32_t bpe_thread(uint32_t L, ByteF byte, const DevTables& tb, OutF out) {
+__device__ __forceinline__ uint32_t bpe_thread(uint32_t L, uint32_t* ids, const DevTables& tb) {
   constexpr int S = SMALL_MAX;
   const u64x2* __restrict__ tab = tb.slots;
   const uint32_t shift = tb.shift;
-  uint32_t id[S], rk[S];
+  uint32_t rk[S];
+  {
+    uint32_t b[S];
 #pragma unroll
-  for (int j = 0; j < S; ++j) id[j] = byte(j);  // bytes past the unit are read but not used
-  // every initial rank load is issued before any is used (no branches)
+    for (int j = 0; j < S; ++j) b[j] = (uint32_t)j < L ? ids[j] : 0u;
+    // every initial rank load is issued before any is used (no branches)
 #pragma unroll
-  for (int j = 0; j < S - 1; ++j) rk[j] = tb.pair0[((id[j] & 255u) << 8) | (id[j + 1] & 255u)];
+    for (int j = 0; j < S - 1; ++j) rk[j] = tb.pair0[(b[j] << 8) | b[j + 1]];
+  }
 #pragma unroll
   for (int j = 0; j < S - 1; ++j)
     rk[j] = ((uint32_t)(j + 1) < L && rk[j] != RANK_INF) ? ((rk[j] << 4) | (uint32_t)j) : RANK_INF;
@@ -96,14 +110,10 @@ __device__ __forceinline__ uint32_t bpe_thread(uint32_t L, ByteF byte, const Dev
     const uint32_t above_m = alive & ~((2u << m) - 1u);
     const uint32_t below_k = alive & ((1u << k) - 1u);
     const bool hr = above_m != 0u, hl = below_k != 0u;
-    const int r_i = hr ? __builtin_ctz(above_m) : 0;
-    const int l_i = hl ? 31 - __builtin_clz(below_k) : 0;
-    uint32_t right = 0, left = 0;
-#pragma unroll
-    for (int j = 0; j < S; ++j) {
-      right = j == r_i ? id[j] : right;
-      left = j == l_i ? id[j] : left;
-    }
+    const uint32_t right = ids[hr ? __builtin_ctz(above_m) : k];
+    const int l_i = hl ? 31 - __builtin_clz(below_k) : k;
+    const uint32_t left = ids[l_i];
+    ids[k] = nid;
     // both lookups are issued unconditionally (a missing neighbour looks up a
     // harmless pair) so that their four loads are in flight together
     const ProbeIssued pr = probe_issue(tab, shift, nid, right);
@@ -112,18 +122,14 @@ __device__ __forceinline__ uint32_t bpe_thread(uint32_t L, ByteF byte, const Dev
     const uint32_t rl = hl ? probe_finish(pl, left, nid) : RANK_INF;
 #pragma unroll
     for (int j = 0; j < S; ++j) {
-      if (j == k) {
-        id[j] = nid;
-        rk[j] = rr == RANK_INF ? RANK_INF : ((rr << 4) | (uint32_t)j);
-      }
+      if (j == k) rk[j] = rr == RANK_INF ? RANK_INF : ((rr << 4) | (uint32_t)j);
       if (j == m) rk[j] = RANK_INF;
       if (hl && j == l_i) rk[j] = rl == RANK_INF ? RANK_INF : ((rl << 4) | (uint32_t)j);
     }
   }
+  // compact in place: the c-th live token moves to ids[c], c <= its slot
   uint32_t c = 0;
-#pragma unroll
-  for (int j = 0; j < S; ++j)
-    if ((alive >> j) & 1u) out(c++, id[j]);
+  for (uint32_t al = alive; al; al &= al - 1u) ids[c++] = ids[__builtin_ctz(al)];
   return c;
 }
 

@@ -213,6 +213,7 @@ struct PtShared {
   uint32_t n_small, n_med, n_big;
   uint32_t wave_tot[PT_THREADS / 64];
   uint32_t tile;
+  uint32_t inc_ids[SMALL_MAX];  // the incoming unit's tokens (thread engine)
   uint32_t s_prev;            // start of the incoming unit
   uint32_t inc_cnt;           // its tokens
   uint32_t carry_n;           // cl100k: number-run chars before the tile, mod 3
@@ -679,7 +680,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
 
   // ---- units: block scan of the start flags --------------------------------
   const uint32_t cnt = __popc(flags);
-  const uint32_t inc = wave_incl_scan(cnt, lane, [](uint32_t a, uint32_t b) { return a + b; });
+  const uint32_t inc = wave_incl_sum(cnt);
   __syncthreads();
   if (lane == 63) sh.wave_tot[wave] = inc;
   __syncthreads();
@@ -761,11 +762,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // the whole block.  The incoming unit is listed last.
   constexpr int UPT = (PT_OWN + 1 + PT_THREADS - 1) / PT_THREADS;  // units per thread
   const uint32_t U = m_proc + (has_inc ? 1u : 0u);
-  uint32_t my_slot[UPT], my_len[UPT];
+  uint32_t mine[UPT];  // small units: (length << 16) | position within its length bucket
 #pragma unroll
   for (int r = 0; r < UPT; ++r) {
-    my_len[r] = 0;
-    my_slot[r] = 0;
+    mine[r] = 0;
     const uint32_t u = (uint32_t)(tid + r * PT_THREADS);
     if (u >= U) continue;
     const bool inc_u = u == m_proc;
@@ -794,8 +794,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         sh.ucnt[u] = (uint16_t)c;
       }
     } else if (L <= (uint32_t)SMALL_MAX) {
-      my_len[r] = L;
-      my_slot[r] = atomicAdd(&sh.hist[L], 1u);
+      mine[r] = (L << 16) | atomicAdd(&sh.hist[L], 1u);
     } else if (L <= (uint32_t)WAVE_MAX) {
       sh.med[atomicAdd(&sh.n_med, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
     } else {
@@ -815,9 +814,9 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < UPT; ++r) {
-    if (my_len[r] == 0) continue;
+    if (mine[r] == 0) continue;
     const uint32_t u = (uint32_t)(tid + r * PT_THREADS);
-    sh.ph.b.small[sh.hist[my_len[r]] + my_slot[r]] = u == m_proc ? U_INCOMING : (uint16_t)u;
+    sh.ph.b.small[sh.hist[mine[r] >> 16] + (mine[r] & 0xFFFFu)] = u == m_proc ? U_INCOMING : (uint16_t)u;
   }
   __syncthreads();
   const uint32_t n_small = sh.n_small, n_med = sh.n_med;
@@ -827,15 +826,16 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   for (uint32_t i = tid; i < n_small; i += PT_THREADS) {
     const uint32_t u = sh.ph.b.small[i];
     if (u == U_INCOMING) {
-      sh.inc_cnt = bpe_thread(
-          L_inc, [&](int j) -> uint32_t { return (uint32_t)j < L_inc ? inc_byte((uint32_t)j) : 0u; }, tb,
-          inc_out);
+      for (uint32_t j = 0; j < L_inc; ++j) sh.inc_ids[j] = inc_byte(j);
+      const uint32_t c = bpe_thread(L_inc, sh.inc_ids, tb);
+      for (uint32_t j = 0; j < c; ++j) inc_out(j, sh.inc_ids[j]);
+      sh.inc_cnt = c;
     } else {
+      // the unit's own window slots hold its tokens while it is encoded
       const uint32_t a = sh.ustart[u];
       const uint32_t L = sh.ustart[u + 1] - a;
-      sh.ucnt[u] = (uint16_t)bpe_thread(
-          L, [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb,
-          [&](uint32_t j, uint32_t id) { sh.ph.b.tok[a + j] = id; });
+      for (uint32_t j = 0; j < L; ++j) sh.ph.b.tok[a + j] = sh.buf[PT_PAD + a + j];
+      sh.ucnt[u] = (uint16_t)bpe_thread(L, &sh.ph.b.tok[a], tb);
     }
   }
 
@@ -904,7 +904,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     const uint32_t k = (uint32_t)(tid * PT_BPT + j);
     csum += k < m_proc ? sh.ucnt[k] : 0u;
   }
-  const uint32_t cinc = wave_incl_scan(csum, lane, [](uint32_t a, uint32_t b) { return a + b; });
+  const uint32_t cinc = wave_incl_sum(csum);
   if (lane == 63) sh.wave_tot[wave] = cinc;
   __syncthreads();
   uint32_t cpre = 0, ctot = 0;
