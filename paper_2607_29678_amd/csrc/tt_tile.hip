@@ -157,6 +157,36 @@ __device__ __forceinline__ int decode(const uint8_t* s, int avail, uint32_t& cp)
   return 4;
 }
 
+// The same decode from bytes already in registers (b1..b3 are read only when
+// the sequence is that long and `avail` allows it).
+__device__ __forceinline__ int decode_bytes(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3, int avail,
+                                            uint32_t& cp) {
+  const int len = lead_len(b0);
+  if (len == 0 || len > avail) return 0;
+  if (len == 1) {
+    cp = b0;
+    return 1;
+  }
+  uint32_t lo = 0x80u, hi = 0xBFu;
+  if (b0 == 0xE0u) lo = 0xA0u;
+  else if (b0 == 0xEDu) hi = 0x9Fu;
+  else if (b0 == 0xF0u) lo = 0x90u;
+  else if (b0 == 0xF4u) hi = 0x8Fu;
+  if (b1 < lo || b1 > hi) return 0;
+  if (len == 2) {
+    cp = ((b0 & 0x1Fu) << 6) | (b1 & 0x3Fu);
+    return 2;
+  }
+  if ((b2 & 0xC0u) != 0x80u) return 0;
+  if (len == 3) {
+    cp = ((b0 & 0x0Fu) << 12) | ((b1 & 0x3Fu) << 6) | (b2 & 0x3Fu);
+    return 3;
+  }
+  if ((b3 & 0xC0u) != 0x80u) return 0;
+  cp = ((b0 & 0x07u) << 18) | ((b1 & 0x3Fu) << 12) | ((b2 & 0x3Fu) << 6) | (b3 & 0x3Fu);
+  return 4;
+}
+
 // Segmented char-count scan state for cl100k: has-head (bit 31), window index
 // of the latest run head (bits 16..27), characters since that head (bits 0..15;
 // or since the tile start when there is no head yet).
@@ -330,45 +360,69 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     __syncthreads();
   }
 
-  // ---- decode, validate, classify: 8 positions per thread ----------------
-  // (rolled loops keep the kernel small enough for the instruction cache)
+  // ---- decode, validate, classify ------------------------------------------
+  // A thread's four positions are one aligned word of the window.  It reads
+  // its word and the words on either side (bytes and document-start flags) and
+  // decides everything from registers: a sequence starts at most three bytes
+  // before a position it covers and ends at most three bytes after.
+  static_assert(PT_BPT == 4 && PT_PAD % 4 == 0, "classification works on aligned 4-byte words");
   bool bad = false;
   {
-    const int qb0 = tid * PT_BPT;
-    auto B = [&](int q) -> uint32_t { return sh.buf[PT_PAD + q]; };
-    auto D = [&](int q) -> bool { return sh.dstart[PT_PAD + q] != 0; };
-#pragma unroll 1
+    const int q0 = tid * PT_BPT;
+    const uint32_t* bw = reinterpret_cast<const uint32_t*>(&sh.buf[PT_PAD + q0 - 4]);
+    const uint32_t* dw = reinterpret_cast<const uint32_t*>(&sh.dstart[PT_PAD + q0 - 4]);
+    const uint64_t blo = bw[0] | ((uint64_t)bw[1] << 32), bhi = bw[1] | ((uint64_t)bw[2] << 32);
+    const uint64_t dlo = dw[0] | ((uint64_t)dw[1] << 32), dhi = dw[1] | ((uint64_t)dw[2] << 32);
+    const int64_t p0 = w0 + q0;  // text position of the first of the four
+    // r is relative to q0, in [-4, 8)
+    auto byt = [&](int r) -> uint32_t {
+      return r < 0 ? (uint32_t)(blo >> (8 * (r + 4))) & 255u : (uint32_t)(bhi >> (8 * r)) & 255u;
+    };
+    auto dst = [&](int r) -> bool {
+      return ((r < 0 ? (uint32_t)(dlo >> (8 * (r + 4))) : (uint32_t)(dhi >> (8 * r))) & 255u) != 0u;
+    };
+    auto ins = [&](int r) -> bool { return p0 + r >= 0 && p0 + r < n; };
+    uint32_t codes = 0;
+#pragma unroll
     for (int j = 0; j < PT_BPT; ++j) {
-      const int q = qb0 + j;
-      const uint32_t ds = D(q) ? CODE_DOCSTART : 0u;
+      const int q = q0 + j;
+      const uint32_t ds = dst(j) ? CODE_DOCSTART : 0u;
       uint32_t code = C_NONE;
-      const bool own = q >= PT_HALO && q < PT_HALO + PT_OWN && inside(q);
-      if (inside(q)) {
-        const uint32_t b = B(q);
+      const bool own = q >= PT_HALO && q < PT_HALO + PT_OWN && ins(j);
+      if (ins(j)) {
+        const uint32_t b = byt(j);
         if ((b & 0xC0u) == 0x80u) {
           if (own) {
             // a continuation byte must lie inside the sequence of a lead byte at
             // most three bytes earlier, with no document start in between
-            bool claimed = false;
-            if (!ds) {
-              for (int k = 1; k <= 3; ++k) {
-                if (!inside(q - k)) break;
-                const uint32_t br = B(q - k);
-                if ((br & 0xC0u) == 0x80u) {
-                  if (D(q - k)) break;
-                  continue;
-                }
-                claimed = lead_len(br) > k;
-                break;
+            bool claimed = false, done = ds != 0u;
+#pragma unroll
+            for (int k = 1; k <= 3; ++k) {
+              if (done) continue;
+              if (!ins(j - k)) {
+                done = true;
+                continue;
               }
+              const uint32_t br = byt(j - k);
+              if ((br & 0xC0u) == 0x80u) {
+                done = dst(j - k);
+                continue;
+              }
+              claimed = lead_len(br) > k;
+              done = true;
             }
             bad |= !claimed;
           }
         } else {
           int avail = 1;
-          while (avail < 4 && inside(q + avail) && !D(q + avail)) ++avail;
+          bool stop = false;
+#pragma unroll
+          for (int k = 1; k <= 3; ++k) {
+            stop = stop || !ins(j + k) || dst(j + k);
+            avail += stop ? 0 : 1;
+          }
           uint32_t cp = 0;
-          const int len = decode(&sh.buf[PT_PAD + q], avail, cp);
+          const int len = decode_bytes(b, byt(j + 1), byt(j + 2), byt(j + 3), avail, cp);
           if (len == 0) {
             bad |= own;
             code = C_O;
@@ -377,11 +431,12 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
           }
         }
       }
-      sh.ph.a.code[PT_PAD + q] = (uint8_t)(code | ds);
+      codes |= (code | ds) << (8 * j);
     }
+    *reinterpret_cast<uint32_t*>(&sh.ph.a.code[PT_PAD + q0]) = codes;
     if (tid < 3) {  // positions outside [0, PT_WIN) carry no character for the rules
-      const int q0 = tid == 0 ? -8 : PT_WIN + 8 * (tid - 1);
-      *reinterpret_cast<uint2*>(&sh.ph.a.code[PT_PAD + q0]) = make_uint2(0x07070707u, 0x07070707u);
+      const int qx = tid == 0 ? -8 : PT_WIN + 8 * (tid - 1);
+      *reinterpret_cast<uint2*>(&sh.ph.a.code[PT_PAD + qx]) = make_uint2(0x07070707u, 0x07070707u);
     }
   }
   if (bad) __hip_atomic_store(&w.ctrl->err, ((uint64_t)w.epoch << 32) | (uint32_t)(-TT_ERR_INVALID_UTF8), __ATOMIC_RELAXED,
@@ -443,21 +498,68 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     return p2 >= 0 && cls(p2) == C_L && contraction_len_at(p2) == 2;
   };
 
-  // ---- cl100k: run scan, run ends, summaries, carries ----------------------
+  // ---- the codes around the thread's positions, in registers ---------------
+  // cr(r) is the code of window position qb + r for r in [-8, 8).  The
+  // neighbour of a position is the position next to it whenever that holds a
+  // character (prev_of / next_of); only continuation bytes and the window edges
+  // need the general walks over LDS.
   const int qb = tid * PT_BPT;
-  // scan element of window position q: a run head restarts the char count
-  auto elem_at = [&](int q) -> uint32_t {
-    if (q < PT_HALO || !is_char(q)) return 0u;
-    const int p = prev(q);
-    const bool head = p < 0 || cls(p) != cls(q);
+  const uint32_t* cwp = reinterpret_cast<const uint32_t*>(&sh.ph.a.code[PT_PAD + qb - 8]);
+  const uint32_t cw0 = cwp[0], cw1 = cwp[1], cw2 = cwp[2], cw3 = cwp[3];
+  auto cr = [&](int r) -> uint32_t {
+    const int i = r + 8;
+    const uint32_t lo = (i & 4) ? cw1 : cw0, hi = (i & 4) ? cw3 : cw2;
+    return (((i & 8) ? hi : lo) >> ((i & 3) * 8)) & 255u;
+  };
+  // prev(qb + r) and its code, for r in [-7, 8)
+  auto prev_of = [&](int r, uint32_t& pc) -> int {
+    if (cr(r) & CODE_DOCSTART) return -1;
+    const uint32_t cm = cr(r - 1);
+    if (code_cls(cm) != C_NONE) {
+      pc = cm;
+      return qb + r - 1;
+    }
+    const int p = prev(qb + r);
+    pc = p >= 0 ? code_at(p) : 0u;
+    return p;
+  };
+  // next(qb + r) and its code, for r in [-8, 7)
+  auto next_of = [&](int r, uint32_t& nc) -> int {
+    const uint32_t c = cr(r + 1);
+    if (c & CODE_DOCSTART) return -1;
+    if (code_cls(c) != C_NONE) {
+      nc = c;
+      return qb + r + 1;
+    }
+    const int x = next(qb + r);
+    nc = x >= 0 ? code_at(x) : 0u;
+    return x;
+  };
+  // an apostrophe one byte before position qb + r (a contraction can start at
+  // qb + r only then), or two or three bytes before (a contraction can end just
+  // before qb + r only then: the suffix is one or two ASCII letters, or U+017F)
+  auto apo_at = [&](int r) -> bool { return code_id(cr(r)) == I_APO; };
+
+  // ---- cl100k: run scan, run ends, summaries, carries ----------------------
+  // scan element of window position qb + j: a run head restarts the char count
+  auto elem_of = [&](int j) -> uint32_t {
+    const int q = qb + j;
+    const uint32_t c = cr(j);
+    if (q < PT_HALO || code_cls(c) == C_NONE) return 0u;
+    uint32_t pc = 0;
+    const int p = prev_of(j, pc);
+    const bool head = p < 0 || code_cls(pc) != code_cls(c);
     return head ? (0x80000000u | ((uint32_t)q << 16) | 1u) : 1u;
   };
+  uint32_t elems[PT_BPT];
+#pragma unroll
+  for (int j = 0; j < PT_BPT; ++j) elems[j] = PAT == TT_PATTERN_CL100K ? elem_of(j) : 0u;
   uint32_t s0 = 0;  // scan state before the thread's first position
   if (PAT == TT_PATTERN_CL100K) {
     // elements over window indices [HALO, WIN)
     uint32_t agg = 0;
-#pragma unroll 1
-    for (int j = 0; j < PT_BPT; ++j) agg = seg_combine(agg, elem_at(qb + j));
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) agg = seg_combine(agg, elems[j]);
     uint32_t inc = wave_incl_scan(agg, lane, seg_combine);
     if (lane == 63) sh.wave_tot[wave] = inc;
     uint32_t lex = __shfl_up(inc, 1, 64);
@@ -472,10 +574,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     uint32_t last_st = 0;
     {
       uint32_t st = s0;
-#pragma unroll 1
+#pragma unroll
       for (int j = 0; j < PT_BPT; ++j) {
         const int q = qb + j;
-        const uint32_t e = elem_at(q);
+        const uint32_t e = elems[j];
         if ((e & 0x80000000u) && seg_has(st)) sh.ph.a.run_end[seg_head(st)] = (int16_t)q;
         st = seg_combine(st, e);
         if (q >= PT_HALO && q < own_end && e != 0u) {
@@ -587,32 +689,38 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // ---- piece-start predicate ----------------------------------------------
   uint32_t flags = 0;
   uint32_t scan_st = s0;  // cl100k: scan state before position q
-#pragma unroll 1
+#pragma unroll
   for (int j = 0; j < PT_BPT; ++j) {
     const int q = qb + j;
     const uint32_t ex = scan_st;
-    if (PAT == TT_PATTERN_CL100K) scan_st = seg_combine(scan_st, elem_at(q));
-    if (q < PT_HALO || q >= PT_HALO + PT_OWN || !is_char(q)) continue;
-    const uint32_t c0 = cls(q);
-    const int p1 = prev(q);
+    if (PAT == TT_PATTERN_CL100K) scan_st = seg_combine(scan_st, elems[j]);
+    const uint32_t cq = cr(j);
+    if (q < PT_HALO || q >= PT_HALO + PT_OWN || code_cls(cq) == C_NONE) continue;
+    const uint32_t c0 = code_cls(cq);
+    uint32_t cp1 = 0;
+    const int p1 = prev_of(j, cp1);
     bool start;
     if (p1 < 0) {
       start = true;
     } else {
-      const uint32_t c1 = cls(p1);
+      const uint32_t c1 = code_cls(cp1);
+      // (contraction tests run only with an apostrophe close enough before q)
+      const bool may_end_contr = apo_at(j - 2) || apo_at(j - 3);
+      const bool may_start_contr = apo_at(j - 1);
       if (PAT == TT_PATTERN_GPT2) {
         if (is_w(c0)) {
           if (!is_w(c1)) {
             start = true;  // whitespace run head
           } else {
-            int n1 = next(q);  // last char of a run of >= 2, followed by non-space
-            start = n1 >= 0 && !is_w(cls(n1));
+            uint32_t cn1 = 0;
+            const int n1 = next_of(j, cn1);  // last char of a run of >= 2, followed by non-space
+            start = n1 >= 0 && !is_w(code_cls(cn1));
           }
         } else if (c1 == c0) {
-          start = c0 == C_L && contraction_ends_here(q);
-        } else if (ident(p1) == I_SP) {
+          start = c0 == C_L && may_end_contr && contraction_ends_here(q);
+        } else if (code_id(cp1) == I_SP) {
           start = false;  // the space before the run opens the piece
-        } else if (c0 == C_L && contraction_len_at(q) > 0) {
+        } else if (c0 == C_L && may_start_contr && contraction_len_at(q) > 0) {
           start = false;
         } else {
           start = true;
@@ -635,8 +743,9 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
             }
             start = (pre == C_O) || ws_stretch_is_last(q);
           } else {
-            int n1 = next(q);
-            start = n1 >= 0 && !is_w(cls(n1));
+            uint32_t cn1 = 0;
+            const int n1 = next_of(j, cn1);
+            start = n1 >= 0 && !is_w(code_cls(cn1));
           }
         } else if (c0 == C_N) {
           if (c1 != C_N) {
@@ -646,17 +755,19 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
             start = off % 3u == 0u;
           }
         } else if (c0 == C_O) {
-          start = c1 != C_O && ident(p1) != I_SP;
+          start = c1 != C_O && code_id(cp1) != I_SP;
         } else {  // letter
           if (c1 == C_L) {
-            start = contraction_ends_here(q);
-          } else if (contraction_len_at(q) > 0) {
+            start = may_end_contr && contraction_ends_here(q);
+          } else if (may_start_contr && contraction_len_at(q) > 0) {
             start = false;
           } else if (c1 == C_WS) {
             start = false;  // one whitespace char is the prefix
           } else if (c1 == C_O) {
-            int p2 = prev(p1);
-            start = !(p2 < 0 || (cls(p2) != C_O && ident(p2) != I_SP));
+            uint32_t cp2 = 0;
+            const int p2 = p1 == q - 1 ? prev_of(j - 1, cp2) : prev(p1);
+            if (p1 != q - 1 && p2 >= 0) cp2 = code_at(p2);
+            start = !(p2 < 0 || (code_cls(cp2) != C_O && code_id(cp2) != I_SP));
           } else {
             start = true;
           }
