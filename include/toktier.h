@@ -157,11 +157,10 @@ const char* tt_status_string(int status);
 int tt_info(const tt_tokenizer* h, int32_t* n_merges, int32_t* vocab_size, int32_t* pattern_id);
 
 /* ---- measurement ------------------------------------------------------- */
-/* Stages of a call, in launch order: the tile kernel (pre-tokenization, BPE
- * and per-tile compaction of every tile, Sec. 4.1-4.2) and the emit stage
- * (placement of every tile's outputs in the dense output, the output length,
- * and for batches the per-document offsets). */
-#define TT_N_STAGES 2
+/* Stages of a call: one, the tile kernel (pre-tokenization, BPE and the
+ * placement of every tile's outputs, Sec. 4.1-4.2), with the per-document
+ * offsets of a batch. */
+#define TT_N_STAGES 1
 
 /* Record HIP events between the stages of every later call on this handle and
  * keep those of the most recent `n_calls` calls of each stream (0 stops

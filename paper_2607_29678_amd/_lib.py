@@ -45,7 +45,7 @@ SIGNATURES = {
     "tt_stage_times": (ctypes.c_int, [_P, _P, _P, _I32, ctypes.POINTER(_I32)]),
 }
 
-STAGES = ["tile", "emit"]  # TT_N_STAGES stages per call, in launch order
+STAGES = ["tile"]  # TT_N_STAGES stages per call, in launch order
 
 _lib = None
 

@@ -4,7 +4,8 @@
 // Chain of one request (all on the caller's stream, no host round trip
 // between kernels; Sec. 4.3 keeps piece counts, dispatch lists and the output
 // length on the device and sizes launches from buffer capacity):
-//   tile (pre-tokenize + BPE + tile compaction) -> emit [-> document offsets]
+//   tile kernel (pre-tokenize + BPE + placement of every tile's outputs)
+//   [-> document offsets, for batches]
 // The host synchronises twice per blocking call: once for the output length,
 // once for the IDs.
 #include <algorithm>
@@ -23,7 +24,7 @@ using namespace tt;
 namespace {
 
 // Stages of one call, in launch order (profiling names them in this order).
-enum { ST_TILE, ST_EMIT, N_STAGES };
+enum { ST_TILE, N_STAGES };
 
 struct Workspace {
   uint64_t cap = 0;           // bytes of request this workspace holds
@@ -103,9 +104,8 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
   size_t o_ctrl = take(sizeof(Ctrl));
   size_t o_tsum = take(8 * NT);
   size_t o_tlast = take(8 * NT);
+  size_t o_tagg = take(8 * NT);
   const size_t ctl_bytes = off;
-  size_t o_tcnt = take(4 * NT);
-  size_t o_tbase = take(4 * NT);
   size_t o_tpre = take(4 * NT);
   size_t o_stage = take(4 * N);
   size_t o_utile = take(4 * N);
@@ -130,8 +130,7 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
   w.ctrl = reinterpret_cast<Ctrl*>(b + o_ctrl);
   w.tile_sum = reinterpret_cast<uint64_t*>(b + o_tsum);
   w.tile_last = reinterpret_cast<uint64_t*>(b + o_tlast);
-  w.tile_cnt = reinterpret_cast<uint32_t*>(b + o_tcnt);
-  w.tile_base = reinterpret_cast<uint32_t*>(b + o_tbase);
+  w.tile_agg = reinterpret_cast<uint64_t*>(b + o_tagg);
   w.tile_pre = reinterpret_cast<uint32_t*>(b + o_tpre);
   w.stage = reinterpret_cast<uint32_t*>(b + o_stage);
   w.unit_tile = reinterpret_cast<uint32_t*>(b + o_utile);
@@ -184,7 +183,7 @@ int get_ws(tt_tokenizer* h, hipStream_t stream, uint64_t need, Workspace** out) 
 // mode 0: split export (out_ids receives piece offsets); mode 1: encode.
 int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, const int64_t* d_docs,
               int32_t n_docs, int32_t* out_ids, int64_t* out_len, int64_t* out_docs, hipStream_t st, int mode) {
-  if (s->epoch == 0xFFFFFFFFu) {
+  if (s->epoch + 1 >= EPOCH_LIMIT) {
     // epochs wrapped: clear the words that carry them and start again
     if (hipMemsetAsync(s->dmem, 0, s->ctl_bytes, st) != hipSuccess) return TT_ERR_HIP;
     s->epoch = 0;
@@ -215,15 +214,13 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   auto mark = [&]() -> bool {
     if (!ring) return true;
     hipEvent_t& e = evs[n_mark++];
-    if (!e && hipEventCreate(&e) != hipSuccess) return false;
+    // timing only: no system-scope fence (no cache writeback) at each mark
+    if (!e && hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return false;
     return hipEventRecord(e, st) == hipSuccess;
   };
   if (!mark()) return TT_ERR_HIP;
   if (launch_tile(w, tb, h->pattern, mode, st) != hipSuccess) return TT_ERR_HIP;
   s->ticket_base += w.n_tiles;  // the tiles took their tickets
-  if (!mark()) return TT_ERR_HIP;
-  if (w.n_tiles > EMIT_DIRECT_TILES && launch_tile_scan(w, st) != hipSuccess) return TT_ERR_HIP;
-  if (launch_emit(w, tb, mode, st) != hipSuccess) return TT_ERR_HIP;
   if (d_docs && launch_doc_offsets(w, st) != hipSuccess) return TT_ERR_HIP;
   if (!mark()) return TT_ERR_HIP;
   if (ring) ++s->n_calls;

@@ -111,8 +111,8 @@ struct DevTables {
 struct Ctrl {
   uint32_t tile_ticket;
   uint32_t pad;
-  uint64_t err;             // (epoch << 32) | error magnitude of the latest failing call
 };
+constexpr uint32_t EPOCH_LIMIT = 0x7FFFFFFFu;  // epochs are 1 .. EPOCH_LIMIT - 1 (31 bits)
 
 constexpr uint32_t NO_START = 0xFFFFFFFFu;  // tile_last: no unit starts in the tile
 
@@ -128,10 +128,9 @@ struct Work {
   uint32_t n_tiles;
   uint64_t* tile_sum;       // [tiles] (epoch << 32) | trailing-run summary (cl100k carries)
   uint64_t* tile_last;      // [tiles] (epoch << 32) | last unit start in the tile, or NO_START
-  uint32_t* tile_cnt;       // [tiles] outputs staged by the tile
-  uint32_t* tile_base;      // [tiles] where they are staged
-  uint32_t* tile_pre;       // [tiles] exclusive prefix of tile_cnt (large requests, batches)
-  uint32_t* stage;          // [n] staged outputs: tile t's at stage[tile_base[t] ..]
+  uint64_t* tile_agg;       // [tiles] output counts for the placement look-back (epoch-tagged)
+  uint32_t* tile_pre;       // batch: [tiles] outputs of all earlier tiles
+  uint32_t* stage;          // [n] tokens of incoming units, at the unit's first byte
   uint32_t* unit_tile;      // batch: [n] processing tile of the unit starting at a byte
   uint32_t* unit_pos;       // batch: [n] its first output within that tile's outputs
   uint32_t* scratch;        // rows of units longer than 64 bytes: 4 * n words, then n / 16 + 8 masks
@@ -149,16 +148,12 @@ constexpr int PT_OWN = PT_WIN - 2 * PT_HALO;       // bytes a tile decides
 
 constexpr int SMALL_MAX = 16;                      // thread-per-unit limit (bytes)
 constexpr int WAVE_MAX = 64;                       // wave-per-unit limit (bytes)
-constexpr uint32_t EMIT_THREADS = 256;
-constexpr uint32_t EMIT_DIRECT_TILES = 4096;       // above this, a scan kernel makes tile_pre
 
 inline uint32_t n_tiles_for(uint32_t n) { return (n + PT_OWN - 1) / PT_OWN; }
 
 // Launchers (defined in the .hip files) -------------------------------------
 // mode 0: split export (outputs are piece byte offsets); mode 1: encode
 hipError_t launch_tile(const Work& w, const DevTables& t, int pattern, int mode, hipStream_t s);
-hipError_t launch_tile_scan(const Work& w, hipStream_t s);
-hipError_t launch_emit(const Work& w, const DevTables& t, int mode, hipStream_t s);
 hipError_t launch_doc_offsets(const Work& w, hipStream_t s);
 
 }  // namespace tt

@@ -245,6 +245,8 @@ struct PtShared {
   uint32_t tile;
   uint32_t inc_ids[SMALL_MAX];  // the incoming unit's tokens (thread engine)
   uint32_t s_prev;            // start of the incoming unit
+  uint32_t prefix;            // outputs of all earlier tiles
+  uint32_t err;               // invalid input in this tile or an earlier one
   uint32_t inc_cnt;           // its tokens
   uint32_t carry_n;           // cl100k: number-run chars before the tile, mod 3
   uint32_t carry_nlpre;       // cl100k: class before a CR/LF stretch entering the tile
@@ -253,6 +255,74 @@ struct PtShared {
 };
 
 }  // namespace
+
+// Word a tile publishes for the placement of its outputs:
+//   bits 0..30 a count, bit 31 set when the count is inclusive (all outputs of
+//   the tiles up to this one) rather than this tile's own, bit 32 set when
+//   invalid input was seen (inclusive: in any tile up to this one), bits 33..63
+//   the epoch of the call.
+constexpr uint64_t PL_INC = 1ull << 31, PL_ERR = 1ull << 32;
+constexpr int PL_EPOCH_SHIFT = 33;
+
+// Decoupled look-back over the tiles' output counts (wave 0): publish this
+// tile's count, then sum the counts of earlier tiles, newest first, until a
+// tile whose published count is already inclusive.  A window of 64 earlier
+// tiles is read at once and read again until every tile the sum needs has
+// published (earlier tiles publish their own count before they look back, so
+// the walk never waits on a tile that is itself waiting).  Returns the number
+// of outputs before this tile, in every thread; the last tile also writes the
+// output length, or the error.
+template <class Sh>
+__device__ uint32_t place_tile(const Work& w, Sh& sh, uint32_t t, uint32_t count, bool bad, int tid, int lane,
+                               int wave) {
+  const uint64_t ep = (uint64_t)w.epoch << PL_EPOCH_SHIFT;
+  uint64_t* pl = w.tile_agg;
+  if (t == 0) {
+    if (tid == 0) {
+      st_word(&pl[0], ep | PL_INC | (bad ? PL_ERR : 0ull) | count);
+      sh.prefix = 0;
+      sh.err = bad ? 1u : 0u;
+    }
+  } else {
+    if (tid == 0) st_word(&pl[t], ep | (bad ? PL_ERR : 0ull) | count);
+    if (wave == 0) {
+      uint32_t prefix = 0;
+      bool err = bad;
+      int64_t base = (int64_t)t - 1;
+      for (;;) {
+        const int64_t j = base - lane;
+        uint64_t x = ep | PL_INC;  // before the first tile: an inclusive zero
+        if (j >= 0) x = ld_word(&pl[j]);
+        const bool ready = (x >> PL_EPOCH_SHIFT) == (uint64_t)w.epoch;
+        const uint64_t m_inc = __ballot(ready && (x & PL_INC));
+        const uint64_t m_rdy = __ballot(ready);
+        const int first = m_inc ? __ffsll((unsigned long long)m_inc) - 1 : 63;
+        const uint64_t need = first >= 63 ? ~0ull : ((2ull << first) - 1ull);
+        if ((m_rdy & need) != need) {
+          __builtin_amdgcn_s_sleep(1);
+          continue;
+        }
+        const bool use = lane <= first;
+        const uint32_t c = use ? (uint32_t)(x & 0x7FFFFFFFull) : 0u;
+        prefix += (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_sum(c), 63);
+        err = err || __ballot(use && (x & PL_ERR)) != 0ull;
+        if (m_inc) break;
+        base -= 64;
+      }
+      if (lane == 0) {
+        st_word(&pl[t], ep | PL_INC | (err ? PL_ERR : 0ull) | (prefix + count));
+        sh.prefix = prefix;
+        sh.err = err ? 1u : 0u;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    if (w.doc_off != nullptr) w.tile_pre[t] = sh.prefix;
+    if (t == w.n_tiles - 1) *w.out_len = sh.err ? (int64_t)TT_ERR_INVALID_UTF8 : (int64_t)(sh.prefix + count);
+  }
+  return sh.prefix;
+}
 
 // MODE 0: split-level export; the outputs are the byte offsets of the pieces.
 // MODE 1: encoding; the outputs are the (internal) IDs of the units' tokens.
@@ -439,10 +509,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       *reinterpret_cast<uint2*>(&sh.ph.a.code[PT_PAD + qx]) = make_uint2(0x07070707u, 0x07070707u);
     }
   }
-  if (bad) __hip_atomic_store(&w.ctrl->err, ((uint64_t)w.epoch << 32) | (uint32_t)(-TT_ERR_INVALID_UTF8), __ATOMIC_RELAXED,
-                              __HIP_MEMORY_SCOPE_AGENT);
   for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.ph.a.run_end[q] = -1;
-  __syncthreads();
+  const bool tile_bad = __syncthreads_or(bad) != 0;
 
   // ---- neighbour helpers (window indices; -1 = none) ----------------------
   auto code_at = [&](int q) -> uint32_t { return sh.ph.a.code[PT_PAD + q]; };
@@ -804,15 +872,12 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   const bool last = t == n_tiles - 1;
 
   if (MODE == 0) {
-    // split export: the tile's piece offsets, staged where its bytes begin
-    uint32_t k = texcl;
+    // split export: the tile's piece offsets go straight to their place
+    const uint32_t prefix = place_tile(w, sh, t, m, tile_bad, tid, lane, wave);
+    uint32_t k = prefix + texcl;
 #pragma unroll 1
     for (int j = 0; j < PT_BPT; ++j)
-      if ((flags >> j) & 1u) w.stage[t0 + k++] = (uint32_t)(w0 + qb + j);
-    if (tid == 0) {
-      w.tile_cnt[t] = m;
-      w.tile_base[t] = (uint32_t)t0;
-    }
+      if (((flags >> j) & 1u) && k < (uint32_t)n) w.out_ids[k++] = (int32_t)(w0 + qb + j);
     return;
   }
 
@@ -1007,8 +1072,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     __syncthreads();
   }
 
-  // ---- compaction: the tile's tokens, in order, where its bytes begin -------
-  // (the incoming unit's tokens are already first there)
+  // ---- output: the tile's tokens, in order, at their place --------------------
   uint32_t csum = 0;
 #pragma unroll 1
   for (int j = 0; j < PT_BPT; ++j) {
@@ -1034,10 +1098,19 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       }
     }
   }
-  __syncthreads();
   const uint32_t inc_cnt = has_inc ? sh.inc_cnt : 0u;
-  const uint32_t base = has_inc ? s_prev : (m > 0 ? (uint32_t)(w0 + sh.ustart[0]) : 0u);
-  uint32_t* dst = w.stage + base + inc_cnt;
+  // (place_tile ends with a barrier, which also publishes uoff to the block)
+  const uint32_t prefix = place_tile(w, sh, t, inc_cnt + ctot, tile_bad, tid, lane, wave);
+  // Valid input gives every tile a disjoint byte range and at most one output
+  // per byte, so every output index is below n.  Invalid input (whose output
+  // is discarded) can break that; the bound keeps it inside the buffer.
+  const uint32_t lim = (uint32_t)n;
+  int32_t* __restrict__ out = w.out_ids;
+  const int32_t* __restrict__ ext = tb.ext_id;
+  auto ext_of = [&](uint32_t v) -> int32_t { return v < tb.n_ids ? ext[v] : -1; };
+  for (uint32_t i = (uint32_t)tid; i < inc_cnt; i += PT_THREADS)
+    if (prefix + i < lim) out[prefix + i] = ext_of(w.stage[s_prev + i]);
+  const uint32_t obase = prefix + inc_cnt;
   uint32_t before = texcl;  // unit starts at or before position q
 #pragma unroll 1
   for (int j = 0; j < PT_BPT; ++j) {
@@ -1047,19 +1120,16 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (before == 0u || before - 1u >= m_proc) continue;
     const uint32_t k = before - 1u;
     const uint32_t o = (uint32_t)q - sh.ustart[k];
-    if (o < sh.ucnt[k]) dst[sh.ph.b.uoff[k] + o] = sh.ph.b.tok[q];
+    const uint32_t at = obase + sh.ph.b.uoff[k] + o;
+    if (o < sh.ucnt[k] && at < lim) out[at] = ext_of(sh.ph.b.tok[q]);
     if (BATCH && st && sh.dstart[PT_PAD + q]) {
       w.unit_tile[w0 + q] = t;
       w.unit_pos[w0 + q] = inc_cnt + sh.ph.b.uoff[k];
     }
   }
-  if (tid == 0) {
-    if (BATCH && has_inc) {
-      w.unit_tile[s_prev] = t;
-      w.unit_pos[s_prev] = 0;
-    }
-    w.tile_cnt[t] = inc_cnt + ctot;
-    w.tile_base[t] = base;
+  if (BATCH && tid == 0 && has_inc) {
+    w.unit_tile[s_prev] = t;
+    w.unit_pos[s_prev] = 0;
   }
 }
 
