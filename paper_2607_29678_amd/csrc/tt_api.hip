@@ -13,6 +13,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
+#include <string>
 #include <unordered_map>
 #include <unordered_set>
 #include <vector>
@@ -58,6 +59,8 @@ struct tt_tokenizer {
   u64x2* d_slots = nullptr;    // cuckoo buckets
   uint32_t shift = 0;          // 32 - log2(bucket count)
   uint32_t* d_pair0 = nullptr;  // [65536] byte-pair ranks
+  u32x4* d_dict = nullptr;      // whole-unit dictionary
+  uint32_t dshift = 0;
   int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
   uint32_t n_ids = 0;
   uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
@@ -200,7 +203,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_ids = out_ids;
   w.out_len = out_len;
   w.out_doc_off = out_docs;
-  DevTables tb{h->d_slots, h->shift, h->d_pair0, h->d_join, h->d_ext, h->n_ids};
+  DevTables tb{h->d_slots, h->shift, h->d_pair0, h->d_join, h->d_ext, h->n_ids, h->d_dict, h->dshift};
   const int ring = h->profile;
   if (ring != s->ring) {  // (re)size the event ring
     for (auto e : s->ev)
@@ -341,6 +344,99 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
     if (nb > (1u << 28)) return TT_ERR_OOM;
   }
 
+  // whole-unit dictionary: every byte string of 3..DICT_MAX bytes that is the
+  // spelling of a merge result and whose BPE (computed here, exactly as the
+  // device computes it) is that single token
+  std::vector<u32x4> dict;
+  uint32_t dbits = 4;
+  {
+    std::unordered_map<uint64_t, uint32_t> rank;
+    rank.reserve((size_t)n_merges * 2 + 16);
+    for (int32_t r = 0; r < n_merges; ++r)
+      rank.emplace(slot_key((uint32_t)internal[merges[r].left], (uint32_t)internal[merges[r].right]), (uint32_t)r);
+    auto lookup = [&](uint32_t a, uint32_t b) -> uint32_t {
+      auto it = rank.find(slot_key(a, b));
+      return it == rank.end() ? RANK_INF : it->second;
+    };
+    struct Entry {
+      uint32_t w[3], len, id;
+    };
+    std::vector<Entry> entries;
+    std::unordered_set<std::string> seen;
+    uint32_t ids[DICT_MAX], rk[DICT_MAX];
+    for (int32_t r = 0; r < n_merges; ++r) {
+      const int32_t res = merges[r].result;
+      const int64_t L = vlen(res);
+      if (L < 3 || L > DICT_MAX) continue;
+      std::string key(reinterpret_cast<const char*>(vptr(res)), (size_t)L);
+      if (!seen.insert(key).second) continue;
+      // greedy lowest-rank BPE of the spelling, leftmost among equal ranks
+      int n = (int)L;
+      for (int i = 0; i < n; ++i) ids[i] = vptr(res)[i];
+      for (int i = 0; i + 1 < n; ++i) rk[i] = lookup(ids[i], ids[i + 1]);
+      while (n > 1) {
+        int k = -1;
+        uint32_t best = RANK_INF;
+        for (int i = 0; i + 1 < n; ++i)
+          if (rk[i] < best) {
+            best = rk[i];
+            k = i;
+          }
+        if (k < 0) break;
+        ids[k] = 256u + best;
+        for (int i = k + 1; i + 1 < n; ++i) {
+          ids[i] = ids[i + 1];
+          rk[i] = rk[i + 1];
+        }
+        --n;
+        rk[k] = k + 1 < n ? lookup(ids[k], ids[k + 1]) : RANK_INF;
+        if (k > 0) rk[k - 1] = lookup(ids[k - 1], ids[k]);
+      }
+      if (n != 1) continue;
+      Entry e{{0u, 0u, 0u}, (uint32_t)L, ids[0]};
+      for (int i = 0; i < L; ++i) e.w[i >> 2] |= (uint32_t)vptr(res)[i] << (8 * (i & 3));
+      entries.push_back(e);
+    }
+    uint32_t nd = 16;
+    while (nd < 2 * (uint32_t)entries.size()) {
+      nd <<= 1;
+      ++dbits;
+    }
+    for (;;) {
+      dict.assign(nd, u32x4{0u, 0u, 0u, 0u});
+      uint64_t rng = 0xD1B54A32D192ED03ull;
+      bool ok = true;
+      for (size_t i = 0; i < entries.size() && ok; ++i) {
+        u32x4 item{entries[i].w[0], entries[i].w[1], entries[i].w[2], (entries[i].id << 4) | entries[i].len};
+        ok = false;
+        for (int kick = 0; kick < 1000; ++kick) {
+          const uint32_t len = item.w & 15u;
+          const uint32_t b1 = unit_hash(item.x, item.y, item.z, len, 32 - dbits);
+          const uint32_t b2 = unit_hash2(item.x, item.y, item.z, len, 32 - dbits);
+          if (dict[b1].w == 0u) {
+            dict[b1] = item;
+            ok = true;
+            break;
+          }
+          if (dict[b2].w == 0u) {
+            dict[b2] = item;
+            ok = true;
+            break;
+          }
+          rng ^= rng << 13;
+          rng ^= rng >> 7;
+          rng ^= rng << 17;
+          const uint32_t v = (rng & 1) ? b1 : b2;
+          std::swap(item, dict[v]);
+        }
+      }
+      if (ok) break;
+      nd <<= 1;
+      ++dbits;
+      if (nd > (1u << 28)) return TT_ERR_OOM;
+    }
+  }
+
   // junction byte pairs: the first merge that ever joins across a byte
   // boundary has its junction exactly there, so a boundary whose byte pair is
   // no merge's junction is never crossed
@@ -358,6 +454,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   h->n_merges = n_merges;
   h->vocab_size = vocab_size;
   h->shift = 32 - bits;
+  h->dshift = 32 - dbits;
   h->n_ids = n_ids;
   if (hipGetDevice(&h->device) != hipSuccess) {
     delete h;
@@ -365,6 +462,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   }
   if (hipMalloc(reinterpret_cast<void**>(&h->d_slots), 16 * (size_t)nb) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_pair0), sizeof(uint32_t) * 65536) != hipSuccess ||
+      hipMalloc(reinterpret_cast<void**>(&h->d_dict), sizeof(u32x4) * dict.size()) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_ext), sizeof(int32_t) * n_ids) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_join), sizeof(uint32_t) * 2048) != hipSuccess) {
     tt_destroy(h);
@@ -372,6 +470,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   }
   if (hipMemcpy(h->d_slots, slots.data(), 16 * (size_t)nb, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_pair0, pair0.data(), sizeof(uint32_t) * 65536, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(h->d_dict, dict.data(), sizeof(u32x4) * dict.size(), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_ext, ext.data(), sizeof(int32_t) * n_ids, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_join, join.data(), sizeof(uint32_t) * 2048, hipMemcpyHostToDevice) != hipSuccess) {
     tt_destroy(h);
@@ -389,6 +488,7 @@ void tt_destroy(tt_tokenizer* h) {
   if (h->d_slots) (void)hipFree(h->d_slots);
   if (h->d_ext) (void)hipFree(h->d_ext);
   if (h->d_pair0) (void)hipFree(h->d_pair0);
+  if (h->d_dict) (void)hipFree(h->d_dict);
   if (h->d_join) (void)hipFree(h->d_join);
   delete h;
 }

@@ -91,6 +91,34 @@ __device__ __forceinline__ uint32_t probe_rank(const u64x2* __restrict__ tab, ui
   return probe_finish(probe_issue(tab, shift, a, b), a, b);
 }
 
+// Whole-unit dictionary: a unit of 3..DICT_MAX bytes whose BPE is a single
+// token is found with one lookup.  An entry holds the unit's bytes (zero
+// padded, little-endian words), and its length and token: (id << 4) | length.
+// Two-choice cuckoo table of one entry per bucket; a unit lives in one of the
+// two buckets its hashes name.
+constexpr int DICT_MAX = 12;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__host__ __device__ inline uint32_t unit_hash(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t len, uint32_t shift) {
+  uint32_t x = w0 * 0x9E3779B1u + w1 * 0x85EBCA77u + w2 * 0xC2B2AE3Du + len;
+  x ^= x >> 15;
+  return (x * 0x2C1B3C6Du) >> shift;
+}
+__host__ __device__ inline uint32_t unit_hash2(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t len, uint32_t shift) {
+  uint32_t x = (w0 * 0x27D4EB2Fu) ^ (w1 * 0x165667B1u) ^ (w2 * 0xD3A2646Cu) ^ (len * 0xFD7046C5u);
+  x ^= x >> 13;
+  return (x * 0x297A2D39u) >> shift;
+}
+constexpr uint32_t DICT_NONE = 0xFFFFFFFFu;
+__device__ __forceinline__ uint32_t dict_find(const u32x4* __restrict__ dict, uint32_t shift, uint32_t w0,
+                                              uint32_t w1, uint32_t w2, uint32_t len) {
+  const u32x4 a = dict[unit_hash(w0, w1, w2, len, shift)];
+  const u32x4 b = dict[unit_hash2(w0, w1, w2, len, shift)];
+  const bool ha = a.x == w0 && a.y == w1 && a.z == w2 && (a.w & 15u) == len;
+  const bool hb = b.x == w0 && b.y == w1 && b.z == w2 && (b.w & 15u) == len;
+  return ha ? a.w >> 4 : hb ? b.w >> 4 : DICT_NONE;
+}
+
 // Everything a kernel needs to know about a tokenizer handle.
 struct DevTables {
   const u64x2* slots;       // cuckoo buckets of two slots: key (left | right << 21), rank in bits 42..63
@@ -100,6 +128,8 @@ struct DevTables {
                             // in byte x to a token starting with byte y
   const int32_t* ext_id;    // [n_ids] caller's ID of every internal ID
   uint32_t n_ids;           // 256 + M
+  const u32x4* dict;        // whole-unit dictionary
+  uint32_t dshift;          // 32 - log2(dictionary buckets)
 };
 
 // ---------------------------------------------------------------------------

@@ -930,7 +930,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   auto inc_out = [&](uint32_t j, uint32_t id) { w.stage[s_prev + j] = id; };
 
   // ---- BPE dispatch ---------------------------------------------------------
-  // Units of one or two bytes are finished here.  Units of 3..16 bytes go to
+  // Units of one or two bytes are finished here, and so are units of up to 12
+  // bytes found in the whole-unit dictionary.  Other units of 3..16 bytes go to
   // one thread each, counting-sorted by length, so that the threads of a wave
   // hold units of similar length (a wave runs as long as its longest unit).
   // Units of 17..64 bytes go to one wave each, first to the waves that have no
@@ -969,12 +970,34 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         if (c == 2) sh.ph.b.tok[a + 1] = t1;
         sh.ucnt[u] = (uint16_t)c;
       }
-    } else if (L <= (uint32_t)SMALL_MAX) {
-      mine[r] = (L << 16) | atomicAdd(&sh.hist[L], 1u);
-    } else if (L <= (uint32_t)WAVE_MAX) {
-      sh.med[atomicAdd(&sh.n_med, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
     } else {
-      sh.big[atomicAdd(&sh.n_big, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
+      // units of 3..12 bytes: the whole-unit dictionary first
+      uint32_t found = DICT_NONE;
+      if (L <= (uint32_t)DICT_MAX) {
+        uint32_t kw[3] = {0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < DICT_MAX; ++j) {
+          uint32_t bj = 0;
+          if ((uint32_t)j < L) bj = inc_u ? inc_byte((uint32_t)j) : (uint32_t)sh.buf[PT_PAD + a + j];
+          kw[j >> 2] |= bj << (8 * (j & 3));
+        }
+        found = dict_find(tb.dict, tb.dshift, kw[0], kw[1], kw[2], L);
+      }
+      if (found != DICT_NONE) {
+        if (inc_u) {
+          inc_out(0, found);
+          sh.inc_cnt = 1;
+        } else {
+          sh.ph.b.tok[a] = found;
+          sh.ucnt[u] = 1;
+        }
+      } else if (L <= (uint32_t)SMALL_MAX) {
+        mine[r] = (L << 16) | atomicAdd(&sh.hist[L], 1u);
+      } else if (L <= (uint32_t)WAVE_MAX) {
+        sh.med[atomicAdd(&sh.n_med, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
+      } else {
+        sh.big[atomicAdd(&sh.n_big, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
+      }
     }
   }
   __syncthreads();
