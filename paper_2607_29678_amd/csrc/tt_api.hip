@@ -88,7 +88,10 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
   if (need <= s->cap) return TT_OK;
   // earlier asynchronous calls on this stream may still use the old buffers
   if (s->dmem && hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
-  uint64_t cap = std::max<uint64_t>(need, std::max<uint64_t>(65536, s->cap * 2));
+  // grow to a power of two, so that requests of about the same size share one
+  // allocation (a reallocation synchronises the stream)
+  uint64_t cap = 65536;
+  while (cap < need || cap < s->cap * 2) cap <<= 1;
   if (cap > (uint64_t)TT_MAX_BYTES) cap = std::max<uint64_t>(need, (uint64_t)TT_MAX_BYTES);
   if (s->dmem) {
     (void)hipFree(s->dmem);

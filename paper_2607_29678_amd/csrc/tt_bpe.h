@@ -175,6 +175,72 @@ __device__ __forceinline__ uint32_t bpe_wave(uint32_t L, ByteF byte, const DevTa
 }
 
 // ---------------------------------------------------------------------------
+// One wave64, at most 128 bytes: lane i holds tokens i and 64 + i and the
+// ranks of the pairs starting there.  A round is the same as in bpe_wave over
+// a 128-bit occurrence mask (the choice in the second row continues the
+// alternation of a run that crosses from the first, through the carry of the
+// first row's last bit); the survivors are compacted through the wave's own
+// 256 words of LDS `scr` (token IDs, then ranks), written and read back by the
+// same wave.  Every lane of the wave calls it with the same arguments.
+// ---------------------------------------------------------------------------
+template <class ByteF, class OutF>
+__device__ __forceinline__ uint32_t bpe_wave2(uint32_t L, ByteF byte, const DevTables& tb, uint32_t* scr, OutF out) {
+  const int lane = (int)(threadIdx.x & 63u);
+  const uint32_t l0 = (uint32_t)lane, l1 = 64u + (uint32_t)lane;
+  uint32_t n = L;  // <= 128
+  uint32_t id0 = l0 < n ? byte(lane) : 0u;
+  uint32_t id1 = l1 < n ? byte(64 + lane) : 0u;
+  auto next0 = [&]() -> uint32_t {  // token after position lane (row 0)
+    const uint32_t nx = (uint32_t)__shfl_down((int)id0, 1, 64);
+    const uint32_t head1 = (uint32_t)__builtin_amdgcn_readlane((int)id1, 0);
+    return lane == 63 ? head1 : nx;
+  };
+  uint32_t nx0 = next0(), nx1 = (uint32_t)__shfl_down((int)id1, 1, 64);
+  uint32_t rk0 = l0 + 1u < n ? tb.pair0[(id0 << 8) | nx0] : RANK_INF;
+  uint32_t rk1 = l1 + 1u < n ? tb.pair0[(id1 << 8) | nx1] : RANK_INF;
+  for (;;) {
+    const uint32_t m = wave_min_u32(min(rk0, rk1));
+    if (m == RANK_INF) break;
+    const uint64_t s0 = leftmost_nonoverlapping(__ballot(rk0 == m));
+    const uint64_t c = s0 >> 63;  // the pair (63, 64) is chosen: token 64 is taken
+    const uint64_t s1 = leftmost_nonoverlapping(__ballot(rk1 == m) & ~c);
+    const uint64_t v0 = n >= 64u ? ~0ull : ((1ull << n) - 1ull);
+    const uint64_t v1 = n >= 128u ? ~0ull : (n > 64u ? ((1ull << (n - 64u)) - 1ull) : 0ull);
+    const uint64_t k0 = v0 & ~(s0 << 1), k1 = v1 & ~((s1 << 1) | c);
+    const bool me0 = (s0 >> lane) & 1ull, me1 = (s1 >> lane) & 1ull;
+    const bool nxs0 = lane < 63 ? ((s0 >> (lane + 1)) & 1ull) != 0ull : (s1 & 1ull) != 0ull;
+    const bool nxs1 = lane < 63 && ((s1 >> (lane + 1)) & 1ull) != 0ull;
+    const uint32_t c0 = (uint32_t)__popcll(k0);
+    if ((k0 >> lane) & 1ull) {
+      const uint32_t p = bits_below(k0);
+      scr[p] = me0 ? 256u + m : id0;
+      scr[128 + p] = (me0 || nxs0) ? RANK_DIRTY : rk0;
+    }
+    if ((k1 >> lane) & 1ull) {
+      const uint32_t p = c0 + bits_below(k1);
+      scr[p] = me1 ? 256u + m : id1;
+      scr[128 + p] = (me1 || nxs1) ? RANK_DIRTY : rk1;
+    }
+    n = c0 + (uint32_t)__popcll(k1);
+    // (one wave writes and reads its own words: LDS operations of a wave are
+    // performed in order)
+    id0 = l0 < n ? scr[l0] : 0u;
+    const uint32_t r0 = l0 < n ? scr[128 + l0] : RANK_INF;
+    id1 = l1 < n ? scr[l1] : 0u;
+    const uint32_t r1 = l1 < n ? scr[128 + l1] : RANK_INF;
+    nx0 = next0();
+    nx1 = (uint32_t)__shfl_down((int)id1, 1, 64);
+    rk0 = r0;
+    if (r0 == RANK_DIRTY) rk0 = l0 + 1u < n ? probe_rank(tb.slots, tb.shift, id0, nx0) : RANK_INF;
+    rk1 = r1;
+    if (r1 == RANK_DIRTY) rk1 = l1 + 1u < n ? probe_rank(tb.slots, tb.shift, id1, nx1) : RANK_INF;
+  }
+  if (l0 < n) out(lane, id0);
+  if (l1 < n) out(64 + lane, id1);
+  return n;
+}
+
+// ---------------------------------------------------------------------------
 // NW waves over rows of 64 tokens.  I0/I1 (IDs) and R0/R1 (pair ranks) are
 // double buffers of at least L words, `sel` holds rows(L) + 1 selection masks;
 // they may live in LDS or in global memory (visible to the whole block).

@@ -177,7 +177,8 @@ constexpr int PT_HALO = 32;                        // context bytes each side
 constexpr int PT_OWN = PT_WIN - 2 * PT_HALO;       // bytes a tile decides
 
 constexpr int SMALL_MAX = 16;                      // thread-per-unit limit (bytes)
-constexpr int WAVE_MAX = 64;                       // wave-per-unit limit (bytes)
+constexpr int WAVE_MAX = 128;                      // wave-per-unit limit (bytes)
+constexpr int ROWS_LDS = 480;                      // longer units: rows in LDS up to this length
 
 inline uint32_t n_tiles_for(uint32_t n) { return (n + PT_OWN - 1) / PT_OWN; }
 

@@ -227,6 +227,13 @@ union PhaseMem {
     uint32_t tok[PT_WIN];     // tokens of unit k at tok[ustart[k] ..]
     uint16_t uoff[PT_WIN];    // first output of each unit within the tile
     uint16_t small[PT_OWN + 2];  // units of 3..16 bytes, sorted by length
+    union {
+      uint32_t wscr[PT_THREADS / 64][256];  // wave engine for 65..128 bytes: one area per wave
+      struct {                              // block engine for 129..ROWS_LDS bytes
+        uint32_t I0[ROWS_LDS], I1[ROWS_LDS], R0[ROWS_LDS], R1[ROWS_LDS];
+        uint64_t sel[ROWS_LDS / 64 + 2];
+      } rows;
+    } x;
   } b;
 };
 
@@ -1048,16 +1055,17 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     for (uint32_t i = ((uint32_t)wave + NWV - first) % NWV; i < n_med; i += NWV) {
       const uint32_t u = sh.med[i];
       if (u == U_INCOMING) {
-        const uint32_t c = bpe_wave(
-            L_inc, [&](int j) -> uint32_t { return inc_byte((uint32_t)j); }, tb,
-            [&](int j, uint32_t id) { inc_out((uint32_t)j, id); });
+        auto by = [&](int j) -> uint32_t { return inc_byte((uint32_t)j); };
+        auto ot = [&](int j, uint32_t id) { inc_out((uint32_t)j, id); };
+        const uint32_t c =
+            L_inc <= 64u ? bpe_wave(L_inc, by, tb, ot) : bpe_wave2(L_inc, by, tb, sh.ph.b.x.wscr[wave], ot);
         if (lane == 0) sh.inc_cnt = c;
       } else {
         const uint32_t a = sh.ustart[u];
         const uint32_t L = sh.ustart[u + 1] - a;
-        const uint32_t c = bpe_wave(
-            L, [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb,
-            [&](int j, uint32_t id) { sh.ph.b.tok[a + j] = id; });
+        auto by = [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; };
+        auto ot = [&](int j, uint32_t id) { sh.ph.b.tok[a + j] = id; };
+        const uint32_t c = L <= 64u ? bpe_wave(L, by, tb, ot) : bpe_wave2(L, by, tb, sh.ph.b.x.wscr[wave], ot);
         if (lane == 0) sh.ucnt[u] = (uint16_t)c;
       }
     }
@@ -1065,9 +1073,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   __syncthreads();
 
   // ---- BPE, whole block per longer unit ------------------------------------
-  // (rare in text: rows in global scratch at the unit's byte offset; the
-  // selection masks of a unit of L > 64 bytes at byte s take words
-  // [s/16, s/16 + L/64 + 2), which never reach the next unit's)
+  // (rare in text: rows in LDS up to ROWS_LDS bytes, else in global scratch
+  // at the unit's byte offset; there the selection masks of a unit of L > 64
+  // bytes at byte s take words [s/16, s/16 + L/64 + 2), which never reach the
+  // next unit's)
   const uint32_t n_big = sh.n_big;
 #pragma unroll 1
   for (uint32_t i = 0; i < n_big; ++i) {
@@ -1076,17 +1085,31 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     const uint32_t a = inc_u ? 0u : sh.ustart[u];
     const uint32_t L = inc_u ? L_inc : sh.ustart[u + 1] - a;
     const uint64_t s0 = inc_u ? (uint64_t)s_prev : (uint64_t)(w0 + a);
-    uint32_t* sc = w.scratch;
-    const uint64_t nn = (uint64_t)n;
-    uint64_t* sel = reinterpret_cast<uint64_t*>(sc + 4 * nn) + s0 / 16;
+    uint32_t *I0, *I1, *R0, *R1;
+    uint64_t* sel;
+    if (L <= (uint32_t)ROWS_LDS) {
+      auto& rw = sh.ph.b.x.rows;
+      I0 = rw.I0;
+      I1 = rw.I1;
+      R0 = rw.R0;
+      R1 = rw.R1;
+      sel = rw.sel;
+    } else {
+      uint32_t* sc = w.scratch;
+      const uint64_t nn = (uint64_t)n;
+      I0 = sc + s0;
+      I1 = sc + nn + s0;
+      R0 = sc + 2 * nn + s0;
+      R1 = sc + 3 * nn + s0;
+      sel = reinterpret_cast<uint64_t*>(sc + 4 * nn) + s0 / 16;
+    }
     uint32_t c;
     if (inc_u) {
-      c = bpe_rows<PT_THREADS / 64>(L, inc_byte, tb, sc + s0, sc + nn + s0, sc + 2 * nn + s0, sc + 3 * nn + s0, sel,
-                                    sh.rows, inc_out);
+      c = bpe_rows<PT_THREADS / 64>(L, inc_byte, tb, I0, I1, R0, R1, sel, sh.rows, inc_out);
     } else {
       c = bpe_rows<PT_THREADS / 64>(
-          L, [&](uint32_t j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb, sc + s0, sc + nn + s0,
-          sc + 2 * nn + s0, sc + 3 * nn + s0, sel, sh.rows, [&](uint32_t j, uint32_t id) { sh.ph.b.tok[a + j] = id; });
+          L, [&](uint32_t j) -> uint32_t { return sh.buf[PT_PAD + a + j]; }, tb, I0, I1, R0, R1, sel, sh.rows,
+          [&](uint32_t j, uint32_t id) { sh.ph.b.tok[a + j] = id; });
     }
     if (tid == 0) {
       if (inc_u) sh.inc_cnt = c;

@@ -46,7 +46,8 @@ def _long_texts(k, seed):
     spaces = _clique(k, b" ")
     assert len(letters) >= 2, "table %d has no two-letter junction clique" % k
     texts = []
-    for n in (17, 40, 63, 64, 65, 100, 300, 700, 1000, 1500, 2000, 2047, 2048, 2049, 2100, 3000, 5000):
+    for n in (17, 40, 63, 64, 65, 100, 127, 128, 129, 300, 479, 480, 481, 700, 1000, 1500, 2000, 2047, 2048, 2049,
+              2100, 3000, 5000):
         body = bytes(rng.choice(letters) for _ in range(n))
         texts.append(b"x " + body + b" y")
         texts.append(body)
