@@ -57,10 +57,10 @@ struct tt_tokenizer {
   int device = 0;
   int profile = 0;  // calls whose stage events are kept (0: no events)
   u64x2* d_slots = nullptr;    // cuckoo buckets
-  uint32_t shift = 0;          // 32 - log2(bucket count)
+  uint32_t nb = 0;             // merge-table buckets
   uint32_t* d_pair0 = nullptr;  // [65536] byte-pair ranks
   u32x4* d_dict = nullptr;      // whole-unit dictionary
-  uint32_t dshift = 0;
+  uint32_t dnb = 0;             // dictionary buckets
   int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
   uint32_t n_ids = 0;
   uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
@@ -206,7 +206,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_ids = out_ids;
   w.out_len = out_len;
   w.out_doc_off = out_docs;
-  DevTables tb{h->d_slots, h->shift, h->d_pair0, h->d_join, h->d_ext, h->n_ids, h->d_dict, h->dshift};
+  DevTables tb{h->d_slots, h->nb, h->d_pair0, h->d_join, h->d_ext, h->n_ids, h->d_dict, h->dnb};
   const int ring = h->profile;
   if (ring != s->ring) {  // (re)size the event ring
     for (auto e : s->ev)
@@ -300,17 +300,14 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   for (int32_t r = 0; r < n_merges; ++r) ext[256 + r] = merges[r].result;
 
   // byte-pair ranks, and the two-choice cuckoo table of all pairs (two slots
-  // per bucket, load <= 1/2; the table doubles if an insertion cannot be placed)
+  // per bucket, load 0.8; the table grows by 1/8 while an insertion cannot be
+  // placed)
   std::vector<uint32_t> pair0(65536, RANK_INF);
   for (int32_t r = 0; r < n_merges; ++r) {
     const int32_t a = internal[merges[r].left], b = internal[merges[r].right];
     if (a < 256 && b < 256) pair0[((uint32_t)a << 8) | (uint32_t)b] = (uint32_t)r;
   }
-  uint32_t nb = 16, bits = 4;
-  while (nb < (uint32_t)n_merges) {
-    nb <<= 1;
-    ++bits;
-  }
+  uint32_t nb = (uint32_t)((uint64_t)n_merges * 5 / 8) + 16;
   std::vector<uint64_t> slots;
   for (;;) {
     slots.assign(2 * (size_t)nb, SLOT_EMPTY);
@@ -322,7 +319,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       ok = false;
       for (int kick = 0; kick < 1000; ++kick) {
         const uint32_t a = (uint32_t)(item & ID_LIMIT), b = (uint32_t)((item >> ID_BITS) & ID_LIMIT);
-        const uint32_t b1 = pair_hash(a, b, 32 - bits), b2 = pair_hash2(a, b, 32 - bits);
+        const uint32_t b1 = bucket_of(pair_hash(a, b), nb), b2 = bucket_of(pair_hash2(a, b), nb);
         size_t free_at = SIZE_MAX;
         for (size_t c : {2 * (size_t)b1, 2 * (size_t)b1 + 1, 2 * (size_t)b2, 2 * (size_t)b2 + 1})
           if (slots[c] == SLOT_EMPTY) {
@@ -342,8 +339,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       }
     }
     if (ok) break;
-    nb <<= 1;
-    ++bits;
+    nb += nb / 8;
     if (nb > (1u << 28)) return TT_ERR_OOM;
   }
 
@@ -351,7 +347,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   // spelling of a merge result and whose BPE (computed here, exactly as the
   // device computes it) is that single token
   std::vector<u32x4> dict;
-  uint32_t dbits = 4;
+  uint32_t dnb = 16;
   {
     std::unordered_map<uint64_t, uint32_t> rank;
     rank.reserve((size_t)n_merges * 2 + 16);
@@ -400,43 +396,40 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       for (int i = 0; i < L; ++i) e.w[i >> 2] |= (uint32_t)vptr(res)[i] << (8 * (i & 3));
       entries.push_back(e);
     }
-    uint32_t nd = 16;
-    while (nd < 2 * (uint32_t)entries.size()) {
-      nd <<= 1;
-      ++dbits;
-    }
+    // two entries per bucket, load 0.8; grows by 1/8 while an entry cannot be placed
+    dnb = (uint32_t)(entries.size() * 5 / 8) + 16;
     for (;;) {
-      dict.assign(nd, u32x4{0u, 0u, 0u, 0u});
+      dict.assign(2 * (size_t)dnb, u32x4{0u, 0u, 0u, 0u});
       uint64_t rng = 0xD1B54A32D192ED03ull;
       bool ok = true;
       for (size_t i = 0; i < entries.size() && ok; ++i) {
         u32x4 item{entries[i].w[0], entries[i].w[1], entries[i].w[2], (entries[i].id << 4) | entries[i].len};
         ok = false;
-        for (int kick = 0; kick < 1000; ++kick) {
+        for (int kick = 0; kick < 2000; ++kick) {
           const uint32_t len = item.w & 15u;
-          const uint32_t b1 = unit_hash(item.x, item.y, item.z, len, 32 - dbits);
-          const uint32_t b2 = unit_hash2(item.x, item.y, item.z, len, 32 - dbits);
-          if (dict[b1].w == 0u) {
-            dict[b1] = item;
-            ok = true;
-            break;
-          }
-          if (dict[b2].w == 0u) {
-            dict[b2] = item;
+          const size_t b1 = 2 * (size_t)bucket_of(unit_hash(item.x, item.y, item.z, len), dnb);
+          const size_t b2 = 2 * (size_t)bucket_of(unit_hash2(item.x, item.y, item.z, len), dnb);
+          size_t free_at = SIZE_MAX;
+          for (size_t c : {b1, b1 + 1, b2, b2 + 1})
+            if (dict[c].w == 0u) {
+              free_at = c;
+              break;
+            }
+          if (free_at != SIZE_MAX) {
+            dict[free_at] = item;
             ok = true;
             break;
           }
           rng ^= rng << 13;
           rng ^= rng >> 7;
           rng ^= rng << 17;
-          const uint32_t v = (rng & 1) ? b1 : b2;
+          const size_t v = ((rng & 2) ? b1 : b2) + (rng & 1);
           std::swap(item, dict[v]);
         }
       }
       if (ok) break;
-      nd <<= 1;
-      ++dbits;
-      if (nd > (1u << 28)) return TT_ERR_OOM;
+      dnb += dnb / 8;
+      if (dnb > (1u << 27)) return TT_ERR_OOM;
     }
   }
 
@@ -456,8 +449,8 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   h->pattern = pattern_id;
   h->n_merges = n_merges;
   h->vocab_size = vocab_size;
-  h->shift = 32 - bits;
-  h->dshift = 32 - dbits;
+  h->nb = nb;
+  h->dnb = dnb;
   h->n_ids = n_ids;
   if (hipGetDevice(&h->device) != hipSuccess) {
     delete h;

@@ -82,7 +82,7 @@ __device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) {
 __device__ __forceinline__ uint32_t bpe_thread(uint32_t L, uint32_t* ids, const DevTables& tb) {
   constexpr int S = SMALL_MAX;
   const u64x2* __restrict__ tab = tb.slots;
-  const uint32_t shift = tb.shift;
+  const uint32_t nb = tb.nb;
   uint32_t rk[S];
   {
     uint32_t b[S];
@@ -116,8 +116,8 @@ __device__ __forceinline__ uint32_t bpe_thread(uint32_t L, uint32_t* ids, const 
     ids[k] = nid;
     // both lookups are issued unconditionally (a missing neighbour looks up a
     // harmless pair) so that their four loads are in flight together
-    const ProbeIssued pr = probe_issue(tab, shift, nid, right);
-    const ProbeIssued pl = probe_issue(tab, shift, left, nid);
+    const ProbeIssued pr = probe_issue(tab, nb, nid, right);
+    const ProbeIssued pl = probe_issue(tab, nb, left, nid);
     const uint32_t rr = hr ? probe_finish(pr, nid, right) : RANK_INF;
     const uint32_t rl = hl ? probe_finish(pl, left, nid) : RANK_INF;
 #pragma unroll
@@ -167,7 +167,7 @@ __device__ __forceinline__ uint32_t bpe_wave(uint32_t L, ByteF byte, const DevTa
     rk = RANK_INF;
     if ((uint32_t)lane < n) {
       rk = r2;
-      if (r2 == RANK_DIRTY) rk = (uint32_t)lane + 1u < n ? probe_rank(tb.slots, tb.shift, id, idn) : RANK_INF;
+      if (r2 == RANK_DIRTY) rk = (uint32_t)lane + 1u < n ? probe_rank(tb.slots, tb.nb, id, idn) : RANK_INF;
     }
   }
   if ((uint32_t)lane < n) out(lane, id);
@@ -231,9 +231,9 @@ __device__ __forceinline__ uint32_t bpe_wave2(uint32_t L, ByteF byte, const DevT
     nx0 = next0();
     nx1 = (uint32_t)__shfl_down((int)id1, 1, 64);
     rk0 = r0;
-    if (r0 == RANK_DIRTY) rk0 = l0 + 1u < n ? probe_rank(tb.slots, tb.shift, id0, nx0) : RANK_INF;
+    if (r0 == RANK_DIRTY) rk0 = l0 + 1u < n ? probe_rank(tb.slots, tb.nb, id0, nx0) : RANK_INF;
     rk1 = r1;
-    if (r1 == RANK_DIRTY) rk1 = l1 + 1u < n ? probe_rank(tb.slots, tb.shift, id1, nx1) : RANK_INF;
+    if (r1 == RANK_DIRTY) rk1 = l1 + 1u < n ? probe_rank(tb.slots, tb.nb, id1, nx1) : RANK_INF;
   }
   if (l0 < n) out(lane, id0);
   if (l1 < n) out(64 + lane, id1);
@@ -368,7 +368,7 @@ __device__ uint32_t bpe_rows(uint32_t L, ByteF byte, const DevTables& tb, uint32
     n = n2;
     // 4. ranks of the pairs next to the merges
     for (uint32_t i = tid; i < n; i += NT) {
-      if (R2[i] == RANK_DIRTY) R2[i] = i + 1 < n ? probe_rank(tb.slots, tb.shift, I2[i], I2[i + 1]) : RANK_INF;
+      if (R2[i] == RANK_DIRTY) R2[i] = i + 1 < n ? probe_rank(tb.slots, tb.nb, I2[i], I2[i + 1]) : RANK_INF;
     }
     __syncthreads();
     cur ^= 1;

@@ -54,12 +54,14 @@ __host__ __device__ inline uint64_t slot_key(uint32_t a, uint32_t b) {
   return (uint64_t)a | ((uint64_t)b << ID_BITS);
 }
 
-// Two bucket hashes of a pair (multiply-shift; `shift` = 32 - log2(buckets)).
-__host__ __device__ inline uint32_t pair_hash(uint32_t a, uint32_t b, uint32_t shift) {
-  return ((a * 0x9E3779B1u + b) * 0x85EBCA77u) >> shift;
-}
-__host__ __device__ inline uint32_t pair_hash2(uint32_t a, uint32_t b, uint32_t shift) {
-  return (((b * 0xC2B2AE3Du) ^ (a + 0x165667B1u)) * 0x27D4EB2Fu) >> shift;
+// Bucket of a 32-bit hash among nb buckets: the high word of hash * nb (any
+// bucket count; the high bits of a multiplicative hash are the good ones).
+__host__ __device__ inline uint32_t bucket_of(uint32_t h, uint32_t nb) { return (uint32_t)(((uint64_t)h * nb) >> 32); }
+
+// Two bucket hashes of a pair (multiplicative).
+__host__ __device__ inline uint32_t pair_hash(uint32_t a, uint32_t b) { return (a * 0x9E3779B1u + b) * 0x85EBCA77u; }
+__host__ __device__ inline uint32_t pair_hash2(uint32_t a, uint32_t b) {
+  return ((b * 0xC2B2AE3Du) ^ (a + 0x165667B1u)) * 0x27D4EB2Fu;
 }
 
 // The merge table is a two-choice cuckoo table of 16-byte buckets holding
@@ -72,9 +74,9 @@ typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
 struct ProbeIssued {
   u64x2 x, y;
 };
-__device__ __forceinline__ ProbeIssued probe_issue(const u64x2* __restrict__ tab, uint32_t shift, uint32_t a,
+__device__ __forceinline__ ProbeIssued probe_issue(const u64x2* __restrict__ tab, uint32_t nb, uint32_t a,
                                                    uint32_t b) {
-  return ProbeIssued{tab[pair_hash(a, b, shift)], tab[pair_hash2(a, b, shift)]};
+  return ProbeIssued{tab[bucket_of(pair_hash(a, b), nb)], tab[bucket_of(pair_hash2(a, b), nb)]};
 }
 __device__ __forceinline__ uint32_t probe_finish(const ProbeIssued& p, uint32_t a, uint32_t b) {
   const uint64_t key = slot_key(a, b);
@@ -86,50 +88,57 @@ __device__ __forceinline__ uint32_t probe_finish(const ProbeIssued& p, uint32_t 
   return hit == SLOT_EMPTY ? RANK_INF : (uint32_t)(hit >> (2 * ID_BITS));
 }
 // Rank of the pair (a, b), or RANK_INF if no merge joins it.
-__device__ __forceinline__ uint32_t probe_rank(const u64x2* __restrict__ tab, uint32_t shift, uint32_t a,
+__device__ __forceinline__ uint32_t probe_rank(const u64x2* __restrict__ tab, uint32_t nb, uint32_t a,
                                                uint32_t b) {
-  return probe_finish(probe_issue(tab, shift, a, b), a, b);
+  return probe_finish(probe_issue(tab, nb, a, b), a, b);
 }
 
 // Whole-unit dictionary: a unit of 3..DICT_MAX bytes whose BPE is a single
 // token is found with one lookup.  An entry holds the unit's bytes (zero
 // padded, little-endian words), and its length and token: (id << 4) | length.
-// Two-choice cuckoo table of one entry per bucket; a unit lives in one of the
-// two buckets its hashes name.
+// Two-choice cuckoo table of two entries per bucket; a unit lives in one of
+// the two buckets its hashes name (four 16-byte loads, one round trip).
 constexpr int DICT_MAX = 12;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__host__ __device__ inline uint32_t unit_hash(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t len, uint32_t shift) {
+__host__ __device__ inline uint32_t unit_hash(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t len) {
   uint32_t x = w0 * 0x9E3779B1u + w1 * 0x85EBCA77u + w2 * 0xC2B2AE3Du + len;
   x ^= x >> 15;
-  return (x * 0x2C1B3C6Du) >> shift;
+  return x * 0x2C1B3C6Du;
 }
-__host__ __device__ inline uint32_t unit_hash2(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t len, uint32_t shift) {
+__host__ __device__ inline uint32_t unit_hash2(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t len) {
   uint32_t x = (w0 * 0x27D4EB2Fu) ^ (w1 * 0x165667B1u) ^ (w2 * 0xD3A2646Cu) ^ (len * 0xFD7046C5u);
   x ^= x >> 13;
-  return (x * 0x297A2D39u) >> shift;
+  return x * 0x297A2D39u;
 }
 constexpr uint32_t DICT_NONE = 0xFFFFFFFFu;
-__device__ __forceinline__ uint32_t dict_find(const u32x4* __restrict__ dict, uint32_t shift, uint32_t w0,
-                                              uint32_t w1, uint32_t w2, uint32_t len) {
-  const u32x4 a = dict[unit_hash(w0, w1, w2, len, shift)];
-  const u32x4 b = dict[unit_hash2(w0, w1, w2, len, shift)];
-  const bool ha = a.x == w0 && a.y == w1 && a.z == w2 && (a.w & 15u) == len;
-  const bool hb = b.x == w0 && b.y == w1 && b.z == w2 && (b.w & 15u) == len;
-  return ha ? a.w >> 4 : hb ? b.w >> 4 : DICT_NONE;
+__device__ __forceinline__ bool dict_match(const u32x4& e, uint32_t w0, uint32_t w1, uint32_t w2, uint32_t len) {
+  return e.x == w0 && e.y == w1 && e.z == w2 && (e.w & 15u) == len;
+}
+__device__ __forceinline__ uint32_t dict_find(const u32x4* __restrict__ dict, uint32_t nb, uint32_t w0, uint32_t w1,
+                                              uint32_t w2, uint32_t len) {
+  const uint32_t b1 = 2u * bucket_of(unit_hash(w0, w1, w2, len), nb);
+  const uint32_t b2 = 2u * bucket_of(unit_hash2(w0, w1, w2, len), nb);
+  const u32x4 e0 = dict[b1], e1 = dict[b1 + 1], e2 = dict[b2], e3 = dict[b2 + 1];
+  uint32_t r = DICT_NONE;
+  r = dict_match(e0, w0, w1, w2, len) ? e0.w >> 4 : r;
+  r = dict_match(e1, w0, w1, w2, len) ? e1.w >> 4 : r;
+  r = dict_match(e2, w0, w1, w2, len) ? e2.w >> 4 : r;
+  r = dict_match(e3, w0, w1, w2, len) ? e3.w >> 4 : r;
+  return r;
 }
 
 // Everything a kernel needs to know about a tokenizer handle.
 struct DevTables {
   const u64x2* slots;       // cuckoo buckets of two slots: key (left | right << 21), rank in bits 42..63
-  uint32_t shift;           // 32 - log2(bucket count)
+  uint32_t nb;              // bucket count
   const uint32_t* pair0;    // [65536] rank of the byte pair (x << 8 | y), or RANK_INF
   const uint32_t* join;     // [2048] bit (x << 8 | y): some merge joins a token ending
                             // in byte x to a token starting with byte y
   const int32_t* ext_id;    // [n_ids] caller's ID of every internal ID
   uint32_t n_ids;           // 256 + M
-  const u32x4* dict;        // whole-unit dictionary
-  uint32_t dshift;          // 32 - log2(dictionary buckets)
+  const u32x4* dict;        // whole-unit dictionary (two entries per bucket)
+  uint32_t dnb;             // dictionary bucket count
 };
 
 // ---------------------------------------------------------------------------

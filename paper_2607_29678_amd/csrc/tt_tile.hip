@@ -988,7 +988,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
           if ((uint32_t)j < L) bj = inc_u ? inc_byte((uint32_t)j) : (uint32_t)sh.buf[PT_PAD + a + j];
           kw[j >> 2] |= bj << (8 * (j & 3));
         }
-        found = dict_find(tb.dict, tb.dshift, kw[0], kw[1], kw[2], L);
+        found = dict_find(tb.dict, tb.dnb, kw[0], kw[1], kw[2], L);
       }
       if (found != DICT_NONE) {
         if (inc_u) {
