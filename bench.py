@@ -11,7 +11,9 @@ HIP events between its stages on the same stream; their average gives the
 duration of the dominant kernel (the tile kernel) for the roofline.
 Per-request latencies (enqueue to completion, input in HBM) give P50/P90/P99
 in a second pass; the host-to-host latency through ``tt_encode`` (PCIe copies
-included) is reported separately.  The CPU oracle is timed on the same timed
+included), a steady-state P50 (100 re-encodes of one sample) and the
+host-to-host time of a 64 x 16,384-char document batch are reported
+separately.  The CPU oracle is timed on the same timed
 samples, single-threaded, and its IDs are compared with the GPU's.
 
 ``--calibrate-copy`` first runs a plain int32 copy kernel of 64 MiB read +
@@ -156,6 +158,35 @@ def main():
         tok.encode(texts[i], sid)
         host_lat.append((time.perf_counter() - a) * 1e3)
 
+    # --- steady state: 100 re-encodes of one sample (input in HBM) --------------
+    steady = []
+    for _ in range(100):
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        run(timed[0])
+        stream.synchronize()
+        steady.append((time.perf_counter() - a) * 1e3)
+
+    # --- shape of the work: pieces of one sample (split-level export) ----------
+    n_pieces = len(tok.pretokenize(texts[timed[0]], sid))
+
+    # --- a batch of 64 independent 16,384-char documents (the stress config's
+    # batch, its own tokenizer), host to host through tt_encode_batch -----------
+    bmerges, bvb, bvo = load_table(5)
+    btok = Tokenizer(bmerges, bvb, bvo, textgen.CONFIGS[5]["pattern"])
+    docs = [d.encode("utf-8") for d in textgen.batch_docs()]
+    btok.encode_batch(docs, sid)
+    blat = []
+    for _ in range(10):
+        a = time.perf_counter()
+        btok.encode_batch(docs, sid)
+        blat.append((time.perf_counter() - a) * 1e3)
+    bchars = sum(len(d.decode("utf-8")) for d in docs)
+    batch = {"docs": len(docs), "chars": bchars, "bytes": sum(len(d) for d in docs),
+             "p50_ms_host_to_host": round(percentile(blat, 50), 4),
+             "chars_per_s": round(bchars / (percentile(blat, 50) * 1e-3), 1)}
+    btok.close()
+
     # --- roofline of the dominant kernel -------------------------------------
     # algorithmic bytes of one tile-kernel launch: the request's bytes are
     # read once and its token IDs written once (merge-table probes are L2
@@ -208,11 +239,14 @@ def main():
         "config": {"workload": "C%d: 1,000,000-char seeded %s request, %s-style pattern, %d merges"
                                % (k, "agent-transcript" if k == 3 else "multilingual agent-transcript",
                                   cfg["pattern"], cfg["merges"]),
-                   "chars": 1_000_000, "bytes_avg": int(B_avg), "tokens_avg": int(T_avg), "samples": len(timed)},
+                   "chars": 1_000_000, "bytes_avg": int(B_avg), "tokens_avg": int(T_avg), "samples": len(timed),
+                   "pieces_sample0": n_pieces},
         "p50_ms": round(percentile(lat, 50), 4),
         "p90_ms": round(percentile(lat, 90), 4),
         "p99_ms": round(percentile(lat, 99), 4),
         "host_to_host_p50_ms": round(percentile(host_lat, 50), 4),
+        "steady_state_p50_ms": round(percentile(steady, 50), 4),
+        "batch_64x16k": batch,
         "stage_ms": {s: round(v, 4) for s, v in stage_avg.items()},
         "roofline": roofline,
         "cpu_baseline": cpu,
