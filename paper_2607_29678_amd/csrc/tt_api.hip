@@ -61,6 +61,8 @@ struct tt_tokenizer {
   uint32_t* d_pair0 = nullptr;  // [65536] byte-pair ranks
   u32x4* d_dict = nullptr;      // whole-unit dictionary
   uint32_t dnb = 0;             // dictionary buckets
+  u32x4* d_dict2 = nullptr;     // long-unit dictionary
+  uint32_t dnb2 = 0;            // its buckets
   int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
   uint32_t n_ids = 0;
   uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
@@ -206,7 +208,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_ids = out_ids;
   w.out_len = out_len;
   w.out_doc_off = out_docs;
-  DevTables tb{h->d_slots, h->nb, h->d_pair0, h->d_join, h->d_ext, h->n_ids, h->d_dict, h->dnb};
+  DevTables tb{h->d_slots, h->nb, h->d_pair0, h->d_join, h->d_ext, h->n_ids, h->d_dict, h->dnb, h->d_dict2, h->dnb2};
   const int ring = h->profile;
   if (ring != s->ring) {  // (re)size the event ring
     for (auto e : s->ev)
@@ -343,11 +345,12 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
     if (nb > (1u << 28)) return TT_ERR_OOM;
   }
 
-  // whole-unit dictionary: every byte string of 3..DICT_MAX bytes that is the
-  // spelling of a merge result and whose BPE (computed here, exactly as the
-  // device computes it) is that single token
-  std::vector<u32x4> dict;
-  uint32_t dnb = 16;
+  // whole-unit dictionaries: every byte string of 3..DICT2_MAX bytes that is
+  // the spelling of a merge result and whose BPE (computed here, exactly as the
+  // device computes it) is that single token; strings of up to DICT_MAX bytes
+  // go to the first, longer ones to the second
+  std::vector<u32x4> dict, dict2;
+  uint32_t dnb = 16, dnb2 = 16;
   {
     std::unordered_map<uint64_t, uint32_t> rank;
     rank.reserve((size_t)n_merges * 2 + 16);
@@ -358,15 +361,15 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       return it == rank.end() ? RANK_INF : it->second;
     };
     struct Entry {
-      uint32_t w[3], len, id;
+      uint32_t w[6], len, id;
     };
-    std::vector<Entry> entries;
+    std::vector<Entry> entries, entries2;
     std::unordered_set<std::string> seen;
-    uint32_t ids[DICT_MAX], rk[DICT_MAX];
+    uint32_t ids[DICT2_MAX], rk[DICT2_MAX];
     for (int32_t r = 0; r < n_merges; ++r) {
       const int32_t res = merges[r].result;
       const int64_t L = vlen(res);
-      if (L < 3 || L > DICT_MAX) continue;
+      if (L < 3 || L > DICT2_MAX) continue;
       std::string key(reinterpret_cast<const char*>(vptr(res)), (size_t)L);
       if (!seen.insert(key).second) continue;
       // greedy lowest-rank BPE of the spelling, leftmost among equal ranks
@@ -392,9 +395,9 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
         if (k > 0) rk[k - 1] = lookup(ids[k - 1], ids[k]);
       }
       if (n != 1) continue;
-      Entry e{{0u, 0u, 0u}, (uint32_t)L, ids[0]};
+      Entry e{{0u, 0u, 0u, 0u, 0u, 0u}, (uint32_t)L, ids[0]};
       for (int i = 0; i < L; ++i) e.w[i >> 2] |= (uint32_t)vptr(res)[i] << (8 * (i & 3));
-      entries.push_back(e);
+      (L <= DICT_MAX ? entries : entries2).push_back(e);
     }
     // two entries per bucket, load 0.8; grows by 1/8 while an entry cannot be placed
     dnb = (uint32_t)(entries.size() * 5 / 8) + 16;
@@ -431,6 +434,53 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       dnb += dnb / 8;
       if (dnb > (1u << 27)) return TT_ERR_OOM;
     }
+    // long units: one entry of two words per bucket, load below 1/2
+    dnb2 = (uint32_t)(entries2.size() * 2) + 16;
+    for (;;) {
+      dict2.assign(2 * (size_t)dnb2, u32x4{0u, 0u, 0u, 0u});
+      uint64_t rng = 0x9E3779B97F4A7C15ull;
+      bool ok = true;
+      for (size_t i = 0; i < entries2.size() && ok; ++i) {
+        const Entry* item = &entries2[i];
+        Entry held;
+        ok = false;
+        for (int kick = 0; kick < 1000; ++kick) {
+          const uint32_t* q = item->w;
+          const size_t b1 = 2 * (size_t)bucket_of(unit_hash6(q[0], q[1], q[2], q[3], q[4], q[5], item->len), dnb2);
+          const size_t b2 = 2 * (size_t)bucket_of(unit_hash6b(q[0], q[1], q[2], q[3], q[4], q[5], item->len), dnb2);
+          const u32x4 x0{q[0], q[1], q[2], q[3]}, x1{q[4], q[5], (item->id << 5) | item->len, 0u};
+          size_t at = SIZE_MAX;
+          if (dict2[b1 + 1].z == 0u) at = b1;
+          else if (dict2[b2 + 1].z == 0u) at = b2;
+          if (at != SIZE_MAX) {
+            dict2[at] = x0;
+            dict2[at + 1] = x1;
+            ok = true;
+            break;
+          }
+          rng ^= rng << 13;
+          rng ^= rng >> 7;
+          rng ^= rng << 17;
+          const size_t v = (rng & 1) ? b1 : b2;
+          Entry out;
+          out.w[0] = dict2[v].x;
+          out.w[1] = dict2[v].y;
+          out.w[2] = dict2[v].z;
+          out.w[3] = dict2[v].w;
+          out.w[4] = dict2[v + 1].x;
+          out.w[5] = dict2[v + 1].y;
+          out.len = dict2[v + 1].z & 31u;
+          out.id = dict2[v + 1].z >> 5;
+          dict2[v] = x0;
+          dict2[v + 1] = x1;
+          held = out;
+          item = &held;
+        }
+      }
+      if (ok) break;
+      dnb2 += dnb2 / 8;
+      if (dnb2 > (1u << 27)) return TT_ERR_OOM;
+    }
   }
 
   // junction byte pairs: the first merge that ever joins across a byte
@@ -451,6 +501,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   h->vocab_size = vocab_size;
   h->nb = nb;
   h->dnb = dnb;
+  h->dnb2 = dnb2;
   h->n_ids = n_ids;
   if (hipGetDevice(&h->device) != hipSuccess) {
     delete h;
@@ -459,6 +510,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   if (hipMalloc(reinterpret_cast<void**>(&h->d_slots), 16 * (size_t)nb) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_pair0), sizeof(uint32_t) * 65536) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_dict), sizeof(u32x4) * dict.size()) != hipSuccess ||
+      hipMalloc(reinterpret_cast<void**>(&h->d_dict2), sizeof(u32x4) * dict2.size()) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_ext), sizeof(int32_t) * n_ids) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_join), sizeof(uint32_t) * 2048) != hipSuccess) {
     tt_destroy(h);
@@ -467,6 +519,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   if (hipMemcpy(h->d_slots, slots.data(), 16 * (size_t)nb, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_pair0, pair0.data(), sizeof(uint32_t) * 65536, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_dict, dict.data(), sizeof(u32x4) * dict.size(), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(h->d_dict2, dict2.data(), sizeof(u32x4) * dict2.size(), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_ext, ext.data(), sizeof(int32_t) * n_ids, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_join, join.data(), sizeof(uint32_t) * 2048, hipMemcpyHostToDevice) != hipSuccess) {
     tt_destroy(h);
@@ -485,6 +538,7 @@ void tt_destroy(tt_tokenizer* h) {
   if (h->d_ext) (void)hipFree(h->d_ext);
   if (h->d_pair0) (void)hipFree(h->d_pair0);
   if (h->d_dict) (void)hipFree(h->d_dict);
+  if (h->d_dict2) (void)hipFree(h->d_dict2);
   if (h->d_join) (void)hipFree(h->d_join);
   delete h;
 }

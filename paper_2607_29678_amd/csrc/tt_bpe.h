@@ -70,48 +70,49 @@ __device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) {
 // ---------------------------------------------------------------------------
 // One thread, at most 16 bytes.  The unit's tokens live in its own LDS words
 // ids[0..L) (the caller puts the bytes there; merged tokens overwrite their
-// left operand in place, and the tokens end compacted in ids[0..count)); the
-// pair ranks stay in registers.  A merge clears the right token's bit in an
-// alive mask instead of shifting the tail.  A pair's rank is kept as
-// (rank << 4) | position so that one unsigned minimum finds the lowest rank
-// and, among equal ranks (the same pair), the leftmost occurrence.  The chain
-// is one round trip for the initial byte pairs (all loads in flight at once)
-// and one per merge (its two neighbour lookups overlap).  Returns the number
-// of tokens.
+// left operand in place, and the tokens end compacted in ids[0..count)).  The
+// rank of the pair at slot j is kept in LDS at rk[j * TH_THREADS]: the caller
+// passes its own column of a [SMALL_MAX - 1][TH_THREADS] array (the last slot
+// never has a pair), so the lanes of a wave never share a bank.  A rank is
+// kept as (rank << 4) | j, so that one unsigned minimum finds the lowest rank
+// and, among equal ranks (the same pair), the leftmost occurrence; a merge
+// rewrites at most three slots with three stores.  A merge clears the right
+// token's bit in an alive mask instead of shifting the tail.  The chain is one
+// round trip for the initial byte pairs (all loads in flight at once) and one
+// per merge (its two neighbour lookups overlap).  Returns the number of tokens.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t bpe_thread(uint32_t L, uint32_t* ids, const DevTables& tb) {
+__device__ __forceinline__ uint32_t bpe_thread(uint32_t L, uint32_t* ids, uint32_t* rk, const DevTables& tb) {
   constexpr int S = SMALL_MAX;
+  constexpr int ST = TH_THREADS;
   const u64x2* __restrict__ tab = tb.slots;
   const uint32_t nb = tb.nb;
-  uint32_t rk[S];
   {
-    uint32_t b[S];
+    uint32_t b[S], r[S - 1];
 #pragma unroll
     for (int j = 0; j < S; ++j) b[j] = (uint32_t)j < L ? ids[j] : 0u;
     // every initial rank load is issued before any is used (no branches)
 #pragma unroll
-    for (int j = 0; j < S - 1; ++j) rk[j] = tb.pair0[(b[j] << 8) | b[j + 1]];
-  }
+    for (int j = 0; j < S - 1; ++j) r[j] = tb.pair0[(b[j] << 8) | b[j + 1]];
 #pragma unroll
-  for (int j = 0; j < S - 1; ++j)
-    rk[j] = ((uint32_t)(j + 1) < L && rk[j] != RANK_INF) ? ((rk[j] << 4) | (uint32_t)j) : RANK_INF;
-  rk[S - 1] = RANK_INF;
+    for (int j = 0; j < S - 1; ++j)
+      rk[j * ST] = ((uint32_t)(j + 1) < L && r[j] != RANK_INF) ? ((r[j] << 4) | (uint32_t)j) : RANK_INF;
+  }
   uint32_t alive = (1u << L) - 1u;  // L <= 16
   for (;;) {
     uint32_t best = RANK_INF;
 #pragma unroll
-    for (int j = 0; j < S - 1; ++j) best = min(best, rk[j]);
+    for (int j = 0; j < S - 1; ++j) best = min(best, rk[j * ST]);
     if (best == RANK_INF) break;
-    const int k = (int)(best & 15u);
+    const uint32_t k = best & 15u;
     const uint32_t nid = 256u + (best >> 4);
     // token k absorbs the next live token m
-    const int m = __builtin_ctz(alive & ~((2u << k) - 1u));
+    const uint32_t m = (uint32_t)__builtin_ctz(alive & ~((2u << k) - 1u));
     alive &= ~(1u << m);
     const uint32_t above_m = alive & ~((2u << m) - 1u);
     const uint32_t below_k = alive & ((1u << k) - 1u);
     const bool hr = above_m != 0u, hl = below_k != 0u;
-    const uint32_t right = ids[hr ? __builtin_ctz(above_m) : k];
-    const int l_i = hl ? 31 - __builtin_clz(below_k) : k;
+    const uint32_t right = ids[hr ? (uint32_t)__builtin_ctz(above_m) : k];
+    const uint32_t l_i = hl ? 31u - (uint32_t)__builtin_clz(below_k) : k;
     const uint32_t left = ids[l_i];
     ids[k] = nid;
     // both lookups are issued unconditionally (a missing neighbour looks up a
@@ -119,13 +120,10 @@ __device__ __forceinline__ uint32_t bpe_thread(uint32_t L, uint32_t* ids, const 
     const ProbeIssued pr = probe_issue(tab, nb, nid, right);
     const ProbeIssued pl = probe_issue(tab, nb, left, nid);
     const uint32_t rr = hr ? probe_finish(pr, nid, right) : RANK_INF;
-    const uint32_t rl = hl ? probe_finish(pl, left, nid) : RANK_INF;
-#pragma unroll
-    for (int j = 0; j < S; ++j) {
-      if (j == k) rk[j] = rr == RANK_INF ? RANK_INF : ((rr << 4) | (uint32_t)j);
-      if (j == m) rk[j] = RANK_INF;
-      if (hl && j == l_i) rk[j] = rl == RANK_INF ? RANK_INF : ((rl << 4) | (uint32_t)j);
-    }
+    const uint32_t rl = probe_finish(pl, left, nid);
+    if (m < (uint32_t)(S - 1)) rk[m * ST] = RANK_INF;
+    rk[k * ST] = rr == RANK_INF ? RANK_INF : ((rr << 4) | k);
+    if (hl) rk[l_i * ST] = rl == RANK_INF ? RANK_INF : ((rl << 4) | l_i);
   }
   // compact in place: the c-th live token moves to ids[c], c <= its slot
   uint32_t c = 0;

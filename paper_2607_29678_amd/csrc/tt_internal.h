@@ -78,14 +78,21 @@ __device__ __forceinline__ ProbeIssued probe_issue(const u64x2* __restrict__ tab
                                                    uint32_t b) {
   return ProbeIssued{tab[bucket_of(pair_hash(a, b), nb)], tab[bucket_of(pair_hash2(a, b), nb)]};
 }
+// Only the high word of the matching slot is kept (key bits 32..41 below the
+// rank): no empty slot matches, because no internal ID has all 21 bits set.
 __device__ __forceinline__ uint32_t probe_finish(const ProbeIssued& p, uint32_t a, uint32_t b) {
-  const uint64_t key = slot_key(a, b);
-  uint64_t hit = SLOT_EMPTY;
-  hit = (p.x.x & KEY_MASK) == key ? p.x.x : hit;
-  hit = (p.x.y & KEY_MASK) == key ? p.x.y : hit;
-  hit = (p.y.x & KEY_MASK) == key ? p.y.x : hit;
-  hit = (p.y.y & KEY_MASK) == key ? p.y.y : hit;
-  return hit == SLOT_EMPTY ? RANK_INF : (uint32_t)(hit >> (2 * ID_BITS));
+  const uint32_t klo = a | (b << ID_BITS), khi = b >> (32 - ID_BITS);
+  constexpr uint32_t HI_KEY = (1u << (2 * ID_BITS - 32)) - 1u;
+  uint32_t hi = 0xFFFFFFFFu;
+  auto check = [&](uint64_t v) {
+    const uint32_t vh = (uint32_t)(v >> 32);
+    hi = ((uint32_t)v == klo && (vh & HI_KEY) == khi) ? vh : hi;
+  };
+  check(p.x.x);
+  check(p.x.y);
+  check(p.y.x);
+  check(p.y.y);
+  return hi == 0xFFFFFFFFu ? RANK_INF : hi >> (2 * ID_BITS - 32);
 }
 // Rank of the pair (a, b), or RANK_INF if no merge joins it.
 __device__ __forceinline__ uint32_t probe_rank(const u64x2* __restrict__ tab, uint32_t nb, uint32_t a,
@@ -128,6 +135,40 @@ __device__ __forceinline__ uint32_t dict_find(const u32x4* __restrict__ dict, ui
   return r;
 }
 
+// Long-unit dictionary: the same for units of DICT_MAX+1..DICT2_MAX bytes.
+// An entry is two 16-byte words, {bytes 0..15} and {bytes 16..23, (id << 5) |
+// length, 0}; one entry per bucket, two choices (four 16-byte loads).
+constexpr int DICT2_MAX = 24;
+
+__host__ __device__ inline uint32_t unit_hash6(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint32_t w4,
+                                               uint32_t w5, uint32_t len) {
+  uint32_t x = w0 * 0x9E3779B1u + w1 * 0x85EBCA77u + w2 * 0xC2B2AE3Du + w3 * 0x27D4EB2Fu + w4 * 0x165667B1u +
+               w5 * 0xD3A2646Cu + len;
+  x ^= x >> 15;
+  return x * 0x2C1B3C6Du;
+}
+__host__ __device__ inline uint32_t unit_hash6b(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint32_t w4,
+                                                uint32_t w5, uint32_t len) {
+  uint32_t x = (w0 * 0x27D4EB2Fu) ^ (w1 * 0x165667B1u) ^ (w2 * 0xD3A2646Cu) ^ (w3 * 0xFD7046C5u) ^
+               (w4 * 0xB55A4F09u) ^ (w5 * 0x9E3779B1u) ^ (len * 0x85EBCA77u);
+  x ^= x >> 13;
+  return x * 0x297A2D39u;
+}
+__device__ __forceinline__ uint32_t dict2_find(const u32x4* __restrict__ dict, uint32_t nb, const uint32_t (&w)[6],
+                                               uint32_t len) {
+  const uint32_t b1 = 2u * bucket_of(unit_hash6(w[0], w[1], w[2], w[3], w[4], w[5], len), nb);
+  const uint32_t b2 = 2u * bucket_of(unit_hash6b(w[0], w[1], w[2], w[3], w[4], w[5], len), nb);
+  const u32x4 a0 = dict[b1], a1 = dict[b1 + 1], c0 = dict[b2], c1 = dict[b2 + 1];
+  uint32_t r = DICT_NONE;
+  if (a0.x == w[0] && a0.y == w[1] && a0.z == w[2] && a0.w == w[3] && a1.x == w[4] && a1.y == w[5] &&
+      (a1.z & 31u) == len)
+    r = a1.z >> 5;
+  if (c0.x == w[0] && c0.y == w[1] && c0.z == w[2] && c0.w == w[3] && c1.x == w[4] && c1.y == w[5] &&
+      (c1.z & 31u) == len)
+    r = c1.z >> 5;
+  return r;
+}
+
 // Everything a kernel needs to know about a tokenizer handle.
 struct DevTables {
   const u64x2* slots;       // cuckoo buckets of two slots: key (left | right << 21), rank in bits 42..63
@@ -139,6 +180,8 @@ struct DevTables {
   uint32_t n_ids;           // 256 + M
   const u32x4* dict;        // whole-unit dictionary (two entries per bucket)
   uint32_t dnb;             // dictionary bucket count
+  const u32x4* dict2;       // long-unit dictionary (one two-word entry per bucket)
+  uint32_t dnb2;            // its bucket count
 };
 
 // ---------------------------------------------------------------------------
@@ -186,6 +229,7 @@ constexpr int PT_HALO = 32;                        // context bytes each side
 constexpr int PT_OWN = PT_WIN - 2 * PT_HALO;       // bytes a tile decides
 
 constexpr int SMALL_MAX = 16;                      // thread-per-unit limit (bytes)
+constexpr int TH_THREADS = 256;                    // threads of a tile that run the thread engine
 constexpr int WAVE_MAX = 128;                      // wave-per-unit limit (bytes)
 constexpr int ROWS_LDS = 480;                      // longer units: rows in LDS up to this length
 

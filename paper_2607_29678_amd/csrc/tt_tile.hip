@@ -209,6 +209,25 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane, F comb)
 
 constexpr int PT_PAD = 8;  // LDS arrays also hold window positions [-8, 0) and [PT_WIN, PT_WIN + 16)
 
+// The NW little-endian words of the L bytes at window index a (bytes past L
+// read as zero), from aligned LDS words: NW + 1 word loads and one byte
+// alignment per word.  Reads window bytes [a & ~3, a + 4 NW + 4).
+template <int NW>
+__device__ __forceinline__ void unit_words(const uint8_t* buf, uint32_t a, uint32_t L, uint32_t (&w)[NW]) {
+  const uint32_t p = PT_PAD + a;
+  const uint32_t* d = reinterpret_cast<const uint32_t*>(buf + (p & ~3u));
+  const uint32_t sh = p & 3u;
+  uint32_t x[NW + 1];
+#pragma unroll
+  for (int i = 0; i <= NW; ++i) x[i] = d[i];
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const uint32_t v = __builtin_amdgcn_alignbyte(x[i + 1], x[i], sh);
+    const int rem = (int)L - 4 * i;  // bytes of word i inside the unit
+    w[i] = rem >= 4 ? v : rem <= 0 ? 0u : (v & ((1u << (8 * rem)) - 1u));
+  }
+}
+
 constexpr int MED_CAP = PT_WIN / (SMALL_MAX + 1) + 2;  // units of 17..64 bytes in a tile
 constexpr int BIG_CAP = PT_WIN / (WAVE_MAX + 1) + 2;   // longer units in a tile
 constexpr uint16_t U_INCOMING = 0xFFFFu;               // list entry for the incoming unit
@@ -234,6 +253,7 @@ union PhaseMem {
         uint64_t sel[ROWS_LDS / 64 + 2];
       } rows;
     } x;
+    uint32_t rk[SMALL_MAX - 1][TH_THREADS];  // thread engine: pair ranks, one column per thread
   } b;
 };
 
@@ -937,8 +957,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   auto inc_out = [&](uint32_t j, uint32_t id) { w.stage[s_prev + j] = id; };
 
   // ---- BPE dispatch ---------------------------------------------------------
-  // Units of one or two bytes are finished here, and so are units of up to 12
-  // bytes found in the whole-unit dictionary.  Other units of 3..16 bytes go to
+  // Units of one or two bytes are finished here, and so are units of up to 24
+  // bytes found in the whole-unit dictionaries.  Other units of 3..16 bytes go to
   // one thread each, counting-sorted by length, so that the threads of a wave
   // hold units of similar length (a wave runs as long as its longest unit).
   // Units of 17..64 bytes go to one wave each, first to the waves that have no
@@ -978,17 +998,21 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         sh.ucnt[u] = (uint16_t)c;
       }
     } else {
-      // units of 3..12 bytes: the whole-unit dictionary first
+      // units of 3..24 bytes: the whole-unit dictionaries first.  Their bytes
+      // are in the window (an incoming unit this short ends at the tile's
+      // first unit start, so it starts at least PT_HALO - 24 bytes into it).
       uint32_t found = DICT_NONE;
-      if (L <= (uint32_t)DICT_MAX) {
-        uint32_t kw[3] = {0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < DICT_MAX; ++j) {
-          uint32_t bj = 0;
-          if ((uint32_t)j < L) bj = inc_u ? inc_byte((uint32_t)j) : (uint32_t)sh.buf[PT_PAD + a + j];
-          kw[j >> 2] |= bj << (8 * (j & 3));
+      const int64_t aw = inc_u ? (int64_t)s_prev - w0 : (int64_t)a;
+      if (L <= (uint32_t)DICT2_MAX && aw >= 0 && aw + DICT2_MAX + 4 <= PT_WIN + 16) {
+        if (L <= (uint32_t)DICT_MAX) {
+          uint32_t kw[3];
+          unit_words(sh.buf, (uint32_t)aw, L, kw);
+          found = dict_find(tb.dict, tb.dnb, kw[0], kw[1], kw[2], L);
+        } else {
+          uint32_t kw[6];
+          unit_words(sh.buf, (uint32_t)aw, L, kw);
+          found = dict2_find(tb.dict2, tb.dnb2, kw, L);
         }
-        found = dict_find(tb.dict, tb.dnb, kw[0], kw[1], kw[2], L);
       }
       if (found != DICT_NONE) {
         if (inc_u) {
@@ -1027,29 +1051,32 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   __syncthreads();
   const uint32_t n_small = sh.n_small, n_med = sh.n_med;
 
-  // thread per unit
+  // thread per unit, on the first TH_THREADS threads
+  if (tid < TH_THREADS) {
+    uint32_t* rk = &sh.ph.b.rk[0][tid];
 #pragma unroll 1
-  for (uint32_t i = tid; i < n_small; i += PT_THREADS) {
-    const uint32_t u = sh.ph.b.small[i];
-    if (u == U_INCOMING) {
-      for (uint32_t j = 0; j < L_inc; ++j) sh.inc_ids[j] = inc_byte(j);
-      const uint32_t c = bpe_thread(L_inc, sh.inc_ids, tb);
-      for (uint32_t j = 0; j < c; ++j) inc_out(j, sh.inc_ids[j]);
-      sh.inc_cnt = c;
-    } else {
-      // the unit's own window slots hold its tokens while it is encoded
-      const uint32_t a = sh.ustart[u];
-      const uint32_t L = sh.ustart[u + 1] - a;
-      for (uint32_t j = 0; j < L; ++j) sh.ph.b.tok[a + j] = sh.buf[PT_PAD + a + j];
-      sh.ucnt[u] = (uint16_t)bpe_thread(L, &sh.ph.b.tok[a], tb);
+    for (uint32_t i = tid; i < n_small; i += TH_THREADS) {
+      const uint32_t u = sh.ph.b.small[i];
+      if (u == U_INCOMING) {
+        for (uint32_t j = 0; j < L_inc; ++j) sh.inc_ids[j] = inc_byte(j);
+        const uint32_t c = bpe_thread(L_inc, sh.inc_ids, rk, tb);
+        for (uint32_t j = 0; j < c; ++j) inc_out(j, sh.inc_ids[j]);
+        sh.inc_cnt = c;
+      } else {
+        // the unit's own window slots hold its tokens while it is encoded
+        const uint32_t a = sh.ustart[u];
+        const uint32_t L = sh.ustart[u + 1] - a;
+        for (uint32_t j = 0; j < L; ++j) sh.ph.b.tok[a + j] = sh.buf[PT_PAD + a + j];
+        sh.ucnt[u] = (uint16_t)bpe_thread(L, &sh.ph.b.tok[a], rk, tb);
+      }
     }
   }
 
-  // wave per unit: unit i runs on wave (first + i) mod 16, where the waves
+  // wave per unit: unit i runs on wave (first + i) mod 8, where the waves
   // from `first` on have no thread work
   {
     constexpr uint32_t NWV = PT_THREADS / 64;
-    const uint32_t busy = n_small >= (uint32_t)PT_THREADS ? NWV : (n_small + 63) / 64;
+    const uint32_t busy = n_small >= (uint32_t)TH_THREADS ? TH_THREADS / 64 : (n_small + 63) / 64;
     const uint32_t first = busy % NWV;
 #pragma unroll 1
     for (uint32_t i = ((uint32_t)wave + NWV - first) % NWV; i < n_med; i += NWV) {
