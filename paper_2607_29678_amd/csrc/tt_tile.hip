@@ -63,10 +63,12 @@ __device__ __forceinline__ void st_word(uint64_t* p, uint64_t v) {
 
 constexpr int CLS_L1_BYTES = 4352, CLS_L2_BYTES = TT_CLS_NBLOCKS * 64;
 
-// The probed class table, staged in LDS by every block.
+// The probed class table, staged in LDS by every block, and the code of every
+// ASCII character (built by the block).
 struct ClassLds {
   uint8_t l1[CLS_L1_BYTES] __attribute__((aligned(16)));
   uint8_t l2[CLS_L2_BYTES] __attribute__((aligned(16)));
+  uint8_t asc[128];
 };
 
 // 2-bit class of a non-ASCII code point from the probed table.
@@ -157,34 +159,33 @@ __device__ __forceinline__ int decode(const uint8_t* s, int avail, uint32_t& cp)
   return 4;
 }
 
-// The same decode from bytes already in registers (b1..b3 are read only when
-// the sequence is that long and `avail` allows it).
-__device__ __forceinline__ int decode_bytes(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3, int avail,
-                                            uint32_t& cp) {
-  const int len = lead_len(b0);
-  if (len == 0 || len > avail) return 0;
-  if (len == 1) {
-    cp = b0;
-    return 1;
-  }
-  uint32_t lo = 0x80u, hi = 0xBFu;
-  if (b0 == 0xE0u) lo = 0xA0u;
-  else if (b0 == 0xEDu) hi = 0x9Fu;
-  else if (b0 == 0xF0u) lo = 0x90u;
-  else if (b0 == 0xF4u) hi = 0x8Fu;
-  if (b1 < lo || b1 > hi) return 0;
-  if (len == 2) {
-    cp = ((b0 & 0x1Fu) << 6) | (b1 & 0x3Fu);
-    return 2;
-  }
-  if ((b2 & 0xC0u) != 0x80u) return 0;
-  if (len == 3) {
-    cp = ((b0 & 0x0Fu) << 12) | ((b1 & 0x3Fu) << 6) | (b2 & 0x3Fu);
-    return 3;
-  }
-  if ((b3 & 0xC0u) != 0x80u) return 0;
-  cp = ((b0 & 0x07u) << 18) | ((b1 & 0x3Fu) << 12) | ((b2 & 0x3Fu) << 6) | (b3 & 0x3Fu);
-  return 4;
+// Strict UTF-8 decode from bytes in registers, with selects only: the length
+// of the sequence that starts with b0 (0 if it is invalid or longer than
+// `avail`) and its code point.
+__device__ __forceinline__ uint32_t decode_sel(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3, uint32_t avail,
+                                               uint32_t& cp) {
+  const uint32_t len = b0 < 0x80u ? 1u : b0 < 0xC2u ? 0u : b0 < 0xE0u ? 2u : b0 < 0xF0u ? 3u : b0 < 0xF5u ? 4u : 0u;
+  const uint32_t lo = b0 == 0xE0u ? 0xA0u : b0 == 0xF0u ? 0x90u : 0x80u;
+  const uint32_t hi = b0 == 0xEDu ? 0x9Fu : b0 == 0xF4u ? 0x8Fu : 0xBFu;
+  const bool ok1 = len < 2u || (b1 >= lo && b1 <= hi);
+  const bool ok2 = len < 3u || (b2 & 0xC0u) == 0x80u;
+  const bool ok3 = len < 4u || (b3 & 0xC0u) == 0x80u;
+  const uint32_t c2 = ((b0 & 0x1Fu) << 6) | (b1 & 0x3Fu);
+  const uint32_t c3 = ((b0 & 0x0Fu) << 12) | ((b1 & 0x3Fu) << 6) | (b2 & 0x3Fu);
+  const uint32_t c4 = ((b0 & 0x07u) << 18) | ((b1 & 0x3Fu) << 12) | ((b2 & 0x3Fu) << 6) | (b3 & 0x3Fu);
+  cp = len <= 1u ? b0 : len == 2u ? c2 : len == 3u ? c3 : c4;
+  return (len != 0u && len <= avail && ok1 && ok2 && ok3) ? len : 0u;
+}
+
+// char_code for any code point of at most U+10FFFF, with selects only (both
+// tables are read).
+template <int PAT>
+__device__ __forceinline__ uint32_t char_code_sel(const ClassLds& ct, uint32_t cp) {
+  const uint32_t a = ct.asc[cp & 127u];
+  const uint32_t c2 = table_class(ct, cp);
+  const uint32_t cls = c2 == 1u ? C_L : c2 == 2u ? C_N : c2 == 3u ? C_WS : C_O;
+  const uint32_t id = (PAT == TT_PATTERN_CL100K && cp == 0x17Fu) ? I_S : I_NONE;
+  return cp < 128u ? a : (cls | (id << 3));
 }
 
 // Segmented char-count scan state for cl100k: has-head (bit 31), window index
@@ -427,6 +428,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       if (i < N1) d1[i] = s1[i];
       else d2[i - N1] = s2[i - N1];
     }
+    if (tid < 128) sh.ph.a.cls.asc[tid] = (uint8_t)char_code<PAT>(sh.ph.a.cls, (uint32_t)tid);
   }
   if (SEG) {
     // the junction bitmap (8 KB) is read once per block
@@ -461,74 +463,67 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // A thread's four positions are one aligned word of the window.  It reads
   // its word and the words on either side (bytes and document-start flags) and
   // decides everything from registers: a sequence starts at most three bytes
-  // before a position it covers and ends at most three bytes after.
+  // before a position it covers and ends at most three bytes after.  Four
+  // ASCII bytes inside the text take their codes from the ASCII table.
   static_assert(PT_BPT == 4 && PT_PAD % 4 == 0, "classification works on aligned 4-byte words");
   bool bad = false;
   {
     const int q0 = tid * PT_BPT;
     const uint32_t* bw = reinterpret_cast<const uint32_t*>(&sh.buf[PT_PAD + q0 - 4]);
     const uint32_t* dw = reinterpret_cast<const uint32_t*>(&sh.dstart[PT_PAD + q0 - 4]);
-    const uint64_t blo = bw[0] | ((uint64_t)bw[1] << 32), bhi = bw[1] | ((uint64_t)bw[2] << 32);
-    const uint64_t dlo = dw[0] | ((uint64_t)dw[1] << 32), dhi = dw[1] | ((uint64_t)dw[2] << 32);
+    const uint32_t bw0 = bw[0], bw1 = bw[1], bw2 = bw[2];
+    const uint32_t dw0 = dw[0], dw1 = dw[1], dw2 = dw[2];
     const int64_t p0 = w0 + q0;  // text position of the first of the four
-    // r is relative to q0, in [-4, 8)
-    auto byt = [&](int r) -> uint32_t {
-      return r < 0 ? (uint32_t)(blo >> (8 * (r + 4))) & 255u : (uint32_t)(bhi >> (8 * r)) & 255u;
-    };
-    auto dst = [&](int r) -> bool {
-      return ((r < 0 ? (uint32_t)(dlo >> (8 * (r + 4))) : (uint32_t)(dhi >> (8 * r))) & 255u) != 0u;
-    };
-    auto ins = [&](int r) -> bool { return p0 + r >= 0 && p0 + r < n; };
-    uint32_t codes = 0;
+    uint32_t codes;
+    if ((bw1 & 0x80808080u) == 0u && p0 >= 0 && p0 + PT_BPT <= n) {
+      const uint8_t* asc = sh.ph.a.cls.asc;
+      codes = (uint32_t)asc[bw1 & 255u] | ((uint32_t)asc[(bw1 >> 8) & 255u] << 8) |
+              ((uint32_t)asc[(bw1 >> 16) & 255u] << 16) | ((uint32_t)asc[bw1 >> 24] << 24);
+      codes |= (dw1 & 0x01010101u) << 7;  // document starts (flags are 0 or 1)
+    } else {
+      const uint64_t blo = bw0 | ((uint64_t)bw1 << 32), bhi = bw1 | ((uint64_t)bw2 << 32);
+      const uint64_t dlo = dw0 | ((uint64_t)dw1 << 32), dhi = dw1 | ((uint64_t)dw2 << 32);
+      // r is relative to q0, in [-4, 8)
+      auto byt = [&](int r) -> uint32_t {
+        return r < 0 ? (uint32_t)(blo >> (8 * (r + 4))) & 255u : (uint32_t)(bhi >> (8 * r)) & 255u;
+      };
+      auto dst = [&](int r) -> bool {
+        return ((r < 0 ? (uint32_t)(dlo >> (8 * (r + 4))) : (uint32_t)(dhi >> (8 * r))) & 255u) != 0u;
+      };
+      auto ins = [&](int r) -> bool { return p0 + r >= 0 && p0 + r < n; };
+      codes = 0;
 #pragma unroll
-    for (int j = 0; j < PT_BPT; ++j) {
-      const int q = q0 + j;
-      const uint32_t ds = dst(j) ? CODE_DOCSTART : 0u;
-      uint32_t code = C_NONE;
-      const bool own = q >= PT_HALO && q < PT_HALO + PT_OWN && ins(j);
-      if (ins(j)) {
+      for (int j = 0; j < PT_BPT; ++j) {
+        const int q = q0 + j;
         const uint32_t b = byt(j);
-        if ((b & 0xC0u) == 0x80u) {
-          if (own) {
-            // a continuation byte must lie inside the sequence of a lead byte at
-            // most three bytes earlier, with no document start in between
-            bool claimed = false, done = ds != 0u;
+        const bool in_j = ins(j);
+        const bool own = q >= PT_HALO && q < PT_HALO + PT_OWN && in_j;
+        const bool cont = (b & 0xC0u) == 0x80u;
+        // a lead byte: its sequence, which a document start or the text end cuts
+        uint32_t avail = 1;
+        bool stop = false;
 #pragma unroll
-            for (int k = 1; k <= 3; ++k) {
-              if (done) continue;
-              if (!ins(j - k)) {
-                done = true;
-                continue;
-              }
-              const uint32_t br = byt(j - k);
-              if ((br & 0xC0u) == 0x80u) {
-                done = dst(j - k);
-                continue;
-              }
-              claimed = lead_len(br) > k;
-              done = true;
-            }
-            bad |= !claimed;
-          }
-        } else {
-          int avail = 1;
-          bool stop = false;
-#pragma unroll
-          for (int k = 1; k <= 3; ++k) {
-            stop = stop || !ins(j + k) || dst(j + k);
-            avail += stop ? 0 : 1;
-          }
-          uint32_t cp = 0;
-          const int len = decode_bytes(b, byt(j + 1), byt(j + 2), byt(j + 3), avail, cp);
-          if (len == 0) {
-            bad |= own;
-            code = C_O;
-          } else {
-            code = char_code<PAT>(sh.ph.a.cls, cp);
-          }
+        for (int k = 1; k <= 3; ++k) {
+          stop = stop || !ins(j + k) || dst(j + k);
+          avail += stop ? 0u : 1u;
         }
+        uint32_t cp = 0;
+        const uint32_t len = decode_sel(b, byt(j + 1), byt(j + 2), byt(j + 3), avail, cp);
+        // a continuation byte must lie inside the sequence of a lead byte at
+        // most three bytes earlier, with no document start in between
+        bool claimed = false, blocked = dst(j);
+#pragma unroll
+        for (int k = 1; k <= 3; ++k) {
+          const uint32_t br = byt(j - k);
+          const bool ok = ins(j - k), c = (br & 0xC0u) == 0x80u;
+          const uint32_t ll = br < 0x80u ? 1u : br < 0xC2u ? 0u : br < 0xE0u ? 2u : br < 0xF0u ? 3u : br < 0xF5u ? 4u : 0u;
+          claimed = claimed || (!blocked && ok && !c && ll > (uint32_t)k);
+          blocked = blocked || !ok || !c || dst(j - k);
+        }
+        const uint32_t code = (!in_j || cont) ? C_NONE : len == 0u ? C_O : char_code_sel<PAT>(sh.ph.a.cls, cp);
+        bad = bad || (own && (cont ? !claimed : len == 0u));
+        codes |= (code | (dst(j) ? CODE_DOCSTART : 0u)) << (8 * j);
       }
-      codes |= (code | ds) << (8 * j);
     }
     *reinterpret_cast<uint32_t*>(&sh.ph.a.code[PT_PAD + q0]) = codes;
     if (tid < 3) {  // positions outside [0, PT_WIN) carry no character for the rules
