@@ -364,8 +364,32 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   const int64_t n = w.n;
 
   if (tid <= SMALL_MAX) sh.hist[tid] = 0;
+  // the ticket's round trip (tickets are handed out one at a time) overlaps
+  // the staging of the tables, which do not depend on the tile
+  uint32_t ticket = 0;
+  if (tid == 0) ticket = atomicAdd(&w.ctrl->tile_ticket, 1u);
+  {
+    // the class table (12.9 KB) is read once per block
+    static_assert(CLS_L1_BYTES % 16 == 0 && CLS_L2_BYTES % 16 == 0, "class table staging uses 16-byte words");
+    constexpr int N1 = CLS_L1_BYTES / 16, N2 = CLS_L2_BYTES / 16;
+    const uint4* s1 = reinterpret_cast<const uint4*>(TT_CLS_L1);
+    const uint4* s2 = reinterpret_cast<const uint4*>(TT_CLS_L2);
+    uint4* d1 = reinterpret_cast<uint4*>(sh.ph.a.cls.l1);
+    uint4* d2 = reinterpret_cast<uint4*>(sh.ph.a.cls.l2);
+    for (int i = tid; i < N1 + N2; i += PT_THREADS) {
+      if (i < N1) d1[i] = s1[i];
+      else d2[i - N1] = s2[i - N1];
+    }
+    if (tid < 128) sh.ph.a.cls.asc[tid] = (uint8_t)char_code<PAT>(sh.ph.a.cls, (uint32_t)tid);
+  }
+  if (SEG) {
+    // the junction bitmap (8 KB) is read once per block
+    const uint4* src = reinterpret_cast<const uint4*>(tb.join);
+    uint4* dst = reinterpret_cast<uint4*>(sh.ph.a.join);
+    for (int i = tid; i < 512; i += PT_THREADS) dst[i] = src[i];
+  }
   if (tid == 0) {
-    sh.tile = atomicAdd(&w.ctrl->tile_ticket, 1u) - w.ticket_base;
+    sh.tile = ticket - w.ticket_base;
     sh.n_med = 0;
     sh.n_big = 0;
     sh.inc_cnt = 0;
@@ -415,26 +439,6 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     constexpr int NCH = PT_WIN / 8;  // chunks of the window proper
     if (tid < NCH) stage_chunk(tid);
     else if (tid < NCH + 3) stage_chunk(tid == NCH ? -1 : tid - 1);  // [-8, 0) and [PT_WIN, PT_WIN + 16)
-  }
-  {
-    // the class table (12.9 KB) is read once per block
-    static_assert(CLS_L1_BYTES % 16 == 0 && CLS_L2_BYTES % 16 == 0, "class table staging uses 16-byte words");
-    constexpr int N1 = CLS_L1_BYTES / 16, N2 = CLS_L2_BYTES / 16;
-    const uint4* s1 = reinterpret_cast<const uint4*>(TT_CLS_L1);
-    const uint4* s2 = reinterpret_cast<const uint4*>(TT_CLS_L2);
-    uint4* d1 = reinterpret_cast<uint4*>(sh.ph.a.cls.l1);
-    uint4* d2 = reinterpret_cast<uint4*>(sh.ph.a.cls.l2);
-    for (int i = tid; i < N1 + N2; i += PT_THREADS) {
-      if (i < N1) d1[i] = s1[i];
-      else d2[i - N1] = s2[i - N1];
-    }
-    if (tid < 128) sh.ph.a.cls.asc[tid] = (uint8_t)char_code<PAT>(sh.ph.a.cls, (uint32_t)tid);
-  }
-  if (SEG) {
-    // the junction bitmap (8 KB) is read once per block
-    const uint4* src = reinterpret_cast<const uint4*>(tb.join);
-    uint4* dst = reinterpret_cast<uint4*>(sh.ph.a.join);
-    for (int i = tid; i < 512; i += PT_THREADS) dst[i] = src[i];
   }
   if (BATCH) {
     if (tid == 0) {
@@ -589,10 +593,9 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   };
 
   // ---- the codes around the thread's positions, in registers ---------------
-  // cr(r) is the code of window position qb + r for r in [-8, 8).  The
-  // neighbour of a position is the position next to it whenever that holds a
-  // character (prev_of / next_of); only continuation bytes and the window edges
-  // need the general walks over LDS.
+  // cr(r) is the code of window position qb + r for r in [-8, 8): enough to
+  // find the characters on either side of the thread's positions (and the one
+  // before that), which are at most four bytes away in valid text.
   const int qb = tid * PT_BPT;
   const uint32_t* cwp = reinterpret_cast<const uint32_t*>(&sh.ph.a.code[PT_PAD + qb - 8]);
   const uint32_t cw0 = cwp[0], cw1 = cwp[1], cw2 = cwp[2], cw3 = cwp[3];
@@ -601,34 +604,42 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     const uint32_t lo = (i & 4) ? cw1 : cw0, hi = (i & 4) ? cw3 : cw2;
     return (((i & 8) ? hi : lo) >> ((i & 3) * 8)) & 255u;
   };
-  // prev(qb + r) and its code, for r in [-7, 8)
-  auto prev_of = [&](int r, uint32_t& pc) -> int {
-    if (cr(r) & CODE_DOCSTART) return -1;
-    const uint32_t cm = cr(r - 1);
-    if (code_cls(cm) != C_NONE) {
-      pc = cm;
-      return qb + r - 1;
-    }
-    const int p = prev(qb + r);
-    pc = p >= 0 ? code_at(p) : 0u;
-    return p;
-  };
-  // next(qb + r) and its code, for r in [-8, 7)
-  auto next_of = [&](int r, uint32_t& nc) -> int {
-    const uint32_t c = cr(r + 1);
-    if (c & CODE_DOCSTART) return -1;
-    if (code_cls(c) != C_NONE) {
-      nc = c;
-      return qb + r + 1;
-    }
-    const int x = next(qb + r);
-    nc = x >= 0 ? code_at(x) : 0u;
-    return x;
-  };
   // an apostrophe one byte before position qb + r (a contraction can start at
   // qb + r only then), or two or three bytes before (a contraction can end just
   // before qb + r only then: the suffix is one or two ASCII letters, or U+017F)
   auto apo_at = [&](int r) -> bool { return code_id(cr(r)) == I_APO; };
+  // The character before window position qb + r (r in [-4, 8)) and its code,
+  // from the register window: in valid text it starts at most four bytes
+  // before (in invalid text, whose output is discarded, the search stops
+  // there).  Returns its distance, 0 when there is none.
+  auto prev_reg = [&](int r, uint32_t& pc) -> uint32_t {
+    uint32_t d = 0, x = 0;
+#pragma unroll
+    for (int k = 4; k >= 1; --k) {
+      const uint32_t c = cr(r - k);
+      const bool ch = code_cls(c) != C_NONE;
+      d = ch ? (uint32_t)k : d;
+      x = ch ? c : x;
+    }
+    pc = x;
+    return (cr(r) & CODE_DOCSTART) ? 0u : d;
+  };
+  // Whether a character follows position qb + r (r in [-8, 4)) in the same
+  // document, within four bytes, and its code.
+  auto next_reg = [&](int r, uint32_t& nc) -> bool {
+    bool found = false, stop = false;
+    uint32_t x = 0;
+#pragma unroll
+    for (int k = 1; k <= 4; ++k) {
+      const uint32_t c = cr(r + k);
+      const bool ds = (c & CODE_DOCSTART) != 0u, ch = code_cls(c) != C_NONE;
+      found = found || (!stop && !ds && ch);
+      x = (!stop && !ds && ch) ? c : x;
+      stop = stop || ds || ch;
+    }
+    nc = x;
+    return found;
+  };
 
   // ---- cl100k: run scan, run ends, summaries, carries ----------------------
   // scan element of window position qb + j: a run head restarts the char count
@@ -637,8 +648,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     const uint32_t c = cr(j);
     if (q < PT_HALO || code_cls(c) == C_NONE) return 0u;
     uint32_t pc = 0;
-    const int p = prev_of(j, pc);
-    const bool head = p < 0 || code_cls(pc) != code_cls(c);
+    const bool head = prev_reg(j, pc) == 0u || code_cls(pc) != code_cls(c);
     return head ? (0x80000000u | ((uint32_t)q << 16) | 1u) : 1u;
   };
   uint32_t elems[PT_BPT];
@@ -777,6 +787,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   };
 
   // ---- piece-start predicate ----------------------------------------------
+  // The run-local rules, from the codes of the position, of the characters
+  // before and after it (register window) and, for cl100k, the run scan.  The
+  // cheap cases are selects; contractions (an apostrophe one to three bytes
+  // back), whitespace after CR/LF and a letter after a lone symbol branch.
   uint32_t flags = 0;
   uint32_t scan_st = s0;  // cl100k: scan state before position q
 #pragma unroll
@@ -785,97 +799,74 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     const uint32_t ex = scan_st;
     if (PAT == TT_PATTERN_CL100K) scan_st = seg_combine(scan_st, elems[j]);
     const uint32_t cq = cr(j);
-    if (q < PT_HALO || q >= PT_HALO + PT_OWN || code_cls(cq) == C_NONE) continue;
     const uint32_t c0 = code_cls(cq);
-    uint32_t cp1 = 0;
-    const int p1 = prev_of(j, cp1);
+    if (q < PT_HALO || q >= PT_HALO + PT_OWN || c0 == C_NONE) continue;
+    uint32_t cp1 = 0, cn1 = 0;
+    const uint32_t d1 = prev_reg(j, cp1);
+    const bool hn = next_reg(j, cn1);
+    const uint32_t c1 = code_cls(cp1);
+    const bool w0c = is_w(c0), w1c = is_w(c1);
+    const bool sp1 = code_id(cp1) == I_SP;
+    const bool run_last = hn && !is_w(code_cls(cn1));  // a following character that is not whitespace
+    const bool apo1 = apo_at(j - 1), apo23 = apo_at(j - 2) || apo_at(j - 3);
     bool start;
-    if (p1 < 0) {
-      start = true;
+    if (PAT == TT_PATTERN_GPT2) {
+      start = w0c ? (!w1c || run_last) : (c1 != c0 && !sp1);
+      if (!w0c && c0 == C_L && (apo1 || apo23)) {
+        if (c1 == c0) start = apo23 && contraction_ends_here(q);
+        else if (!sp1 && apo1 && contraction_len_at(q) > 0) start = false;
+      }
     } else {
-      const uint32_t c1 = code_cls(cp1);
-      // (contraction tests run only with an apostrophe close enough before q)
-      const bool may_end_contr = apo_at(j - 2) || apo_at(j - 3);
-      const bool may_start_contr = apo_at(j - 1);
-      if (PAT == TT_PATTERN_GPT2) {
-        if (is_w(c0)) {
-          if (!is_w(c1)) {
-            start = true;  // whitespace run head
+      if (w0c) {
+        start = !w1c ? !(c1 == C_O && c0 == C_NL) : (c0 == C_NL ? false : run_last);
+        if (w1c && c0 != C_NL && c1 == C_NL) {
+          // first whitespace after a CR/LF stretch
+          uint32_t pre;
+          if (seg_has(ex)) {
+            int hp = prev(seg_head(ex));
+            pre = hp >= 0 ? cls(hp) : (uint32_t)C_NONE;
           } else {
-            uint32_t cn1 = 0;
-            const int n1 = next_of(j, cn1);  // last char of a run of >= 2, followed by non-space
-            start = n1 >= 0 && !is_w(code_cls(cn1));
+            pre = sh.carry_nlpre;
           }
-        } else if (c1 == c0) {
-          start = c0 == C_L && may_end_contr && contraction_ends_here(q);
-        } else if (code_id(cp1) == I_SP) {
-          start = false;  // the space before the run opens the piece
-        } else if (c0 == C_L && may_start_contr && contraction_len_at(q) > 0) {
-          start = false;
-        } else {
-          start = true;
+          start = (pre == C_O) || ws_stretch_is_last(q);
         }
-      } else {
-        if (is_w(c0)) {
-          if (!is_w(c1)) {
-            // head of a whitespace run; after "other", leading CR/LF joins the symbol piece
-            start = !(c1 == C_O && c0 == C_NL);
-          } else if (c0 == C_NL) {
-            start = false;
-          } else if (c1 == C_NL) {
-            // first whitespace after a CR/LF stretch
-            uint32_t pre;
-            if (seg_has(ex)) {
-              int hp = prev(seg_head(ex));
-              pre = hp >= 0 ? cls(hp) : (uint32_t)C_NONE;
-            } else {
-              pre = sh.carry_nlpre;
-            }
-            start = (pre == C_O) || ws_stretch_is_last(q);
-          } else {
-            uint32_t cn1 = 0;
-            const int n1 = next_of(j, cn1);
-            start = n1 >= 0 && !is_w(code_cls(cn1));
-          }
-        } else if (c0 == C_N) {
-          if (c1 != C_N) {
-            start = true;
-          } else {
-            uint32_t off = seg_cnt(ex) + (seg_has(ex) ? 0u : sh.carry_n);
-            start = off % 3u == 0u;
-          }
-        } else if (c0 == C_O) {
-          start = c1 != C_O && code_id(cp1) != I_SP;
-        } else {  // letter
-          if (c1 == C_L) {
-            start = may_end_contr && contraction_ends_here(q);
-          } else if (may_start_contr && contraction_len_at(q) > 0) {
-            start = false;
-          } else if (c1 == C_WS) {
-            start = false;  // one whitespace char is the prefix
-          } else if (c1 == C_O) {
-            uint32_t cp2 = 0;
-            const int p2 = p1 == q - 1 ? prev_of(j - 1, cp2) : prev(p1);
-            if (p1 != q - 1 && p2 >= 0) cp2 = code_at(p2);
-            start = !(p2 < 0 || (code_cls(cp2) != C_O && code_id(cp2) != I_SP));
-          } else {
-            start = true;
-          }
+      } else if (c0 == C_N) {
+        const uint32_t off = seg_cnt(ex) + (seg_has(ex) ? 0u : sh.carry_n);
+        start = c1 != C_N || off % 3u == 0u;
+      } else if (c0 == C_O) {
+        start = c1 != C_O && !sp1;
+      } else {  // letter
+        start = c1 != C_L && c1 != C_WS;
+        if (c1 == C_O) {
+          // a lone symbol not preceded by U+0020 is the letter run's prefix
+          uint32_t cp2 = 0;
+          const uint32_t d2 = d1 == 1u ? prev_reg(j - 1, cp2) : d1 == 2u ? prev_reg(j - 2, cp2)
+                            : d1 == 3u ? prev_reg(j - 3, cp2) : prev_reg(j - 4, cp2);
+          start = d2 != 0u && (code_cls(cp2) == C_O || code_id(cp2) == I_SP);
+        }
+        if (apo1 || apo23) {
+          if (c1 == C_L) start = apo23 && contraction_ends_here(q);
+          else if (apo1 && contraction_len_at(q) > 0) start = false;
         }
       }
     }
+    if (d1 == 0u) start = true;
     if (start) flags |= 1u << j;
   }
   if (SEG) {
     // BPE segments: add the byte positions inside pieces that no merge spans
-#pragma unroll 1
+    // (q is not a piece start, so q - 1 lies in the same piece)
+    const uint32_t* bwp = reinterpret_cast<const uint32_t*>(&sh.buf[PT_PAD + qb - 4]);
+    const uint64_t bb = bwp[0] | ((uint64_t)bwp[1] << 32);  // bytes of positions qb - 4 .. qb + 3
+#pragma unroll
     for (int j = 0; j < PT_BPT; ++j) {
       const int q = qb + j;
-      if (q < PT_HALO || q >= PT_HALO + PT_OWN || !inside(q) || (flags & (1u << j))) continue;
-      if (sh.dstart[PT_PAD + q] || !inside(q - 1)) continue;  // piece starts are already flagged
-      // q is not a piece start, so q - 1 lies in the same piece
-      const uint32_t key = ((uint32_t)sh.buf[PT_PAD + q - 1] << 8) | sh.buf[PT_PAD + q];
-      if (!((sh.ph.a.join[key >> 5] >> (key & 31u)) & 1u)) flags |= 1u << j;
+      const uint32_t key = (uint32_t)((bb >> (8 * (j + 3))) & 0xFFFFull);  // (b[q-1], b[q]) as b[q-1] | b[q] << 8
+      const uint32_t k2 = ((key & 255u) << 8) | (key >> 8);
+      const bool joined = (sh.ph.a.join[k2 >> 5] >> (k2 & 31u)) & 1u;
+      const bool eligible = q >= PT_HALO && q < PT_HALO + PT_OWN && inside(q) && inside(q - 1) &&
+                            !(flags & (1u << j)) && !(cr(j) & CODE_DOCSTART);
+      if (eligible && !joined) flags |= 1u << j;
     }
   }
 
@@ -1052,17 +1043,20 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
 #pragma unroll 1
     for (uint32_t i = tid; i < n_small; i += TH_THREADS) {
       const uint32_t u = sh.ph.b.small[i];
-      if (u == U_INCOMING) {
-        for (uint32_t j = 0; j < L_inc; ++j) sh.inc_ids[j] = inc_byte(j);
-        const uint32_t c = bpe_thread(L_inc, sh.inc_ids, rk, tb);
-        for (uint32_t j = 0; j < c; ++j) inc_out(j, sh.inc_ids[j]);
+      const bool inc_u = u == U_INCOMING;
+      // a unit's own window slots hold its tokens while it is encoded (the
+      // incoming unit's are in inc_ids); one call site, so that a wave does
+      // not run the merge loop twice when it holds the incoming unit
+      const uint32_t a = inc_u ? 0u : sh.ustart[u];
+      const uint32_t L = inc_u ? L_inc : sh.ustart[u + 1] - a;
+      uint32_t* ids = inc_u ? sh.inc_ids : &sh.ph.b.tok[a];
+      for (uint32_t j = 0; j < L; ++j) ids[j] = inc_u ? inc_byte(j) : (uint32_t)sh.buf[PT_PAD + a + j];
+      const uint32_t c = bpe_thread(L, ids, rk, tb);
+      if (inc_u) {
+        for (uint32_t j = 0; j < c; ++j) inc_out(j, ids[j]);
         sh.inc_cnt = c;
       } else {
-        // the unit's own window slots hold its tokens while it is encoded
-        const uint32_t a = sh.ustart[u];
-        const uint32_t L = sh.ustart[u + 1] - a;
-        for (uint32_t j = 0; j < L; ++j) sh.ph.b.tok[a + j] = sh.buf[PT_PAD + a + j];
-        sh.ucnt[u] = (uint16_t)bpe_thread(L, &sh.ph.b.tok[a], rk, tb);
+        sh.ucnt[u] = (uint16_t)c;
       }
     }
   }
