@@ -138,6 +138,42 @@ int tt_encode_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_
 int tt_encode_batch(tt_tokenizer* h, const uint8_t* concat, const int64_t* doc_offsets,
                     int32_t n_docs, int32_t* out_ids, int64_t* out_doc_offsets, void* stream);
 
+/* ---- span export -------------------------------------------------------- */
+/* Token IDs together with the source span of every token (Appendix, Route C:
+ * span export; the records (id, a, b) of Definition d:records).  For
+ * byte-level BPE a token's byte length is fixed by the vocabulary, so byte
+ * offsets are a running sum of token lengths, and a running count of the
+ * request's non-continuation bytes lifts them to character spans.  Span i is
+ * four int32 values:
+ *   [0] byte begin, [1] byte end      the token's bytes utf8[begin, end);
+ *                                      the byte spans partition [0, len);
+ *   [2] char begin, [3] char end      the characters (Unicode scalar values,
+ *                                      counted from 0) that hold the token's
+ *                                      first through last byte; tokens that
+ *                                      split one multi-byte character all
+ *                                      report that character.
+ * Single requests only (no batches).
+ *  utf8[len]      request bytes (host).
+ *  out_ids        host buffer of at least max(len, 1) IDs.
+ *  out_spans      host buffer of at least 4 * max(len, 1) int32 values.
+ *  out_len        receives the number of IDs (and spans).
+ * Blocks until the outputs are valid (two synchronisations; IDs and spans are
+ * copied back together).  Invalid UTF-8 returns TT_ERR_INVALID_UTF8 and no
+ * output.  The spans buffer of a stream's workspace is allocated on the first
+ * call (16 bytes per byte of capacity). */
+int tt_encode_spans(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_ids, int32_t* out_spans,
+                    int64_t* out_len, void* stream);
+
+/* The same for a request already in device memory; fully asynchronous.
+ *  d_utf8[len]    request bytes (device), read-only, may be unaligned.
+ *  d_out_ids      device buffer of at least max(len, 1) IDs.
+ *  d_out_spans    device buffer of at least 4 * max(len, 1) int32 values.
+ *  d_out_len      device int64_t: the number of IDs, or a negative TT_ERR_*
+ *                 code (invalid UTF-8), in which case IDs and spans are
+ *                 unspecified. */
+int tt_encode_spans_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_t* d_out_ids,
+                           int32_t* d_out_spans, int64_t* d_out_len, void* stream);
+
 /* ---- split-level export (tests) ---------------------------------------- */
 /* Pre-tokenization only: the UTF-8 byte offset of the first byte of every
  * piece, in order (Sec. 4.1: differential testing compares piece boundaries as

@@ -38,6 +38,8 @@ SIGNATURES = {
     "tt_encode": (ctypes.c_int, [_P, _P, _I64, _P, ctypes.POINTER(_I64), _P]),
     "tt_encode_device": (ctypes.c_int, [_P, _P, _I64, _P, _P, _P]),
     "tt_encode_batch": (ctypes.c_int, [_P, _P, _P, _I32, _P, _P, _P]),
+    "tt_encode_spans": (ctypes.c_int, [_P, _P, _I64, _P, _P, ctypes.POINTER(_I64), _P]),
+    "tt_encode_spans_device": (ctypes.c_int, [_P, _P, _I64, _P, _P, _P, _P]),
     "tt_pretokenize": (ctypes.c_int, [_P, _P, _I64, _P, ctypes.POINTER(_I64), _P]),
     "tt_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "tt_info": (ctypes.c_int, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32), ctypes.POINTER(_I32)]),

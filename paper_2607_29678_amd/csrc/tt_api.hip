@@ -40,6 +40,8 @@ struct Workspace {
   int64_t* d_len = nullptr;   // output length (host calls)
   int64_t* d_docs = nullptr;  // batch: document byte offsets
   int64_t* d_out_docs = nullptr;
+  int32_t* d_spans = nullptr;  // span export (host calls): [span_cap][4], allocated on first use
+  uint64_t span_cap = 0;
   int64_t* h_len = nullptr;   // pinned readback word
   // profiling: stage boundaries of the most recent calls, a ring of
   // `ring` calls with N_STAGES + 1 events each
@@ -64,6 +66,7 @@ struct tt_tokenizer {
   u32x4* d_dict2 = nullptr;     // long-unit dictionary
   uint32_t dnb2 = 0;            // its buckets
   int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
+  uint32_t* d_toklen = nullptr;  // [256 + M] byte length of every internal ID
   uint32_t n_ids = 0;
   uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
                                // byte x to a token starting with byte y
@@ -79,6 +82,7 @@ void free_ws(Workspace* s) {
   if (!s) return;
   if (s->dmem) (void)hipFree(s->dmem);
   if (s->d_docs) (void)hipFree(s->d_docs);
+  if (s->d_spans) (void)hipFree(s->d_spans);
   if (s->h_len) (void)hipHostFree(s->h_len);
   for (auto e : s->ev)
     if (e) (void)hipEventDestroy(e);
@@ -113,12 +117,14 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
   size_t o_tsum = take(8 * NT);
   size_t o_tlast = take(8 * NT);
   size_t o_tagg = take(8 * NT);
+  size_t o_tcagg = take(8 * NT);
   const size_t ctl_bytes = off;
   size_t o_tpre = take(4 * NT);
   size_t o_stage = take(4 * N);
   size_t o_utile = take(4 * N);
   size_t o_upos = take(4 * N);
   size_t o_scr = take(4 * 4 * N + 8 * (N / 16 + 8));
+  size_t o_ccount = take(4 * (N / 4 + 2));
   size_t o_in = take(N + 64);
   size_t o_out = take(4 * N);
   size_t o_len = take(8);
@@ -139,6 +145,8 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
   w.tile_sum = reinterpret_cast<uint64_t*>(b + o_tsum);
   w.tile_last = reinterpret_cast<uint64_t*>(b + o_tlast);
   w.tile_agg = reinterpret_cast<uint64_t*>(b + o_tagg);
+  w.tile_cagg = reinterpret_cast<uint64_t*>(b + o_tcagg);
+  w.ccount = reinterpret_cast<uint32_t*>(b + o_ccount);
   w.tile_pre = reinterpret_cast<uint32_t*>(b + o_tpre);
   w.stage = reinterpret_cast<uint32_t*>(b + o_stage);
   w.unit_tile = reinterpret_cast<uint32_t*>(b + o_utile);
@@ -188,9 +196,11 @@ int get_ws(tt_tokenizer* h, hipStream_t stream, uint64_t need, Workspace** out) 
 }
 
 // Enqueue the whole chain for `n` bytes at device address `text`.
-// mode 0: split export (out_ids receives piece offsets); mode 1: encode.
+// mode 0: split export (out_ids receives piece offsets); mode 1: encode;
+// mode 2: encode with span export into out_spans ([n][4], single requests).
 int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, const int64_t* d_docs,
-              int32_t n_docs, int32_t* out_ids, int64_t* out_len, int64_t* out_docs, hipStream_t st, int mode) {
+              int32_t n_docs, int32_t* out_ids, int64_t* out_len, int64_t* out_docs, hipStream_t st, int mode,
+              int32_t* out_spans = nullptr) {
   if (s->epoch + 1 >= EPOCH_LIMIT) {
     // epochs wrapped: clear the words that carry them and start again
     if (hipMemsetAsync(s->dmem, 0, s->ctl_bytes, st) != hipSuccess) return TT_ERR_HIP;
@@ -208,7 +218,9 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_ids = out_ids;
   w.out_len = out_len;
   w.out_doc_off = out_docs;
-  DevTables tb{h->d_slots, h->nb, h->d_pair0, h->d_join, h->d_ext, h->n_ids, h->d_dict, h->dnb, h->d_dict2, h->dnb2};
+  w.out_spans = out_spans;
+  DevTables tb{h->d_slots, h->nb,    h->d_pair0, h->d_join,  h->d_ext,     h->n_ids,
+               h->d_dict,  h->dnb,   h->d_dict2, h->dnb2,    h->d_toklen};
   const int ring = h->profile;
   if (ring != s->ring) {  // (re)size the event ring
     for (auto e : s->ev)
@@ -230,6 +242,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   if (launch_tile(w, tb, h->pattern, mode, st) != hipSuccess) return TT_ERR_HIP;
   s->ticket_base += w.n_tiles;  // the tiles took their tickets
   if (d_docs && launch_doc_offsets(w, st) != hipSuccess) return TT_ERR_HIP;
+  if (mode == 2 && launch_spans(w, st) != hipSuccess) return TT_ERR_HIP;
   if (!mark()) return TT_ERR_HIP;
   if (ring) ++s->n_calls;
   return TT_OK;
@@ -300,6 +313,13 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   std::vector<int32_t> ext(n_ids);
   for (int b = 0; b < 256; ++b) ext[b] = byte_id[b];
   for (int32_t r = 0; r < n_merges; ++r) ext[256 + r] = merges[r].result;
+  // byte length of every internal ID (span export): a merge result spells its
+  // operands back to back, and both operands come before it
+  std::vector<uint32_t> toklen(n_ids, 1u);
+  for (int32_t r = 0; r < n_merges; ++r) {
+    const uint64_t l = (uint64_t)toklen[(size_t)internal[merges[r].left]] + toklen[(size_t)internal[merges[r].right]];
+    toklen[256 + (size_t)r] = l > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)l;
+  }
 
   // byte-pair ranks, and the two-choice cuckoo table of all pairs (two slots
   // per bucket, load 0.8; the table grows by 1/8 while an insertion cannot be
@@ -512,6 +532,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       hipMalloc(reinterpret_cast<void**>(&h->d_dict), sizeof(u32x4) * dict.size()) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_dict2), sizeof(u32x4) * dict2.size()) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_ext), sizeof(int32_t) * n_ids) != hipSuccess ||
+      hipMalloc(reinterpret_cast<void**>(&h->d_toklen), sizeof(uint32_t) * n_ids) != hipSuccess ||
       hipMalloc(reinterpret_cast<void**>(&h->d_join), sizeof(uint32_t) * 2048) != hipSuccess) {
     tt_destroy(h);
     return TT_ERR_OOM;
@@ -521,6 +542,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       hipMemcpy(h->d_dict, dict.data(), sizeof(u32x4) * dict.size(), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_dict2, dict2.data(), sizeof(u32x4) * dict2.size(), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_ext, ext.data(), sizeof(int32_t) * n_ids, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(h->d_toklen, toklen.data(), sizeof(uint32_t) * n_ids, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_join, join.data(), sizeof(uint32_t) * 2048, hipMemcpyHostToDevice) != hipSuccess) {
     tt_destroy(h);
     return TT_ERR_HIP;
@@ -539,6 +561,7 @@ void tt_destroy(tt_tokenizer* h) {
   if (h->d_pair0) (void)hipFree(h->d_pair0);
   if (h->d_dict) (void)hipFree(h->d_dict);
   if (h->d_dict2) (void)hipFree(h->d_dict2);
+  if (h->d_toklen) (void)hipFree(h->d_toklen);
   if (h->d_join) (void)hipFree(h->d_join);
   delete h;
 }
@@ -590,6 +613,64 @@ int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_id
   if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
   if (T > 0) {
     if (hipMemcpyAsync(out_ids, s->d_out, (size_t)T * 4, hipMemcpyDeviceToHost, st) != hipSuccess)
+      return TT_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  }
+  *out_len = T;
+  return TT_OK;
+}
+
+int tt_encode_spans_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_t* d_out_ids,
+                           int32_t* d_out_spans, int64_t* d_out_len, void* stream) {
+  if (!h || !d_out_len || (len > 0 && (!d_utf8 || !d_out_ids || !d_out_spans))) return TT_ERR_NULL_ARG;
+  if (len < 0) return TT_ERR_BAD_ARG;
+  if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  if (len == 0) {
+    static const int64_t zero = 0;
+    return hipMemcpyAsync(d_out_len, &zero, 8, hipMemcpyHostToDevice, st) == hipSuccess ? TT_OK : TT_ERR_HIP;
+  }
+  Workspace* s = nullptr;
+  int rc = get_ws(h, st, (uint64_t)len, &s);
+  if (rc) return rc;
+  return run_chain(h, s, d_utf8, (uint32_t)len, nullptr, 0, d_out_ids, d_out_len, nullptr, st, 2, d_out_spans);
+}
+
+int tt_encode_spans(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_ids, int32_t* out_spans,
+                    int64_t* out_len, void* stream) {
+  if (!h || !out_len || (len > 0 && (!utf8 || !out_ids || !out_spans))) return TT_ERR_NULL_ARG;
+  if (len < 0) return TT_ERR_BAD_ARG;
+  if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
+  *out_len = 0;
+  if (len == 0) return TT_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  Workspace* s = nullptr;
+  int rc = get_ws(h, st, (uint64_t)len, &s);
+  if (rc) return rc;
+  if ((uint64_t)len > s->span_cap) {  // the spans buffer follows the workspace's capacity
+    if (s->d_spans) {
+      if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+      (void)hipFree(s->d_spans);
+      s->d_spans = nullptr;
+      s->span_cap = 0;
+    }
+    if (hipMalloc(reinterpret_cast<void**>(&s->d_spans), 16 * (size_t)s->cap) != hipSuccess) return TT_ERR_OOM;
+    s->span_cap = s->cap;
+  }
+  if (hipMemcpyAsync(s->d_in, utf8, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, 2, s->d_spans);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->h_len, s->d_len, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return TT_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  const int64_t T = *s->h_len;
+  if (T < 0) return (int)T;
+  if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
+  if (T > 0) {
+    // IDs and spans leave the device back to back, with one synchronisation
+    if (hipMemcpyAsync(out_ids, s->d_out, (size_t)T * 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipMemcpyAsync(out_spans, s->d_spans, (size_t)T * 16, hipMemcpyDeviceToHost, st) != hipSuccess)
       return TT_ERR_HIP;
     if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
   }

@@ -182,6 +182,7 @@ struct DevTables {
   uint32_t dnb;             // dictionary bucket count
   const u32x4* dict2;       // long-unit dictionary (one two-word entry per bucket)
   uint32_t dnb2;            // its bucket count
+  const uint32_t* tok_len;  // [n_ids] byte length of every internal ID (span export)
 };
 
 // ---------------------------------------------------------------------------
@@ -211,11 +212,14 @@ struct Work {
   uint64_t* tile_sum;       // [tiles] (epoch << 32) | trailing-run summary (cl100k carries)
   uint64_t* tile_last;      // [tiles] (epoch << 32) | last unit start in the tile, or NO_START
   uint64_t* tile_agg;       // [tiles] output counts for the placement look-back (epoch-tagged)
+  uint64_t* tile_cagg;      // [tiles] span export: non-continuation byte counts, same protocol
   uint32_t* tile_pre;       // batch: [tiles] outputs of all earlier tiles
   uint32_t* stage;          // [n] tokens of incoming units, at the unit's first byte
   uint32_t* unit_tile;      // batch: [n] processing tile of the unit starting at a byte
   uint32_t* unit_pos;       // batch: [n] its first output within that tile's outputs
   uint32_t* scratch;        // rows of units longer than 64 bytes: 4 * n words, then n / 16 + 8 masks
+  uint32_t* ccount;         // span export: [n/4 + 1] non-continuation bytes before byte 4w
+  int32_t* out_spans;       // span export: [T][4] byte begin, byte end, char begin, char end
   int32_t* out_ids;         // output (caller IDs, or piece offsets for the split export)
   int64_t* out_len;         // output length, or -error
   int64_t* out_doc_off;     // batch: n_docs+1 output offsets (device)
@@ -236,8 +240,11 @@ constexpr int ROWS_LDS = 480;                      // longer units: rows in LDS 
 inline uint32_t n_tiles_for(uint32_t n) { return (n + PT_OWN - 1) / PT_OWN; }
 
 // Launchers (defined in the .hip files) -------------------------------------
-// mode 0: split export (outputs are piece byte offsets); mode 1: encode
+// mode 0: split export (outputs are piece byte offsets); mode 1: encode;
+// mode 2: encode with span export (single requests)
 hipError_t launch_tile(const Work& w, const DevTables& t, int pattern, int mode, hipStream_t s);
 hipError_t launch_doc_offsets(const Work& w, hipStream_t s);
+// span export, after the tile kernel: byte ends and character spans
+hipError_t launch_spans(const Work& w, hipStream_t s);
 
 }  // namespace tt

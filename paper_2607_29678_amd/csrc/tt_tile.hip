@@ -278,6 +278,9 @@ struct PtShared {
   uint32_t inc_cnt;           // its tokens
   uint32_t carry_n;           // cl100k: number-run chars before the tile, mod 3
   uint32_t carry_nlpre;       // cl100k: class before a CR/LF stretch entering the tile
+  uint32_t cwave[PT_THREADS / 64];  // span export: per-wave sums
+  uint32_t cbase;             // span export: non-continuation bytes before the tile
+  uint32_t ctile;             // span export: non-continuation bytes the tile owns
   int64_t doc_lo_idx;         // batch: first document start index touching the window
   int last_own;               // cl100k: window index of the tile's last own character
 };
@@ -300,10 +303,54 @@ constexpr int PL_EPOCH_SHIFT = 33;
 // the walk never waits on a tile that is itself waiting).  Returns the number
 // of outputs before this tile, in every thread; the last tile also writes the
 // output length, or the error.
+//
+// With span export (cagg != nullptr), wave 1 runs the same look-back over the
+// tiles' non-continuation byte counts at the same time; each tile published
+// its own count early, so this walk rarely waits.  The sum before the tile
+// ends in sh.cbase.
+__device__ __forceinline__ uint32_t lookback_counts(uint64_t* words, uint32_t t, uint64_t ep, uint32_t epoch,
+                                                    int lane) {
+  uint32_t prefix = 0;
+  int64_t base = (int64_t)t - 1;
+  for (;;) {
+    const int64_t j = base - lane;
+    uint64_t x = ep | PL_INC;  // before the first tile: an inclusive zero
+    if (j >= 0) x = ld_word(&words[j]);
+    const bool ready = (x >> PL_EPOCH_SHIFT) == (uint64_t)epoch;
+    const uint64_t m_inc = __ballot(ready && (x & PL_INC));
+    const uint64_t m_rdy = __ballot(ready);
+    const int first = m_inc ? __ffsll((unsigned long long)m_inc) - 1 : 63;
+    const uint64_t need = first >= 63 ? ~0ull : ((2ull << first) - 1ull);
+    if ((m_rdy & need) != need) {
+      __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    const uint32_t c = lane <= first ? (uint32_t)(x & 0x7FFFFFFFull) : 0u;
+    prefix += (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_sum(c), 63);
+    if (m_inc) break;
+    base -= 64;
+  }
+  return prefix;
+}
+
 template <class Sh>
 __device__ uint32_t place_tile(const Work& w, Sh& sh, uint32_t t, uint32_t count, bool bad, int tid, int lane,
-                               int wave) {
+                               int wave, uint64_t* cagg = nullptr, uint32_t c_tile = 0) {
   const uint64_t ep = (uint64_t)w.epoch << PL_EPOCH_SHIFT;
+  if (cagg != nullptr) {
+    if (t == 0) {
+      if (tid == 0) {
+        st_word(&cagg[0], ep | PL_INC | c_tile);
+        sh.cbase = 0;
+      }
+    } else if (wave == 1) {
+      const uint32_t cpre = lookback_counts(cagg, t, ep, w.epoch, lane);
+      if (lane == 0) {
+        st_word(&cagg[t], ep | PL_INC | (cpre + c_tile));
+        sh.cbase = cpre;
+      }
+    }
+  }
   uint64_t* pl = w.tile_agg;
   if (t == 0) {
     if (tid == 0) {
@@ -354,9 +401,12 @@ __device__ uint32_t place_tile(const Work& w, Sh& sh, uint32_t t, uint32_t count
 
 // MODE 0: split-level export; the outputs are the byte offsets of the pieces.
 // MODE 1: encoding; the outputs are the (internal) IDs of the units' tokens.
+// MODE 2: encoding with span export: also the byte start of every token and the
+//         non-continuation byte count at every 4-byte word of the request.
 template <int PAT, bool BATCH, int MODE>
 __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void tile_kernel(Work w, DevTables tb) {
-  constexpr bool SEG = MODE == 1;
+  constexpr bool SEG = MODE >= 1;
+  constexpr bool SPANS = MODE == 2;
   __shared__ PtShared sh;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -471,6 +521,19 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // ASCII bytes inside the text take their codes from the ASCII table.
   static_assert(PT_BPT == 4 && PT_PAD % 4 == 0, "classification works on aligned 4-byte words");
   bool bad = false;
+  uint32_t nc_own = 0;  // span export: non-continuation bytes among the thread's own positions
+  // (also counted again at the end, from the window bytes, instead of being kept)
+  auto own_noncont = [&](uint32_t bytes, int q0, int64_t p0) -> uint32_t {
+    const uint32_t cont = bytes & ~(bytes << 1) & 0x80808080u;  // bit 7 of each continuation byte
+    uint32_t c = 0;
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) {
+      const int q = q0 + j;
+      const bool own = q >= PT_HALO && q < PT_HALO + PT_OWN && p0 + j >= 0 && p0 + j < n;
+      c += (own && !((cont >> (8 * j + 7)) & 1u)) ? 1u : 0u;
+    }
+    return c;
+  };
   {
     const int q0 = tid * PT_BPT;
     const uint32_t* bw = reinterpret_cast<const uint32_t*>(&sh.buf[PT_PAD + q0 - 4]);
@@ -478,6 +541,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     const uint32_t bw0 = bw[0], bw1 = bw[1], bw2 = bw[2];
     const uint32_t dw0 = dw[0], dw1 = dw[1], dw2 = dw[2];
     const int64_t p0 = w0 + q0;  // text position of the first of the four
+    if (SPANS) nc_own = own_noncont(bw1, q0, p0);
     uint32_t codes;
     if ((bw1 & 0x80808080u) == 0u && p0 >= 0 && p0 + PT_BPT <= n) {
       const uint8_t* asc = sh.ph.a.cls.asc;
@@ -536,7 +600,19 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     }
   }
   for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.ph.a.run_end[q] = -1;
+  if (SPANS) {
+    const uint32_t nc_incl = wave_incl_sum(nc_own);
+    if (lane == 63) sh.cwave[wave] = nc_incl;
+  }
   const bool tile_bad = __syncthreads_or(bad) != 0;
+  // span export: the tile's count is published before this block waits on
+  // anything (the look-back that sums it runs at the end)
+  if (SPANS && tid == 0) {
+    uint32_t c_tile = 0;
+    for (int v = 0; v < PT_THREADS / 64; ++v) c_tile += sh.cwave[v];
+    sh.ctile = c_tile;
+    st_word(&w.tile_cagg[t], ((uint64_t)w.epoch << PL_EPOCH_SHIFT) | c_tile);
+  }
 
   // ---- neighbour helpers (window indices; -1 = none) ----------------------
   auto code_at = [&](int q) -> uint32_t { return sh.ph.a.code[PT_PAD + q]; };
@@ -1162,7 +1238,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   }
   const uint32_t inc_cnt = has_inc ? sh.inc_cnt : 0u;
   // (place_tile ends with a barrier, which also publishes uoff to the block)
-  const uint32_t prefix = place_tile(w, sh, t, inc_cnt + ctot, tile_bad, tid, lane, wave);
+  const uint32_t prefix = place_tile(w, sh, t, inc_cnt + ctot, tile_bad, tid, lane, wave,
+                                     SPANS ? w.tile_cagg : nullptr, SPANS ? sh.ctile : 0u);
   // Valid input gives every tile a disjoint byte range and at most one output
   // per byte, so every output index is below n.  Invalid input (whose output
   // is discarded) can break that; the bound keeps it inside the buffer.
@@ -1193,12 +1270,94 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     w.unit_tile[s_prev] = t;
     w.unit_pos[s_prev] = 0;
   }
+  if (SPANS) {
+    // byte start of every token: its unit's start plus the byte lengths of the
+    // unit's earlier tokens (byte-level BPE fixes every token's length)
+    auto len_of = [&](uint32_t v) -> uint32_t { return v < tb.n_ids ? tb.tok_len[v] : 0u; };
+    // the incoming unit's tokens, PT_THREADS at a time
+    uint32_t carry = 0;
+#pragma unroll 1
+    for (uint32_t base = 0; base < inc_cnt; base += PT_THREADS) {
+      const uint32_t i = base + (uint32_t)tid;
+      const uint32_t len = i < inc_cnt ? len_of(w.stage[s_prev + i]) : 0u;
+      const uint32_t wi = wave_incl_sum(len);
+      if (lane == 63) sh.cwave[wave] = wi;
+      __syncthreads();
+      uint32_t pre = 0, tot = 0;
+      for (int v = 0; v < PT_THREADS / 64; ++v) {
+        if (v < wave) pre += sh.cwave[v];
+        tot += sh.cwave[v];
+      }
+      if (i < inc_cnt && prefix + i < lim) w.out_spans[4 * (size_t)(prefix + i)] = (int32_t)(s_prev + carry + pre + wi - len);
+      carry += tot;
+      __syncthreads();
+    }
+    // the tile's own units: a scan over the window positions, restarted at
+    // every unit start, of the lengths of the tokens held there
+    constexpr uint32_t HEAD = 0x80000000u;
+    auto seg_add = [](uint32_t a, uint32_t b) -> uint32_t {
+      return (b & HEAD) ? b : ((a & HEAD) | ((a + b) & ~HEAD));
+    };
+    uint32_t e[PT_BPT];
+    uint32_t agg = 0;
+    {
+      uint32_t bf = texcl;
+#pragma unroll
+      for (int j = 0; j < PT_BPT; ++j) {
+        const int q = qb + j;
+        const uint32_t hd = (flags >> j) & 1u;
+        bf += hd;
+        const uint32_t k = bf - 1u;
+        const bool tokq = bf != 0u && k < m_proc && (uint32_t)q - sh.ustart[k] < sh.ucnt[k];
+        e[j] = tokq ? len_of(sh.ph.b.tok[q]) : 0u;
+        agg = seg_add(agg, (hd ? HEAD : 0u) | e[j]);
+      }
+    }
+    const uint32_t winc = wave_incl_scan(agg, lane, seg_add);
+    if (lane == 63) sh.cwave[wave] = winc;
+    uint32_t st = (uint32_t)__shfl_up((int)winc, 1, 64);
+    if (lane == 0) st = 0;
+    __syncthreads();
+    uint32_t wpre = 0;
+    for (int v = 0; v < wave; ++v) wpre = seg_add(wpre, sh.cwave[v]);
+    st = seg_add(wpre, st);
+    uint32_t bf = texcl;
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) {
+      const int q = qb + j;
+      const uint32_t hd = (flags >> j) & 1u;
+      bf += hd;
+      const uint32_t k = bf - 1u;
+      if (bf != 0u && k < m_proc) {
+        const uint32_t o = (uint32_t)q - sh.ustart[k];
+        const uint32_t at = obase + sh.ph.b.uoff[k] + o;
+        const uint32_t within = hd ? 0u : (st & ~HEAD);
+        if (o < sh.ucnt[k] && at < lim) w.out_spans[4 * (size_t)at] = (int32_t)(w0 + sh.ustart[k] + within);
+      }
+      st = seg_add(st, (hd ? HEAD : 0u) | e[j]);
+    }
+    // non-continuation bytes before every 4-byte word of the tile's own range
+    // (and before the end of the text), for the character spans
+    const int q0 = tid * PT_BPT;
+    const int64_t p0 = w0 + q0;
+    const uint32_t nc = own_noncont(*reinterpret_cast<const uint32_t*>(&sh.buf[PT_PAD + q0]), q0, p0);
+    const uint32_t nci = wave_incl_sum(nc);
+    __syncthreads();  // (the scan above has read sh.cwave)
+    if (lane == 63) sh.cwave[wave] = nci;
+    __syncthreads();
+    uint32_t c_excl = nci - nc;
+    for (int v = 0; v < wave; ++v) c_excl += sh.cwave[v];
+    if (q0 >= PT_HALO && q0 < PT_HALO + PT_OWN && p0 < n) w.ccount[p0 >> 2] = sh.cbase + c_excl;
+    if (last && tid == 0 && (n & 3) == 0) w.ccount[n >> 2] = sh.cbase + sh.ctile;
+  }
 }
 
 hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode, hipStream_t s) {
   dim3 grid(w.n_tiles), block(PT_THREADS);
   const bool batch = w.doc_off != nullptr;
-  const int variant = (pattern == TT_PATTERN_GPT2 ? 0 : 4) + (batch ? 2 : 0) + (mode ? 1 : 0);
+  if (mode == 2 && batch) return hipErrorInvalidValue;  // span export is for single requests
+  const int variant = mode == 2 ? 8 + (pattern == TT_PATTERN_GPT2 ? 0 : 1)
+                                : (pattern == TT_PATTERN_GPT2 ? 0 : 4) + (batch ? 2 : 0) + (mode ? 1 : 0);
   switch (variant) {
 #define TT_TILE_CASE(V, P, B, M) \
   case V: hipLaunchKernelGGL((tile_kernel<P, B, M>), grid, block, 0, s, w, tb); break;
@@ -1210,6 +1369,8 @@ hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode
     TT_TILE_CASE(5, TT_PATTERN_CL100K, false, 1)
     TT_TILE_CASE(6, TT_PATTERN_CL100K, true, 0)
     TT_TILE_CASE(7, TT_PATTERN_CL100K, true, 1)
+    TT_TILE_CASE(8, TT_PATTERN_GPT2, false, 2)
+    TT_TILE_CASE(9, TT_PATTERN_CL100K, false, 2)
 #undef TT_TILE_CASE
   }
   return hipGetLastError();

@@ -86,6 +86,18 @@ class Tokenizer:
         _lib.check(st, "tt_encode")
         return out[: n.value].copy()
 
+    def encode_spans(self, data, stream=None):
+        """``tt_encode_spans``: (IDs int32 [T], spans int32 [T, 4]) of one UTF-8 request; a span is
+        (byte begin, byte end, char begin, char end)."""
+        src = _u8(data)
+        ids = np.empty(max(1, src.size), dtype=np.int32)
+        spans = np.empty((max(1, src.size), 4), dtype=np.int32)
+        n = ctypes.c_int64(0)
+        st = self._lib.tt_encode_spans(self._h, _ptr(src) if src.size else None, src.size, _ptr(ids), _ptr(spans),
+                                       ctypes.byref(n), _stream(stream))
+        _lib.check(st, "tt_encode_spans")
+        return ids[: n.value].copy(), spans[: n.value].copy()
+
     def encode_batch(self, docs, stream=None):
         """``tt_encode_batch``: list of int32 ID arrays, one per document."""
         parts = [bytes(d) for d in docs]
@@ -115,6 +127,12 @@ class Tokenizer:
         st = self._lib.tt_encode_device(self._h, _ptr(d_utf8), int(length), _ptr(d_out_ids), _ptr(d_out_len),
                                         _stream(stream))
         _lib.check(st, "tt_encode_device")
+
+    def encode_spans_device(self, d_utf8, length, d_out_ids, d_out_spans, d_out_len, stream=None):
+        """``tt_encode_spans_device``: enqueue on ``stream``; d_out_spans holds 4 int32 per token."""
+        st = self._lib.tt_encode_spans_device(self._h, _ptr(d_utf8), int(length), _ptr(d_out_ids),
+                                              _ptr(d_out_spans), _ptr(d_out_len), _stream(stream))
+        _lib.check(st, "tt_encode_spans_device")
 
 
     # -- measurement -------------------------------------------------------

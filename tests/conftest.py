@@ -63,6 +63,12 @@ def oracle_ids(data: bytes, table, pattern: str, memo=None) -> list:
     return out
 
 
+@functools.lru_cache(maxsize=None)
+def oracle_config_ids(k):
+    """Oracle IDs of configuration k's full text (computed once per session)."""
+    return tuple(oracle_ids(config_bytes(k), oracle_table(k), pattern_of(k)))
+
+
 @pytest.fixture(scope="session")
 def gpu():
     torch = pytest.importorskip("torch")

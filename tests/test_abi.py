@@ -22,8 +22,8 @@ def _declared():
 
 def test_header_declares_the_boundary():
     assert _declared() == sorted(["tt_create", "tt_destroy", "tt_encode", "tt_encode_device", "tt_encode_batch",
-                                  "tt_pretokenize", "tt_status_string", "tt_info", "tt_set_profiling",
-                                  "tt_stage_times"])
+                                  "tt_encode_spans", "tt_encode_spans_device", "tt_pretokenize",
+                                  "tt_status_string", "tt_info", "tt_set_profiling", "tt_stage_times"])
 
 
 def test_library_exports_every_declared_symbol():

@@ -15,7 +15,6 @@ from conftest import config_bytes, lib_tokenizer, oracle_ids, oracle_table, patt
 
 pytestmark = pytest.mark.gpu
 
-_ORACLE_CACHE = {}
 
 
 def _oracle_pieces(data: bytes, pattern: str):
@@ -25,9 +24,9 @@ def _oracle_pieces(data: bytes, pattern: str):
 
 
 def _oracle_config_ids(k):
-    if k not in _ORACLE_CACHE:
-        _ORACLE_CACHE[k] = oracle_ids(config_bytes(k), oracle_table(k), pattern_of(k))
-    return _ORACLE_CACHE[k]
+    from conftest import oracle_config_ids
+
+    return list(oracle_config_ids(k))
 
 
 def _first_diff(a, b):
