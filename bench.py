@@ -11,10 +11,11 @@ HIP events between its stages on the same stream; their average gives the
 duration of the dominant kernel (the tile kernel) for the roofline.
 Per-request latencies (enqueue to completion, input in HBM) give P50/P90/P99
 in a second pass; the host-to-host latency through ``tt_encode`` (PCIe copies
-included), a steady-state P50 (100 re-encodes of one sample) and the
-host-to-host time of a 64 x 16,384-char document batch are reported
-separately.  The CPU oracle is timed on the same timed
-samples, single-threaded, and its IDs are compared with the GPU's.
+included), a steady-state P50 (100 re-encodes of one sample), the P50 of the
+same requests with span export (IDs plus byte and character spans, device
+resident) and the host-to-host time of a 64 x 16,384-char document batch are
+reported separately.  The CPU oracle is timed on the same timed samples, one
+thread pinned to one core, and its IDs are compared with the GPU's.
 
 ``--calibrate-copy`` first runs a plain int32 copy kernel of 64 MiB read +
 64 MiB written, so that a hardware-counter profile of this command can scale
@@ -167,8 +168,24 @@ def main():
         stream.synchronize()
         steady.append((time.perf_counter() - a) * 1e3)
 
+    # --- span export: IDs with byte and character spans (device-resident) -----
+    d_spans = torch.empty((cap, 4), dtype=torch.int32, device=dev)
+    d_sids = torch.empty(cap, dtype=torch.int32, device=dev)
+    d_slen = torch.zeros(1, dtype=torch.int64, device=dev)
+    span_lat = []
+    for i in timed:
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        tok.encode_spans_device(d_in[i], len(texts[i]), d_sids, d_spans, d_slen, sid)
+        stream.synchronize()
+        span_lat.append((time.perf_counter() - a) * 1e3)
+    if int(d_slen.item()) != int(lens[timed[-1]]):
+        raise SystemExit("span export returned a different token count")
+
     # --- shape of the work: pieces of one sample (split-level export) ----------
-    n_pieces = len(tok.pretokenize(texts[timed[0]], sid))
+    starts = tok.pretokenize(texts[timed[0]], sid)
+    n_pieces = len(starts)
+    longest_piece = int(np.max(np.diff(np.append(starts, len(texts[timed[0]]))))) if n_pieces else 0
 
     # --- a batch of 64 independent 16,384-char documents (the stress config's
     # batch, its own tokenizer), host to host through tt_encode_batch -----------
@@ -212,16 +229,30 @@ def main():
         host_ids = d_out.cpu().numpy()
         same = True
         dt = 0.0
-        for i in timed:
-            a = time.perf_counter()
-            ids = oracle_encode(texts[i], table, cfg["pattern"])
-            dt += time.perf_counter() - a
-            same &= host_ids[i, : int(lens[i])].tolist() == ids
+        # one process pinned to one core, timing the tokenize call only
+        affinity = os.sched_getaffinity(0)
+        core = min(affinity)
+        os.sched_setaffinity(0, {core})
+        try:
+            for i in timed:
+                a = time.perf_counter()
+                ids = oracle_encode(texts[i], table, cfg["pattern"])
+                dt += time.perf_counter() - a
+                same &= host_ids[i, : int(lens[i])].tolist() == ids
+        finally:
+            os.sched_setaffinity(0, affinity)
+        model = ""
+        try:
+            with open("/proc/cpuinfo") as f:
+                model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+        except OSError:
+            pass
         cpu = {"value": round(sum(n_chars[i] for i in timed) / dt, 1), "unit": "chars/s", "cores": 1,
                "kind": "oracle",
-               "sample": "the %d timed 1,000,000-char samples, one after another, single thread, pure Python"
-                         % len(timed),
-               "seconds": round(dt, 2), "ids_identical_to_gpu": bool(same)}
+               "sample": "the %d timed 1,000,000-char samples, one after another, one thread pinned to core %d, "
+                         "pure Python" % (len(timed), core),
+               "seconds": round(dt, 2), "ids_identical_to_gpu": bool(same),
+               "host": {"cpu_model": model, "cores_visible": len(affinity), "python": sys.version.split()[0]}}
 
     out = {
         "metric": "exact-tokenization chars/sec and P50 latency for a 1M-char request, 1 MI355X",
@@ -240,12 +271,13 @@ def main():
                                % (k, "agent-transcript" if k == 3 else "multilingual agent-transcript",
                                   cfg["pattern"], cfg["merges"]),
                    "chars": 1_000_000, "bytes_avg": int(B_avg), "tokens_avg": int(T_avg), "samples": len(timed),
-                   "pieces_sample0": n_pieces},
+                   "pieces_sample0": n_pieces, "longest_piece_bytes_sample0": longest_piece},
         "p50_ms": round(percentile(lat, 50), 4),
         "p90_ms": round(percentile(lat, 90), 4),
         "p99_ms": round(percentile(lat, 99), 4),
         "host_to_host_p50_ms": round(percentile(host_lat, 50), 4),
         "steady_state_p50_ms": round(percentile(steady, 50), 4),
+        "span_export_p50_ms": round(percentile(span_lat, 50), 4),
         "batch_64x16k": batch,
         "stage_ms": {s: round(v, 4) for s, v in stage_avg.items()},
         "roofline": roofline,
