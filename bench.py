@@ -71,6 +71,53 @@ def measured_traffic(config):
     return rec.get("traffic_bytes_per_launch")
 
 
+def incremental_repair(tok, k, sid, n_appends=24):
+    """Append latency of a session (window re-tokenization and splice, host to
+    host) against re-tokenizing the whole text through tt_encode, at two
+    context sizes; appends are seeded lognormal sizes around 1,500 characters
+    (the paper's median append), cut from a separate sample."""
+    import random
+
+    import numpy as np
+
+    from paper_2607_29678_amd import Session
+    from workloads import textgen
+
+    feed = textgen.latency_sample(k, 30)
+    rows = []
+    for ctx_chars, ctx_seed in ((100_000, 28), (1_000_000, 29)):
+        base = textgen.latency_sample(k, ctx_seed)[:ctx_chars]
+        rng = random.Random(0xA5 + ctx_chars)
+        sess = Session(tok)
+        sess.append(base.encode("utf-8"), sid)
+        text = base.encode("utf-8")
+        pos = 0
+        rep, full, sizes, first, fallbacks, same = [], [], [], 0, 0, True
+        for _ in range(n_appends):
+            n = max(1, min(20000, int(rng.lognormvariate(np.log(1500.0), 0.8))))
+            piece = feed[pos:pos + n].encode("utf-8")
+            pos += n
+            a = time.perf_counter()
+            info = sess.append(piece, sid)
+            rep.append((time.perf_counter() - a) * 1e3)
+            text += piece
+            a = time.perf_counter()
+            want = tok.encode(text, sid)
+            full.append((time.perf_counter() - a) * 1e3)
+            sizes.append(n)
+            first += info["windows"] == 1 and not info["full"]
+            fallbacks += info["full"]
+            same &= np.array_equal(sess.ids(), want)
+        sess.close()
+        rows.append({"ctx_chars": ctx_chars, "appends": n_appends, "append_chars_p50": int(percentile(sizes, 50)),
+                     "repair_p50_ms": round(percentile(rep, 50), 4), "repair_p90_ms": round(percentile(rep, 90), 4),
+                     "full_reencode_p50_ms": round(percentile(full, 50), 4),
+                     "first_window_admitted": int(first), "full_fallbacks": int(fallbacks),
+                     "ids_identical_to_full_encode": bool(same)})
+    return {"window_chars": 512, "shapes": rows,
+            "context": {"paper_repair_p50_ms_1M": 1.23, "paper_hardware": "CPU session store (Qwen3 real text)"}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -204,6 +251,9 @@ def main():
              "chars_per_s": round(bchars / (percentile(blat, 50) * 1e-3), 1)}
     btok.close()
 
+    # --- incremental repair: appends to a stored session (Sec. 3.2) ------------
+    repair = incremental_repair(tok, k, sid)
+
     # --- roofline of the dominant kernel -------------------------------------
     # algorithmic bytes of one tile-kernel launch: the request's bytes are
     # read once and its token IDs written once (merge-table probes are L2
@@ -279,6 +329,7 @@ def main():
         "steady_state_p50_ms": round(percentile(steady, 50), 4),
         "span_export_p50_ms": round(percentile(span_lat, 50), 4),
         "batch_64x16k": batch,
+        "incremental_repair": repair,
         "stage_ms": {s: round(v, 4) for s, v in stage_avg.items()},
         "roofline": roofline,
         "cpu_baseline": cpu,

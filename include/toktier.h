@@ -185,6 +185,103 @@ int tt_encode_spans_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, 
 int tt_pretokenize(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int64_t* out_piece_starts,
                    int64_t* out_n, void* stream);
 
+/* ---- incremental repair (stateful sessions) ------------------------------ */
+/* A session holds the text of a growing request and the records (ID, byte
+ * span, character span) of its full tokenization.  Appending text B to the
+ * stored text A re-tokenizes only a window, the last w characters of A
+ * followed by B, with this library, and splices the fresh records onto the
+ * cached ones (Sec. 3.2, "Incremental repair"):
+ *  - find the longest run of records on which cached and fresh tokenization
+ *    agree in byte span and ID;
+ *  - admit it only if it holds at least two tokens, covers more characters
+ *    than the longest token of the vocabulary, and contains a synchronizing
+ *    boundary (see tt_sync_boundaries) with its left neighbour inside the
+ *    window (Appendix, Definition d:cert: such a boundary is a splice
+ *    certificate, and Theorem t:main makes the splice exact);
+ *  - keep the cached records up to the end of the run and the fresh records
+ *    after it (Corollary c:shift: splicing at the end of the run equals
+ *    splicing at the boundary inside it);
+ *  - otherwise double w and try again, at most five times, then tokenize the
+ *    whole text.
+ * The resulting IDs are always identical to full tokenization of A ++ B; a
+ * rejected window only costs more work.  Mid-text edits are not supported. */
+typedef struct tt_session tt_session; /* opaque; not thread-safe */
+
+/* Outcome of one append. */
+typedef struct {
+  int64_t kept;         /* leading tokens of the previous sequence kept as they were */
+  int64_t n_tokens;     /* tokens of the whole text after the append             */
+  int32_t windows;      /* windows tokenized (0 when the whole text was tokenized
+                           directly: empty session, or a window reaching the
+                           start of the text)                                    */
+  int32_t full;         /* 1 if the whole text was tokenized                      */
+  int64_t window_chars; /* width w of the window that was accepted (0 if full)  */
+} tt_append_info;
+
+/* New empty session on handle h.  window_chars is the first window width w in
+ * characters (0 selects the paper's default, 512).  The session keeps a
+ * pointer to h, which must outlive it; host memory grows with the text
+ * (the bytes, 4 bytes per token ID and 16 bytes per token span). */
+int tt_session_create(tt_tokenizer* h, int32_t window_chars, tt_session** out);
+
+/* Free a session.  NULL is ignored. */
+void tt_session_destroy(tt_session* s);
+
+/* Append utf8[len] (host) to the session text and update its tokens.
+ * The append must consist of whole characters: the text stays strict UTF-8,
+ * else TT_ERR_INVALID_UTF8 and the session is unchanged.  The windows run on
+ * `stream` (blocking calls of tt_encode_spans).  info (may be NULL) receives
+ * the outcome; the new IDs are tokens [info.kept, info.n_tokens) of
+ * tt_session_ids.  len == 0 changes nothing. */
+int tt_session_append(tt_session* s, const uint8_t* utf8, int64_t len, tt_append_info* info, void* stream);
+
+/* Copy tokens [from, from + count) of the session: IDs into out_ids (host,
+ * count entries; may be NULL) and spans into out_spans (host, 4 * count
+ * int32 values laid out as in tt_encode_spans; may be NULL).  The range must
+ * lie inside [0, n_tokens), else TT_ERR_BAD_ARG. */
+int tt_session_tokens(const tt_session* s, int64_t from, int64_t count, int32_t* out_ids, int32_t* out_spans);
+
+/* Bytes, characters and tokens of the session text (any may be NULL). */
+int tt_session_info(const tt_session* s, int64_t* n_bytes, int64_t* n_chars, int64_t* n_tokens);
+
+/* Synchronizing boundaries of a text (host only; no GPU work, no handle):
+ * out_mask[p] = 1 if byte position p (0 < p < len) lies between two
+ * characters whose classes form a synchronizing transition of the pattern,
+ * else 0.  At such a position every text that contains the two characters
+ * there has a piece boundary, the pieces to its right do not depend on the
+ * text before its left neighbour, and the pieces to its left do not depend on
+ * the text after its right neighbour (Appendix, "Discharging the certificate
+ * per family": the deployed check requires a class transition from a
+ * per-family synchronizing set, proven to reset the pre-tokenizer under every
+ * left context; the sets are derived per pattern).  Transitions, with O other,
+ * L letter, N number, WS whitespace but CR/LF, NL CR/LF, SP U+0020, APO U+0027:
+ *   GPT-2:   left and right classes differ, counting WS and NL as one class,
+ *            and the left character is neither SP nor APO;
+ *   cl100k:  (non-N, N); (N or NL, L); (L, N, NL or WS but SP, O);
+ *            (L, N or O, WS); (L or N, NL).
+ * Invalid UTF-8 next to a position gives 0 there.  out_mask has len entries
+ * (host). */
+int tt_sync_boundaries(int32_t pattern_id, const uint8_t* utf8, int64_t len, uint8_t* out_mask);
+
+/* The splice decision of one window (host only; exported so that the
+ * decision can be tested against records from any tokenizer).
+ *  text[len]        the whole new text A ++ B (host).
+ *  a_len            bytes of A; x  first byte of the window (a character
+ *                   start, 0 < x < a_len).
+ *  c_ids, c_spans   the n_c records of the tokenization of A (spans as in
+ *                   tt_encode_spans, in text coordinates).
+ *  f_ids, f_spans   the n_f records of the tokenization of text[x, len),
+ *                   shifted to text coordinates (byte spans + x, character
+ *                   spans + the characters before x).
+ *  max_token_chars  the check's length bound (the longest token).
+ * Returns 1 and sets *keep_c, *from_f when the window is admitted: the new
+ * records are c[0, keep_c) followed by f[from_f, n_f).  Returns 0 when it is
+ * rejected, or a negative TT_ERR_* code. */
+int tt_splice_plan(int32_t pattern_id, const uint8_t* text, int64_t len, int64_t a_len, int64_t x,
+                   const int32_t* c_ids, const int32_t* c_spans, int64_t n_c, const int32_t* f_ids,
+                   const int32_t* f_spans, int64_t n_f, int64_t max_token_chars, int64_t* keep_c,
+                   int64_t* from_f);
+
 /* ---- misc ------------------------------------------------------------ */
 /* Static English text for a status code. */
 const char* tt_status_string(int status);

@@ -43,9 +43,25 @@ SIGNATURES = {
     "tt_pretokenize": (ctypes.c_int, [_P, _P, _I64, _P, ctypes.POINTER(_I64), _P]),
     "tt_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "tt_info": (ctypes.c_int, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32), ctypes.POINTER(_I32)]),
+    "tt_session_create": (ctypes.c_int, [_P, _I32, ctypes.POINTER(_P)]),
+    "tt_session_destroy": (None, [_P]),
+    "tt_session_append": (ctypes.c_int, [_P, _P, _I64, _P, _P]),
+    "tt_session_tokens": (ctypes.c_int, [_P, _I64, _I64, _P, _P]),
+    "tt_session_info": (ctypes.c_int, [_P, ctypes.POINTER(_I64), ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
+    "tt_sync_boundaries": (ctypes.c_int, [_I32, _P, _I64, _P]),
+    "tt_splice_plan": (ctypes.c_int, [_I32, _P, _I64, _I64, _I64, _P, _P, _I64, _P, _P, _I64, _I64,
+                                      ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
     "tt_set_profiling": (ctypes.c_int, [_P, _I32]),
     "tt_stage_times": (ctypes.c_int, [_P, _P, _P, _I32, ctypes.POINTER(_I32)]),
 }
+
+
+
+class AppendInfo(ctypes.Structure):
+    """``tt_append_info``: the outcome of one session append."""
+
+    _fields_ = [("kept", _I64), ("n_tokens", _I64), ("windows", _I32), ("full", _I32), ("window_chars", _I64)]
+
 
 STAGES = ["tile"]  # TT_N_STAGES stages per call, in launch order
 

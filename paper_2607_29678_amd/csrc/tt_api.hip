@@ -68,6 +68,7 @@ struct tt_tokenizer {
   int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
   uint32_t* d_toklen = nullptr;  // [256 + M] byte length of every internal ID
   uint32_t n_ids = 0;
+  uint32_t max_tok_bytes = 1;  // byte length of the longest token (incremental repair)
   uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
                                // byte x to a token starting with byte y
   std::mutex mu;
@@ -249,6 +250,11 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
 }
 
 }  // namespace
+
+namespace tt {
+int handle_pattern(const tt_tokenizer* h) { return h->pattern; }
+uint32_t handle_max_token_bytes(const tt_tokenizer* h) { return h->max_tok_bytes; }
+}  // namespace tt
 
 extern "C" {
 
@@ -523,6 +529,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
   h->dnb = dnb;
   h->dnb2 = dnb2;
   h->n_ids = n_ids;
+  h->max_tok_bytes = *std::max_element(toklen.begin(), toklen.end());
   if (hipGetDevice(&h->device) != hipSuccess) {
     delete h;
     return TT_ERR_HIP;

@@ -247,4 +247,8 @@ hipError_t launch_doc_offsets(const Work& w, hipStream_t s);
 // span export, after the tile kernel: byte ends and character spans
 hipError_t launch_spans(const Work& w, hipStream_t s);
 
+// Facts of a handle for the host-side session code.
+int handle_pattern(const tt_tokenizer* h);
+uint32_t handle_max_token_bytes(const tt_tokenizer* h);  // longest token, in bytes
+
 }  // namespace tt

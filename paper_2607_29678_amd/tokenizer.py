@@ -150,5 +150,93 @@ class Tokenizer:
         return [{_lib.STAGES[i]: float(out[c * ns + i]) for i in range(ns)} for c in range(n.value // ns)]
 
 
+class Session:
+    """Incremental repair over a growing request (``tt_session_*``).
+
+    After every ``append`` the session's IDs equal full tokenization of the
+    whole text; ``append`` returns the ``tt_append_info`` fields as a dict.
+    """
+
+    def __init__(self, tokenizer: Tokenizer, window_chars: int = 0):
+        self._lib = tokenizer._lib
+        self._tok = tokenizer  # the handle must outlive the session
+        h = ctypes.c_void_p()
+        _lib.check(self._lib.tt_session_create(tokenizer._h, int(window_chars), ctypes.byref(h)),
+                   "tt_session_create")
+        self._s = h
+
+    def close(self):
+        if getattr(self, "_s", None):
+            self._lib.tt_session_destroy(self._s)
+            self._s = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def append(self, data, stream=None) -> dict:
+        src = _u8(data)
+        info = _lib.AppendInfo()
+        st = self._lib.tt_session_append(self._s, _ptr(src) if src.size else None, src.size, ctypes.byref(info),
+                                         _stream(stream))
+        _lib.check(st, "tt_session_append")
+        return {k: int(getattr(info, k)) for k, _ in _lib.AppendInfo._fields_}
+
+    def info(self) -> dict:
+        b, c, t = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int64(0)
+        _lib.check(self._lib.tt_session_info(self._s, ctypes.byref(b), ctypes.byref(c), ctypes.byref(t)),
+                   "tt_session_info")
+        return {"bytes": b.value, "chars": c.value, "tokens": t.value}
+
+    def tokens(self, start=0, count=None):
+        """(IDs int32 [count], spans int32 [count, 4]) of tokens [start, start + count)."""
+        n = self.info()["tokens"]
+        count = n - start if count is None else count
+        ids = np.empty(max(1, count), dtype=np.int32)
+        spans = np.empty((max(1, count), 4), dtype=np.int32)
+        _lib.check(self._lib.tt_session_tokens(self._s, int(start), int(count), _ptr(ids), _ptr(spans)),
+                   "tt_session_tokens")
+        return ids[:count].copy(), spans[:count].copy()
+
+    def ids(self) -> np.ndarray:
+        return self.tokens()[0]
+
+
+def sync_boundaries(data, pattern="gpt2") -> np.ndarray:
+    """``tt_sync_boundaries``: uint8 mask of the synchronizing byte positions of a text (host only)."""
+    lib = _lib.load()
+    pat = PATTERNS[pattern] if isinstance(pattern, str) else int(pattern)
+    src = _u8(data)
+    out = np.zeros(max(1, src.size), dtype=np.uint8)
+    _lib.check(lib.tt_sync_boundaries(pat, _ptr(src) if src.size else None, src.size, _ptr(out)),
+               "tt_sync_boundaries")
+    return out[: src.size].copy()
+
+
+def splice_plan(text, a_len, x, c_ids, c_spans, f_ids, f_spans, max_token_chars, pattern="gpt2"):
+    """``tt_splice_plan``: (keep_c, from_f) when the window is admitted, else None (host only)."""
+    lib = _lib.load()
+    pat = PATTERNS[pattern] if isinstance(pattern, str) else int(pattern)
+    src = _u8(text)
+    ci = np.ascontiguousarray(c_ids, dtype=np.int32)
+    cs = np.ascontiguousarray(np.asarray(c_spans, dtype=np.int32).reshape(-1, 4))
+    fi = np.ascontiguousarray(f_ids, dtype=np.int32)
+    fs = np.ascontiguousarray(np.asarray(f_spans, dtype=np.int32).reshape(-1, 4))
+    kc, ff = ctypes.c_int64(0), ctypes.c_int64(0)
+    st = lib.tt_splice_plan(pat, _ptr(src), src.size, int(a_len), int(x), _ptr(ci), _ptr(cs), len(ci), _ptr(fi),
+                            _ptr(fs), len(fi), int(max_token_chars), ctypes.byref(kc), ctypes.byref(ff))
+    if st < 0:
+        _lib.check(st, "tt_splice_plan")
+    return (kc.value, ff.value) if st == 1 else None
+
+
 def status_string(status: int) -> str:
     return _lib.load().tt_status_string(status).decode()

@@ -23,7 +23,9 @@ def _declared():
 def test_header_declares_the_boundary():
     assert _declared() == sorted(["tt_create", "tt_destroy", "tt_encode", "tt_encode_device", "tt_encode_batch",
                                   "tt_encode_spans", "tt_encode_spans_device", "tt_pretokenize",
-                                  "tt_status_string", "tt_info", "tt_set_profiling", "tt_stage_times"])
+                                  "tt_status_string", "tt_info", "tt_set_profiling", "tt_stage_times",
+                                  "tt_session_create", "tt_session_destroy", "tt_session_append",
+                                  "tt_session_tokens", "tt_session_info", "tt_sync_boundaries", "tt_splice_plan"])
 
 
 def test_library_exports_every_declared_symbol():
