@@ -196,6 +196,21 @@ int get_ws(tt_tokenizer* h, hipStream_t stream, uint64_t need, Workspace** out) 
   return TT_OK;
 }
 
+// The spans buffer of a workspace (host span export), allocated on first use
+// and grown with the workspace's capacity.
+int reserve_spans(Workspace* s, uint64_t len, hipStream_t st) {
+  if (len <= s->span_cap) return TT_OK;
+  if (s->d_spans) {
+    if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+    (void)hipFree(s->d_spans);
+    s->d_spans = nullptr;
+    s->span_cap = 0;
+  }
+  if (hipMalloc(reinterpret_cast<void**>(&s->d_spans), 16 * (size_t)s->cap) != hipSuccess) return TT_ERR_OOM;
+  s->span_cap = s->cap;
+  return TT_OK;
+}
+
 // Enqueue the whole chain for `n` bytes at device address `text`.
 // mode 0: split export (out_ids receives piece offsets); mode 1: encode;
 // mode 2: encode with span export into out_spans ([n][4], single requests).
@@ -254,6 +269,36 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
 namespace tt {
 int handle_pattern(const tt_tokenizer* h) { return h->pattern; }
 uint32_t handle_max_token_bytes(const tt_tokenizer* h) { return h->max_tok_bytes; }
+
+// Span export of a small host request with one synchronisation: the length,
+// and `len` ID and span slots (at least the T written, since T <= len), leave
+// the device together.  h_in, h_ids, h_spans and h_len are pinned host memory
+// of at least len, len, 4 len and 1 entries.
+int encode_spans_pinned(tt_tokenizer* h, const uint8_t* h_in, int64_t len, int32_t* h_ids, int32_t* h_spans,
+                        int64_t* h_len, void* stream) {
+  if (!h || !h_in || !h_ids || !h_spans || !h_len) return TT_ERR_NULL_ARG;
+  if (len <= 0) return TT_ERR_BAD_ARG;
+  if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  Workspace* s = nullptr;
+  int rc = get_ws(h, st, (uint64_t)len, &s);
+  if (rc) return rc;
+  rc = reserve_spans(s, (uint64_t)len, st);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->d_in, h_in, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, 2, s->d_spans);
+  if (rc) return rc;
+  if (hipMemcpyAsync(h_len, s->d_len, 8, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(h_ids, s->d_out, (size_t)len * 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(h_spans, s->d_spans, (size_t)len * 16, hipMemcpyDeviceToHost, st) != hipSuccess)
+    return TT_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  const int64_t T = *h_len;
+  if (T < 0) return (int)T;
+  if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
+  return TT_OK;
+}
 }  // namespace tt
 
 extern "C" {
@@ -656,16 +701,8 @@ int tt_encode_spans(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* 
   Workspace* s = nullptr;
   int rc = get_ws(h, st, (uint64_t)len, &s);
   if (rc) return rc;
-  if ((uint64_t)len > s->span_cap) {  // the spans buffer follows the workspace's capacity
-    if (s->d_spans) {
-      if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
-      (void)hipFree(s->d_spans);
-      s->d_spans = nullptr;
-      s->span_cap = 0;
-    }
-    if (hipMalloc(reinterpret_cast<void**>(&s->d_spans), 16 * (size_t)s->cap) != hipSuccess) return TT_ERR_OOM;
-    s->span_cap = s->cap;
-  }
+  rc = reserve_spans(s, (uint64_t)len, st);
+  if (rc) return rc;
   if (hipMemcpyAsync(s->d_in, utf8, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
   rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, 2, s->d_spans);
   if (rc) return rc;

@@ -250,5 +250,8 @@ hipError_t launch_spans(const Work& w, hipStream_t s);
 // Facts of a handle for the host-side session code.
 int handle_pattern(const tt_tokenizer* h);
 uint32_t handle_max_token_bytes(const tt_tokenizer* h);  // longest token, in bytes
+// span export of a small host request with one synchronisation (pinned buffers)
+int encode_spans_pinned(tt_tokenizer* h, const uint8_t* h_in, int64_t len, int32_t* h_ids, int32_t* h_spans,
+                        int64_t* h_len, void* stream);
 
 }  // namespace tt

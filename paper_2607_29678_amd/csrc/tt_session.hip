@@ -17,7 +17,8 @@
 // the run).
 //
 // Everything here is host code; the windows are tokenized by the library's
-// span export (tt_encode_spans) on the caller's stream.
+// span export on the caller's stream, through pinned buffers with one
+// synchronisation per window.
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
@@ -190,7 +191,20 @@ struct tt_session {
   int64_t n_chars = 0;
   std::vector<int32_t> ids;       // records of the full tokenization of `text`
   std::vector<int32_t> spans;     // 4 per token, text coordinates
-  std::vector<int32_t> f_ids, f_spans;  // window records (reused)
+  std::vector<int32_t> f_ids, f_spans;  // records of a whole-text tokenization
+  // windows go through pinned buffers (one synchronisation per window)
+  int64_t pin_cap = 0;
+  uint8_t* p_in = nullptr;
+  int32_t* p_ids = nullptr;
+  int32_t* p_spans = nullptr;
+  int64_t* p_len = nullptr;
+
+  ~tt_session() {
+    if (p_in) (void)hipHostFree(p_in);
+    if (p_ids) (void)hipHostFree(p_ids);
+    if (p_spans) (void)hipHostFree(p_spans);
+    if (p_len) (void)hipHostFree(p_len);
+  }
 };
 
 namespace {
@@ -201,21 +215,60 @@ int64_t count_chars(const uint8_t* s, int64_t n) {
   return c;
 }
 
-// Tokenize text[from, len) with spans into the session's window buffers,
-// shifted to text coordinates; returns the token count or an error.
-int64_t encode_window(tt_session* s, int64_t from, int64_t chars_before, void* stream) {
+constexpr int64_t PIN_MAX = 1 << 20;  // largest window staged in pinned memory (bytes)
+
+int grow_pinned(tt_session* s, int64_t n) {
+  if (n <= s->pin_cap) return TT_OK;
+  int64_t cap = 65536;
+  while (cap < n) cap <<= 1;
+  if (s->p_in) (void)hipHostFree(s->p_in);
+  if (s->p_ids) (void)hipHostFree(s->p_ids);
+  if (s->p_spans) (void)hipHostFree(s->p_spans);
+  s->p_in = nullptr;
+  s->p_ids = nullptr;
+  s->p_spans = nullptr;
+  s->pin_cap = 0;
+  if (!s->p_len && hipHostMalloc(reinterpret_cast<void**>(&s->p_len), 8, hipHostMallocDefault) != hipSuccess)
+    return TT_ERR_OOM;
+  if (hipHostMalloc(reinterpret_cast<void**>(&s->p_in), (size_t)cap, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc(reinterpret_cast<void**>(&s->p_ids), 4 * (size_t)cap, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc(reinterpret_cast<void**>(&s->p_spans), 16 * (size_t)cap, hipHostMallocDefault) != hipSuccess)
+    return TT_ERR_OOM;
+  s->pin_cap = cap;
+  return TT_OK;
+}
+
+// Records of text[from, end) with spans shifted to text coordinates, in
+// *ids / *spans (the session's pinned buffers for a window, its vectors for a
+// longer range); returns the token count or an error.
+int64_t encode_range(tt_session* s, int64_t from, int64_t chars_before, void* stream, int32_t** ids,
+                     int32_t** spans) {
   const int64_t n = (int64_t)s->text.size() - from;
-  s->f_ids.resize((size_t)std::max<int64_t>(n, 1));
-  s->f_spans.resize(4 * (size_t)std::max<int64_t>(n, 1));
   int64_t T = 0;
-  const int rc = tt_encode_spans(s->h, s->text.data() + from, n, s->f_ids.data(), s->f_spans.data(), &T, stream);
-  if (rc != TT_OK) return rc;
+  if (n <= PIN_MAX) {
+    int rc = grow_pinned(s, n);
+    if (rc != TT_OK) return rc;
+    std::memcpy(s->p_in, s->text.data() + from, (size_t)n);
+    rc = tt::encode_spans_pinned(s->h, s->p_in, n, s->p_ids, s->p_spans, s->p_len, stream);
+    if (rc != TT_OK) return rc;
+    T = *s->p_len;
+    *ids = s->p_ids;
+    *spans = s->p_spans;
+  } else {
+    s->f_ids.resize((size_t)n);
+    s->f_spans.resize(4 * (size_t)n);
+    const int rc = tt_encode_spans(s->h, s->text.data() + from, n, s->f_ids.data(), s->f_spans.data(), &T, stream);
+    if (rc != TT_OK) return rc;
+    *ids = s->f_ids.data();
+    *spans = s->f_spans.data();
+  }
   if (from != 0) {
+    int32_t* sp = *spans;
     for (int64_t k = 0; k < T; ++k) {
-      s->f_spans[4 * k] += (int32_t)from;
-      s->f_spans[4 * k + 1] += (int32_t)from;
-      s->f_spans[4 * k + 2] += (int32_t)chars_before;
-      s->f_spans[4 * k + 3] += (int32_t)chars_before;
+      sp[4 * k] += (int32_t)from;
+      sp[4 * k + 1] += (int32_t)from;
+      sp[4 * k + 2] += (int32_t)chars_before;
+      sp[4 * k + 3] += (int32_t)chars_before;
     }
   }
   return T;
@@ -285,12 +338,7 @@ int tt_session_append(tt_session* s, const uint8_t* utf8, int64_t len, tt_append
     s->text.resize((size_t)a_len);
     return rc;
   };
-  auto take_all = [&](int64_t T) {  // the window records are the whole text's
-    s->ids.assign(s->f_ids.begin(), s->f_ids.begin() + T);
-    s->spans.assign(s->f_spans.begin(), s->f_spans.begin() + 4 * T);
-    r.kept = 0;
-    r.full = 1;
-  };
+  int32_t *f_ids = nullptr, *f_spans = nullptr;
   bool done = false;
   if (a_len > 0) {
     for (int attempt = 0; attempt <= 5 && !done; ++attempt) {
@@ -302,26 +350,29 @@ int tt_session_append(tt_session* s, const uint8_t* utf8, int64_t len, tt_append
         c += (t[x] & 0xC0u) != 0x80u;
       }
       if (x == 0) break;  // the window reaches the text start: tokenize the whole text
-      const int64_t T = encode_window(s, x, s->n_chars - w, stream);
+      const int64_t T = encode_range(s, x, s->n_chars - w, stream, &f_ids, &f_spans);
       if (T < 0) return fail((int)T);
       ++r.windows;
-      const Plan p = plan_splice(s->pattern, t, n, a_len, x, s->ids.data(), s->spans.data(), T_old,
-                                 s->f_ids.data(), s->f_spans.data(), T, s->max_tok_chars);
+      const Plan p = plan_splice(s->pattern, t, n, a_len, x, s->ids.data(), s->spans.data(), T_old, f_ids,
+                                 f_spans, T, s->max_tok_chars);
       if (!p.accept) continue;
       // in place: drop the cached tail, append the fresh records after the run
       s->ids.resize((size_t)p.keep_c);
       s->spans.resize(4 * (size_t)p.keep_c);
-      s->ids.insert(s->ids.end(), s->f_ids.begin() + p.from_f, s->f_ids.begin() + T);
-      s->spans.insert(s->spans.end(), s->f_spans.begin() + 4 * p.from_f, s->f_spans.begin() + 4 * T);
+      s->ids.insert(s->ids.end(), f_ids + p.from_f, f_ids + T);
+      s->spans.insert(s->spans.end(), f_spans + 4 * p.from_f, f_spans + 4 * T);
       r.kept = p.keep_c;
       r.window_chars = w;
       done = true;
     }
   }
-  if (!done) {
-    const int64_t T = encode_window(s, 0, 0, stream);
+  if (!done) {  // the whole text
+    const int64_t T = encode_range(s, 0, 0, stream, &f_ids, &f_spans);
     if (T < 0) return fail((int)T);
-    take_all(T);
+    s->ids.assign(f_ids, f_ids + T);
+    s->spans.assign(f_spans, f_spans + 4 * T);
+    r.kept = 0;
+    r.full = 1;
   }
   s->n_chars += count_chars(utf8, len);
   r.n_tokens = (int64_t)s->ids.size();
