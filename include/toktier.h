@@ -99,6 +99,39 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
               const int64_t* vocab_offsets, int32_t vocab_size, int32_t pattern_id,
               tt_tokenizer** out);
 
+/* Front-end options of tt_create_ex. */
+typedef struct {
+  /* 1: the model stage probes the vocabulary first and a piece that is a
+   * vocabulary entry becomes that entry's single ID, without merging
+   * (Sec. 4.2: families configured with ignore_merges).  Where several IDs
+   * spell the same bytes the lowest is taken. */
+  int32_t ignore_merges;
+  /* Added tokens: literal strings that the model reserves as single IDs
+   * (Sec. 4.5).  A leftmost-longest pass extracts them before
+   * pre-tokenization, and the text between them is tokenized segment by
+   * segment (no piece crosses a literal).  Literal i is
+   * added_bytes[added_offsets[i] .. added_offsets[i+1]) (non-empty, strict
+   * UTF-8, at most TT_MAX_ADDED_BYTES bytes, pairwise distinct) with ID
+   * added_ids[i] (any non-negative value; it need not be in the vocabulary).
+   * n_added == 0 means none. */
+  int32_t n_added;
+  const uint8_t* added_bytes;
+  const int64_t* added_offsets; /* n_added + 1 entries, from 0, increasing */
+  const int32_t* added_ids;
+} tt_options;
+
+#define TT_MAX_ADDED_BYTES 1024
+
+/* tt_create with front-end options (opt may be NULL: no options).  All option
+ * arrays are copied.  Handles with added tokens support tt_encode and
+ * tt_encode_batch; the literal pass runs on the host before the request goes
+ * to the device (as in the paper's service, Sec. 4.5), and the other entry
+ * points return TT_ERR_BAD_ARG on such handles.  Invalid options return
+ * TT_ERR_BAD_ARG (literals) or the codes of tt_create. */
+int tt_create_ex(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_bytes,
+                 const int64_t* vocab_offsets, int32_t vocab_size, int32_t pattern_id,
+                 const tt_options* opt, tt_tokenizer** out);
+
 /* Free the handle, its device tables and all its workspaces.  The caller must
  * not destroy a handle while a call on it is running.  NULL is ignored. */
 void tt_destroy(tt_tokenizer* h);

@@ -34,6 +34,7 @@ _I32 = ctypes.c_int32
 _I64 = ctypes.c_int64
 SIGNATURES = {
     "tt_create": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _I32, ctypes.POINTER(_P)]),
+    "tt_create_ex": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _I32, _P, ctypes.POINTER(_P)]),
     "tt_destroy": (None, [_P]),
     "tt_encode": (ctypes.c_int, [_P, _P, _I64, _P, ctypes.POINTER(_I64), _P]),
     "tt_encode_device": (ctypes.c_int, [_P, _P, _I64, _P, _P, _P]),
@@ -55,6 +56,13 @@ SIGNATURES = {
     "tt_stage_times": (ctypes.c_int, [_P, _P, _P, _I32, ctypes.POINTER(_I32)]),
 }
 
+
+
+class Options(ctypes.Structure):
+    """``tt_options``: front-end options of ``tt_create_ex``."""
+
+    _fields_ = [("ignore_merges", _I32), ("n_added", _I32), ("added_bytes", _P), ("added_offsets", _P),
+                ("added_ids", _P)]
 
 
 class AppendInfo(ctypes.Structure):

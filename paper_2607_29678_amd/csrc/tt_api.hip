@@ -50,6 +50,96 @@ struct Workspace {
   int64_t n_calls = 0;   // calls recorded since profiling was enabled
 };
 
+// Strict UTF-8 validation on the host (added-token literals).
+bool valid_utf8(const uint8_t* t, int64_t n) {
+  int64_t i = 0;
+  while (i < n) {
+    const uint32_t b0 = t[i];
+    const int len = b0 < 0x80u ? 1 : b0 < 0xC2u ? 0 : b0 < 0xE0u ? 2 : b0 < 0xF0u ? 3 : b0 < 0xF5u ? 4 : 0;
+    if (len == 0 || i + len > n) return false;
+    if (len > 1) {
+      const uint32_t b1 = t[i + 1];
+      const uint32_t lo = b0 == 0xE0u ? 0xA0u : b0 == 0xF0u ? 0x90u : 0x80u;
+      const uint32_t hi = b0 == 0xEDu ? 0x9Fu : b0 == 0xF4u ? 0x8Fu : 0xBFu;
+      if (b1 < lo || b1 > hi) return false;
+      for (int k = 2; k < len; ++k)
+        if ((t[i + k] & 0xC0u) != 0x80u) return false;
+    }
+    i += len;
+  }
+  return true;
+}
+
+// Added-token literals and their leftmost-longest extraction (Sec. 4.5: a
+// leftmost-longest literal pass runs before the tokenizer family handles the
+// remaining segments).  Candidates are found per distinct first byte with
+// memchr, the longest literal at each candidate position is kept, and the
+// scan takes every candidate that starts at or after the end of the last
+// literal taken.
+struct AddedSet {
+  std::vector<std::string> lits;
+  std::vector<int32_t> ids;
+  std::vector<std::vector<uint32_t>> by_first;  // [256] literal indices, longest first
+  std::vector<uint8_t> firsts;                  // distinct first bytes
+  struct Match {
+    int64_t s, e;
+    int32_t id;
+  };
+
+  bool empty() const { return lits.empty(); }
+  void add(const std::string& lit, int32_t id) {
+    lits.push_back(lit);
+    ids.push_back(id);
+  }
+  void finish() {
+    by_first.assign(256, {});
+    for (uint32_t i = 0; i < lits.size(); ++i) by_first[(uint8_t)lits[i][0]].push_back(i);
+    firsts.clear();
+    for (int b = 0; b < 256; ++b) {
+      auto& v = by_first[b];
+      if (v.empty()) continue;
+      firsts.push_back((uint8_t)b);
+      std::stable_sort(v.begin(), v.end(), [&](uint32_t x, uint32_t y) { return lits[x].size() > lits[y].size(); });
+    }
+  }
+  // the longest literal starting at t[p] (first byte already known to match)
+  bool longest_at(const uint8_t* t, int64_t n, int64_t p, Match& m) const {
+    for (uint32_t i : by_first[t[p]]) {
+      const std::string& l = lits[i];
+      if ((int64_t)l.size() <= n - p && std::memcmp(t + p, l.data(), l.size()) == 0) {
+        m = Match{p, p + (int64_t)l.size(), ids[i]};
+        return true;
+      }
+    }
+    return false;
+  }
+  void extract(const uint8_t* t, int64_t n, std::vector<Match>& out) const {
+    out.clear();
+    std::vector<Match> cand;
+    Match m;
+    if (firsts.size() <= 4) {
+      for (uint8_t b : firsts) {
+        const uint8_t* q = t;
+        while ((q = static_cast<const uint8_t*>(std::memchr(q, b, (size_t)(t + n - q)))) != nullptr) {
+          if (longest_at(t, n, q - t, m)) cand.push_back(m);
+          ++q;
+        }
+      }
+      if (firsts.size() > 1)
+        std::sort(cand.begin(), cand.end(), [](const Match& x, const Match& y) { return x.s < y.s; });
+    } else {
+      for (int64_t p = 0; p < n; ++p)
+        if (!by_first[t[p]].empty() && longest_at(t, n, p, m)) cand.push_back(m);
+    }
+    int64_t covered = 0;
+    for (const Match& c : cand)
+      if (c.s >= covered) {
+        out.push_back(c);
+        covered = c.e;
+      }
+  }
+};
+
 }  // namespace
 
 struct tt_tokenizer {
@@ -69,6 +159,16 @@ struct tt_tokenizer {
   uint32_t* d_toklen = nullptr;  // [256 + M] byte length of every internal ID
   uint32_t n_ids = 0;
   uint32_t max_tok_bytes = 1;  // byte length of the longest token (incremental repair)
+  bool ignore = false;         // ignore_merges: whole pieces probed in the vocabulary first
+  uint32_t vmax = 0;           // longest vocabulary string (bytes) of the probes
+  u32x4* d_vdict = nullptr;    // probe tables (see DevTables)
+  uint32_t vdnb = 0;
+  u32x4* d_vdict2 = nullptr;
+  uint32_t vdnb2 = 0;
+  u32x4* d_vlong = nullptr;
+  uint32_t vlnb = 0;
+  uint8_t* d_vblob = nullptr;
+  AddedSet added;              // added-token literals (host-side extraction)
   uint32_t* d_join = nullptr;  // [2048] bit (x << 8 | y) set if some merge joins a token ending in
                                // byte x to a token starting with byte y
   std::mutex mu;
@@ -235,8 +335,10 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_len = out_len;
   w.out_doc_off = out_docs;
   w.out_spans = out_spans;
-  DevTables tb{h->d_slots, h->nb,    h->d_pair0, h->d_join,  h->d_ext,     h->n_ids,
-               h->d_dict,  h->dnb,   h->d_dict2, h->dnb2,    h->d_toklen};
+  DevTables tb{h->d_slots, h->nb,     h->d_pair0,  h->d_join,  h->d_ext,     h->n_ids,
+               h->d_dict,  h->dnb,    h->d_dict2,  h->dnb2,    h->d_toklen,  h->vmax,
+               h->d_vdict, h->vdnb,   h->d_vdict2, h->vdnb2,   h->d_vlong,   h->vlnb,
+               h->d_vblob};
   const int ring = h->profile;
   if (ring != s->ring) {  // (re)size the event ring
     for (auto e : s->ev)
@@ -255,7 +357,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
     return hipEventRecord(e, st) == hipSuccess;
   };
   if (!mark()) return TT_ERR_HIP;
-  if (launch_tile(w, tb, h->pattern, mode, st) != hipSuccess) return TT_ERR_HIP;
+  if (launch_tile(w, tb, h->pattern, mode, h->ignore && mode != 0, st) != hipSuccess) return TT_ERR_HIP;
   s->ticket_base += w.n_tiles;  // the tiles took their tickets
   if (d_docs && launch_doc_offsets(w, st) != hipSuccess) return TT_ERR_HIP;
   if (mode == 2 && launch_spans(w, st) != hipSuccess) return TT_ERR_HIP;
@@ -264,10 +366,168 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   return TT_OK;
 }
 
+// An entry of the whole-unit dictionaries: up to DICT2_MAX bytes as words.
+struct DictEntry {
+  uint32_t w[6], len, id;
+};
+
+DictEntry make_entry(const uint8_t* p, uint32_t L, uint32_t id) {
+  DictEntry e{{0u, 0u, 0u, 0u, 0u, 0u}, L, id};
+  for (uint32_t i = 0; i < L; ++i) e.w[i >> 2] |= (uint32_t)p[i] << (8 * (i & 3));
+  return e;
+}
+
+// Two-choice cuckoo table of 2..DICT_MAX-byte strings, two entries per bucket,
+// load 0.8; grows by 1/8 while an entry cannot be placed.  Returns nonzero if
+// the table would not fit.
+int build_dict(const std::vector<DictEntry>& entries, std::vector<u32x4>& dict, uint32_t& dnb) {
+  dnb = (uint32_t)(entries.size() * 5 / 8) + 16;
+  for (;;) {
+    dict.assign(2 * (size_t)dnb, u32x4{0u, 0u, 0u, 0u});
+    uint64_t rng = 0xD1B54A32D192ED03ull;
+    bool ok = true;
+    for (size_t i = 0; i < entries.size() && ok; ++i) {
+      u32x4 item{entries[i].w[0], entries[i].w[1], entries[i].w[2], (entries[i].id << 4) | entries[i].len};
+      ok = false;
+      for (int kick = 0; kick < 2000; ++kick) {
+        const uint32_t len = item.w & 15u;
+        const size_t b1 = 2 * (size_t)bucket_of(unit_hash(item.x, item.y, item.z, len), dnb);
+        const size_t b2 = 2 * (size_t)bucket_of(unit_hash2(item.x, item.y, item.z, len), dnb);
+        size_t free_at = SIZE_MAX;
+        for (size_t c : {b1, b1 + 1, b2, b2 + 1})
+          if (dict[c].w == 0u) {
+            free_at = c;
+            break;
+          }
+        if (free_at != SIZE_MAX) {
+          dict[free_at] = item;
+          ok = true;
+          break;
+        }
+        rng ^= rng << 13;
+        rng ^= rng >> 7;
+        rng ^= rng << 17;
+        const size_t v = ((rng & 2) ? b1 : b2) + (rng & 1);
+        std::swap(item, dict[v]);
+      }
+    }
+    if (ok) return 0;
+    dnb += dnb / 8;
+    if (dnb > (1u << 27)) return 1;
+  }
+}
+
+// Two-choice cuckoo table of DICT_MAX+1..DICT2_MAX-byte strings, one entry of
+// two words per bucket, load below 1/2.
+int build_dict2(const std::vector<DictEntry>& entries2, std::vector<u32x4>& dict2, uint32_t& dnb2) {
+  dnb2 = (uint32_t)(entries2.size() * 2) + 16;
+  for (;;) {
+    dict2.assign(2 * (size_t)dnb2, u32x4{0u, 0u, 0u, 0u});
+    uint64_t rng = 0x9E3779B97F4A7C15ull;
+    bool ok = true;
+    for (size_t i = 0; i < entries2.size() && ok; ++i) {
+      const DictEntry* item = &entries2[i];
+      DictEntry held;
+      ok = false;
+      for (int kick = 0; kick < 1000; ++kick) {
+        const uint32_t* q = item->w;
+        const size_t b1 = 2 * (size_t)bucket_of(unit_hash6(q[0], q[1], q[2], q[3], q[4], q[5], item->len), dnb2);
+        const size_t b2 = 2 * (size_t)bucket_of(unit_hash6b(q[0], q[1], q[2], q[3], q[4], q[5], item->len), dnb2);
+        const u32x4 x0{q[0], q[1], q[2], q[3]}, x1{q[4], q[5], (item->id << 5) | item->len, 0u};
+        size_t at = SIZE_MAX;
+        if (dict2[b1 + 1].z == 0u) at = b1;
+        else if (dict2[b2 + 1].z == 0u) at = b2;
+        if (at != SIZE_MAX) {
+          dict2[at] = x0;
+          dict2[at + 1] = x1;
+          ok = true;
+          break;
+        }
+        rng ^= rng << 13;
+        rng ^= rng >> 7;
+        rng ^= rng << 17;
+        const size_t v = (rng & 1) ? b1 : b2;
+        DictEntry out;
+        out.w[0] = dict2[v].x;
+        out.w[1] = dict2[v].y;
+        out.w[2] = dict2[v].z;
+        out.w[3] = dict2[v].w;
+        out.w[4] = dict2[v + 1].x;
+        out.w[5] = dict2[v + 1].y;
+        out.len = dict2[v + 1].z & 31u;
+        out.id = dict2[v + 1].z >> 5;
+        dict2[v] = x0;
+        dict2[v + 1] = x1;
+        held = out;
+        item = &held;
+      }
+    }
+    if (ok) return 0;
+    dnb2 += dnb2 / 8;
+    if (dnb2 > (1u << 27)) return 1;
+  }
+}
+
+}  // namespace
+
+namespace {
+
+// The batch chain over host documents, with the IDs and per-document output
+// offsets copied back into host vectors (used by the added-token paths, whose
+// documents are the text segments and the literals between them).
+int batch_host(tt_tokenizer* h, hipStream_t st, const uint8_t* concat, int64_t len,
+               const std::vector<int64_t>& docs, std::vector<int32_t>& ids, std::vector<int64_t>& out_docs) {
+  const int64_t n_docs = (int64_t)docs.size() - 1;
+  if (n_docs > INT32_MAX) return TT_ERR_TOO_LARGE;
+  out_docs.assign(docs.size(), 0);
+  ids.clear();
+  if (len == 0) return TT_OK;
+  if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
+  Workspace* s = nullptr;
+  int rc = get_ws(h, st, (uint64_t)len, &s);
+  if (rc) return rc;
+  rc = ws_reserve_docs(s, n_docs, st);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->d_in, concat, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess ||
+      hipMemcpyAsync(s->d_docs, docs.data(), 8 * docs.size(), hipMemcpyHostToDevice, st) != hipSuccess)
+    return TT_ERR_HIP;
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, s->d_docs, (int32_t)n_docs, s->d_out, s->d_len, s->d_out_docs, st, 1);
+  if (rc) return rc;
+  if (hipMemcpyAsync(s->h_len, s->d_len, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return TT_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  const int64_t T = *s->h_len;
+  if (T < 0) return (int)T;
+  if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
+  ids.resize((size_t)std::max<int64_t>(T, 1));
+  if (hipMemcpyAsync(ids.data(), s->d_out, (size_t)T * 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(out_docs.data(), s->d_out_docs, 8 * docs.size(), hipMemcpyDeviceToHost, st) != hipSuccess)
+    return TT_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
+  ids.resize((size_t)T);
+  return TT_OK;
+}
+
+// Documents of one text [a, b) of `t` around its added-token literals: text
+// before the first literal, the literal, text up to the next literal, and so
+// on (text documents may be empty); appends the boundaries after a to `docs`
+// and the literals to `lits`.
+void added_documents(const AddedSet& added, const uint8_t* t, int64_t a, int64_t b, std::vector<int64_t>& docs,
+                     std::vector<AddedSet::Match>& lits) {
+  std::vector<AddedSet::Match> m;
+  added.extract(t + a, b - a, m);
+  for (const auto& x : m) {
+    docs.push_back(a + x.s);
+    docs.push_back(a + x.e);
+    lits.push_back(x);
+  }
+  docs.push_back(b);
+}
+
 }  // namespace
 
 namespace tt {
 int handle_pattern(const tt_tokenizer* h) { return h->pattern; }
+bool handle_has_added(const tt_tokenizer* h) { return !h->added.empty(); }
 uint32_t handle_max_token_bytes(const tt_tokenizer* h) { return h->max_tok_bytes; }
 
 // Span export of a small host request with one synchronisation: the length,
@@ -277,6 +537,7 @@ uint32_t handle_max_token_bytes(const tt_tokenizer* h) { return h->max_tok_bytes
 int encode_spans_pinned(tt_tokenizer* h, const uint8_t* h_in, int64_t len, int32_t* h_ids, int32_t* h_spans,
                         int64_t* h_len, void* stream) {
   if (!h || !h_in || !h_ids || !h_spans || !h_len) return TT_ERR_NULL_ARG;
+  if (!h->added.empty()) return TT_ERR_BAD_ARG;
   if (len <= 0) return TT_ERR_BAD_ARG;
   if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -321,9 +582,33 @@ const char* tt_status_string(int status) {
 
 int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_bytes,
               const int64_t* vocab_offsets, int32_t vocab_size, int32_t pattern_id, tt_tokenizer** out) {
+  return tt_create_ex(merges, n_merges, vocab_bytes, vocab_offsets, vocab_size, pattern_id, nullptr, out);
+}
+
+int tt_create_ex(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_bytes,
+                 const int64_t* vocab_offsets, int32_t vocab_size, int32_t pattern_id, const tt_options* opt,
+                 tt_tokenizer** out) {
   if (!out || !vocab_offsets || (n_merges > 0 && !merges)) return TT_ERR_NULL_ARG;
   *out = nullptr;
   if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K) return TT_ERR_BAD_PATTERN;
+  const bool ignore = opt && opt->ignore_merges != 0;
+  // added tokens: non-empty, strict UTF-8, bounded, distinct, non-negative IDs
+  AddedSet added;
+  if (opt && opt->n_added != 0) {
+    if (opt->n_added < 0) return TT_ERR_BAD_ARG;
+    if (!opt->added_bytes || !opt->added_offsets || !opt->added_ids) return TT_ERR_NULL_ARG;
+    if (opt->added_offsets[0] != 0) return TT_ERR_BAD_ARG;
+    std::unordered_set<std::string> lits;
+    for (int32_t i = 0; i < opt->n_added; ++i) {
+      const int64_t a = opt->added_offsets[i], b = opt->added_offsets[i + 1];
+      if (b <= a || b - a > TT_MAX_ADDED_BYTES || opt->added_ids[i] < 0) return TT_ERR_BAD_ARG;
+      std::string lit(reinterpret_cast<const char*>(opt->added_bytes + a), (size_t)(b - a));
+      if (!valid_utf8(reinterpret_cast<const uint8_t*>(lit.data()), (int64_t)lit.size())) return TT_ERR_BAD_ARG;
+      if (!lits.insert(lit).second) return TT_ERR_BAD_ARG;
+      added.add(lit, opt->added_ids[i]);
+    }
+    added.finish();
+  }
   if (n_merges < 0 || vocab_size < 256 || (uint32_t)n_merges > MAX_MERGES) return TT_ERR_BAD_ARG;
   if (vocab_offsets[0] != 0) return TT_ERR_BAD_VOCAB;
   for (int32_t i = 0; i < vocab_size; ++i)
@@ -360,16 +645,30 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       return TT_ERR_BAD_VOCAB;
     internal[m.result] = 256 + r;
   }
-  const uint32_t n_ids = 256u + (uint32_t)n_merges;
+  // under ignore_merges every other vocabulary ID becomes reachable (a piece
+  // can be that entry): internal IDs 256 + M + j follow the merge results
+  std::vector<int32_t> extras;
+  if (ignore)
+    for (int32_t i = 0; i < vocab_size; ++i)
+      if (internal[i] < 0) {
+        internal[i] = (int32_t)(256 + n_merges + (int32_t)extras.size());
+        extras.push_back(i);
+      }
+  const uint32_t n_ids = 256u + (uint32_t)n_merges + (uint32_t)extras.size();
   std::vector<int32_t> ext(n_ids);
   for (int b = 0; b < 256; ++b) ext[b] = byte_id[b];
   for (int32_t r = 0; r < n_merges; ++r) ext[256 + r] = merges[r].result;
+  for (size_t j = 0; j < extras.size(); ++j) ext[256 + (size_t)n_merges + j] = extras[j];
   // byte length of every internal ID (span export): a merge result spells its
   // operands back to back, and both operands come before it
   std::vector<uint32_t> toklen(n_ids, 1u);
   for (int32_t r = 0; r < n_merges; ++r) {
     const uint64_t l = (uint64_t)toklen[(size_t)internal[merges[r].left]] + toklen[(size_t)internal[merges[r].right]];
     toklen[256 + (size_t)r] = l > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)l;
+  }
+  for (size_t j = 0; j < extras.size(); ++j) {
+    const int64_t l = vlen(extras[j]);
+    toklen[256 + (size_t)n_merges + j] = l > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)l;
   }
 
   // byte-pair ranks, and the two-choice cuckoo table of all pairs (two slots
@@ -431,10 +730,7 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       auto it = rank.find(slot_key(a, b));
       return it == rank.end() ? RANK_INF : it->second;
     };
-    struct Entry {
-      uint32_t w[6], len, id;
-    };
-    std::vector<Entry> entries, entries2;
+    std::vector<DictEntry> entries, entries2;
     std::unordered_set<std::string> seen;
     uint32_t ids[DICT2_MAX], rk[DICT2_MAX];
     for (int32_t r = 0; r < n_merges; ++r) {
@@ -466,31 +762,69 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
         if (k > 0) rk[k - 1] = lookup(ids[k - 1], ids[k]);
       }
       if (n != 1) continue;
-      Entry e{{0u, 0u, 0u, 0u, 0u, 0u}, (uint32_t)L, ids[0]};
-      for (int i = 0; i < L; ++i) e.w[i >> 2] |= (uint32_t)vptr(res)[i] << (8 * (i & 3));
-      (L <= DICT_MAX ? entries : entries2).push_back(e);
+      (L <= DICT_MAX ? entries : entries2).push_back(make_entry(vptr(res), (uint32_t)L, ids[0]));
     }
-    // two entries per bucket, load 0.8; grows by 1/8 while an entry cannot be placed
-    dnb = (uint32_t)(entries.size() * 5 / 8) + 16;
+    if (build_dict(entries, dict, dnb) || build_dict2(entries2, dict2, dnb2)) return TT_ERR_OOM;
+  }
+
+  // ignore_merges: every vocabulary string of at least two bytes, with the
+  // internal ID of its lowest vocabulary ID, in tables by length
+  std::vector<u32x4> vdict, vdict2, vlong;
+  std::vector<uint8_t> vblob;
+  uint32_t vdnb = 0, vdnb2 = 0, vlnb = 0, vmax = 0;
+  if (ignore) {
+    std::vector<DictEntry> e1, e2;
+    std::vector<std::pair<int32_t, uint32_t>> longs;  // (vocabulary ID, internal ID)
+    std::unordered_set<std::string> seen;
+    for (int32_t i = 0; i < vocab_size; ++i) {
+      const int64_t L = vlen(i);
+      if (L < 2) continue;
+      if (!seen.insert(std::string(reinterpret_cast<const char*>(vptr(i)), (size_t)L)).second) continue;
+      vmax = std::max<uint32_t>(vmax, (uint32_t)std::min<int64_t>(L, 0x7FFFFFFF));
+      if (L <= DICT_MAX) e1.push_back(make_entry(vptr(i), (uint32_t)L, (uint32_t)internal[i]));
+      else if (L <= DICT2_MAX) e2.push_back(make_entry(vptr(i), (uint32_t)L, (uint32_t)internal[i]));
+      else longs.emplace_back(i, (uint32_t)internal[i]);
+    }
+    vmax = std::max<uint32_t>(vmax, 2u);
+    if (build_dict(e1, vdict, vdnb) || build_dict2(e2, vdict2, vdnb2)) return TT_ERR_OOM;
+    // longer strings: cuckoo buckets of two {hash, length, ID, offset} slots
+    vlnb = (uint32_t)(longs.size() * 5 / 8) + 16;
     for (;;) {
-      dict.assign(2 * (size_t)dnb, u32x4{0u, 0u, 0u, 0u});
-      uint64_t rng = 0xD1B54A32D192ED03ull;
+      vlong.assign(2 * (size_t)vlnb, u32x4{0u, 0u, 0u, 0u});
+      vblob.clear();
+      uint64_t rng = 0x2545F4914F6CDD1Dull;
       bool ok = true;
-      for (size_t i = 0; i < entries.size() && ok; ++i) {
-        u32x4 item{entries[i].w[0], entries[i].w[1], entries[i].w[2], (entries[i].id << 4) | entries[i].len};
+      for (size_t k = 0; k < longs.size() && ok; ++k) {
+        const int32_t vid = longs[k].first;
+        const uint32_t L = (uint32_t)vlen(vid);
+        uint32_t h1 = LONG_SEED1, h2 = LONG_SEED2;
+        for (uint32_t j = 0; j < L; ++j) {
+          h1 = long_hash_step(h1, vptr(vid)[j]);
+          h2 = long_hash_step(h2, vptr(vid)[j]);
+        }
+        h1 = long_hash_final(h1, L);
+        h2 = long_hash_final(h2, L);
+        const uint32_t off = (uint32_t)vblob.size();
+        vblob.insert(vblob.end(), vptr(vid), vptr(vid) + L);
+        // (the bucket choice of a displaced entry is recomputed from its bytes)
+        u32x4 item{h1, L, longs[k].second, off};
         ok = false;
-        for (int kick = 0; kick < 2000; ++kick) {
-          const uint32_t len = item.w & 15u;
-          const size_t b1 = 2 * (size_t)bucket_of(unit_hash(item.x, item.y, item.z, len), dnb);
-          const size_t b2 = 2 * (size_t)bucket_of(unit_hash2(item.x, item.y, item.z, len), dnb);
+        for (int kick = 0; kick < 1000; ++kick) {
+          uint32_t g1 = LONG_SEED1, g2 = LONG_SEED2;
+          for (uint32_t j = 0; j < item.y; ++j) {
+            g1 = long_hash_step(g1, vblob[item.w + j]);
+            g2 = long_hash_step(g2, vblob[item.w + j]);
+          }
+          const size_t b1 = 2 * (size_t)bucket_of(long_hash_final(g1, item.y), vlnb);
+          const size_t b2 = 2 * (size_t)bucket_of(long_hash_final(g2, item.y), vlnb);
           size_t free_at = SIZE_MAX;
           for (size_t c : {b1, b1 + 1, b2, b2 + 1})
-            if (dict[c].w == 0u) {
+            if (vlong[c].y == 0u) {
               free_at = c;
               break;
             }
           if (free_at != SIZE_MAX) {
-            dict[free_at] = item;
+            vlong[free_at] = item;
             ok = true;
             break;
           }
@@ -498,60 +832,14 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
           rng ^= rng >> 7;
           rng ^= rng << 17;
           const size_t v = ((rng & 2) ? b1 : b2) + (rng & 1);
-          std::swap(item, dict[v]);
+          std::swap(item, vlong[v]);
         }
       }
       if (ok) break;
-      dnb += dnb / 8;
-      if (dnb > (1u << 27)) return TT_ERR_OOM;
+      vlnb += vlnb / 8;
+      if (vlnb > (1u << 27)) return TT_ERR_OOM;
     }
-    // long units: one entry of two words per bucket, load below 1/2
-    dnb2 = (uint32_t)(entries2.size() * 2) + 16;
-    for (;;) {
-      dict2.assign(2 * (size_t)dnb2, u32x4{0u, 0u, 0u, 0u});
-      uint64_t rng = 0x9E3779B97F4A7C15ull;
-      bool ok = true;
-      for (size_t i = 0; i < entries2.size() && ok; ++i) {
-        const Entry* item = &entries2[i];
-        Entry held;
-        ok = false;
-        for (int kick = 0; kick < 1000; ++kick) {
-          const uint32_t* q = item->w;
-          const size_t b1 = 2 * (size_t)bucket_of(unit_hash6(q[0], q[1], q[2], q[3], q[4], q[5], item->len), dnb2);
-          const size_t b2 = 2 * (size_t)bucket_of(unit_hash6b(q[0], q[1], q[2], q[3], q[4], q[5], item->len), dnb2);
-          const u32x4 x0{q[0], q[1], q[2], q[3]}, x1{q[4], q[5], (item->id << 5) | item->len, 0u};
-          size_t at = SIZE_MAX;
-          if (dict2[b1 + 1].z == 0u) at = b1;
-          else if (dict2[b2 + 1].z == 0u) at = b2;
-          if (at != SIZE_MAX) {
-            dict2[at] = x0;
-            dict2[at + 1] = x1;
-            ok = true;
-            break;
-          }
-          rng ^= rng << 13;
-          rng ^= rng >> 7;
-          rng ^= rng << 17;
-          const size_t v = (rng & 1) ? b1 : b2;
-          Entry out;
-          out.w[0] = dict2[v].x;
-          out.w[1] = dict2[v].y;
-          out.w[2] = dict2[v].z;
-          out.w[3] = dict2[v].w;
-          out.w[4] = dict2[v + 1].x;
-          out.w[5] = dict2[v + 1].y;
-          out.len = dict2[v + 1].z & 31u;
-          out.id = dict2[v + 1].z >> 5;
-          dict2[v] = x0;
-          dict2[v + 1] = x1;
-          held = out;
-          item = &held;
-        }
-      }
-      if (ok) break;
-      dnb2 += dnb2 / 8;
-      if (dnb2 > (1u << 27)) return TT_ERR_OOM;
-    }
+    if (vblob.empty()) vblob.push_back(0);
   }
 
   // junction byte pairs: the first merge that ever joins across a byte
@@ -568,6 +856,12 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
 
   tt_tokenizer* h = new tt_tokenizer();
   h->pattern = pattern_id;
+  h->ignore = ignore;
+  h->vmax = vmax;
+  h->vdnb = vdnb;
+  h->vdnb2 = vdnb2;
+  h->vlnb = vlnb;
+  h->added = std::move(added);
   h->n_merges = n_merges;
   h->vocab_size = vocab_size;
   h->nb = nb;
@@ -588,6 +882,21 @@ int tt_create(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_byt
       hipMalloc(reinterpret_cast<void**>(&h->d_join), sizeof(uint32_t) * 2048) != hipSuccess) {
     tt_destroy(h);
     return TT_ERR_OOM;
+  }
+  if (ignore && (hipMalloc(reinterpret_cast<void**>(&h->d_vdict), sizeof(u32x4) * vdict.size()) != hipSuccess ||
+                 hipMalloc(reinterpret_cast<void**>(&h->d_vdict2), sizeof(u32x4) * vdict2.size()) != hipSuccess ||
+                 hipMalloc(reinterpret_cast<void**>(&h->d_vlong), sizeof(u32x4) * vlong.size()) != hipSuccess ||
+                 hipMalloc(reinterpret_cast<void**>(&h->d_vblob), vblob.size()) != hipSuccess)) {
+    tt_destroy(h);
+    return TT_ERR_OOM;
+  }
+  if (ignore &&
+      (hipMemcpy(h->d_vdict, vdict.data(), sizeof(u32x4) * vdict.size(), hipMemcpyHostToDevice) != hipSuccess ||
+       hipMemcpy(h->d_vdict2, vdict2.data(), sizeof(u32x4) * vdict2.size(), hipMemcpyHostToDevice) != hipSuccess ||
+       hipMemcpy(h->d_vlong, vlong.data(), sizeof(u32x4) * vlong.size(), hipMemcpyHostToDevice) != hipSuccess ||
+       hipMemcpy(h->d_vblob, vblob.data(), vblob.size(), hipMemcpyHostToDevice) != hipSuccess)) {
+    tt_destroy(h);
+    return TT_ERR_HIP;
   }
   if (hipMemcpy(h->d_slots, slots.data(), 16 * (size_t)nb, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(h->d_pair0, pair0.data(), sizeof(uint32_t) * 65536, hipMemcpyHostToDevice) != hipSuccess ||
@@ -615,6 +924,10 @@ void tt_destroy(tt_tokenizer* h) {
   if (h->d_dict2) (void)hipFree(h->d_dict2);
   if (h->d_toklen) (void)hipFree(h->d_toklen);
   if (h->d_join) (void)hipFree(h->d_join);
+  if (h->d_vdict) (void)hipFree(h->d_vdict);
+  if (h->d_vdict2) (void)hipFree(h->d_vdict2);
+  if (h->d_vlong) (void)hipFree(h->d_vlong);
+  if (h->d_vblob) (void)hipFree(h->d_vblob);
   delete h;
 }
 
@@ -629,6 +942,7 @@ int tt_info(const tt_tokenizer* h, int32_t* n_merges, int32_t* vocab_size, int32
 int tt_encode_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_t* d_out_ids,
                      int64_t* d_out_len, void* stream) {
   if (!h || !d_out_len || (len > 0 && (!d_utf8 || !d_out_ids))) return TT_ERR_NULL_ARG;
+  if (!h->added.empty()) return TT_ERR_BAD_ARG;  // literals are extracted by the host entry points
   if (len < 0) return TT_ERR_BAD_ARG;
   if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -651,6 +965,32 @@ int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_id
   *out_len = 0;
   if (len == 0) return TT_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (!h->added.empty()) {
+    // literals first (host, leftmost-longest); the text segments and the
+    // literals are the documents of one batch, and a literal's document is
+    // replaced by its ID
+    std::vector<int64_t> docs{0};
+    std::vector<AddedSet::Match> lits;
+    added_documents(h->added, utf8, 0, len, docs, lits);
+    if (!lits.empty()) {
+      std::vector<int32_t> ids;
+      std::vector<int64_t> od;
+      int rc = batch_host(h, st, utf8, len, docs, ids, od);
+      if (rc) return rc;
+      int64_t T = 0;
+      for (size_t j = 0; j + 1 < docs.size(); ++j) {
+        if (j & 1) {
+          out_ids[T++] = lits[j / 2].id;
+        } else {
+          const int64_t c = od[j + 1] - od[j];
+          if (c > 0) std::memcpy(out_ids + T, ids.data() + od[j], 4 * (size_t)c);
+          T += c;
+        }
+      }
+      *out_len = T;
+      return TT_OK;
+    }
+  }
   if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
   Workspace* s = nullptr;
   int rc = get_ws(h, st, (uint64_t)len, &s);
@@ -675,6 +1015,7 @@ int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_id
 int tt_encode_spans_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_t* d_out_ids,
                            int32_t* d_out_spans, int64_t* d_out_len, void* stream) {
   if (!h || !d_out_len || (len > 0 && (!d_utf8 || !d_out_ids || !d_out_spans))) return TT_ERR_NULL_ARG;
+  if (!h->added.empty()) return TT_ERR_BAD_ARG;  // literals are extracted by the host entry points
   if (len < 0) return TT_ERR_BAD_ARG;
   if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -692,6 +1033,7 @@ int tt_encode_spans_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, 
 int tt_encode_spans(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_ids, int32_t* out_spans,
                     int64_t* out_len, void* stream) {
   if (!h || !out_len || (len > 0 && (!utf8 || !out_ids || !out_spans))) return TT_ERR_NULL_ARG;
+  if (!h->added.empty()) return TT_ERR_BAD_ARG;  // literals are extracted by the host entry points
   if (len < 0) return TT_ERR_BAD_ARG;
   if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
   *out_len = 0;
@@ -736,6 +1078,38 @@ int tt_encode_batch(tt_tokenizer* h, const uint8_t* concat, const int64_t* doc_o
     return TT_OK;
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (!h->added.empty()) {
+    // every caller document becomes its text segments and literals
+    std::vector<int64_t> docs{0};
+    std::vector<AddedSet::Match> lits;
+    std::vector<int64_t> first_doc((size_t)n_docs + 1), first_lit((size_t)n_docs + 1);
+    for (int32_t d = 0; d < n_docs; ++d) {
+      first_doc[(size_t)d] = (int64_t)docs.size() - 1;
+      first_lit[(size_t)d] = (int64_t)lits.size();
+      added_documents(h->added, concat, doc_offsets[d], doc_offsets[d + 1], docs, lits);
+    }
+    first_doc[(size_t)n_docs] = (int64_t)docs.size() - 1;
+    first_lit[(size_t)n_docs] = (int64_t)lits.size();
+    std::vector<int32_t> ids;
+    std::vector<int64_t> od;
+    int rc = batch_host(h, st, concat, len, docs, ids, od);
+    if (rc) return rc;
+    int64_t T = 0;
+    for (int32_t d = 0; d < n_docs; ++d) {
+      out_doc_offsets[d] = T;
+      for (int64_t j = first_doc[(size_t)d]; j < first_doc[(size_t)d + 1]; ++j) {
+        if ((j - first_doc[(size_t)d]) & 1) {
+          out_ids[T++] = lits[(size_t)(first_lit[(size_t)d] + (j - first_doc[(size_t)d]) / 2)].id;
+        } else {
+          const int64_t c = od[(size_t)j + 1] - od[(size_t)j];
+          if (c > 0) std::memcpy(out_ids + T, ids.data() + od[(size_t)j], 4 * (size_t)c);
+          T += c;
+        }
+      }
+    }
+    out_doc_offsets[n_docs] = T;
+    return TT_OK;
+  }
   if (hipSetDevice(h->device) != hipSuccess) return TT_ERR_HIP;
   Workspace* s = nullptr;
   int rc = get_ws(h, st, (uint64_t)len, &s);
@@ -763,6 +1137,7 @@ int tt_encode_batch(tt_tokenizer* h, const uint8_t* concat, const int64_t* doc_o
 int tt_pretokenize(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int64_t* out_piece_starts, int64_t* out_n,
                    void* stream) {
   if (!h || !out_n || (len > 0 && (!utf8 || !out_piece_starts))) return TT_ERR_NULL_ARG;
+  if (!h->added.empty()) return TT_ERR_BAD_ARG;  // literals are extracted by the host entry points
   if (len < 0) return TT_ERR_BAD_ARG;
   if (len > TT_MAX_BYTES) return TT_ERR_TOO_LARGE;
   *out_n = 0;

@@ -169,6 +169,20 @@ __device__ __forceinline__ uint32_t dict2_find(const u32x4* __restrict__ dict, u
   return r;
 }
 
+// Vocabulary strings longer than DICT2_MAX (piece probes under
+// ignore_merges): one 16-byte entry {hash, length, ID, offset of the bytes in
+// a blob} per bucket slot, two slots per bucket, two choices from two hashes
+// of the bytes; a hit on (hash, length) is confirmed by comparing the bytes.
+__host__ __device__ inline uint32_t long_hash_step(uint32_t h, uint32_t b) { return (h ^ b) * 0x01000193u; }
+constexpr uint32_t LONG_SEED1 = 0x811C9DC5u, LONG_SEED2 = 0x9747B28Cu;
+__host__ __device__ inline uint32_t long_hash_final(uint32_t h, uint32_t len) {
+  h ^= len * 0x9E3779B1u;
+  h ^= h >> 16;
+  h *= 0x85EBCA6Bu;
+  h ^= h >> 13;
+  return h;
+}
+
 // Everything a kernel needs to know about a tokenizer handle.
 struct DevTables {
   const u64x2* slots;       // cuckoo buckets of two slots: key (left | right << 21), rank in bits 42..63
@@ -183,6 +197,15 @@ struct DevTables {
   const u32x4* dict2;       // long-unit dictionary (one two-word entry per bucket)
   uint32_t dnb2;            // its bucket count
   const uint32_t* tok_len;  // [n_ids] byte length of every internal ID (span export)
+  // ignore_merges: whole-piece probes of every vocabulary string (lowest ID)
+  uint32_t vmax;            // longest vocabulary string in bytes (0: no probes)
+  const u32x4* vdict;       // strings of 2..DICT_MAX bytes, whole-unit dictionary layout
+  uint32_t vdnb;
+  const u32x4* vdict2;      // strings of DICT_MAX+1..DICT2_MAX bytes, long-unit dictionary layout
+  uint32_t vdnb2;
+  const u32x4* vlong;       // longer strings: {hash, length, ID, blob offset}, two per bucket
+  uint32_t vlnb;
+  const uint8_t* vblob;     // bytes of the longer strings
 };
 
 // ---------------------------------------------------------------------------
@@ -242,13 +265,15 @@ inline uint32_t n_tiles_for(uint32_t n) { return (n + PT_OWN - 1) / PT_OWN; }
 // Launchers (defined in the .hip files) -------------------------------------
 // mode 0: split export (outputs are piece byte offsets); mode 1: encode;
 // mode 2: encode with span export (single requests)
-hipError_t launch_tile(const Work& w, const DevTables& t, int pattern, int mode, hipStream_t s);
+// ignore: probe whole pieces in the vocabulary first (modes 1 and 2)
+hipError_t launch_tile(const Work& w, const DevTables& t, int pattern, int mode, bool ignore, hipStream_t s);
 hipError_t launch_doc_offsets(const Work& w, hipStream_t s);
 // span export, after the tile kernel: byte ends and character spans
 hipError_t launch_spans(const Work& w, hipStream_t s);
 
 // Facts of a handle for the host-side session code.
 int handle_pattern(const tt_tokenizer* h);
+bool handle_has_added(const tt_tokenizer* h);  // added-token literals (sessions do not take them)
 uint32_t handle_max_token_bytes(const tt_tokenizer* h);  // longest token, in bytes
 // span export of a small host request with one synchronisation (pinned buffers)
 int encode_spans_pinned(tt_tokenizer* h, const uint8_t* h_in, int64_t len, int32_t* h_ids, int32_t* h_spans,

@@ -306,7 +306,7 @@ int tt_splice_plan(int32_t pattern_id, const uint8_t* text, int64_t len, int64_t
 int tt_session_create(tt_tokenizer* h, int32_t window_chars, tt_session** out) {
   if (!h || !out) return TT_ERR_NULL_ARG;
   *out = nullptr;
-  if (window_chars < 0) return TT_ERR_BAD_ARG;
+  if (window_chars < 0 || tt::handle_has_added(h)) return TT_ERR_BAD_ARG;
   tt_session* s = new tt_session();
   s->h = h;
   s->pattern = tt::handle_pattern(h);

@@ -229,6 +229,42 @@ __device__ __forceinline__ void unit_words(const uint8_t* buf, uint32_t a, uint3
   }
 }
 
+// ignore_merges: the internal ID of the vocabulary string equal to the L
+// bytes byte(0 .. L) (2 <= L), or DICT_NONE.  Strings of up to DICT2_MAX bytes
+// are probed with their bytes as the key (from the window when aw >= 0, i.e.
+// the bytes start at window index aw); longer ones by two hashes of their
+// bytes, confirmed by comparing the bytes with the stored string.
+template <class ByteF>
+__device__ uint32_t piece_find(const DevTables& tb, const uint8_t* buf, int64_t aw, uint32_t L, ByteF byte) {
+  if (L <= (uint32_t)DICT2_MAX) {
+    uint32_t kw[6] = {0u, 0u, 0u, 0u, 0u, 0u};
+    if (aw >= 0 && aw + DICT2_MAX + 4 <= PT_WIN + 16) {
+      unit_words(buf, (uint32_t)aw, L, kw);
+    } else {
+      for (uint32_t j = 0; j < L; ++j) kw[j >> 2] |= byte(j) << (8 * (j & 3));
+    }
+    if (L <= (uint32_t)DICT_MAX) return dict_find(tb.vdict, tb.vdnb, kw[0], kw[1], kw[2], L);
+    return dict2_find(tb.vdict2, tb.vdnb2, kw, L);
+  }
+  uint32_t h1 = LONG_SEED1, h2 = LONG_SEED2;
+  for (uint32_t j = 0; j < L; ++j) {
+    const uint32_t b = byte(j);
+    h1 = long_hash_step(h1, b);
+    h2 = long_hash_step(h2, b);
+  }
+  h1 = long_hash_final(h1, L);
+  h2 = long_hash_final(h2, L);
+  const uint32_t b1 = 2u * bucket_of(h1, tb.vlnb), b2 = 2u * bucket_of(h2, tb.vlnb);
+  const u32x4 e[4] = {tb.vlong[b1], tb.vlong[b1 + 1], tb.vlong[b2], tb.vlong[b2 + 1]};
+  for (int i = 0; i < 4; ++i) {
+    if (e[i].x != h1 || e[i].y != L) continue;
+    bool same = true;
+    for (uint32_t j = 0; j < L && same; ++j) same = tb.vblob[e[i].w + j] == byte(j);
+    if (same) return e[i].z;
+  }
+  return DICT_NONE;
+}
+
 constexpr int MED_CAP = PT_WIN / (SMALL_MAX + 1) + 2;  // units of 17..64 bytes in a tile
 constexpr int BIG_CAP = PT_WIN / (WAVE_MAX + 1) + 2;   // longer units in a tile
 constexpr uint16_t U_INCOMING = 0xFFFFu;               // list entry for the incoming unit
@@ -279,6 +315,8 @@ struct PtShared {
   uint32_t carry_n;           // cl100k: number-run chars before the tile, mod 3
   uint32_t carry_nlpre;       // cl100k: class before a CR/LF stretch entering the tile
   uint32_t cwave[PT_THREADS / 64];  // span export: per-wave sums
+  uint32_t nocut[PT_WIN / 32];  // ignore_merges: window positions no junction cut may split
+  uint32_t whole[PT_WIN / 32];  // ignore_merges: starts of pieces that are vocabulary entries
   uint32_t cbase;             // span export: non-continuation bytes before the tile
   uint32_t ctile;             // span export: non-continuation bytes the tile owns
   int64_t doc_lo_idx;         // batch: first document start index touching the window
@@ -403,7 +441,7 @@ __device__ uint32_t place_tile(const Work& w, Sh& sh, uint32_t t, uint32_t count
 // MODE 1: encoding; the outputs are the (internal) IDs of the units' tokens.
 // MODE 2: encoding with span export: also the byte start of every token and the
 //         non-continuation byte count at every 4-byte word of the request.
-template <int PAT, bool BATCH, int MODE>
+template <int PAT, bool BATCH, int MODE, bool IGN>
 __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void tile_kernel(Work w, DevTables tb) {
   constexpr bool SEG = MODE >= 1;
   constexpr bool SPANS = MODE == 2;
@@ -414,6 +452,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   const int64_t n = w.n;
 
   if (tid <= SMALL_MAX) sh.hist[tid] = 0;
+  if (IGN && tid < PT_WIN / 32) {
+    sh.nocut[tid] = 0;
+    sh.whole[tid] = 0;
+  }
   // the ticket's round trip (tickets are handed out one at a time) overlaps
   // the staging of the tables, which do not depend on the tile
   uint32_t ticket = 0;
@@ -929,6 +971,58 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (d1 == 0u) start = true;
     if (start) flags |= 1u << j;
   }
+  const bool last = t == n_tiles - 1;
+  if (IGN) {
+    // ignore_merges: a piece that is a vocabulary entry is that entry's ID
+    // (Sec. 4.2: the vocabulary is probed first and the merge loop skipped).
+    // Pieces are numbered by a block scan (their starts go to sh.ustart until
+    // the unit scan), every piece that ends inside the tile is probed, and no
+    // junction cut may split a piece found in the vocabulary.  The pieces that
+    // cross the tile's edges are not cut at all: the next tile encodes the
+    // last one whole, as its incoming unit, and probes it there.
+    const uint32_t pc = __popc(flags);
+    const uint32_t pinc = wave_incl_sum(pc);
+    __syncthreads();
+    if (lane == 63) sh.wave_tot[wave] = pinc;
+    __syncthreads();
+    uint32_t pw = 0, pm = 0;
+    for (int v = 0; v < PT_THREADS / 64; ++v) {
+      if (v < wave) pw += sh.wave_tot[v];
+      pm += sh.wave_tot[v];
+    }
+    {
+      uint32_t k = pw + pinc - pc;
+#pragma unroll 1
+      for (int j = 0; j < PT_BPT; ++j)
+        if ((flags >> j) & 1u) sh.ustart[k++] = (uint16_t)(qb + j);
+    }
+    if (tid == 0) sh.ustart[pm] = (uint16_t)(last ? n - w0 : 0xFFFFu);  // end of the last piece, if known
+    __syncthreads();
+#pragma unroll 1
+    for (uint32_t k = (uint32_t)tid; k < pm; k += PT_THREADS) {
+      const uint32_t a = sh.ustart[k], e = sh.ustart[k + 1];
+      if (e == 0xFFFFu) continue;
+      const uint32_t L = e - a;
+      if (L < 2u || L > tb.vmax) continue;
+      const uint32_t id = piece_find(tb, sh.buf, (int64_t)a, L, [&](uint32_t j) -> uint32_t { return sh.buf[PT_PAD + a + j]; });
+      if (id == DICT_NONE) continue;
+      w.stage[w0 + a] = id;
+      atomicOr(&sh.whole[a >> 5], 1u << (a & 31u));
+      for (uint32_t q = a + 1; q < e; ++q) atomicOr(&sh.nocut[q >> 5], 1u << (q & 31u));
+    }
+    // the incoming piece's tail and the tile's last piece
+    const uint32_t first = pm > 0 ? sh.ustart[0] : (uint32_t)(PT_HALO + PT_OWN);
+    const uint32_t lastp = pm > 0 ? sh.ustart[pm - 1] : (uint32_t)PT_HALO;
+    uint32_t mask = 0;
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) {
+      const uint32_t q = (uint32_t)(qb + j);
+      const bool own = q >= (uint32_t)PT_HALO && q < (uint32_t)(PT_HALO + PT_OWN);
+      if (own && ((t > 0 && q < first) || (!last && q > lastp))) mask |= 1u << j;
+    }
+    if (mask) atomicOr(&sh.nocut[qb >> 5], mask << (qb & 31));
+    __syncthreads();
+  }
   if (SEG) {
     // BPE segments: add the byte positions inside pieces that no merge spans
     // (q is not a piece start, so q - 1 lies in the same piece)
@@ -941,7 +1035,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       const uint32_t k2 = ((key & 255u) << 8) | (key >> 8);
       const bool joined = (sh.ph.a.join[k2 >> 5] >> (k2 & 31u)) & 1u;
       const bool eligible = q >= PT_HALO && q < PT_HALO + PT_OWN && inside(q) && inside(q - 1) &&
-                            !(flags & (1u << j)) && !(cr(j) & CODE_DOCSTART);
+                            !(flags & (1u << j)) && !(cr(j) & CODE_DOCSTART) &&
+                            !(IGN && ((sh.nocut[q >> 5] >> (q & 31)) & 1u));
       if (eligible && !joined) flags |= 1u << j;
     }
   }
@@ -958,7 +1053,6 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     m += sh.wave_tot[v];
   }
   const uint32_t texcl = wpre + inc - cnt;  // unit starts before this thread's positions
-  const bool last = t == n_tiles - 1;
 
   if (MODE == 0) {
     // split export: the tile's piece offsets go straight to their place
@@ -1037,6 +1131,26 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     const bool inc_u = u == m_proc;
     const uint32_t a = inc_u ? 0u : sh.ustart[u];
     const uint32_t L = inc_u ? L_inc : sh.ustart[u + 1] - a;
+    if (IGN) {
+      // a piece found in the vocabulary (its ID was staged at its first byte);
+      // the incoming unit is a whole piece and is probed here
+      uint32_t id = DICT_NONE;
+      if (!inc_u && ((sh.whole[a >> 5] >> (a & 31u)) & 1u)) {
+        id = w.stage[w0 + a];
+      } else if (inc_u && L >= 2u && L <= tb.vmax) {
+        id = piece_find(tb, sh.buf, (int64_t)s_prev - w0, L, [&](uint32_t j) -> uint32_t { return inc_byte(j); });
+      }
+      if (id != DICT_NONE) {
+        if (inc_u) {
+          inc_out(0, id);
+          sh.inc_cnt = 1;
+        } else {
+          sh.ph.b.tok[a] = id;
+          sh.ucnt[u] = 1;
+        }
+        continue;
+      }
+    }
     if (L <= 2u) {
       const uint32_t b0 = inc_u ? inc_byte(0) : sh.buf[PT_PAD + a];
       uint32_t c = 1, t0 = b0, t1 = 0;
@@ -1352,26 +1466,35 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   }
 }
 
-hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode, hipStream_t s) {
+hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode, bool ignore, hipStream_t s) {
   dim3 grid(w.n_tiles), block(PT_THREADS);
   const bool batch = w.doc_off != nullptr;
   if (mode == 2 && batch) return hipErrorInvalidValue;  // span export is for single requests
-  const int variant = mode == 2 ? 8 + (pattern == TT_PATTERN_GPT2 ? 0 : 1)
-                                : (pattern == TT_PATTERN_GPT2 ? 0 : 4) + (batch ? 2 : 0) + (mode ? 1 : 0);
+  if (ignore && mode == 0) return hipErrorInvalidValue;  // the split export has no model stage
+  const int variant = (mode == 2 ? 8 + (pattern == TT_PATTERN_GPT2 ? 0 : 1)
+                                 : (pattern == TT_PATTERN_GPT2 ? 0 : 4) + (batch ? 2 : 0) + (mode ? 1 : 0)) +
+                      (ignore ? 16 : 0);
   switch (variant) {
-#define TT_TILE_CASE(V, P, B, M) \
-  case V: hipLaunchKernelGGL((tile_kernel<P, B, M>), grid, block, 0, s, w, tb); break;
-    TT_TILE_CASE(0, TT_PATTERN_GPT2, false, 0)
-    TT_TILE_CASE(1, TT_PATTERN_GPT2, false, 1)
-    TT_TILE_CASE(2, TT_PATTERN_GPT2, true, 0)
-    TT_TILE_CASE(3, TT_PATTERN_GPT2, true, 1)
-    TT_TILE_CASE(4, TT_PATTERN_CL100K, false, 0)
-    TT_TILE_CASE(5, TT_PATTERN_CL100K, false, 1)
-    TT_TILE_CASE(6, TT_PATTERN_CL100K, true, 0)
-    TT_TILE_CASE(7, TT_PATTERN_CL100K, true, 1)
-    TT_TILE_CASE(8, TT_PATTERN_GPT2, false, 2)
-    TT_TILE_CASE(9, TT_PATTERN_CL100K, false, 2)
+#define TT_TILE_CASE(V, P, B, M, I) \
+  case V: hipLaunchKernelGGL((tile_kernel<P, B, M, I>), grid, block, 0, s, w, tb); break;
+    TT_TILE_CASE(0, TT_PATTERN_GPT2, false, 0, false)
+    TT_TILE_CASE(1, TT_PATTERN_GPT2, false, 1, false)
+    TT_TILE_CASE(2, TT_PATTERN_GPT2, true, 0, false)
+    TT_TILE_CASE(3, TT_PATTERN_GPT2, true, 1, false)
+    TT_TILE_CASE(4, TT_PATTERN_CL100K, false, 0, false)
+    TT_TILE_CASE(5, TT_PATTERN_CL100K, false, 1, false)
+    TT_TILE_CASE(6, TT_PATTERN_CL100K, true, 0, false)
+    TT_TILE_CASE(7, TT_PATTERN_CL100K, true, 1, false)
+    TT_TILE_CASE(8, TT_PATTERN_GPT2, false, 2, false)
+    TT_TILE_CASE(9, TT_PATTERN_CL100K, false, 2, false)
+    TT_TILE_CASE(17, TT_PATTERN_GPT2, false, 1, true)
+    TT_TILE_CASE(19, TT_PATTERN_GPT2, true, 1, true)
+    TT_TILE_CASE(21, TT_PATTERN_CL100K, false, 1, true)
+    TT_TILE_CASE(23, TT_PATTERN_CL100K, true, 1, true)
+    TT_TILE_CASE(24, TT_PATTERN_GPT2, false, 2, true)
+    TT_TILE_CASE(25, TT_PATTERN_CL100K, false, 2, true)
 #undef TT_TILE_CASE
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

@@ -43,7 +43,8 @@ def _u8(data):
 class Tokenizer:
     """An immutable tokenizer handle (``tt_create`` / ``tt_destroy``)."""
 
-    def __init__(self, merges, vocab_bytes, vocab_offsets, pattern="gpt2"):
+    def __init__(self, merges, vocab_bytes, vocab_offsets, pattern="gpt2", ignore_merges=False, added=None):
+        """``added``: optional list of (literal bytes or str, ID) added tokens (``tt_create_ex``)."""
         lib = _lib.load()
         self._lib = lib
         pat = PATTERNS[pattern] if isinstance(pattern, str) else int(pattern)
@@ -51,8 +52,19 @@ class Tokenizer:
         vb = np.ascontiguousarray(np.asarray(vocab_bytes, dtype=np.uint8))
         vo = np.ascontiguousarray(np.asarray(vocab_offsets, dtype=np.int64))
         h = ctypes.c_void_p()
-        st = lib.tt_create(_ptr(m), len(m), _ptr(vb) if vb.size else None, _ptr(vo), len(vo) - 1, pat,
-                           ctypes.byref(h))
+        if ignore_merges or added:
+            lits = [(x.encode("utf-8") if isinstance(x, str) else bytes(x), int(i)) for x, i in (added or [])]
+            ab = np.frombuffer(b"".join(x for x, _ in lits) or b"\0", dtype=np.uint8).copy()
+            ao = np.zeros(len(lits) + 1, dtype=np.int64)
+            np.cumsum([len(x) for x, _ in lits], out=ao[1:])
+            ai = np.asarray([i for _, i in lits] or [0], dtype=np.int32)
+            self._added = (ab, ao, ai)  # kept alive for the call
+            opt = _lib.Options(int(bool(ignore_merges)), len(lits), _ptr(ab).value, _ptr(ao).value, _ptr(ai).value)
+            st = lib.tt_create_ex(_ptr(m), len(m), _ptr(vb) if vb.size else None, _ptr(vo), len(vo) - 1, pat,
+                                  ctypes.byref(opt), ctypes.byref(h))
+        else:
+            st = lib.tt_create(_ptr(m), len(m), _ptr(vb) if vb.size else None, _ptr(vo), len(vo) - 1, pat,
+                               ctypes.byref(h))
         _lib.check(st, "tt_create")
         self._h = h
         self.pattern = pat

@@ -21,7 +21,7 @@ def _declared():
 
 
 def test_header_declares_the_boundary():
-    assert _declared() == sorted(["tt_create", "tt_destroy", "tt_encode", "tt_encode_device", "tt_encode_batch",
+    assert _declared() == sorted(["tt_create", "tt_create_ex", "tt_destroy", "tt_encode", "tt_encode_device", "tt_encode_batch",
                                   "tt_encode_spans", "tt_encode_spans_device", "tt_pretokenize",
                                   "tt_status_string", "tt_info", "tt_set_profiling", "tt_stage_times",
                                   "tt_session_create", "tt_session_destroy", "tt_session_append",
@@ -122,3 +122,32 @@ def test_binding_fails_loudly_without_library(monkeypatch):
     monkeypatch.setattr(_lib, "LIB_PATH", "/nonexistent/libtoktier.so")
     with pytest.raises(ImportError):
         _lib.load()
+
+
+def _create_ex(lits, ids, ignore=0):
+    lib = _lib.load()
+    vb, vo = _base_vocab()
+    ab = np.frombuffer(b"".join(lits) or b"\0", dtype=np.uint8).copy()
+    ao = np.zeros(len(lits) + 1, dtype=np.int64)
+    np.cumsum([len(x) for x in lits], out=ao[1:])
+    ai = np.asarray(ids or [0], dtype=np.int32)
+    opt = _lib.Options(ignore, len(lits), ab.ctypes.data, ao.ctypes.data, ai.ctypes.data)
+    h = ctypes.c_void_p()
+    return lib.tt_create_ex(None, 0, vb.ctypes.data_as(ctypes.c_void_p), vo.ctypes.data_as(ctypes.c_void_p),
+                            len(vo) - 1, 0, ctypes.byref(opt), ctypes.byref(h))
+
+
+def test_create_ex_rejects_bad_literals():
+    """Literals are validated on the host before any device work."""
+    assert _create_ex([b"<a>", b"<a>"], [1, 2]) == -9      # duplicate
+    assert _create_ex([b"<a>", b""], [1, 2]) == -9         # empty
+    assert _create_ex([b"<\xff>"], [1]) == -9              # not UTF-8
+    assert _create_ex([b"\xe2\x82"], [1]) == -9            # truncated character
+    assert _create_ex([b"<a>"], [-1]) == -9                # negative ID
+    assert _create_ex([b"x" * 1025], [1]) == -9            # longer than TT_MAX_ADDED_BYTES
+
+
+def test_host_only_exports_need_no_gpu():
+    from paper_2607_29678_amd import sync_boundaries
+
+    assert list(sync_boundaries(b"ab 1", "gpt2")) == [0, 0, 1, 0]
