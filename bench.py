@@ -14,8 +14,11 @@ in a second pass; the host-to-host latency through ``tt_encode`` (PCIe copies
 included), a steady-state P50 (100 re-encodes of one sample), the P50 of the
 same requests with span export (IDs plus byte and character spans, device
 resident) and the host-to-host time of a 64 x 16,384-char document batch are
-reported separately.  The CPU oracle is timed on the same timed samples, one
-thread pinned to one core, and its IDs are compared with the GPU's.
+reported separately, and so are the append latency of incremental-repair
+sessions at 100,000 and 1,000,000 characters and the latency of the two
+front-end options (ignore_merges, added-token literals).  The CPU oracle is
+timed on the same timed samples, one thread pinned to one core, and its IDs
+are compared with the GPU's.
 
 ``--calibrate-copy`` first runs a plain int32 copy kernel of 64 MiB read +
 64 MiB written, so that a hardware-counter profile of this command can scale
@@ -116,6 +119,73 @@ def incremental_repair(tok, k, sid, n_appends=24):
                      "ids_identical_to_full_encode": bool(same)})
     return {"window_chars": 512, "shapes": rows,
             "context": {"paper_repair_p50_ms_1M": 1.23, "paper_hardware": "CPU session store (Qwen3 real text)"}}
+
+
+def front_end_options(sid, n=10):
+    """ignore_merges and added tokens (Sec. 4.2, Sec. 4.5) on 1,000,000-character
+    requests.  ignore_merges: the multilingual samples with the cl100k-style
+    table, device-resident P50 with and without the option.  Added tokens: the
+    transcript samples with a chat-template literal before every turn (about
+    one per 1,400 characters), host to host through tt_encode, against the same
+    text on a handle without literals."""
+    import numpy as np
+    import torch
+
+    from paper_2607_29678_amd import Tokenizer
+    from workloads import textgen
+    from workloads.tables import load_table
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    out = {}
+    m, vb, vo = load_table(4)
+    texts = [textgen.latency_sample(4, s).encode("utf-8") for s in range(n)]
+    d_in = [torch.from_numpy(np.frombuffer(t, dtype=np.uint8).copy()).to(dev) for t in texts]
+    d_out = torch.empty(max(len(t) for t in texts), dtype=torch.int32, device=dev)
+    d_len = torch.zeros(1, dtype=torch.int64, device=dev)
+    for ignore in (False, True):
+        tok = Tokenizer(m, vb, vo, "cl100k", ignore_merges=ignore)
+        lat = []
+        for i in range(n + 2):
+            j = i % n
+            torch.cuda.synchronize()
+            a = time.perf_counter()
+            tok.encode_device(d_in[j], len(texts[j]), d_out, d_len, sid)
+            stream.synchronize()
+            if i >= 2:
+                lat.append((time.perf_counter() - a) * 1e3)
+        out["ignore_merges" if ignore else "plain"] = round(percentile(lat, 50), 4)
+        tok.close()
+    ign = {"workload": "C4 samples (1,000,000 chars, cl100k-style, 100,000 merges)", "p50_ms_plain": out["plain"],
+           "p50_ms_ignore_merges": out["ignore_merges"]}
+
+    m, vb, vo = load_table(3)
+    lits = [("<|im_start|>", 50300), ("<|im_end|>", 50301), ("<|endoftext|>", 50302)]
+    texts = []
+    for s in range(n):
+        t = textgen.latency_sample(3, s)
+        parts, pos, k = [], 0, 0
+        while pos < len(t):
+            parts.append(lits[k % 2][0] + t[pos:pos + 1400])
+            pos += 1400
+            k += 1
+        texts.append("".join(parts).encode("utf-8"))
+    res = {}
+    for name, added in (("no_literals", None), ("literals", lits)):
+        tok = Tokenizer(m, vb, vo, "gpt2", added=added)
+        tok.encode(texts[0], sid)
+        lat = []
+        for t in texts:
+            a = time.perf_counter()
+            tok.encode(t, sid)
+            lat.append((time.perf_counter() - a) * 1e3)
+        res[name] = round(percentile(lat, 50), 4)
+        tok.close()
+    lit = {"workload": "C3 samples with a literal before every 1,400 characters (%d literals, %d bytes)"
+                       % (len(texts[0].split(b"<|im_")) - 1, len(texts[0])),
+           "host_to_host_p50_ms_literal_handle": res["literals"],
+           "host_to_host_p50_ms_same_text_plain_handle": res["no_literals"]}
+    return {"ignore_merges": ign, "added_tokens": lit}
 
 
 def main():
@@ -254,6 +324,9 @@ def main():
     # --- incremental repair: appends to a stored session (Sec. 3.2) ------------
     repair = incremental_repair(tok, k, sid)
 
+    # --- front-end options: ignore_merges and added-token literals ----------------
+    options = front_end_options(sid)
+
     # --- roofline of the dominant kernel -------------------------------------
     # algorithmic bytes of one tile-kernel launch: the request's bytes are
     # read once and its token IDs written once (merge-table probes are L2
@@ -330,6 +403,7 @@ def main():
         "span_export_p50_ms": round(percentile(span_lat, 50), 4),
         "batch_64x16k": batch,
         "incremental_repair": repair,
+        "front_end_options": options,
         "stage_ms": {s: round(v, 4) for s, v in stage_avg.items()},
         "roofline": roofline,
         "cpu_baseline": cpu,
