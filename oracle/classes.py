@@ -8,6 +8,11 @@ table pinning; Sec. 5.2, the Unicode table skew).  ``data/onig_classes.txt``
 holds that probe for Oniguruma inside HF tokenizers 0.22.2; it was written by
 ``data/probe_onig.py``.
 
+The o200k-style pattern also tells upper-case from lower-case letters and
+treats combining marks as letter material; ``data/onig_o200k_classes.txt``
+holds those sub-classes (Lu|Lt, Ll, Lm|Lo, M), probed from the same engine by
+``data/probe_onig_o200k.py``.
+
 Parity pins: the whole table is compared with a fresh probe of the engine
 (tests), and the 25 whitespace code points are checked against the Unicode
 White_Space list written out in the test.
@@ -58,3 +63,34 @@ def classes_of(text: str) -> list:
 def folds_to(ch: str, letter: str) -> bool:
     """True iff ``ch`` matches the ASCII ``letter`` case-insensitively in the engine."""
     return ord(ch) in FOLDS[letter]
+
+
+# ---- o200k-style sub-classes ---------------------------------------------------
+UP, LO, BO, MK = 11, 12, 13, 14  # Lu|Lt, Ll, Lm|Lo, M
+O200K_PATH = os.path.join(_HERE, "data", "onig_o200k_classes.txt")
+
+
+def _load_o200k():
+    table = bytearray(0x110000)  # 0: no sub-class
+    code = {"UP": UP, "LO": LO, "BO": BO, "MK": MK}
+    with open(O200K_PATH) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            a, b, k = line.split()
+            for c in range(int(a, 16), int(b, 16) + 1):
+                table[c] = code[k]
+    return table
+
+
+O200K_TABLE = _load_o200k()
+
+
+def o200k_class(cp: int) -> int:
+    """UP, LO, BO or MK for letters and marks, else the class of ``char_class`` (N, W or O)."""
+    return O200K_TABLE[cp] or TABLE[cp]
+
+
+def o200k_classes_of(text: str) -> list:
+    return [o200k_class(ord(c)) for c in text]

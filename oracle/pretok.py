@@ -31,17 +31,28 @@ cl100k style, alternatives in order
   C6  = G5
   C7  = G6
 
+o200k style, alternatives in order (letters split into upper-case UP = Lu|Lt,
+lower-case LO = Ll, "both" BO = Lm|Lo, and marks MK = M, which count as letter
+material in the letter sets and as "other" elsewhere; CT is the case-insensitive
+contraction suffix of C1, optional here)
+  P1  ``[^\r\n\p{L}\p{N}]?[UP BO MK]*[LO BO MK]+CT?``
+  P2  ``[^\r\n\p{L}\p{N}]?[UP BO MK]+[LO BO MK]*CT?``
+  P3  = C3
+  P4  optional U+0020, "other" chars, then CR/LF and "/"  `` ?[^\s\p{L}\p{N}]+[\r\n/]*``
+  P5  = C5,  P6 = G5,  P7 = G6
+
 Readings taken where the paper is silent: ``\\s`` is the engine's whitespace
 class (25 code points), "space" in the optional-space alternatives is U+0020
 only, case-insensitive contractions use the engine's case folding (which maps
 U+017F to ``s``), and only U+0027 is an apostrophe.
 """
 
-from .classes import L, N, O, W, classes_of, folds_to
+from .classes import BO, LO, MK, UP, L, N, O, W, classes_of, folds_to, o200k_classes_of
 
 GPT2 = "gpt2"
 CL100K = "cl100k"
-PATTERNS = (GPT2, CL100K)
+O200K = "o200k"
+PATTERNS = (GPT2, CL100K, O200K)
 
 SUFFIXES = ("s", "t", "re", "ve", "m", "ll", "d")
 SP = " "
@@ -164,15 +175,85 @@ def _cl100k_at(text, cl, p):
             or _ws(text, cl, p))
 
 
+# o200k style ---------------------------------------------------------------
+_UB = (UP, BO, MK)  # the upper-case letter set [\p{Lu}\p{Lt}\p{Lm}\p{Lo}\p{M}]
+_LB = (LO, BO, MK)  # the lower-case letter set [\p{Ll}\p{Lm}\p{Lo}\p{M}]
+
+
+def _run_in(ol, i, ks):
+    """First index >= i whose sub-class is not in ks."""
+    n = len(ol)
+    while i < n and ol[i] in ks:
+        i += 1
+    return i
+
+
+def _o200k_suffix(text, e):
+    """The optional case-insensitive contraction after a letter body ending at e."""
+    if e < len(text):
+        c = _contraction(text, e, True)
+        if c is not None:
+            return c
+    return e
+
+
+def _o200k_letters(text, ol, p, upper_first):
+    """P1 (``upper_first`` False): prefix? [UB]* [LB]+ CT?;  P2: prefix? [UB]+ [LB]* CT?.
+    The optional prefix is tried first, then the match without it; [UB]* gives
+    back characters until [LB]+ can match."""
+    n = len(text)
+    bodies = []
+    if text[p] not in NL and ol[p] in (O, MK, W):  # [^\r\n\p{L}\p{N}]
+        bodies.append(p + 1)
+    bodies.append(p)
+    for b0 in bodies:
+        k_end = _run_in(ol, b0, _UB)
+        if not upper_first:
+            for q in range(k_end, b0 - 1, -1):
+                if q < n and ol[q] in _LB:
+                    return _o200k_suffix(text, _run_in(ol, q, _LB))
+        elif k_end > b0:
+            return _o200k_suffix(text, _run_in(ol, k_end, _LB))
+    return None
+
+
+def _o200k_other(text, ol, p):
+    """`` ?[^\s\p{L}\p{N}]+[\r\n/]*`` (marks are in the set)"""
+    n = len(text)
+    starts = (p + 1, p) if text[p] == SP else (p,)
+    for s in starts:
+        e = _run_in(ol, s, (O, MK))
+        if e > s:
+            while e < n and (text[e] in NL or text[e] == "/"):
+                e += 1
+            return e
+    return None
+
+
+def _o200k_at(text, cl, ol, p):
+    return (_o200k_letters(text, ol, p, False)
+            or _o200k_letters(text, ol, p, True)
+            or _cl_numbers(text, cl, p)
+            or _o200k_other(text, ol, p)
+            or _cl_ws_newlines(text, cl, p)
+            or _ws_not_before_nonws(text, cl, p)
+            or _ws(text, cl, p))
+
+
 def pretokenize(text: str, pattern: str) -> list:
     """Pieces of ``text`` as (start, end) character spans, in order, tiling the text."""
+    cl = classes_of(text)
     if pattern == GPT2:
         step = _gpt2_at
     elif pattern == CL100K:
         step = _cl100k_at
+    elif pattern == O200K:
+        ol = o200k_classes_of(text)
+
+        def step(t, c, p):
+            return _o200k_at(t, c, ol, p)
     else:
         raise ValueError("unknown pattern %r" % (pattern,))
-    cl = classes_of(text)
     spans = []
     p = 0
     n = len(text)

@@ -8,7 +8,7 @@ leftmost-first matching.  The pattern ASTs below are transcriptions of the
 regex text of the two pattern families.
 """
 
-from oracle.classes import char_class, folds_to, L, N, W
+from oracle.classes import BO, LO, MK, UP, char_class, folds_to, o200k_class, L, N, W
 
 
 class Node:
@@ -137,7 +137,23 @@ CL100K = Alt(Alt(*[lit(c, ci=True) for c in CONTRACTIONS]),
              Seq(plus(WS), NotAhead(NONWS)),
              plus(WS))
 
-PATTERNS = {"gpt2": GPT2, "cl100k": CL100K}
+UB = Cls(lambda c: o200k_class(ord(c)) in (UP, BO, MK))  # [\p{Lu}\p{Lt}\p{Lm}\p{Lo}\p{M}]
+LB = Cls(lambda c: o200k_class(ord(c)) in (LO, BO, MK))  # [\p{Ll}\p{Lm}\p{Lo}\p{M}]
+CRLF_SLASH = Cls(lambda c: c in "\r\n/")
+CONTRACTION = Alt(*[lit(c, ci=True) for c in CONTRACTIONS])
+
+# [^\r\n\p{L}\p{N}]?[\p{Lu}\p{Lt}\p{Lm}\p{Lo}\p{M}]*[\p{Ll}\p{Lm}\p{Lo}\p{M}]+(?i:'s|'t|'re|'ve|'m|'ll|'d)?
+# |[^\r\n\p{L}\p{N}]?[\p{Lu}\p{Lt}\p{Lm}\p{Lo}\p{M}]+[\p{Ll}\p{Lm}\p{Lo}\p{M}]*(?i:'s|'t|'re|'ve|'m|'ll|'d)?
+# |\p{N}{1,3}| ?[^\s\p{L}\p{N}]+[\r\n/]*|\s*[\r\n]+|\s+(?!\S)|\s+
+O200K = Alt(Seq(opt(NOT_CRLF_L_N), star(UB), plus(LB), opt(CONTRACTION)),
+            Seq(opt(NOT_CRLF_L_N), plus(UB), star(LB), opt(CONTRACTION)),
+            Rep(NUM, 1, 3),
+            Seq(opt(SP), plus(OTHER), star(CRLF_SLASH)),
+            Seq(star(WS), plus(CRLF)),
+            Seq(plus(WS), NotAhead(NONWS)),
+            plus(WS))
+
+PATTERNS = {"gpt2": GPT2, "cl100k": CL100K, "o200k": O200K}
 
 
 def split(text, pattern):

@@ -20,12 +20,15 @@ from oracle.pretok import pretokenize, pieces
 from regex_interp import split as interp_split
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-PATTERNS = ("gpt2", "cl100k")
+PATTERNS = ("gpt2", "cl100k", "o200k")
 
 REGEX = {
     "gpt2": r"'s|'t|'re|'ve|'m|'ll|'d| ?\p{L}+| ?\p{N}+| ?[^\s\p{L}\p{N}]+|\s+(?!\S)|\s+",
     "cl100k": r"(?i:'s|'t|'re|'ve|'m|'ll|'d)|[^\r\n\p{L}\p{N}]?\p{L}+|\p{N}{1,3}| ?[^\s\p{L}\p{N}]+[\r\n]*"
               r"|\s*[\r\n]+|\s+(?!\S)|\s+",
+    "o200k": r"[^\r\n\p{L}\p{N}]?[\p{Lu}\p{Lt}\p{Lm}\p{Lo}\p{M}]*[\p{Ll}\p{Lm}\p{Lo}\p{M}]+(?i:'s|'t|'re|'ve|'m|'ll|'d)?"
+             r"|[^\r\n\p{L}\p{N}]?[\p{Lu}\p{Lt}\p{Lm}\p{Lo}\p{M}]+[\p{Ll}\p{Lm}\p{Lo}\p{M}]*(?i:'s|'t|'re|'ve|'m|'ll|'d)?"
+             r"|\p{N}{1,3}| ?[^\s\p{L}\p{N}]+[\r\n/]*|\s*[\r\n]+|\s+(?!\S)|\s+",
 }
 
 
@@ -54,22 +57,44 @@ def test_worked_examples(row):
 
 
 ALPHA13 = list("asl'S1 \n\t.re\r")
+# o200k: upper, lower, title-case (Lt), other letter (Lo), modifier letter (Lm),
+# combining mark, and the characters its other alternatives single out
+ALPHA_O200K = list("aS1 \n\t'./\r") + ["ǅ", "中", "ʰ", "\u0301"]
+
+
+def _golden_o200k():
+    rows = []
+    with open(os.path.join(HERE, "golden", "pretok_o200k_examples.txt"), encoding="utf-8") as f:
+        for line in f:
+            if not line.strip() or line.startswith("#"):
+                continue
+            src, pcs = line.rstrip("\n").split("\t")
+            rows.append((_unescape(src), [_unescape(p) for p in pcs.split(" | ")]))
+    return rows
+
+
+@pytest.mark.parametrize("row", _golden_o200k(), ids=lambda r: repr(r[0]))
+def test_worked_examples_o200k(row):
+    src, want = row
+    assert pieces(src, "o200k") == want
 
 
 @pytest.mark.parametrize("pattern", PATTERNS)
 def test_brute_force_against_backtracking_interpreter(pattern):
+    alpha = ALPHA_O200K if pattern == "o200k" else ALPHA13
     n = 0
     for length in range(1, 5):
-        for tup in itertools.product(ALPHA13, repeat=length):
+        for tup in itertools.product(alpha, repeat=length):
             s = "".join(tup)
             assert pretokenize(s, pattern) == interp_split(s, pattern), repr(s)
             n += 1
-    assert n == sum(13 ** k for k in range(1, 5))
+    assert n == sum(len(alpha) ** k for k in range(1, 5))
 
 
 WIDE = list("asS1 \n\t'.\r") + ["\u0085", " ", "ſ", "²", "中", "。", "\U0001f600",
                                  "́", "　", "½", "А", "t", "T", "d", "D", "m", "M",
-                                 "l", "L", "v", "V", "e", "E", "R", "_", "-", " ", "\x1c"]
+                                 "l", "L", "v", "V", "e", "E", "R", "_", "-", " ", "\x1c", "/", "ǅ", "ʰ",
+                                 "É", "ä", "\u0308", "Ж"]
 
 
 @pytest.mark.parametrize("pattern", PATTERNS)
@@ -93,6 +118,12 @@ def test_random_against_oniguruma(pattern):
     for _ in range(20000):
         s = "".join(rng.choice(WIDE) for _ in range(rng.randint(1, 16)))
         assert pretokenize(s, pattern) == onig(s), repr(s)
+
+
+def test_worked_examples_o200k_against_oniguruma():
+    onig = _onig("o200k")
+    for src, want in _golden_o200k():
+        assert [src[a:b] for a, b in onig(src)] == want, repr(src)
 
 
 @pytest.mark.parametrize("k", [1, 2, 4])

@@ -107,6 +107,40 @@ def test_class_table_file_pinned():
             "316e731861e64a3ef93bf357e77bcf74fb590852d0654deb2869f91f4d3628e1"
 
 
+def test_o200k_class_table_file_pinned():
+    from oracle.classes import O200K_PATH
+
+    with open(O200K_PATH, "rb") as f:
+        assert hashlib.sha256(f.read()).hexdigest() == \
+            "6abc8e629552010cc1dcd36fc4a5e1304673a577c290d061a62ba04536c394e4"
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("code,pats", [("UP", (r"\p{Lu}", r"\p{Lt}")), ("LO", (r"\p{Ll}",)),
+                                       ("BO", (r"\p{Lm}", r"\p{Lo}")), ("MK", (r"\p{M}",))])
+def test_o200k_class_table_equals_fresh_engine_probe(code, pats):
+    tk = pytest.importorskip("tokenizers")
+    from oracle.classes import BO, LO, MK, O200K_TABLE, UP
+
+    cps = [c for c in range(0x110000) if not 0xD800 <= c <= 0xDFFF]
+    text = "".join(map(chr, cps))
+    members = set()
+    for pat in pats:
+        sp = tk.pre_tokenizers.Split(tk.Regex(pat), behavior="removed")
+        left = bytearray(len(cps))
+        for _, (a, b) in sp.pre_tokenize_str(text):
+            left[a:b] = b"\x01" * (b - a)
+        members |= {cps[i] for i in range(len(cps)) if not left[i]}
+    want = {"UP": UP, "LO": LO, "BO": BO, "MK": MK}[code]
+    assert members == {c for c in range(0x110000) if O200K_TABLE[c] == want}
+
+
+def test_o200k_classes_spot_checks():
+    from oracle.classes import BO, LO, MK, N, O, UP, W, o200k_class
+
+    assert [o200k_class(ord(c)) for c in "Aaǅ中ʰ\u03011 ./"] == [UP, LO, UP, BO, BO, MK, N, W, O, O]
+
+
 # -- seeded inputs --------------------------------------------------------------
 
 @pytest.mark.parametrize("k,chars,nbytes", [
