@@ -61,9 +61,14 @@ enum {
  *  TT_PATTERN_CL100K: (?i:'s|'t|'re|'ve|'m|'ll|'d) | [^\r\n\p{L}\p{N}]?\p{L}+ |
  *                     \p{N}{1,3} | ?[^\s\p{L}\p{N}]+[\r\n]* | \s*[\r\n]+ |
  *                     \s+(?!\S) | \s+
+ *  TT_PATTERN_O200K:  [^\r\n\p{L}\p{N}]?[\p{Lu}\p{Lt}\p{Lm}\p{Lo}\p{M}]*[\p{Ll}\p{Lm}\p{Lo}\p{M}]+CT? |
+ *                     [^\r\n\p{L}\p{N}]?[\p{Lu}\p{Lt}\p{Lm}\p{Lo}\p{M}]+[\p{Ll}\p{Lm}\p{Lo}\p{M}]*CT? |
+ *                     \p{N}{1,3} | ?[^\s\p{L}\p{N}]+[\r\n/]* | \s*[\r\n]+ | \s+(?!\S) | \s+
+ *                     with CT = (?i:'s|'t|'re|'ve|'m|'ll|'d) (Sec. 4.1: the o200k lineage's
+ *                     case boundaries; marks are letter material here)
  * Character classes are those of the Oniguruma engine of HF tokenizers 0.22.2
  * (the paper pins class tables probed from the reference engine, Sec. 4.1). */
-enum { TT_PATTERN_GPT2 = 0, TT_PATTERN_CL100K = 1 };
+enum { TT_PATTERN_GPT2 = 0, TT_PATTERN_CL100K = 1, TT_PATTERN_O200K = 2 };
 
 typedef struct tt_tokenizer tt_tokenizer; /* opaque */
 

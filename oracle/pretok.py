@@ -35,10 +35,10 @@ o200k style, alternatives in order (letters split into upper-case UP = Lu|Lt,
 lower-case LO = Ll, "both" BO = Lm|Lo, and marks MK = M, which count as letter
 material in the letter sets and as "other" elsewhere; CT is the case-insensitive
 contraction suffix of C1, optional here)
-  P1  ``[^\r\n\p{L}\p{N}]?[UP BO MK]*[LO BO MK]+CT?``
-  P2  ``[^\r\n\p{L}\p{N}]?[UP BO MK]+[LO BO MK]*CT?``
+  P1  ``[^\\r\\n\\p{L}\\p{N}]?[UP BO MK]*[LO BO MK]+CT?``
+  P2  ``[^\\r\\n\\p{L}\\p{N}]?[UP BO MK]+[LO BO MK]*CT?``
   P3  = C3
-  P4  optional U+0020, "other" chars, then CR/LF and "/"  `` ?[^\s\p{L}\p{N}]+[\r\n/]*``
+  P4  optional U+0020, "other" chars, then CR/LF and "/"  `` ?[^\\s\\p{L}\\p{N}]+[\\r\\n/]*``
   P5  = C5,  P6 = G5,  P7 = G6
 
 Readings taken where the paper is silent: ``\\s`` is the engine's whitespace
@@ -218,7 +218,7 @@ def _o200k_letters(text, ol, p, upper_first):
 
 
 def _o200k_other(text, ol, p):
-    """`` ?[^\s\p{L}\p{N}]+[\r\n/]*`` (marks are in the set)"""
+    """`` ?[^\\s\\p{L}\\p{N}]+[\\r\\n/]*`` (marks are in the set)"""
     n = len(text)
     starts = (p + 1, p) if text[p] == SP else (p,)
     for s in starts:

@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(HERE, "libtoktier.so")
 TT_OK = 0
 TT_PATTERN_GPT2 = 0
 TT_PATTERN_CL100K = 1
+TT_PATTERN_O200K = 2
 TT_MAX_BYTES = 1 << 30
 
 STATUS = {

@@ -254,6 +254,7 @@ constexpr int PT_BPT = 4;                          // bytes per thread
 constexpr int PT_WIN = PT_THREADS * PT_BPT;        // window bytes in LDS
 constexpr int PT_HALO = 32;                        // context bytes each side
 constexpr int PT_OWN = PT_WIN - 2 * PT_HALO;       // bytes a tile decides
+constexpr int PT_PAD = 8;  // LDS arrays also hold window positions [-8, 0) and [PT_WIN, PT_WIN + 16)
 
 constexpr int SMALL_MAX = 16;                      // thread-per-unit limit (bytes)
 constexpr int TH_THREADS = 256;                    // threads of a tile that run the thread engine

@@ -40,8 +40,10 @@
 // blocks that started before it, and every block publishes what later blocks
 // wait for before it waits on anything itself.
 #include "class_table.inc"
+#include "class_table_o200k.inc"
 #include "tt_bpe.h"
 #include "tt_internal.h"
+#include "tt_o200k.h"
 
 namespace tt {
 
@@ -71,6 +73,14 @@ struct ClassLds {
   uint8_t asc[128];
 };
 
+// The o200k-style pattern's 4-bit class table, staged in LDS by every block
+// of that pattern, and the code of every ASCII character.
+struct O2Lds {
+  uint8_t l1[4352] __attribute__((aligned(16)));
+  uint8_t l2[TT_O2_NBLOCKS * 128] __attribute__((aligned(16)));
+  uint8_t asc[128];
+};
+
 // 2-bit class of a non-ASCII code point from the probed table.
 __device__ __forceinline__ uint32_t table_class(const ClassLds& ct, uint32_t cp) {
   const uint32_t blk = ct.l1[cp >> 8];
@@ -95,6 +105,20 @@ __device__ __forceinline__ uint32_t letter_ident(uint32_t lower) {
 // Class and identity code of one code point.  Contraction letters are
 // case-sensitive for GPT-2 and folded for cl100k, where the engine also folds
 // U+017F (long s) to 's'.
+// Code of one code point for the o200k-style pattern: its class only (the
+// walks read apostrophes, "/" and contraction letters from the bytes).
+__device__ __forceinline__ uint32_t o2_code(const O2Lds& t, uint32_t cp) {
+  if (cp < 128u) {
+    if ((cp - 'A') < 26u) return O2_UP;
+    if ((cp - 'a') < 26u) return O2_LO;
+    if ((cp - '0') < 10u) return O2_N;
+    if (cp == 10u || cp == 13u) return O2_NL;
+    if (cp == 32u || (cp - 9u) < 5u) return O2_WS;
+    return O2_O;
+  }
+  return o2_table_class(t.l1, t.l2, cp);
+}
+
 template <int PAT>
 __device__ __forceinline__ uint32_t char_code(const ClassLds& ct, uint32_t cp) {
   uint32_t cls, id = I_NONE;
@@ -208,7 +232,6 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane, F comb)
   return v;
 }
 
-constexpr int PT_PAD = 8;  // LDS arrays also hold window positions [-8, 0) and [PT_WIN, PT_WIN + 16)
 
 // The NW little-endian words of the L bytes at window index a (bytes past L
 // read as zero), from aligned LDS words: NW + 1 word loads and one byte
@@ -274,10 +297,18 @@ constexpr uint16_t U_INCOMING = 0xFFFFu;               // list entry for the inc
 // written before it.
 union PhaseMem {
   struct {
-    ClassLds cls;             // character classes
+    union {
+      ClassLds cls;           // character classes (GPT-2, cl100k)
+      O2Lds o2;               // character classes (o200k)
+    };
     uint32_t join[2048];      // junction byte pairs of the merges
     uint8_t code[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));  // class/identity/doc-start codes
-    int16_t run_end[PT_WIN];  // cl100k: window index of the head after a run's head
+    union {
+      int16_t run_end[PT_WIN];  // cl100k: window index of the head after a run's head
+      uint8_t o2piece[PT_WIN];  // o200k: 1 at the piece starts the walks find
+    };
+    uint32_t o2seg[PT_WIN / 32];    // o200k: segment starts (synchronizing positions, document starts)
+    uint32_t nocut[PT_WIN / 32];    // ignore_merges: window positions no junction cut may split
   } a;
   struct {
     uint32_t tok[PT_WIN];     // tokens of unit k at tok[ustart[k] ..]
@@ -315,7 +346,7 @@ struct PtShared {
   uint32_t carry_n;           // cl100k: number-run chars before the tile, mod 3
   uint32_t carry_nlpre;       // cl100k: class before a CR/LF stretch entering the tile
   uint32_t cwave[PT_THREADS / 64];  // span export: per-wave sums
-  uint32_t nocut[PT_WIN / 32];  // ignore_merges: window positions no junction cut may split
+  int64_t o2_doc_after;          // o200k, batch: first document start after the window
   uint32_t whole[PT_WIN / 32];  // ignore_merges: starts of pieces that are vocabulary entries
   uint32_t cbase;             // span export: non-continuation bytes before the tile
   uint32_t ctile;             // span export: non-continuation bytes the tile owns
@@ -453,9 +484,11 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
 
   if (tid <= SMALL_MAX) sh.hist[tid] = 0;
   if (IGN && tid < PT_WIN / 32) {
-    sh.nocut[tid] = 0;
+    sh.ph.a.nocut[tid] = 0;
     sh.whole[tid] = 0;
   }
+  constexpr bool O2 = PAT == TT_PATTERN_O200K;
+  if (O2 && tid < PT_WIN / 32) sh.ph.a.o2seg[tid] = 0;
   // the ticket's round trip (tickets are handed out one at a time) overlaps
   // the staging of the tables, which do not depend on the tile
   uint32_t ticket = 0;
@@ -463,16 +496,29 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   {
     // the class table (12.9 KB) is read once per block
     static_assert(CLS_L1_BYTES % 16 == 0 && CLS_L2_BYTES % 16 == 0, "class table staging uses 16-byte words");
-    constexpr int N1 = CLS_L1_BYTES / 16, N2 = CLS_L2_BYTES / 16;
-    const uint4* s1 = reinterpret_cast<const uint4*>(TT_CLS_L1);
-    const uint4* s2 = reinterpret_cast<const uint4*>(TT_CLS_L2);
-    uint4* d1 = reinterpret_cast<uint4*>(sh.ph.a.cls.l1);
-    uint4* d2 = reinterpret_cast<uint4*>(sh.ph.a.cls.l2);
-    for (int i = tid; i < N1 + N2; i += PT_THREADS) {
-      if (i < N1) d1[i] = s1[i];
-      else d2[i - N1] = s2[i - N1];
+    if (O2) {
+      constexpr int N1 = 4352 / 16, N2 = TT_O2_NBLOCKS * 128 / 16;
+      const uint4* s1 = reinterpret_cast<const uint4*>(TT_O2_L1);
+      const uint4* s2 = reinterpret_cast<const uint4*>(TT_O2_L2);
+      uint4* d1 = reinterpret_cast<uint4*>(sh.ph.a.o2.l1);
+      uint4* d2 = reinterpret_cast<uint4*>(sh.ph.a.o2.l2);
+      for (int i = tid; i < N1 + N2; i += PT_THREADS) {
+        if (i < N1) d1[i] = s1[i];
+        else d2[i - N1] = s2[i - N1];
+      }
+      if (tid < 128) sh.ph.a.o2.asc[tid] = (uint8_t)o2_code(sh.ph.a.o2, (uint32_t)tid);
+    } else {
+      constexpr int N1 = CLS_L1_BYTES / 16, N2 = CLS_L2_BYTES / 16;
+      const uint4* s1 = reinterpret_cast<const uint4*>(TT_CLS_L1);
+      const uint4* s2 = reinterpret_cast<const uint4*>(TT_CLS_L2);
+      uint4* d1 = reinterpret_cast<uint4*>(sh.ph.a.cls.l1);
+      uint4* d2 = reinterpret_cast<uint4*>(sh.ph.a.cls.l2);
+      for (int i = tid; i < N1 + N2; i += PT_THREADS) {
+        if (i < N1) d1[i] = s1[i];
+        else d2[i - N1] = s2[i - N1];
+      }
+      if (tid < 128) sh.ph.a.cls.asc[tid] = (uint8_t)char_code<PAT>(sh.ph.a.cls, (uint32_t)tid);
     }
-    if (tid < 128) sh.ph.a.cls.asc[tid] = (uint8_t)char_code<PAT>(sh.ph.a.cls, (uint32_t)tid);
   }
   if (SEG) {
     // the junction bitmap (8 KB) is read once per block
@@ -542,6 +588,15 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         else hi = mid;
       }
       sh.doc_lo_idx = lo;
+      if (O2) {
+        int a = lo, b = w.n_docs;  // first document start >= w0 + PT_WIN
+        while (a < b) {
+          int mid = (a + b) >> 1;
+          if (w.doc_off[mid] < w0 + PT_WIN) a = mid + 1;
+          else b = mid;
+        }
+        sh.o2_doc_after = a < w.n_docs ? w.doc_off[a] : n;
+      }
     }
   }
   __syncthreads();
@@ -586,7 +641,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (SPANS) nc_own = own_noncont(bw1, q0, p0);
     uint32_t codes;
     if ((bw1 & 0x80808080u) == 0u && p0 >= 0 && p0 + PT_BPT <= n) {
-      const uint8_t* asc = sh.ph.a.cls.asc;
+      const uint8_t* asc = O2 ? sh.ph.a.o2.asc : sh.ph.a.cls.asc;
       codes = (uint32_t)asc[bw1 & 255u] | ((uint32_t)asc[(bw1 >> 8) & 255u] << 8) |
               ((uint32_t)asc[(bw1 >> 16) & 255u] << 16) | ((uint32_t)asc[bw1 >> 24] << 24);
       codes |= (dw1 & 0x01010101u) << 7;  // document starts (flags are 0 or 1)
@@ -630,7 +685,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
           claimed = claimed || (!blocked && ok && !c && ll > (uint32_t)k);
           blocked = blocked || !ok || !c || dst(j - k);
         }
-        const uint32_t code = (!in_j || cont) ? C_NONE : len == 0u ? C_O : char_code_sel<PAT>(sh.ph.a.cls, cp);
+        const uint32_t code = O2 ? ((!in_j || cont) ? O2_NONE : len == 0u ? O2_O : o2_code(sh.ph.a.o2, cp))
+                                 : (!in_j || cont) ? C_NONE : len == 0u ? C_O : char_code_sel<PAT>(sh.ph.a.cls, cp);
         bad = bad || (own && (cont ? !claimed : len == 0u));
         codes |= (code | (dst(j) ? CODE_DOCSTART : 0u)) << (8 * j);
       }
@@ -638,10 +694,13 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     *reinterpret_cast<uint32_t*>(&sh.ph.a.code[PT_PAD + q0]) = codes;
     if (tid < 3) {  // positions outside [0, PT_WIN) carry no character for the rules
       const int qx = tid == 0 ? -8 : PT_WIN + 8 * (tid - 1);
-      *reinterpret_cast<uint2*>(&sh.ph.a.code[PT_PAD + qx]) = make_uint2(0x07070707u, 0x07070707u);
+      const uint32_t none4 = O2 ? 0x0F0F0F0Fu : 0x07070707u;
+      *reinterpret_cast<uint2*>(&sh.ph.a.code[PT_PAD + qx]) = make_uint2(none4, none4);
     }
   }
-  for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.ph.a.run_end[q] = -1;
+  if (PAT == TT_PATTERN_CL100K)
+    for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.ph.a.run_end[q] = -1;
+  if (O2) *reinterpret_cast<uint32_t*>(&sh.ph.a.o2piece[tid * PT_BPT]) = 0u;
   if (SPANS) {
     const uint32_t nc_incl = wave_incl_sum(nc_own);
     if (lane == 63) sh.cwave[wave] = nc_incl;
@@ -910,9 +969,106 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // cheap cases are selects; contractions (an apostrophe one to three bytes
   // back), whitespace after CR/LF and a letter after a lone symbol branch.
   uint32_t flags = 0;
+  if (O2) {
+    // o200k: segment starts are document starts and synchronizing positions
+    // (their two neighbouring characters form a transition of o2_sync); the
+    // pieces of a segment come from running the pattern's alternatives from
+    // its start, one thread per segment
+    uint32_t seg = 0;
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j) {
+      const int q = qb + j;
+      const uint32_t c = cr(j);
+      if (!inside(q) || (c & 15u) == O2_NONE) continue;
+      bool st = (c & CODE_DOCSTART) != 0u;
+      if (!st) {
+        int k = 0;  // the character before q starts at most four bytes back
+#pragma unroll
+        for (int d = 4; d >= 1; --d)
+          if ((cr(j - d) & 15u) != O2_NONE) k = d;
+        if (k > 0 && q - k >= 0) {
+          const uint32_t bx = sh.buf[PT_PAD + q - k];
+          st = o2_sync(cr(j - k) & 15u, c & 15u, k == 1 ? bx : 0x80u, sh.buf[PT_PAD + q]);
+        }
+      }
+      if (st) seg |= 1u << j;
+    }
+    if (seg) atomicOr(&sh.ph.a.o2seg[qb >> 5], seg << (qb & 31));
+    __syncthreads();
+    const O2View v{(lds_u8*)sh.buf, (lds_u8*)sh.ph.a.code, (lds_u8*)sh.ph.a.o2.l1, (lds_u8*)sh.ph.a.o2.l2,
+                   w.text, w0, n, BATCH ? sh.o2_doc_after : n};
+    const int64_t own_end = n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN;
+    auto segbit = [&](int64_t q) -> bool { return q >= 0 && q < PT_WIN && ((sh.ph.a.o2seg[q >> 5] >> (q & 31)) & 1u); };
+    // one loop per lane, one piece per step: the lane's walk starts in order
+    // (thread 0's continued segment first, then its own segment starts), so
+    // a wave runs as long as its busiest lane, not its longest segment of
+    // every start
+    // thread 0 first walks the segment that the tile's first bytes continue,
+    // from its start in the left context, else from the last piece start the
+    // previous tile published
+    int64_t first = -1;
+    if (tid == 0 && !segbit(PT_HALO)) {
+      for (int q = PT_HALO - 1; q >= 0 && first < 0; --q)
+        if (segbit(q)) first = q;
+      if (first < 0 && t == 0) first = PT_HALO;  // (invalid text: no character at the text start)
+      if (first < 0) {
+        uint64_t x;
+        do {
+          x = ld_word(&w.tile_sum[t - 1]);
+        } while ((uint32_t)(x >> 32) != w.epoch);
+        first = (int64_t)(uint32_t)x - w0;
+      }
+    }
+    uint32_t todo = 0;  // bit j: own position qb + j starts a segment to walk
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j)
+      if (((seg >> j) & 1u) && qb + j >= PT_HALO && qb + j < own_end) todo |= 1u << j;
+    int64_t s = first;
+    bool on_first = first != -1;
+    if (!on_first && todo) {
+      s = qb + __builtin_ctz(todo);
+      todo &= todo - 1u;
+    }
+    bool active = on_first || s != -1;
+    int64_t first_end = PT_HALO;  // the last start thread 0's first walk visits (stays so only for invalid text)
+#pragma unroll 1
+    while (active) {
+      if (s >= PT_HALO) sh.ph.a.o2piece[s] = 1;  // (s < own_end <= PT_WIN)
+      if (on_first) first_end = s;
+      const int64_t e = o2_piece_end(v, s);
+      if (e < own_end && !segbit(e)) {
+        s = e;
+      } else if (todo) {
+        on_first = false;
+        s = qb + __builtin_ctz(todo);
+        todo &= todo - 1u;
+      } else {
+        active = false;
+      }
+    }
+    __syncthreads();
+    const uint32_t pw = *reinterpret_cast<const uint32_t*>(&sh.ph.a.o2piece[qb]);
+    flags = (pw & 1u) | ((pw >> 7) & 2u) | ((pw >> 14) & 4u) | ((pw >> 21) & 8u);
+    // later tiles may start from this tile's last piece: the last start in
+    // its bytes, else the last one the first walk visited (before them)
+    {
+      const uint64_t any = __ballot(flags != 0u);
+      const int hi_lane = any ? 63 - __builtin_clzll(any) : -1;
+      if (lane == hi_lane) sh.wave_tot[wave] = (uint32_t)(qb + 31 - __builtin_clz(flags));
+      if (lane == 0 && !any) sh.wave_tot[wave] = 0xFFFFFFFFu;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int64_t lastp = INT64_MIN;
+      for (int v2 = PT_THREADS / 64 - 1; v2 >= 0 && lastp == INT64_MIN; --v2)
+        if (sh.wave_tot[v2] != 0xFFFFFFFFu) lastp = sh.wave_tot[v2];
+      if (lastp == INT64_MIN) lastp = first_end;
+      st_word(&w.tile_sum[t], ((uint64_t)w.epoch << 32) | (uint32_t)(w0 + lastp));
+    }
+  }
   uint32_t scan_st = s0;  // cl100k: scan state before position q
 #pragma unroll
-  for (int j = 0; j < PT_BPT; ++j) {
+  for (int j = 0; j < (O2 ? 0 : PT_BPT); ++j) {
     const int q = qb + j;
     const uint32_t ex = scan_st;
     if (PAT == TT_PATTERN_CL100K) scan_st = seg_combine(scan_st, elems[j]);
@@ -1008,7 +1164,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       if (id == DICT_NONE) continue;
       w.stage[w0 + a] = id;
       atomicOr(&sh.whole[a >> 5], 1u << (a & 31u));
-      for (uint32_t q = a + 1; q < e; ++q) atomicOr(&sh.nocut[q >> 5], 1u << (q & 31u));
+      for (uint32_t q = a + 1; q < e; ++q) atomicOr(&sh.ph.a.nocut[q >> 5], 1u << (q & 31u));
     }
     // the incoming piece's tail and the tile's last piece
     const uint32_t first = pm > 0 ? sh.ustart[0] : (uint32_t)(PT_HALO + PT_OWN);
@@ -1020,7 +1176,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       const bool own = q >= (uint32_t)PT_HALO && q < (uint32_t)(PT_HALO + PT_OWN);
       if (own && ((t > 0 && q < first) || (!last && q > lastp))) mask |= 1u << j;
     }
-    if (mask) atomicOr(&sh.nocut[qb >> 5], mask << (qb & 31));
+    if (mask) atomicOr(&sh.ph.a.nocut[qb >> 5], mask << (qb & 31));
     __syncthreads();
   }
   if (SEG) {
@@ -1036,7 +1192,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       const bool joined = (sh.ph.a.join[k2 >> 5] >> (k2 & 31u)) & 1u;
       const bool eligible = q >= PT_HALO && q < PT_HALO + PT_OWN && inside(q) && inside(q - 1) &&
                             !(flags & (1u << j)) && !(cr(j) & CODE_DOCSTART) &&
-                            !(IGN && ((sh.nocut[q >> 5] >> (q & 31)) & 1u));
+                            !(IGN && ((sh.ph.a.nocut[q >> 5] >> (q & 31)) & 1u));
       if (eligible && !joined) flags |= 1u << j;
     }
   }
@@ -1466,37 +1622,38 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   }
 }
 
-hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode, bool ignore, hipStream_t s) {
+namespace {
+template <int PAT>
+hipError_t launch_pat(const Work& w, const DevTables& tb, int mode, bool batch, bool ignore, hipStream_t s) {
   dim3 grid(w.n_tiles), block(PT_THREADS);
+#define TT_TILE(B, M, I) hipLaunchKernelGGL((tile_kernel<PAT, B, M, I>), grid, block, 0, s, w, tb)
+  if (mode == 0) {
+    if (ignore) return hipErrorInvalidValue;  // the split export has no model stage
+    if (batch) TT_TILE(true, 0, false);
+    else TT_TILE(false, 0, false);
+  } else if (mode == 1) {
+    if (batch && ignore) TT_TILE(true, 1, true);
+    else if (batch) TT_TILE(true, 1, false);
+    else if (ignore) TT_TILE(false, 1, true);
+    else TT_TILE(false, 1, false);
+  } else {
+    if (batch) return hipErrorInvalidValue;  // span export is for single requests
+    if (ignore) TT_TILE(false, 2, true);
+    else TT_TILE(false, 2, false);
+  }
+#undef TT_TILE
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode, bool ignore, hipStream_t s) {
   const bool batch = w.doc_off != nullptr;
-  if (mode == 2 && batch) return hipErrorInvalidValue;  // span export is for single requests
-  if (ignore && mode == 0) return hipErrorInvalidValue;  // the split export has no model stage
-  const int variant = (mode == 2 ? 8 + (pattern == TT_PATTERN_GPT2 ? 0 : 1)
-                                 : (pattern == TT_PATTERN_GPT2 ? 0 : 4) + (batch ? 2 : 0) + (mode ? 1 : 0)) +
-                      (ignore ? 16 : 0);
-  switch (variant) {
-#define TT_TILE_CASE(V, P, B, M, I) \
-  case V: hipLaunchKernelGGL((tile_kernel<P, B, M, I>), grid, block, 0, s, w, tb); break;
-    TT_TILE_CASE(0, TT_PATTERN_GPT2, false, 0, false)
-    TT_TILE_CASE(1, TT_PATTERN_GPT2, false, 1, false)
-    TT_TILE_CASE(2, TT_PATTERN_GPT2, true, 0, false)
-    TT_TILE_CASE(3, TT_PATTERN_GPT2, true, 1, false)
-    TT_TILE_CASE(4, TT_PATTERN_CL100K, false, 0, false)
-    TT_TILE_CASE(5, TT_PATTERN_CL100K, false, 1, false)
-    TT_TILE_CASE(6, TT_PATTERN_CL100K, true, 0, false)
-    TT_TILE_CASE(7, TT_PATTERN_CL100K, true, 1, false)
-    TT_TILE_CASE(8, TT_PATTERN_GPT2, false, 2, false)
-    TT_TILE_CASE(9, TT_PATTERN_CL100K, false, 2, false)
-    TT_TILE_CASE(17, TT_PATTERN_GPT2, false, 1, true)
-    TT_TILE_CASE(19, TT_PATTERN_GPT2, true, 1, true)
-    TT_TILE_CASE(21, TT_PATTERN_CL100K, false, 1, true)
-    TT_TILE_CASE(23, TT_PATTERN_CL100K, true, 1, true)
-    TT_TILE_CASE(24, TT_PATTERN_GPT2, false, 2, true)
-    TT_TILE_CASE(25, TT_PATTERN_CL100K, false, 2, true)
-#undef TT_TILE_CASE
+  switch (pattern) {
+    case TT_PATTERN_GPT2: return launch_pat<TT_PATTERN_GPT2>(w, tb, mode, batch, ignore, s);
+    case TT_PATTERN_CL100K: return launch_pat<TT_PATTERN_CL100K>(w, tb, mode, batch, ignore, s);
+    case TT_PATTERN_O200K: return launch_pat<TT_PATTERN_O200K>(w, tb, mode, batch, ignore, s);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace tt

@@ -15,7 +15,8 @@ from . import _lib
 
 GPT2 = _lib.TT_PATTERN_GPT2
 CL100K = _lib.TT_PATTERN_CL100K
-PATTERNS = {"gpt2": GPT2, "cl100k": CL100K}
+O200K = _lib.TT_PATTERN_O200K
+PATTERNS = {"gpt2": GPT2, "cl100k": CL100K, "o200k": O200K}
 
 
 def _ptr(x):

@@ -27,8 +27,10 @@ from paper_2607_29678_amd import splice_plan, sync_boundaries
 ALPHA = {
     "gpt2": list("as1 \n\t'.rel") + ["\r"],
     "cl100k": list("aS1 \n\t'.rl") + ["\r", "ſ", " "],
+    # upper, lower, Lo, Lm, a mark, "/" (absorbed after CR/LF by symbol pieces)
+    "o200k": list("aS1 \n\t'./") + ["\u4e2d", "\u02b0", "\u0301", "\r"],
 }
-EXTRA = ["中", "。", "²", "\U0001f600", "́", "　", "\u0085", "А"]
+EXTRA = ["中", "。", "²", "\U0001f600", "́", "　", "\u0085", "А", "\u00c9", "\u01c5", "\u02b0", "/", "T", "D"]
 
 
 def _starts(text, pattern, memo):
@@ -82,7 +84,7 @@ def _check_string(text, pattern, memo):
     return hits
 
 
-@pytest.mark.parametrize("pattern", ["gpt2", "cl100k"])
+@pytest.mark.parametrize("pattern", ["gpt2", "cl100k", "o200k"])
 def test_sync_boundaries_exhaustive_short_strings(pattern):
     """Every string of up to 5 characters over the alphabet: each position the
     library calls synchronizing is a certificate for every split."""
@@ -94,7 +96,7 @@ def test_sync_boundaries_exhaustive_short_strings(pattern):
     assert hits > 10000  # the sets are not empty
 
 
-@pytest.mark.parametrize("pattern", ["gpt2", "cl100k"])
+@pytest.mark.parametrize("pattern", ["gpt2", "cl100k", "o200k"])
 def test_sync_boundaries_random_strings(pattern):
     rng = random.Random(0x5A11 + len(pattern))
     alphabet = ALPHA[pattern] + EXTRA + ["a"] * 6 + ["1"] * 4 + [" "] * 4
@@ -121,8 +123,16 @@ def test_certificate_checker_catches_unsafe_transitions():
     assert certificate_violation("12345", 3, "cl100k", memo) is not None
     # cl100k: a symbol piece absorbs the CR/LF after it
     assert certificate_violation("a.\nb", 2, "cl100k", memo) is not None
-    # and a safe one passes
+    # o200k: an upper-case run is split after its last Lo/Lm letter only if no
+    # lower-case letter follows the run ("中A." splits at 1, "中Ab" does not)
+    assert certificate_violation("\u4e2dAb", 1, "o200k", memo) is not None
+    # o200k: a symbol piece absorbs CR/LF and "/" after it
+    assert certificate_violation("x.\n/y", 3, "o200k", memo) is not None
+    # o200k: a mark extends the letters before it
+    assert certificate_violation("a\u0301b", 1, "o200k", memo) is not None
+    # and safe ones pass
     assert certificate_violation("ab.c", 2, "cl100k", memo) is None
+    assert certificate_violation("abCd", 2, "o200k", memo) is None
 
 
 def test_sync_boundaries_reject_invalid_neighbours():
