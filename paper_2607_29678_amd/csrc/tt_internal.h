@@ -54,6 +54,12 @@ __host__ __device__ inline uint64_t slot_key(uint32_t a, uint32_t b) {
   return (uint64_t)a | ((uint64_t)b << ID_BITS);
 }
 
+// A value that is the same in every lane of the wave, moved to a scalar
+// register (values read from LDS otherwise occupy a vector register per lane).
+__device__ __forceinline__ uint32_t wave_uniform(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)x);
+}
+
 // Bucket of a 32-bit hash among nb buckets: the high word of hash * nb (any
 // bucket count; the high bits of a multiplicative hash are the good ones).
 __host__ __device__ inline uint32_t bucket_of(uint32_t h, uint32_t nb) { return (uint32_t)(((uint64_t)h * nb) >> 32); }

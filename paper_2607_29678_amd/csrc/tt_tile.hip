@@ -288,7 +288,10 @@ __device__ uint32_t piece_find(const DevTables& tb, const uint8_t* buf, int64_t 
   return DICT_NONE;
 }
 
-constexpr int MED_CAP = PT_WIN / (SMALL_MAX + 1) + 2;  // units of 17..64 bytes in a tile
+constexpr int MED_CAP = PT_WIN / (SMALL_MAX + 1) + 2;  // units of 17..WAVE_MAX bytes in a tile
+// wave units are taken longest first, in classes of 8 bytes
+constexpr int MED_CLASSES = (WAVE_MAX - SMALL_MAX + 7) / 8;
+__device__ __forceinline__ uint32_t med_class(uint32_t L) { return (uint32_t)(WAVE_MAX - L) >> 3; }
 constexpr int BIG_CAP = PT_WIN / (WAVE_MAX + 1) + 2;   // longer units in a tile
 constexpr uint16_t U_INCOMING = 0xFFFFu;               // list entry for the incoming unit
 
@@ -335,7 +338,9 @@ struct PtShared {
   uint16_t med[MED_CAP];
   uint16_t big[BIG_CAP];
   uint32_t hist[SMALL_MAX + 1];  // small units per length, then where each length starts
+  uint32_t hmed[MED_CLASSES];    // wave units per length class, then where each class starts
   uint32_t n_small, n_med, n_big;
+  uint32_t med_next;             // next wave unit to take
   uint32_t wave_tot[PT_THREADS / 64];
   uint32_t tile;
   uint32_t inc_ids[SMALL_MAX];  // the incoming unit's tokens (thread engine)
@@ -483,6 +488,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   const int64_t n = w.n;
 
   if (tid <= SMALL_MAX) sh.hist[tid] = 0;
+  if (tid >= 64 && tid < 64 + MED_CLASSES) sh.hmed[tid - 64] = 0;
   if (IGN && tid < PT_WIN / 32) {
     sh.ph.a.nocut[tid] = 0;
     sh.whole[tid] = 0;
@@ -529,11 +535,12 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   if (tid == 0) {
     sh.tile = ticket - w.ticket_base;
     sh.n_med = 0;
+    sh.med_next = 0;
     sh.n_big = 0;
     sh.inc_cnt = 0;
   }
   __syncthreads();
-  const uint32_t t = sh.tile;
+  const uint32_t t = wave_uniform(sh.tile);
   const uint32_t n_tiles = w.n_tiles;
   if (t >= n_tiles) return;
   const int64_t t0 = (int64_t)t * PT_OWN;
@@ -1208,6 +1215,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (v < wave) wpre += sh.wave_tot[v];
     m += sh.wave_tot[v];
   }
+  wpre = wave_uniform(wpre);
+  m = wave_uniform(m);
   const uint32_t texcl = wpre + inc - cnt;  // unit starts before this thread's positions
 
   if (MODE == 0) {
@@ -1258,8 +1267,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   __syncthreads();
   // (only invalid input, whose text starts with a continuation byte, leaves
   // no unit start before the tile; its output is discarded)
-  const uint32_t s_prev = has_inc && sh.s_prev != NO_START ? sh.s_prev : 0u;
-  const uint32_t e_inc = m > 0 ? (uint32_t)(w0 + sh.ustart[0]) : (uint32_t)n;
+  const uint32_t s_prev = wave_uniform(has_inc && sh.s_prev != NO_START ? sh.s_prev : 0u);
+  const uint32_t e_inc = wave_uniform(m > 0 ? (uint32_t)(w0 + sh.ustart[0]) : (uint32_t)n);
   const uint32_t L_inc = has_inc ? e_inc - s_prev : 0u;
   auto byte_abs = [&](uint32_t p) -> uint32_t {
     const int64_t q = (int64_t)p - w0;
@@ -1273,12 +1282,12 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // bytes found in the whole-unit dictionaries.  Other units of 3..16 bytes go to
   // one thread each, counting-sorted by length, so that the threads of a wave
   // hold units of similar length (a wave runs as long as its longest unit).
-  // Units of 17..64 bytes go to one wave each, first to the waves that have no
-  // thread work, with no block barrier between the two, and longer units to
-  // the whole block.  The incoming unit is listed last.
+  // Units of 17..WAVE_MAX bytes go to one wave each, longest first, to the
+  // waves as they become free (no block barrier between the two engines), and
+  // longer units to the whole block.
   constexpr int UPT = (PT_OWN + 1 + PT_THREADS - 1) / PT_THREADS;  // units per thread
   const uint32_t U = m_proc + (has_inc ? 1u : 0u);
-  uint32_t mine[UPT];  // small units: (length << 16) | position within its length bucket
+  uint32_t mine[UPT];  // thread and wave units: (length << 16) | position within its length class
 #pragma unroll
   for (int r = 0; r < UPT; ++r) {
     mine[r] = 0;
@@ -1357,7 +1366,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       } else if (L <= (uint32_t)SMALL_MAX) {
         mine[r] = (L << 16) | atomicAdd(&sh.hist[L], 1u);
       } else if (L <= (uint32_t)WAVE_MAX) {
-        sh.med[atomicAdd(&sh.n_med, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
+        mine[r] = (L << 16) | atomicAdd(&sh.hmed[med_class(L)], 1u);
       } else {
         sh.big[atomicAdd(&sh.n_big, 1u)] = inc_u ? U_INCOMING : (uint16_t)u;
       }
@@ -1372,16 +1381,27 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       acc += c;
     }
     sh.n_small = acc;
+  } else if (tid == 64) {
+    uint32_t acc = 0;
+    for (int k = 0; k < MED_CLASSES; ++k) {
+      const uint32_t c = sh.hmed[k];
+      sh.hmed[k] = acc;
+      acc += c;
+    }
+    sh.n_med = acc;
   }
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < UPT; ++r) {
     if (mine[r] == 0) continue;
     const uint32_t u = (uint32_t)(tid + r * PT_THREADS);
-    sh.ph.b.small[sh.hist[mine[r] >> 16] + (mine[r] & 0xFFFFu)] = u == m_proc ? U_INCOMING : (uint16_t)u;
+    const uint16_t e = u == m_proc ? U_INCOMING : (uint16_t)u;
+    const uint32_t L = mine[r] >> 16, pos = mine[r] & 0xFFFFu;
+    if (L <= (uint32_t)SMALL_MAX) sh.ph.b.small[sh.hist[L] + pos] = e;
+    else sh.med[sh.hmed[med_class(L)] + pos] = e;
   }
   __syncthreads();
-  const uint32_t n_small = sh.n_small, n_med = sh.n_med;
+  const uint32_t n_small = wave_uniform(sh.n_small), n_med = wave_uniform(sh.n_med);
 
   // thread per unit, on the first TH_THREADS threads
   if (tid < TH_THREADS) {
@@ -1407,28 +1427,33 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     }
   }
 
-  // wave per unit: unit i runs on wave (first + i) mod 8, where the waves
-  // from `first` on have no thread work
+  // wave per unit: the units are taken longest first from a shared queue,
+  // each by the next wave that is free (the waves with thread work join when
+  // it is done), so that no wave runs two long units while another idles
   {
-    constexpr uint32_t NWV = PT_THREADS / 64;
-    const uint32_t busy = n_small >= (uint32_t)TH_THREADS ? TH_THREADS / 64 : (n_small + 63) / 64;
-    const uint32_t first = busy % NWV;
 #pragma unroll 1
-    for (uint32_t i = ((uint32_t)wave + NWV - first) % NWV; i < n_med; i += NWV) {
-      const uint32_t u = sh.med[i];
-      if (u == U_INCOMING) {
-        auto by = [&](int j) -> uint32_t { return inc_byte((uint32_t)j); };
-        auto ot = [&](int j, uint32_t id) { inc_out((uint32_t)j, id); };
-        const uint32_t c =
-            L_inc <= 64u ? bpe_wave(L_inc, by, tb, ot) : bpe_wave2(L_inc, by, tb, sh.ph.b.x.wscr[wave], ot);
-        if (lane == 0) sh.inc_cnt = c;
-      } else {
-        const uint32_t a = sh.ustart[u];
-        const uint32_t L = sh.ustart[u + 1] - a;
-        auto by = [&](int j) -> uint32_t { return sh.buf[PT_PAD + a + j]; };
-        auto ot = [&](int j, uint32_t id) { sh.ph.b.tok[a + j] = id; };
-        const uint32_t c = L <= 64u ? bpe_wave(L, by, tb, ot) : bpe_wave2(L, by, tb, sh.ph.b.x.wscr[wave], ot);
-        if (lane == 0) sh.ucnt[u] = (uint16_t)c;
+    for (;;) {
+      // all 64 lanes add one (no branch on the lane before the broadcast,
+      // which would make the loop exit divergent), so a wave's grab moves the
+      // counter by 64 and lane 0 reads a multiple of 64
+      const uint32_t i = wave_uniform(atomicAdd(&sh.med_next, 1u)) / 64u;
+      if (i >= n_med) break;
+      const uint32_t u = wave_uniform(sh.med[i]);
+      const bool inc_u = u == U_INCOMING;
+      const uint32_t a = inc_u ? 0u : sh.ustart[u];
+      const uint32_t L = inc_u ? L_inc : sh.ustart[u + 1] - a;
+      auto by = [&](int j) -> uint32_t {
+        return inc_u ? inc_byte((uint32_t)j) : (uint32_t)sh.buf[PT_PAD + a + (uint32_t)j];
+      };
+      auto ot = [&](int j, uint32_t id) {
+        if (inc_u) inc_out((uint32_t)j, id);
+        else sh.ph.b.tok[a + (uint32_t)j] = id;
+      };
+      uint32_t* scr = sh.ph.b.x.wscr[wave];
+      const uint32_t c = L <= 64u ? bpe_wave(L, by, tb, ot) : bpe_wave2(L, by, tb, scr, ot);
+      if (lane == 0) {
+        if (inc_u) sh.inc_cnt = c;
+        else sh.ucnt[u] = (uint16_t)c;
       }
     }
   }
