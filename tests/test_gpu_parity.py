@@ -47,11 +47,7 @@ def test_split_parity_config(gpu, k):
         k, d, got[d:d + 3], want[d:d + 3])
 
 
-BLOCK_ENGINE_STALL = ("the stress request has pieces over 512 bytes; the block BPE engine that takes them "
-                      "did not finish on the GPU and stays off the GPU until the cause is shown")
-
-
-@pytest.mark.parametrize("k", [1, 2, 3, 4, pytest.param(5, marks=pytest.mark.skip(reason=BLOCK_ENGINE_STALL))])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_id_parity_config(gpu, k):
     got = lib_tokenizer(k).encode(config_bytes(k)).tolist()
     want = _oracle_config_ids(k)
