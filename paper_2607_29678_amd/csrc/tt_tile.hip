@@ -291,6 +291,7 @@ __device__ uint32_t piece_find(const DevTables& tb, const uint8_t* buf, int64_t 
 constexpr int MED_CAP = PT_WIN / (SMALL_MAX + 1) + 2;  // units of 17..WAVE_MAX bytes in a tile
 // wave units are taken longest first, in classes of 8 bytes
 constexpr int MED_CLASSES = (WAVE_MAX - SMALL_MAX + 7) / 8;
+static_assert(SMALL_MAX < 64 && MED_CLASSES <= 64, "the start of each length (class) is one wave scan");
 __device__ __forceinline__ uint32_t med_class(uint32_t L) { return (uint32_t)(WAVE_MAX - L) >> 3; }
 constexpr int BIG_CAP = PT_WIN / (WAVE_MAX + 1) + 2;   // longer units in a tile
 constexpr uint16_t U_INCOMING = 0xFFFFu;               // list entry for the incoming unit
@@ -1373,22 +1374,20 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     }
   }
   __syncthreads();
-  if (tid == 0) {
-    uint32_t acc = 0;
-    for (int L = 3; L <= SMALL_MAX; ++L) {
-      const uint32_t c = sh.hist[L];
-      sh.hist[L] = acc;
-      acc += c;
-    }
-    sh.n_small = acc;
-  } else if (tid == 64) {
-    uint32_t acc = 0;
-    for (int k = 0; k < MED_CLASSES; ++k) {
-      const uint32_t c = sh.hmed[k];
-      sh.hmed[k] = acc;
-      acc += c;
-    }
-    sh.n_med = acc;
+  // where each length (class) starts: a wave scan over the counts (wave 0 for
+  // the thread units, wave 1 for the wave units)
+  if (wave == 0) {
+    const bool in = lane >= 3 && lane <= SMALL_MAX;
+    const uint32_t c = in ? sh.hist[lane] : 0u;
+    const uint32_t incl = wave_incl_sum(c);
+    if (in) sh.hist[lane] = incl - c;
+    if (lane == SMALL_MAX) sh.n_small = incl;
+  } else if (wave == 1) {
+    const bool in = lane < MED_CLASSES;
+    const uint32_t c = in ? sh.hmed[lane] : 0u;
+    const uint32_t incl = wave_incl_sum(c);
+    if (in) sh.hmed[lane] = incl - c;
+    if (lane == MED_CLASSES - 1) sh.n_med = incl;
   }
   __syncthreads();
 #pragma unroll
