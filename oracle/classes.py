@@ -13,6 +13,11 @@ treats combining marks as letter material; ``data/onig_o200k_classes.txt``
 holds those sub-classes (Lu|Lt, Ll, Lm|Lo, M), probed from the same engine by
 ``data/probe_onig_o200k.py``.
 
+The DeepSeek-style pattern also tests punctuation and symbols (``\\p{P}``,
+``\\p{S}``); ``data/onig_deepseek_classes.txt`` holds those code points, probed
+from the same engine by ``data/probe_onig_deepseek.py``, and its second
+splitter names the CJK ideograph, hiragana and katakana ranges directly.
+
 Parity pins: the whole table is compared with a fresh probe of the engine
 (tests), and the 25 whitespace code points are checked against the Unicode
 White_Space list written out in the test.
@@ -94,3 +99,34 @@ def o200k_class(cp: int) -> int:
 
 def o200k_classes_of(text: str) -> list:
     return [o200k_class(ord(c)) for c in text]
+
+
+# ---- DeepSeek-style: punctuation and symbols ------------------------------------
+DEEPSEEK_PATH = os.path.join(_HERE, "data", "onig_deepseek_classes.txt")
+
+
+def _load_deepseek():
+    table = bytearray(0x110000)  # 1 where \p{P} or \p{S}
+    with open(DEEPSEEK_PATH) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            a, b, k = line.split()
+            assert k == "PS"
+            for c in range(int(a, 16), int(b, 16) + 1):
+                table[c] = 1
+    return table
+
+
+PS_TABLE = _load_deepseek()
+
+
+def is_punct_or_symbol(cp: int) -> bool:
+    """\\p{P} or \\p{S} in the engine."""
+    return PS_TABLE[cp] != 0
+
+
+def is_mark(cp: int) -> bool:
+    """\\p{M} in the engine."""
+    return O200K_TABLE[cp] == MK

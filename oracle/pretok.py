@@ -41,18 +41,37 @@ contraction suffix of C1, optional here)
   P4  optional U+0020, "other" chars, then CR/LF and "/"  `` ?[^\\s\\p{L}\\p{N}]+[\\r\\n/]*``
   P5  = C5,  P6 = G5,  P7 = G6
 
+DeepSeek style (the paper: three splitters applied in sequence, each one
+re-splitting every piece of the previous stage, with unmatched stretches kept
+as pieces).  Each splitter isolates the leftmost matches of its regex in a
+piece, scanning from the piece start; the matches and the stretches between
+them are the next stage's pieces, and a regex sees the piece's end as the end
+of the text.  The splitters, in order:
+  S1  one to three numbers                                ``\\p{N}{1,3}``
+  S2  a run of CJK ideographs, hiragana or katakana       ``[\\u4E00-\\u9FA5\\u3040-\\u309F\\u30A0-\\u30FF]+``
+  S3  alternatives in order:
+      D1  one ASCII punctuation or symbol char, then ASCII letters
+                                                          ``[!-/:-@[-`{-~][A-Za-z]+``
+      D2  one optional char that is not CR/LF, letter, punctuation or symbol,
+          then letters and marks                          ``[^\\r\\n\\p{L}\\p{P}\\p{S}]?[\\p{L}\\p{M}]+``
+      D3  optional U+0020, punctuation and symbols, then CR/LF
+                                                          `` ?[\\p{P}\\p{S}]+[\\r\\n]*``
+      D4  = C5,  D5 = G5,  D6 = G6
+
 Readings taken where the paper is silent: ``\\s`` is the engine's whitespace
 class (25 code points), "space" in the optional-space alternatives is U+0020
 only, case-insensitive contractions use the engine's case folding (which maps
 U+017F to ``s``), and only U+0027 is an apostrophe.
 """
 
-from .classes import BO, LO, MK, UP, L, N, O, W, classes_of, folds_to, o200k_classes_of
+from .classes import (BO, LO, MK, UP, L, N, O, W, classes_of, folds_to, is_mark, is_punct_or_symbol,
+                      o200k_classes_of)
 
 GPT2 = "gpt2"
 CL100K = "cl100k"
 O200K = "o200k"
-PATTERNS = (GPT2, CL100K, O200K)
+DEEPSEEK = "deepseek"
+PATTERNS = (GPT2, CL100K, O200K, DEEPSEEK)
 
 SUFFIXES = ("s", "t", "re", "ve", "m", "ll", "d")
 SP = " "
@@ -240,9 +259,108 @@ def _o200k_at(text, cl, ol, p):
             or _ws(text, cl, p))
 
 
+# -- DeepSeek style: three splitters ---------------------------------------------
+
+ASCII_PUNCT = frozenset('!"#$%&\'()*+,-./:;<=>?@[\\]^_`{|}~')
+ASCII_LETTERS = frozenset("ABCDEFGHIJKLMNOPQRSTUVWXYZabcdefghijklmnopqrstuvwxyz")
+
+
+def in_kana_cjk(cp: int) -> bool:
+    """The second splitter's set: CJK ideographs U+4E00-9FA5, hiragana U+3040-309F, katakana U+30A0-30FF."""
+    return 0x4E00 <= cp <= 0x9FA5 or 0x3040 <= cp <= 0x30FF
+
+
+def _ds_numbers(text, cl, p, b):
+    """S1 ``\\p{N}{1,3}`` at p, inside [p, b)."""
+    e = p
+    while e < b and e - p < 3 and cl[e] == N:
+        e += 1
+    return e if e > p else None
+
+
+def _ds_kana_cjk(text, cl, p, b):
+    """S2: a run of the CJK/kana set at p, inside [p, b)."""
+    e = p
+    while e < b and in_kana_cjk(ord(text[e])):
+        e += 1
+    return e if e > p else None
+
+
+def _ds_main(text, cl, p, b):
+    """S3 at p, inside [p, b); b is the end of the text for the lookahead."""
+    def letter_or_mark(i):
+        return cl[i] == L or is_mark(ord(text[i]))
+
+    def ps(i):
+        return is_punct_or_symbol(ord(text[i]))
+
+    def run(i, pred):
+        while i < b and pred(i):
+            i += 1
+        return i
+
+    ch = text[p]
+    # D1: one ASCII punctuation or symbol char, then ASCII letters
+    if ch in ASCII_PUNCT and p + 1 < b and text[p + 1] in ASCII_LETTERS:
+        return run(p + 1, lambda i: text[i] in ASCII_LETTERS)
+    # D2: the optional prefix first, then without it
+    if ch not in NL and cl[p] != L and not ps(p):
+        e = run(p + 1, letter_or_mark)
+        if e > p + 1:
+            return e
+    e = run(p, letter_or_mark)
+    if e > p:
+        return e
+    # D3: optional U+0020, punctuation and symbols, then CR/LF
+    for st in ((p + 1, p) if ch == SP else (p,)):
+        e = run(st, ps)
+        if e > st:
+            return run(e, lambda i: text[i] in NL)
+    # D4-D6: whitespace
+    if cl[p] == W:
+        e = run(p, lambda i: cl[i] == W)
+        for j in range(e - 1, p - 1, -1):  # \s*[\r\n]+ ends after the last CR/LF of the run
+            if text[j] in NL:
+                return j + 1
+        for j in range(e, p, -1):  # \s+(?!\S)
+            if j == b or cl[j] == W:
+                return j
+        return e  # \s+
+    return None
+
+
+def _isolated(text, cl, spans, match_at):
+    """One splitter with the Isolated behaviour over each span: the leftmost
+    matches, scanning from the span start, and the stretches between them."""
+    out = []
+    for a, b in spans:
+        p = gap = a
+        while p < b:
+            e = match_at(text, cl, p, b)
+            if e is None:
+                p += 1
+                continue
+            if gap < p:
+                out.append((gap, p))
+            out.append((p, e))
+            p = gap = e
+        if gap < b:
+            out.append((gap, b))
+    return out
+
+
+def _deepseek(text, cl):
+    spans = [(0, len(text))] if text else []
+    for match_at in (_ds_numbers, _ds_kana_cjk, _ds_main):
+        spans = _isolated(text, cl, spans, match_at)
+    return spans
+
+
 def pretokenize(text: str, pattern: str) -> list:
     """Pieces of ``text`` as (start, end) character spans, in order, tiling the text."""
     cl = classes_of(text)
+    if pattern == DEEPSEEK:
+        return _deepseek(text, cl)
     if pattern == GPT2:
         step = _gpt2_at
     elif pattern == CL100K:
