@@ -66,9 +66,15 @@ enum {
  *                     \p{N}{1,3} | ?[^\s\p{L}\p{N}]+[\r\n/]* | \s*[\r\n]+ | \s+(?!\S) | \s+
  *                     with CT = (?i:'s|'t|'re|'ve|'m|'ll|'d) (Sec. 4.1: the o200k lineage's
  *                     case boundaries; marks are letter material here)
+ *  TT_PATTERN_DEEPSEEK: three splitters in sequence, each re-splitting every piece of the
+ *                     one before, unmatched stretches kept as pieces (Sec. 4.1, the DeepSeek
+ *                     family): \p{N}{1,3}; then [\u4E00-\u9FA5\u3040-\u309F\u30A0-\u30FF]+;
+ *                     then [ASCII punctuation or symbol][A-Za-z]+ |
+ *                     [^\r\n\p{L}\p{P}\p{S}]?[\p{L}\p{M}]+ | ?[\p{P}\p{S}]+[\r\n]* |
+ *                     \s*[\r\n]+ | \s+(?!\S) | \s+
  * Character classes are those of the Oniguruma engine of HF tokenizers 0.22.2
  * (the paper pins class tables probed from the reference engine, Sec. 4.1). */
-enum { TT_PATTERN_GPT2 = 0, TT_PATTERN_CL100K = 1, TT_PATTERN_O200K = 2 };
+enum { TT_PATTERN_GPT2 = 0, TT_PATTERN_CL100K = 1, TT_PATTERN_O200K = 2, TT_PATTERN_DEEPSEEK = 3 };
 
 typedef struct tt_tokenizer tt_tokenizer; /* opaque */
 

@@ -7,7 +7,7 @@ with token IDs identical to full reference tokenization.  This package holds
 the library sources (``csrc/``), its build script and a thin ctypes binding.
 """
 
-from .tokenizer import (CL100K, GPT2, O200K, PATTERNS, Session, Tokenizer, splice_plan,  # noqa: F401
+from .tokenizer import (CL100K, DEEPSEEK, GPT2, O200K, PATTERNS, Session, Tokenizer, splice_plan,  # noqa: F401
                         status_string, sync_boundaries)
 from ._lib import TokTierError  # noqa: F401
 

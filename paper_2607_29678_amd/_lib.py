@@ -14,6 +14,7 @@ TT_OK = 0
 TT_PATTERN_GPT2 = 0
 TT_PATTERN_CL100K = 1
 TT_PATTERN_O200K = 2
+TT_PATTERN_DEEPSEEK = 3
 TT_MAX_BYTES = 1 << 30
 
 STATUS = {

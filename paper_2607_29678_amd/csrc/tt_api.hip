@@ -590,7 +590,8 @@ int tt_create_ex(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_
                  tt_tokenizer** out) {
   if (!out || !vocab_offsets || (n_merges > 0 && !merges)) return TT_ERR_NULL_ARG;
   *out = nullptr;
-  if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K && pattern_id != TT_PATTERN_O200K) return TT_ERR_BAD_PATTERN;
+  if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K && pattern_id != TT_PATTERN_O200K &&
+      pattern_id != TT_PATTERN_DEEPSEEK) return TT_ERR_BAD_PATTERN;
   const bool ignore = opt && opt->ignore_merges != 0;
   // added tokens: non-empty, strict UTF-8, bounded, distinct, non-negative IDs
   AddedSet added;

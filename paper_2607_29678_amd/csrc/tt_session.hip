@@ -27,7 +27,9 @@
 #define TT_CLS_STORAGE static
 #include "class_table.inc"
 #include "class_table_o200k.inc"
+#include "class_table_deepseek.inc"
 #include "tt_internal.h"
+#include "tt_deepseek.h"
 #include "tt_o200k.h"
 
 namespace {
@@ -93,7 +95,7 @@ int decode_at(const uint8_t* s, int64_t n, int64_t i, uint32_t& cp) {
 // after a symbol when the head is not CR/LF), but a change between CR/LF and
 // other whitespace is not.
 //
-// o200k: see o2_sync.
+// o200k: see o2_sync.  DeepSeek: see ds_sync.
 bool sync_at(int pattern, const uint8_t* s, int64_t n, int64_t p) {
   if (p <= 0 || p >= n) return false;
   uint32_t cr = 0, cl = 0;
@@ -101,6 +103,8 @@ bool sync_at(int pattern, const uint8_t* s, int64_t n, int64_t p) {
   int64_t q = p - 1;  // lead byte of the character before p
   while (q > 0 && p - q < 4 && (s[q] & 0xC0u) == 0x80u) --q;
   if (decode_at(s, n, q, cl) != (int)(p - q)) return false;
+  if (pattern == TT_PATTERN_DEEPSEEK)
+    return tt::ds_sync(tt::ds_table_class(TT_DS_L1, TT_DS_L2, cl), tt::ds_table_class(TT_DS_L1, TT_DS_L2, cr));
   if (pattern == TT_PATTERN_O200K)
     return tt::o2_sync(tt::o2_table_class(TT_O2_L1, TT_O2_L2, cl), tt::o2_table_class(TT_O2_L1, TT_O2_L2, cr), cl, cr);
   const int x = host_class(cl), y = host_class(cr);
@@ -287,7 +291,8 @@ extern "C" {
 int tt_sync_boundaries(int32_t pattern_id, const uint8_t* utf8, int64_t len, uint8_t* out_mask) {
   if (len < 0) return TT_ERR_BAD_ARG;
   if (len > 0 && (!utf8 || !out_mask)) return TT_ERR_NULL_ARG;
-  if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K && pattern_id != TT_PATTERN_O200K) return TT_ERR_BAD_PATTERN;
+  if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K && pattern_id != TT_PATTERN_O200K &&
+      pattern_id != TT_PATTERN_DEEPSEEK) return TT_ERR_BAD_PATTERN;
   for (int64_t p = 0; p < len; ++p) out_mask[p] = sync_at(pattern_id, utf8, len, p) ? 1 : 0;
   return TT_OK;
 }
@@ -298,7 +303,8 @@ int tt_splice_plan(int32_t pattern_id, const uint8_t* text, int64_t len, int64_t
                    int64_t* from_f) {
   if (!text || !keep_c || !from_f || (n_c > 0 && (!c_ids || !c_spans)) || (n_f > 0 && (!f_ids || !f_spans)))
     return TT_ERR_NULL_ARG;
-  if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K && pattern_id != TT_PATTERN_O200K) return TT_ERR_BAD_PATTERN;
+  if (pattern_id != TT_PATTERN_GPT2 && pattern_id != TT_PATTERN_CL100K && pattern_id != TT_PATTERN_O200K &&
+      pattern_id != TT_PATTERN_DEEPSEEK) return TT_ERR_BAD_PATTERN;
   if (len <= 0 || a_len <= 0 || a_len > len || x <= 0 || x >= a_len || n_c < 0 || n_f < 0 || len > TT_MAX_BYTES)
     return TT_ERR_BAD_ARG;
   const Plan p = plan_splice(pattern_id, text, len, a_len, x, c_ids, c_spans, n_c, f_ids, f_spans, n_f,

@@ -41,8 +41,10 @@
 // wait for before it waits on anything itself.
 #include "class_table.inc"
 #include "class_table_o200k.inc"
+#include "class_table_deepseek.inc"
 #include "tt_bpe.h"
 #include "tt_internal.h"
+#include "tt_deepseek.h"
 #include "tt_o200k.h"
 
 namespace tt {
@@ -75,9 +77,12 @@ struct ClassLds {
 
 // The o200k-style pattern's 4-bit class table, staged in LDS by every block
 // of that pattern, and the code of every ASCII character.
+// the 4-bit tables of the patterns whose pieces are walked (o200k-style,
+// DeepSeek-style): same layout, room for the larger
+constexpr int WALK_NBLOCKS = TT_O2_NBLOCKS > TT_DS_NBLOCKS ? TT_O2_NBLOCKS : TT_DS_NBLOCKS;
 struct O2Lds {
   uint8_t l1[4352] __attribute__((aligned(16)));
-  uint8_t l2[TT_O2_NBLOCKS * 128] __attribute__((aligned(16)));
+  uint8_t l2[WALK_NBLOCKS * 128] __attribute__((aligned(16)));
   uint8_t asc[128];
 };
 
@@ -117,6 +122,19 @@ __device__ __forceinline__ uint32_t o2_code(const O2Lds& t, uint32_t cp) {
     return O2_O;
   }
   return o2_table_class(t.l1, t.l2, cp);
+}
+
+// Code of one code point for the DeepSeek-style pattern: its class only.
+// ASCII classes are computed: the ASCII table is built while the class table
+// is still being staged.
+__device__ __forceinline__ uint32_t ds_code(const O2Lds& t, uint32_t cp) {
+  return cp < 128u ? ds_ascii_class(cp) : ds_table_class(t.l1, t.l2, cp);
+}
+
+// Code of a code point for a walked pattern.
+template <int PAT>
+__device__ __forceinline__ uint32_t walk_code(const O2Lds& t, uint32_t cp) {
+  return PAT == TT_PATTERN_DEEPSEEK ? ds_code(t, cp) : o2_code(t, cp);
 }
 
 template <int PAT>
@@ -494,7 +512,9 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     sh.ph.a.nocut[tid] = 0;
     sh.whole[tid] = 0;
   }
-  constexpr bool O2 = PAT == TT_PATTERN_O200K;
+  // the patterns whose pieces are walked between synchronizing positions
+  constexpr bool DS = PAT == TT_PATTERN_DEEPSEEK;
+  constexpr bool O2 = PAT == TT_PATTERN_O200K || DS;
   if (O2 && tid < PT_WIN / 32) sh.ph.a.o2seg[tid] = 0;
   // the ticket's round trip (tickets are handed out one at a time) overlaps
   // the staging of the tables, which do not depend on the tile
@@ -504,16 +524,16 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     // the class table (12.9 KB) is read once per block
     static_assert(CLS_L1_BYTES % 16 == 0 && CLS_L2_BYTES % 16 == 0, "class table staging uses 16-byte words");
     if (O2) {
-      constexpr int N1 = 4352 / 16, N2 = TT_O2_NBLOCKS * 128 / 16;
-      const uint4* s1 = reinterpret_cast<const uint4*>(TT_O2_L1);
-      const uint4* s2 = reinterpret_cast<const uint4*>(TT_O2_L2);
+      constexpr int N1 = 4352 / 16, N2 = (DS ? TT_DS_NBLOCKS : TT_O2_NBLOCKS) * 128 / 16;
+      const uint4* s1 = reinterpret_cast<const uint4*>(DS ? TT_DS_L1 : TT_O2_L1);
+      const uint4* s2 = reinterpret_cast<const uint4*>(DS ? TT_DS_L2 : TT_O2_L2);
       uint4* d1 = reinterpret_cast<uint4*>(sh.ph.a.o2.l1);
       uint4* d2 = reinterpret_cast<uint4*>(sh.ph.a.o2.l2);
       for (int i = tid; i < N1 + N2; i += PT_THREADS) {
         if (i < N1) d1[i] = s1[i];
         else d2[i - N1] = s2[i - N1];
       }
-      if (tid < 128) sh.ph.a.o2.asc[tid] = (uint8_t)o2_code(sh.ph.a.o2, (uint32_t)tid);
+      if (tid < 128) sh.ph.a.o2.asc[tid] = (uint8_t)walk_code<PAT>(sh.ph.a.o2, (uint32_t)tid);
     } else {
       constexpr int N1 = CLS_L1_BYTES / 16, N2 = CLS_L2_BYTES / 16;
       const uint4* s1 = reinterpret_cast<const uint4*>(TT_CLS_L1);
@@ -693,7 +713,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
           claimed = claimed || (!blocked && ok && !c && ll > (uint32_t)k);
           blocked = blocked || !ok || !c || dst(j - k);
         }
-        const uint32_t code = O2 ? ((!in_j || cont) ? O2_NONE : len == 0u ? O2_O : o2_code(sh.ph.a.o2, cp))
+        const uint32_t code = O2 ? ((!in_j || cont) ? O2_NONE : len == 0u ? O2_O : walk_code<PAT>(sh.ph.a.o2, cp))
                                  : (!in_j || cont) ? C_NONE : len == 0u ? C_O : char_code_sel<PAT>(sh.ph.a.cls, cp);
         bad = bad || (own && (cont ? !claimed : len == 0u));
         codes |= (code | (dst(j) ? CODE_DOCSTART : 0u)) << (8 * j);
@@ -978,10 +998,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // back), whitespace after CR/LF and a letter after a lone symbol branch.
   uint32_t flags = 0;
   if (O2) {
-    // o200k: segment starts are document starts and synchronizing positions
-    // (their two neighbouring characters form a transition of o2_sync); the
-    // pieces of a segment come from running the pattern's alternatives from
-    // its start, one thread per segment
+    // o200k- and DeepSeek-style: segment starts are document starts and
+    // synchronizing positions (their two neighbouring characters form a
+    // transition of o2_sync or ds_sync); the pieces of a segment come from
+    // running the pattern's alternatives from its start, one thread per segment
     uint32_t seg = 0;
 #pragma unroll
     for (int j = 0; j < PT_BPT; ++j) {
@@ -996,7 +1016,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
           if ((cr(j - d) & 15u) != O2_NONE) k = d;
         if (k > 0 && q - k >= 0) {
           const uint32_t bx = sh.buf[PT_PAD + q - k];
-          st = o2_sync(cr(j - k) & 15u, c & 15u, k == 1 ? bx : 0x80u, sh.buf[PT_PAD + q]);
+          st = DS ? ds_sync(cr(j - k) & 15u, c & 15u)
+                  : o2_sync(cr(j - k) & 15u, c & 15u, k == 1 ? bx : 0x80u, sh.buf[PT_PAD + q]);
         }
       }
       if (st) seg |= 1u << j;
@@ -1043,7 +1064,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     while (active) {
       if (s >= PT_HALO) sh.ph.a.o2piece[s] = 1;  // (s < own_end <= PT_WIN)
       if (on_first) first_end = s;
-      const int64_t e = o2_piece_end(v, s);
+      const int64_t e = DS ? ds_piece_end(v, s) : o2_piece_end(v, s);
       if (e < own_end && !segbit(e)) {
         s = e;
       } else if (todo) {
@@ -1676,6 +1697,7 @@ hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode
     case TT_PATTERN_GPT2: return launch_pat<TT_PATTERN_GPT2>(w, tb, mode, batch, ignore, s);
     case TT_PATTERN_CL100K: return launch_pat<TT_PATTERN_CL100K>(w, tb, mode, batch, ignore, s);
     case TT_PATTERN_O200K: return launch_pat<TT_PATTERN_O200K>(w, tb, mode, batch, ignore, s);
+    case TT_PATTERN_DEEPSEEK: return launch_pat<TT_PATTERN_DEEPSEEK>(w, tb, mode, batch, ignore, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -16,7 +16,8 @@ from . import _lib
 GPT2 = _lib.TT_PATTERN_GPT2
 CL100K = _lib.TT_PATTERN_CL100K
 O200K = _lib.TT_PATTERN_O200K
-PATTERNS = {"gpt2": GPT2, "cl100k": CL100K, "o200k": O200K}
+DEEPSEEK = _lib.TT_PATTERN_DEEPSEEK
+PATTERNS = {"gpt2": GPT2, "cl100k": CL100K, "o200k": O200K, "deepseek": DEEPSEEK}
 
 
 def _ptr(x):

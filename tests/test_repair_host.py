@@ -29,7 +29,12 @@ ALPHA = {
     "cl100k": list("aS1 \n\t'.rl") + ["\r", "ſ", " "],
     # upper, lower, Lo, Lm, a mark, "/" (absorbed after CR/LF by symbol pieces)
     "o200k": list("aS1 \n\t'./") + ["\u4e2d", "\u02b0", "\u0301", "\r"],
+    # ASCII and other letters, a mark, a number, ASCII and other punctuation,
+    # U+0020, tab, LF, a control char, and letter, mark, symbol and unassigned
+    # code point of the CJK/kana ranges
+    "deepseek": list("a1. \t\n\x01") + ["\u00e9", "\u0301", "\u3002", "\u4e2d", "\u3099", "\u309b", "\u3040"],
 }
+MAX_LEN = {"gpt2": 5, "cl100k": 5, "o200k": 5, "deepseek": 4}
 EXTRA = ["中", "。", "²", "\U0001f600", "́", "　", "\u0085", "А", "\u00c9", "\u01c5", "\u02b0", "/", "T", "D"]
 
 
@@ -84,19 +89,20 @@ def _check_string(text, pattern, memo):
     return hits
 
 
-@pytest.mark.parametrize("pattern", ["gpt2", "cl100k", "o200k"])
+@pytest.mark.parametrize("pattern", ["gpt2", "cl100k", "o200k", "deepseek"])
 def test_sync_boundaries_exhaustive_short_strings(pattern):
-    """Every string of up to 5 characters over the alphabet: each position the
-    library calls synchronizing is a certificate for every split."""
+    """Every string of up to 5 characters over the alphabet (4 for the
+    DeepSeek-style alphabet of 14): each position the library calls
+    synchronizing is a certificate for every split."""
     memo = {}
     hits = 0
-    for n in range(2, 6):
+    for n in range(2, MAX_LEN[pattern] + 1):
         for tup in itertools.product(ALPHA[pattern], repeat=n):
             hits += _check_string("".join(tup), pattern, memo)
     assert hits > 10000  # the sets are not empty
 
 
-@pytest.mark.parametrize("pattern", ["gpt2", "cl100k", "o200k"])
+@pytest.mark.parametrize("pattern", ["gpt2", "cl100k", "o200k", "deepseek"])
 def test_sync_boundaries_random_strings(pattern):
     rng = random.Random(0x5A11 + len(pattern))
     alphabet = ALPHA[pattern] + EXTRA + ["a"] * 6 + ["1"] * 4 + [" "] * 4
@@ -130,7 +136,12 @@ def test_certificate_checker_catches_unsafe_transitions():
     assert certificate_violation("x.\n/y", 3, "o200k", memo) is not None
     # o200k: a mark extends the letters before it
     assert certificate_violation("a\u0301b", 1, "o200k", memo) is not None
+    # DeepSeek: ASCII punctuation takes the ASCII letters after it
+    assert certificate_violation("x.ab", 2, "deepseek", memo) is not None
+    # DeepSeek: a punctuation run takes the CR/LF after it
+    assert certificate_violation("a.\nb", 2, "deepseek", memo) is not None
     # and safe ones pass
+    assert certificate_violation(".\u00e9", 1, "deepseek", memo) is None
     assert certificate_violation("ab.c", 2, "cl100k", memo) is None
     assert certificate_violation("abCd", 2, "o200k", memo) is None
 
