@@ -17,7 +17,7 @@ resident) and the host-to-host time of a 64 x 16,384-char document batch are
 reported separately, and so are the append latency of incremental-repair
 sessions at 100,000 and 1,000,000 characters and the latency of the two
 front-end options (ignore_merges, added-token literals) and of the
-o200k-style pattern.  The CPU oracle is
+o200k-style and DeepSeek-style patterns.  The CPU oracle is
 timed on the same timed samples, one thread pinned to one core, and its IDs
 are compared with the GPU's.
 
@@ -186,8 +186,9 @@ def front_end_options(sid, n=10):
                        % (len(texts[0].split(b"<|im_")) - 1, len(texts[0])),
            "host_to_host_p50_ms_literal_handle": res["literals"],
            "host_to_host_p50_ms_same_text_plain_handle": res["no_literals"]}
-    # the o200k-style pattern (no table of its own: the multilingual table
-    # serves it), against cl100k-style on the same samples and table
+    # the o200k-style and DeepSeek-style patterns (no table of their own: the
+    # multilingual table serves them), against cl100k-style on the same
+    # samples and table
     m, vb, vo = load_table(4)
     o2 = {}
     for k in (3, 4):
@@ -195,7 +196,7 @@ def front_end_options(sid, n=10):
         d_in = [torch.from_numpy(np.frombuffer(t, dtype=np.uint8).copy()).to(dev) for t in texts]
         d_out = torch.empty(max(len(t) for t in texts), dtype=torch.int32, device=dev)
         row = {}
-        for pat in ("cl100k", "o200k"):
+        for pat in ("cl100k", "o200k", "deepseek"):
             tok = Tokenizer(m, vb, vo, pat)
             lat = []
             for i in range(n + 2):
@@ -210,7 +211,7 @@ def front_end_options(sid, n=10):
             tok.close()
         o2["C%d_samples" % k] = row
     o2["table"] = "C4 (100,000 merges)"
-    return {"ignore_merges": ign, "added_tokens": lit, "o200k_pattern": o2}
+    return {"ignore_merges": ign, "added_tokens": lit, "other_patterns": o2}
 
 
 def main():
