@@ -1270,9 +1270,19 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // that ends at its first unit start.
   const bool has_inc = t > 0 && (m > 0 || last);
   const uint32_t m_proc = last ? m : (m > 0 ? m - 1 : 0);
-  if (tid == 0 && has_inc) {
-    // the incoming unit starts at the last unit start of the nearest earlier
-    // tile that has one (usually the previous tile)
+  __syncthreads();
+  const uint32_t e_inc = wave_uniform(m > 0 ? (uint32_t)(w0 + sh.ustart[0]) : (uint32_t)n);
+  auto byte_abs = [&](uint32_t p) -> uint32_t {
+    const int64_t q = (int64_t)p - w0;
+    return (q >= -PT_PAD && q < PT_WIN + 16) ? (uint32_t)sh.buf[PT_PAD + q] : (uint32_t)w.text[p];
+  };
+  // The incoming unit starts at the last unit start of the nearest earlier
+  // tile that has one (usually the previous tile).  Only the thread that
+  // dispatches it waits for that word; the others dispatch their own units
+  // meanwhile.  (Only invalid input, whose text starts with a continuation
+  // byte, leaves no unit start before the tile; its output is discarded.)
+  uint32_t sp_own = 0;
+  if (has_inc && (uint32_t)tid == m_proc % (uint32_t)PT_THREADS) {
     uint32_t found = NO_START;
     for (int64_t j = (int64_t)t - 1; j >= 0; --j) {
       uint64_t x;
@@ -1285,19 +1295,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       }
     }
     sh.s_prev = found;
+    sp_own = found != NO_START ? found : 0u;
   }
-  __syncthreads();
-  // (only invalid input, whose text starts with a continuation byte, leaves
-  // no unit start before the tile; its output is discarded)
-  const uint32_t s_prev = wave_uniform(has_inc && sh.s_prev != NO_START ? sh.s_prev : 0u);
-  const uint32_t e_inc = wave_uniform(m > 0 ? (uint32_t)(w0 + sh.ustart[0]) : (uint32_t)n);
-  const uint32_t L_inc = has_inc ? e_inc - s_prev : 0u;
-  auto byte_abs = [&](uint32_t p) -> uint32_t {
-    const int64_t q = (int64_t)p - w0;
-    return (q >= -PT_PAD && q < PT_WIN + 16) ? (uint32_t)sh.buf[PT_PAD + q] : (uint32_t)w.text[p];
-  };
-  auto inc_byte = [&](uint32_t j) -> uint32_t { return byte_abs(s_prev + j); };
-  auto inc_out = [&](uint32_t j, uint32_t id) { w.stage[s_prev + j] = id; };
+  auto inc_byte_own = [&](uint32_t j) -> uint32_t { return byte_abs(sp_own + j); };
+  auto inc_out_own = [&](uint32_t j, uint32_t id) { w.stage[sp_own + j] = id; };
 
   // ---- BPE dispatch ---------------------------------------------------------
   // Units of one or two bytes are finished here, and so are units of up to 24
@@ -1317,7 +1318,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (u >= U) continue;
     const bool inc_u = u == m_proc;
     const uint32_t a = inc_u ? 0u : sh.ustart[u];
-    const uint32_t L = inc_u ? L_inc : sh.ustart[u + 1] - a;
+    const uint32_t L = inc_u ? e_inc - sp_own : sh.ustart[u + 1] - a;
     if (IGN) {
       // a piece found in the vocabulary (its ID was staged at its first byte);
       // the incoming unit is a whole piece and is probed here
@@ -1325,11 +1326,11 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       if (!inc_u && ((sh.whole[a >> 5] >> (a & 31u)) & 1u)) {
         id = w.stage[w0 + a];
       } else if (inc_u && L >= 2u && L <= tb.vmax) {
-        id = piece_find(tb, sh.buf, (int64_t)s_prev - w0, L, [&](uint32_t j) -> uint32_t { return inc_byte(j); });
+        id = piece_find(tb, sh.buf, (int64_t)sp_own - w0, L, [&](uint32_t j) -> uint32_t { return inc_byte_own(j); });
       }
       if (id != DICT_NONE) {
         if (inc_u) {
-          inc_out(0, id);
+          inc_out_own(0, id);
           sh.inc_cnt = 1;
         } else {
           sh.ph.b.tok[a] = id;
@@ -1339,10 +1340,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       }
     }
     if (L <= 2u) {
-      const uint32_t b0 = inc_u ? inc_byte(0) : sh.buf[PT_PAD + a];
+      const uint32_t b0 = inc_u ? inc_byte_own(0) : sh.buf[PT_PAD + a];
       uint32_t c = 1, t0 = b0, t1 = 0;
       if (L == 2u) {
-        const uint32_t b1 = inc_u ? inc_byte(1) : sh.buf[PT_PAD + a + 1];
+        const uint32_t b1 = inc_u ? inc_byte_own(1) : sh.buf[PT_PAD + a + 1];
         const uint32_t r2 = tb.pair0[(b0 << 8) | b1];
         if (r2 != RANK_INF) {
           t0 = 256u + r2;
@@ -1352,8 +1353,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         }
       }
       if (inc_u) {
-        inc_out(0, t0);
-        if (c == 2) inc_out(1, t1);
+        inc_out_own(0, t0);
+        if (c == 2) inc_out_own(1, t1);
         sh.inc_cnt = c;
       } else {
         sh.ph.b.tok[a] = t0;
@@ -1365,7 +1366,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       // are in the window (an incoming unit this short ends at the tile's
       // first unit start, so it starts at least PT_HALO - 24 bytes into it).
       uint32_t found = DICT_NONE;
-      const int64_t aw = inc_u ? (int64_t)s_prev - w0 : (int64_t)a;
+      const int64_t aw = inc_u ? (int64_t)sp_own - w0 : (int64_t)a;
       if (L <= (uint32_t)DICT2_MAX && aw >= 0 && aw + DICT2_MAX + 4 <= PT_WIN + 16) {
         if (L <= (uint32_t)DICT_MAX) {
           uint32_t kw[3];
@@ -1379,7 +1380,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       }
       if (found != DICT_NONE) {
         if (inc_u) {
-          inc_out(0, found);
+          inc_out_own(0, found);
           sh.inc_cnt = 1;
         } else {
           sh.ph.b.tok[a] = found;
@@ -1395,6 +1396,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     }
   }
   __syncthreads();
+  const uint32_t s_prev = wave_uniform(has_inc && sh.s_prev != NO_START ? sh.s_prev : 0u);
+  const uint32_t L_inc = has_inc ? e_inc - s_prev : 0u;
+  auto inc_byte = [&](uint32_t j) -> uint32_t { return byte_abs(s_prev + j); };
+  auto inc_out = [&](uint32_t j, uint32_t id) { w.stage[s_prev + j] = id; };
   // where each length (class) starts: a wave scan over the counts (wave 0 for
   // the thread units, wave 1 for the wave units)
   if (wave == 0) {
