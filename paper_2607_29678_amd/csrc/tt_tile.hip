@@ -75,10 +75,9 @@ struct ClassLds {
   uint8_t asc[128];
 };
 
-// The o200k-style pattern's 4-bit class table, staged in LDS by every block
-// of that pattern, and the code of every ASCII character.
-// the 4-bit tables of the patterns whose pieces are walked (o200k-style,
-// DeepSeek-style): same layout, room for the larger
+// The 4-bit class table of a pattern whose pieces are walked (o200k-style,
+// DeepSeek-style; same layout, room for the larger), staged in LDS by every
+// block of that pattern, and the code of every ASCII character.
 constexpr int WALK_NBLOCKS = TT_O2_NBLOCKS > TT_DS_NBLOCKS ? TT_O2_NBLOCKS : TT_DS_NBLOCKS;
 struct O2Lds {
   uint8_t l1[4352] __attribute__((aligned(16)));
@@ -321,15 +320,15 @@ union PhaseMem {
   struct {
     union {
       ClassLds cls;           // character classes (GPT-2, cl100k)
-      O2Lds o2;               // character classes (o200k)
+      O2Lds o2;               // character classes (o200k, DeepSeek)
     };
     uint32_t join[2048];      // junction byte pairs of the merges
     uint8_t code[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));  // class/identity/doc-start codes
     union {
       int16_t run_end[PT_WIN];  // cl100k: window index of the head after a run's head
-      uint8_t o2piece[PT_WIN];  // o200k: 1 at the piece starts the walks find
+      uint8_t o2piece[PT_WIN];  // walked patterns: 1 at the piece starts the walks find
     };
-    uint32_t o2seg[PT_WIN / 32];    // o200k: segment starts (synchronizing positions, document starts)
+    uint32_t o2seg[PT_WIN / 32];    // walked patterns: segment starts (synchronizing positions, document starts)
     uint32_t nocut[PT_WIN / 32];    // ignore_merges: window positions no junction cut may split
   } a;
   struct {
@@ -370,7 +369,7 @@ struct PtShared {
   uint32_t carry_n;           // cl100k: number-run chars before the tile, mod 3
   uint32_t carry_nlpre;       // cl100k: class before a CR/LF stretch entering the tile
   uint32_t cwave[PT_THREADS / 64];  // span export: per-wave sums
-  int64_t o2_doc_after;          // o200k, batch: first document start after the window
+  int64_t o2_doc_after;          // walked patterns, batch: first document start after the window
   uint32_t whole[PT_WIN / 32];  // ignore_merges: starts of pieces that are vocabulary entries
   uint32_t cbase;             // span export: non-continuation bytes before the tile
   uint32_t ctile;             // span export: non-continuation bytes the tile owns
@@ -514,8 +513,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   }
   // the patterns whose pieces are walked between synchronizing positions
   constexpr bool DS = PAT == TT_PATTERN_DEEPSEEK;
-  constexpr bool O2 = PAT == TT_PATTERN_O200K || DS;
-  if (O2 && tid < PT_WIN / 32) sh.ph.a.o2seg[tid] = 0;
+  constexpr bool WALK = PAT == TT_PATTERN_O200K || DS;
+  if (WALK && tid < PT_WIN / 32) sh.ph.a.o2seg[tid] = 0;
   // the ticket's round trip (tickets are handed out one at a time) overlaps
   // the staging of the tables, which do not depend on the tile
   uint32_t ticket = 0;
@@ -523,7 +522,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   {
     // the class table (12.9 KB) is read once per block
     static_assert(CLS_L1_BYTES % 16 == 0 && CLS_L2_BYTES % 16 == 0, "class table staging uses 16-byte words");
-    if (O2) {
+    if (WALK) {
       constexpr int N1 = 4352 / 16, N2 = (DS ? TT_DS_NBLOCKS : TT_O2_NBLOCKS) * 128 / 16;
       const uint4* s1 = reinterpret_cast<const uint4*>(DS ? TT_DS_L1 : TT_O2_L1);
       const uint4* s2 = reinterpret_cast<const uint4*>(DS ? TT_DS_L2 : TT_O2_L2);
@@ -616,7 +615,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         else hi = mid;
       }
       sh.doc_lo_idx = lo;
-      if (O2) {
+      if (WALK) {
         int a = lo, b = w.n_docs;  // first document start >= w0 + PT_WIN
         while (a < b) {
           int mid = (a + b) >> 1;
@@ -669,7 +668,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (SPANS) nc_own = own_noncont(bw1, q0, p0);
     uint32_t codes;
     if ((bw1 & 0x80808080u) == 0u && p0 >= 0 && p0 + PT_BPT <= n) {
-      const uint8_t* asc = O2 ? sh.ph.a.o2.asc : sh.ph.a.cls.asc;
+      const uint8_t* asc = WALK ? sh.ph.a.o2.asc : sh.ph.a.cls.asc;
       codes = (uint32_t)asc[bw1 & 255u] | ((uint32_t)asc[(bw1 >> 8) & 255u] << 8) |
               ((uint32_t)asc[(bw1 >> 16) & 255u] << 16) | ((uint32_t)asc[bw1 >> 24] << 24);
       codes |= (dw1 & 0x01010101u) << 7;  // document starts (flags are 0 or 1)
@@ -713,7 +712,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
           claimed = claimed || (!blocked && ok && !c && ll > (uint32_t)k);
           blocked = blocked || !ok || !c || dst(j - k);
         }
-        const uint32_t code = O2 ? ((!in_j || cont) ? O2_NONE : len == 0u ? O2_O : walk_code<PAT>(sh.ph.a.o2, cp))
+        const uint32_t code = WALK ? ((!in_j || cont) ? O2_NONE : len == 0u ? O2_O : walk_code<PAT>(sh.ph.a.o2, cp))
                                  : (!in_j || cont) ? C_NONE : len == 0u ? C_O : char_code_sel<PAT>(sh.ph.a.cls, cp);
         bad = bad || (own && (cont ? !claimed : len == 0u));
         codes |= (code | (dst(j) ? CODE_DOCSTART : 0u)) << (8 * j);
@@ -722,13 +721,13 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     *reinterpret_cast<uint32_t*>(&sh.ph.a.code[PT_PAD + q0]) = codes;
     if (tid < 3) {  // positions outside [0, PT_WIN) carry no character for the rules
       const int qx = tid == 0 ? -8 : PT_WIN + 8 * (tid - 1);
-      const uint32_t none4 = O2 ? 0x0F0F0F0Fu : 0x07070707u;
+      const uint32_t none4 = WALK ? 0x0F0F0F0Fu : 0x07070707u;
       *reinterpret_cast<uint2*>(&sh.ph.a.code[PT_PAD + qx]) = make_uint2(none4, none4);
     }
   }
   if (PAT == TT_PATTERN_CL100K)
     for (int q = tid; q < PT_WIN; q += PT_THREADS) sh.ph.a.run_end[q] = -1;
-  if (O2) *reinterpret_cast<uint32_t*>(&sh.ph.a.o2piece[tid * PT_BPT]) = 0u;
+  if (WALK) *reinterpret_cast<uint32_t*>(&sh.ph.a.o2piece[tid * PT_BPT]) = 0u;
   if (SPANS) {
     const uint32_t nc_incl = wave_incl_sum(nc_own);
     if (lane == 63) sh.cwave[wave] = nc_incl;
@@ -997,7 +996,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // cheap cases are selects; contractions (an apostrophe one to three bytes
   // back), whitespace after CR/LF and a letter after a lone symbol branch.
   uint32_t flags = 0;
-  if (O2) {
+  if (WALK) {
     // o200k- and DeepSeek-style: segment starts are document starts and
     // synchronizing positions (their two neighbouring characters form a
     // transition of o2_sync or ds_sync); the pieces of a segment come from
@@ -1097,7 +1096,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   }
   uint32_t scan_st = s0;  // cl100k: scan state before position q
 #pragma unroll
-  for (int j = 0; j < (O2 ? 0 : PT_BPT); ++j) {
+  for (int j = 0; j < (WALK ? 0 : PT_BPT); ++j) {
     const int q = qb + j;
     const uint32_t ex = scan_st;
     if (PAT == TT_PATTERN_CL100K) scan_st = seg_combine(scan_st, elems[j]);
