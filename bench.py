@@ -13,13 +13,14 @@ Per-request latencies (enqueue to completion, input in HBM) give P50/P90/P99
 in a second pass; the host-to-host latency through ``tt_encode`` (PCIe copies
 included), a steady-state P50 (100 re-encodes of one sample), the P50 of the
 same requests with span export (IDs plus byte and character spans, device
-resident) and the host-to-host time of a 64 x 16,384-char document batch are
-reported separately, and so are the append latency of incremental-repair
-sessions at 100,000 and 1,000,000 characters and the latency of the two
-front-end options (ignore_merges, added-token literals) and of the
-o200k-style and DeepSeek-style patterns.  The CPU oracle is
-timed on the same timed samples, one thread pinned to one core, and its IDs
-are compared with the GPU's.
+resident), the P50 of all timed samples joined into one request (many tiles
+per resident slot: the throughput with the chip full) and the host-to-host
+time of a 64 x 16,384-char document batch are reported separately, and so
+are the append latency of incremental-repair sessions at 100,000 and
+1,000,000 characters and the latency of the two front-end options
+(ignore_merges, added-token literals) and of the o200k-style and
+DeepSeek-style patterns.  The CPU oracle is timed on the same timed samples,
+one thread pinned to one core, and its IDs are compared with the GPU's.
 
 ``--calibrate-copy`` first runs a plain int32 copy kernel of 64 MiB read +
 64 MiB written, so that a hardware-counter profile of this command can scale
@@ -330,6 +331,32 @@ def main():
     n_pieces = len(starts)
     longest_piece = int(np.max(np.diff(np.append(starts, len(texts[timed[0]]))))) if n_pieces else 0
 
+    # --- throughput with the chip full: the timed samples as one request -------
+    # (a 1,000,000-char request fills about two thirds of the resident tile
+    # slots once, so its time is one tile's latency; a request of all timed
+    # samples runs many tiles per slot)
+    big = b"".join(texts[i] for i in timed)
+    d_big = torch.from_numpy(np.frombuffer(big, dtype=np.uint8).copy()).to(dev)
+    d_bout = torch.empty(len(big), dtype=torch.int32, device=dev)
+    d_blen = torch.zeros(1, dtype=torch.int64, device=dev)
+    tok.encode_device(d_big, len(big), d_bout, d_blen, sid)
+    torch.cuda.synchronize()
+    big_lat = []
+    for _ in range(10):
+        a = time.perf_counter()
+        tok.encode_device(d_big, len(big), d_bout, d_blen, sid)
+        stream.synchronize()
+        big_lat.append((time.perf_counter() - a) * 1e3)
+    big_T = int(d_blen.item())
+    if big_T <= 0:
+        raise SystemExit("tokenizer reported an error on the joined request: %d" % big_T)
+    big_chars = sum(n_chars[i] for i in timed)
+    big_ms = percentile(big_lat, 50)
+    large_request = {"chars": big_chars, "bytes": len(big), "tokens": big_T, "p50_ms": round(big_ms, 4),
+                     "chars_per_s": round(big_chars / (big_ms * 1e-3), 1),
+                     "hbm_frac": round((len(big) + 4.0 * big_T) / (big_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)}
+    del d_big, d_bout
+
     # --- a batch of 64 independent 16,384-char documents (the stress config's
     # batch, its own tokenizer), host to host through tt_encode_batch -----------
     bmerges, bvb, bvo = load_table(5)
@@ -427,6 +454,7 @@ def main():
         "host_to_host_p50_ms": round(percentile(host_lat, 50), 4),
         "steady_state_p50_ms": round(percentile(steady, 50), 4),
         "span_export_p50_ms": round(percentile(span_lat, 50), 4),
+        "large_request": large_request,
         "batch_64x16k": batch,
         "incremental_repair": repair,
         "front_end_options": options,
