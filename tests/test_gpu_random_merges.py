@@ -28,18 +28,20 @@ def _pack(vocab):
 
 
 def random_merges(seed, letters, n_merges, max_len=24, allow_same_spelling=False):
-    """A proper merge list over single letters: each merge joins two existing
-    tokens (short ones more often) into a new vocabulary entry."""
+    """A proper merge list over the bytes of the letters' UTF-8 encodings: each
+    merge joins two existing tokens (short ones more often) into a new
+    vocabulary entry; a result may hold part of a multi-byte character."""
     rng = random.Random(seed)
     vocab = [bytes([i]) for i in range(256)]
-    toks = [ord(c) for c in letters]
+    toks = sorted(set(letters.encode("utf-8")))
+    n0 = len(toks)
     spelled = set(vocab)
     pairs = set()
     merges = []
     tries = 0
     while len(merges) < n_merges and tries < 100000:
         tries += 1
-        a = rng.choice(toks[: max(len(letters), len(toks) * rng.choice((1, 2, 4)) // 4)])
+        a = rng.choice(toks[: max(n0, len(toks) * rng.choice((1, 2, 4)) // 4)])
         b = rng.choice(toks)
         s = vocab[a] + vocab[b]
         if (a, b) in pairs or len(s) > max_len or (s in spelled and not allow_same_spelling):
@@ -99,6 +101,16 @@ def test_random_merge_lists(gpu, seed, letters, n_merges):
     merges, vocab = random_merges(seed, letters, n_merges)
     assert max(len(v) for v in vocab) <= 24
     _check(merges, vocab, _docs(100 + seed, letters, 1500))
+
+
+@pytest.mark.parametrize("seed,letters,n_merges", [(11, "éж", 600), (12, "aé中", 1500), (13, "ж中😀", 800)])
+def test_random_merge_lists_multibyte(gpu, seed, letters, n_merges):
+    """Letters of two to four bytes: byte tokens above 127, merges inside and
+    across characters, units of up to 240 bytes (the block engine beyond 128),
+    and symbol pieces between letter runs where the emoji occurs."""
+    merges, vocab = random_merges(seed, letters, n_merges)
+    assert any(len(v) > 1 and v[0] >= 0x80 for v in vocab)
+    _check(merges, vocab, _docs(300 + seed, letters, 1200, hi=60))
 
 
 @pytest.mark.parametrize("seed", [6, 7])
