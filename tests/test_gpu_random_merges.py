@@ -6,8 +6,9 @@ one letter run under the GPT-2-style pattern, so units of 1 to 120 bytes
 reach the thread, wave and two-row wave engines with merge structures no
 trained table has: results of up to 24 or 40 bytes, two results that spell
 the same bytes, and a chain a, aa, ..., a^24 under which every substring of
-a run of one letter is a token.  Each unit is encoded as a document of a
-batch and again inside one request.
+a run of one letter is a token.  Lists over the bytes of multi-byte letters
+add byte tokens above 127 and merges inside characters.  Each unit is encoded
+as a document of a batch and again inside one request.
 """
 
 import random
