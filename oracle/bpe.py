@@ -62,11 +62,12 @@ def bpe_naive(piece: bytes, table: MergeTable) -> list:
     return ids
 
 
-def bpe_heap(piece: bytes, table: MergeTable) -> list:
+def bpe_heap(piece: bytes, table: MergeTable, applied=None) -> list:
     """The same definition with a heap of (rank, left position) over a doubly linked list.
 
     A token keeps the byte position of its first byte, so equal ranks pop in
-    left-to-right order, which is the leftmost-first rule.
+    left-to-right order, which is the leftmost-first rule.  ``applied``, if
+    given, receives the rank of every merge in the order they are applied.
     """
     n = len(piece)
     if n == 0:
@@ -95,6 +96,8 @@ def bpe_heap(piece: bytes, table: MergeTable) -> list:
         if j >= n or ids[i] != a or ids[j] != b:
             continue  # stale entry: the pair changed after it was pushed
         ids[i] = c
+        if applied is not None:
+            applied.append(r)
         alive[j] = False
         k = nxt[j]
         nxt[i] = k
@@ -119,3 +122,16 @@ def bpe(piece: bytes, table: MergeTable) -> list:
     if len(piece) <= NAIVE_MAX:
         return bpe_naive(piece, table)
     return bpe_heap(piece, table)
+
+
+def bpe_rounds(piece: bytes, table: MergeTable) -> int:
+    """Rounds of the round-parallel schedule on one piece (Sec. 4.2: a round
+    merges every leftmost non-overlapping occurrence of the lowest-ranked pair
+    present).  A merge only creates pairs that hold its result, whose ranks are
+    higher in a proper table, so greedy BPE applies its ranks in non-decreasing
+    order and each rank in one round: the rounds are the distinct ranks applied.
+    The dependency chain of a piece is this many rounds long (Sec. 6: the chain
+    depth of exact BPE bounds the GPU's latency)."""
+    applied = []
+    bpe_heap(piece, table, applied)
+    return len(set(applied))

@@ -16,7 +16,7 @@ import random
 import pytest
 
 from conftest import oracle_table, stored_table
-from oracle.bpe import MergeTable, bpe, bpe_heap, bpe_naive
+from oracle.bpe import MergeTable, bpe, bpe_heap, bpe_naive, bpe_rounds
 
 # r0 (a,a)->256, r1 (256,a)->257, r2 (a,b)->258, r3 (258,c)->259, r4 (c,d)->260
 HAND = [(97, 97, 256), (256, 97, 257), (97, 98, 258), (258, 99, 259), (99, 100, 260)]
@@ -93,6 +93,51 @@ def test_round_schedule_equals_greedy(k):
     for _ in range(2000):
         p = bytes(rng.choice(b"aaabbcdeet ") for _ in range(rng.randint(1, 60)))
         assert _round_schedule(p, t) == bpe(p, t)
+
+
+def test_rounds_hand_worked():
+    """Rounds of the hand-worked merges: aaaa merges (a, a) twice in one round;
+    aaaaa and aaab need (a, a) then (256, a); abcd needs (a, b) then (258, c)."""
+    t = _hand_table()
+    assert bpe_rounds(b"aaaa", t) == 1
+    assert bpe_rounds(b"aaaaa", t) == 2
+    assert bpe_rounds(b"aaab", t) == 2
+    assert bpe_rounds(b"abcd", t) == 2
+    assert bpe_rounds(b"xyz", t) == 0
+    assert bpe_rounds(b"", t) == 0
+
+
+def _rounds_of_schedule(piece, t):
+    """Number of rounds the parallel schedule runs (counted by the schedule itself)."""
+    ids = [t.byte_id[b] for b in piece]
+    rounds = 0
+    while True:
+        ranks = [t.rank.get((ids[i], ids[i + 1])) for i in range(len(ids) - 1)]
+        present = [r for r in ranks if r is not None]
+        if not present:
+            return rounds
+        rounds += 1
+        best = min(present)
+        out = []
+        i = 0
+        while i < len(ids):
+            if i + 1 < len(ids) and ranks[i] is not None and ranks[i][0] == best[0]:
+                out.append(best[1])
+                i += 2
+            else:
+                out.append(ids[i])
+                i += 1
+        ids = out
+
+
+@pytest.mark.parametrize("k", [1, 3])
+def test_rounds_equal_the_schedule(k):
+    """The distinct ranks greedy BPE applies equal the rounds of the parallel schedule."""
+    t = oracle_table(k)
+    rng = random.Random(20 + k)
+    for _ in range(1500):
+        p = bytes(rng.choice(b"aaabbcdeet ") for _ in range(rng.randint(1, 80)))
+        assert bpe_rounds(p, t) == _rounds_of_schedule(p, t)
 
 
 def test_planted_fault_is_caught():
