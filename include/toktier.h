@@ -26,6 +26,14 @@
  *    immutable after registration).  Calls on one handle from several host
  *    threads are allowed if each thread uses its own stream; the handle keeps
  *    one workspace per stream.
+ *  - Memory: a stream's workspace takes about 35 bytes of device memory per
+ *    byte of request capacity (epoch-tagged tile words, staging of tokens,
+ *    rows of long units, the request bytes and IDs of host calls).  Host
+ *    calls of tt_encode_spans add 16 bytes of device memory per byte, and
+ *    host calls of tt_encode 5 bytes of pinned host memory per byte.  The
+ *    capacity grows in powers of two from 64 KiB to the largest request seen
+ *    on the stream (about 37 GB of device memory at TT_MAX_BYTES) and is freed
+ *    by tt_destroy.
  */
 #ifndef TOKTIER_H
 #define TOKTIER_H
@@ -91,7 +99,8 @@ typedef struct {
  *  vocab_bytes, vocab_offsets  token i is vocab_bytes[vocab_offsets[i] ..
  *                            vocab_offsets[i+1]) (host; offsets has
  *                            vocab_size+1 entries, non-decreasing, from 0).
- *  pattern_id                TT_PATTERN_GPT2 or TT_PATTERN_CL100K.
+ *  pattern_id                TT_PATTERN_GPT2, TT_PATTERN_CL100K, TT_PATTERN_O200K
+ *                            or TT_PATTERN_DEEPSEEK.
  *  out                       receives the handle.
  *
  * The base ID of byte b is the lowest ID whose vocabulary entry is the single
@@ -152,10 +161,19 @@ void tt_destroy(tt_tokenizer* h);
  *  utf8[len]      request bytes (host); len == 0 gives *out_len = 0.
  *  out_ids        host buffer of at least max(len, 1) IDs.
  *  out_len        receives the number of IDs written.
- * Blocks until out_ids/out_len are valid (two host synchronisations: one for
- * the device-side output length, one for the IDs).  NUL bytes are ordinary
- * characters; no byte-order mark is stripped.  Invalid UTF-8 returns
- * TT_ERR_INVALID_UTF8 and writes no IDs (*out_len = 0). */
+ * Blocks until out_ids/out_len are valid, with one host synchronisation for
+ * requests up to 256 MiB (Sec. 4.3: the single-request path keeps the host
+ * out of the chain).  The request goes to the device in one copy, straight
+ * from utf8 when it is pinned host memory, else through pinned staging; the
+ * IDs come back in one copy started before their count is known, sized from
+ * the IDs-per-byte ratio of the stream's recent requests (a request with more
+ * IDs takes a second copy of the rest), straight into out_ids when it is
+ * pinned.  Staging copies of at least 256 KiB are split among the calling
+ * thread and up to three worker threads of the library, which spin for 2 ms
+ * after a copy, then sleep.  Longer requests take the length and the IDs back
+ * in two copies.  NUL bytes are ordinary characters; no byte-order mark is
+ * stripped.  Invalid UTF-8 returns TT_ERR_INVALID_UTF8 with *out_len = 0; the
+ * contents of out_ids are then unspecified. */
 int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_ids,
               int64_t* out_len, void* stream);
 
@@ -294,10 +312,10 @@ int tt_session_info(const tt_session* s, int64_t* n_bytes, int64_t* n_chars, int
  * else 0.  At such a position every text that contains the two characters
  * there has a piece boundary, the pieces to its right do not depend on the
  * text before its left neighbour, and the pieces to its left do not depend on
- * the text after its right neighbour (Appendix, "Discharging the certificate
- * per family": the deployed check requires a class transition from a
- * per-family synchronizing set, proven to reset the pre-tokenizer under every
- * left context; the sets are derived per pattern).  Transitions, with O other,
+ * the text after its right neighbour.  This is the certificate the paper's
+ * splice check asks for (Appendix, "Discharging the certificate per family");
+ * each pattern has its own set of such class pairs, derived here from its
+ * alternatives.  Transitions, with O other,
  * L letter, N number, WS whitespace but CR/LF, NL CR/LF, SP U+0020, APO U+0027:
  *   GPT-2:   left and right classes differ, counting WS and NL as one class,
  *            and the left character is neither SP nor APO;

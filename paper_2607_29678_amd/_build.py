@@ -9,7 +9,7 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libtoktier.so")
-SOURCES = ["tt_api.hip", "tt_tile.hip", "tt_batch.hip", "tt_spans.hip", "tt_session.hip"]
+SOURCES = ["tt_api.hip", "tt_tile.hip", "tt_batch.hip", "tt_spans.hip", "tt_session.hip", "tt_copy.cpp"]
 ARCH = "gfx950"
 
 FLAGS = [
@@ -37,7 +37,7 @@ def build(verbose: bool = False) -> str:
     os.makedirs(objdir, exist_ok=True)
 
     def compile_one(src):
-        obj = os.path.join(objdir, src.replace(".hip", ".o"))
+        obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
         cmd = [cc] + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:

@@ -43,6 +43,11 @@ struct Workspace {
   int32_t* d_spans = nullptr;  // span export (host calls): [span_cap][4], allocated on first use
   uint64_t span_cap = 0;
   int64_t* h_len = nullptr;   // pinned readback word
+  // tt_encode: pinned staging, sized with the capacity
+  uint64_t pin_cap = 0;        // bytes of request it holds
+  uint8_t* h_in = nullptr;     // request bytes for the DMA (pageable callers)
+  int32_t* h_ids = nullptr;    // IDs back from the device (pageable callers)
+  double id_ratio = 1.0;       // IDs per byte to copy back before the length is known
   // profiling: stage boundaries of the most recent calls, a ring of
   // `ring` calls with N_STAGES + 1 events each
   std::vector<hipEvent_t> ev;
@@ -185,6 +190,8 @@ void free_ws(Workspace* s) {
   if (s->d_docs) (void)hipFree(s->d_docs);
   if (s->d_spans) (void)hipFree(s->d_spans);
   if (s->h_len) (void)hipHostFree(s->h_len);
+  if (s->h_in) (void)hipHostFree(s->h_in);
+  if (s->h_ids) (void)hipHostFree(s->h_ids);
   for (auto e : s->ev)
     if (e) (void)hipEventDestroy(e);
   delete s;
@@ -311,6 +318,44 @@ int reserve_spans(Workspace* s, uint64_t len, hipStream_t st) {
   return TT_OK;
 }
 
+// The pinned staging buffers of tt_encode, allocated on first use and grown
+// with the workspace's capacity (5 bytes per byte of capacity).  Only blocking
+// calls use them, so none is in use when they grow.
+int reserve_pinned(Workspace* s, uint64_t len) {
+  if (len <= s->pin_cap) return TT_OK;
+  auto drop = [&]() {
+    if (s->h_in) (void)hipHostFree(s->h_in);
+    if (s->h_ids) (void)hipHostFree(s->h_ids);
+    s->h_in = nullptr;
+    s->h_ids = nullptr;
+    s->pin_cap = 0;
+  };
+  drop();
+  const uint64_t cap = s->cap;  // >= len (the device workspace was reserved first)
+  if (hipHostMalloc(reinterpret_cast<void**>(&s->h_in), cap + 64, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc(reinterpret_cast<void**>(&s->h_ids), 4 * cap, hipHostMallocDefault) != hipSuccess) {
+    drop();
+    return TT_ERR_OOM;
+  }
+  s->pin_cap = cap;
+  return TT_OK;
+}
+
+// Whether [p, p + len) is pinned host memory the device can read directly.
+bool host_pinned(const void* p, int64_t len) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();  // pageable memory may report an error; it is not sticky
+    return false;
+  }
+  if (a.type != hipMemoryTypeHost) return false;
+  if (hipPointerGetAttributes(&a, static_cast<const uint8_t*>(p) + (len - 1)) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeHost;
+}
+
 // Enqueue the whole chain for `n` bytes at device address `text`.
 // mode 0: split export (out_ids receives piece offsets); mode 1: encode;
 // mode 2: encode with span export into out_spans ([n][4], single requests).
@@ -363,6 +408,59 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   if (mode == 2 && launch_spans(w, st) != hipSuccess) return TT_ERR_HIP;
   if (!mark()) return TT_ERR_HIP;
   if (ring) ++s->n_calls;
+  return TT_OK;
+}
+
+// Largest request that tt_encode stages through pinned buffers; longer ones
+// are copied from and to the caller's memory directly.
+constexpr uint64_t PINNED_MAX = 1ull << 28;
+
+// tt_encode through pinned staging, with one host synchronisation.
+//  - stage-in: one DMA, from the caller's buffer when it is pinned, else from a
+//    pinned copy;
+//  - the tile kernel places the IDs in device memory and its last tile writes
+//    the output length straight into pinned host memory;
+//  - stage-out: the IDs are copied back before their count is known, as many as
+//    the recent IDs-per-byte ratio of this workspace predicts (plus a margin);
+//    the rare request with more IDs takes a second copy of the rest.  The copy
+//    goes straight into the caller's buffer when it is pinned.
+int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t len, int32_t* out_ids,
+                  int64_t* out_len, hipStream_t st) {
+  int rc = reserve_pinned(s, (uint64_t)len);
+  if (rc) return rc;
+  const uint8_t* src = utf8;
+  const bool pin_out = host_pinned(out_ids, 4 * len);
+  if (!host_pinned(utf8, len)) {
+    host_copy_wake();
+    host_copy(s->h_in, utf8, (size_t)len);
+    src = s->h_in;
+  } else if (!pin_out) {
+    host_copy_wake();  // for the copy of the IDs
+  }
+  if (hipMemcpyAsync(s->d_in, src, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
+  *s->h_len = 0;
+  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->h_len, nullptr, st, 1);
+  if (rc) return rc;
+  int32_t* dst = pin_out ? out_ids : s->h_ids;
+  const int64_t guess = std::min<int64_t>(len, (int64_t)(s->id_ratio * (double)len) + 1024);
+  if (hipMemcpyAsync(dst, s->d_out, 4 * (size_t)guess, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return TT_ERR_HIP;
+  const int64_t T = *s->h_len;
+  if (T < 0) return (int)T;
+  if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
+  if (T > guess) {
+    if (hipMemcpyAsync(dst + guess, s->d_out + guess, 4 * (size_t)(T - guess), hipMemcpyDeviceToHost, st) !=
+            hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+      return TT_ERR_HIP;
+  }
+  // the next guess: 5% above this request's ratio, falling slowly after text
+  // with many IDs per byte
+  const double r = 1.05 * (double)T / (double)len;
+  s->id_ratio = std::min(1.0, std::max(r, 0.9 * s->id_ratio));
+  if (!pin_out && T > 0) host_copy(out_ids, s->h_ids, 4 * (size_t)T);
+  *out_len = T;
   return TT_OK;
 }
 
@@ -996,6 +1094,9 @@ int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_id
   Workspace* s = nullptr;
   int rc = get_ws(h, st, (uint64_t)len, &s);
   if (rc) return rc;
+  if ((uint64_t)len <= PINNED_MAX) return encode_staged(h, s, utf8, len, out_ids, out_len, st);
+  // very long requests: the length, then the IDs, straight between the caller's
+  // memory and the device
   if (hipMemcpyAsync(s->d_in, utf8, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
   rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->d_len, nullptr, st, 1);
   if (rc) return rc;

@@ -1,0 +1,19 @@
+// Host copies of the staging buffers (tt_copy.cpp), split among a few worker
+// threads.  Plain C++ (no HIP), so that the pool can also be built and
+// stress-tested on its own.
+#pragma once
+
+#include <cstddef>
+
+namespace tt {
+
+// Copy n bytes (the regions must not overlap).  Copies of at least 256 KB are
+// split among the calling thread and the pool's workers; smaller ones, and
+// copies while another thread's copy is running, are a plain memcpy.
+void host_copy(void* dst, const void* src, size_t n);
+
+// Let sleeping workers start spinning ahead of a copy (cheap when they are
+// awake).
+void host_copy_wake();
+
+}  // namespace tt

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "../../include/toktier.h"
+#include "tt_copy.h"
 
 namespace tt {
 

@@ -100,6 +100,29 @@ class Tokenizer:
         _lib.check(st, "tt_encode")
         return out[: n.value].copy()
 
+    def encode_into(self, data, out, stream=None) -> int:
+        """``tt_encode`` into a caller-provided int32 array ``out`` (numpy or a CPU torch tensor, at
+        least ``max(1, len(data))`` entries, reusable across calls; pinned memory is copied into
+        directly).  Returns the number of IDs written."""
+        if hasattr(data, "data_ptr"):  # a CPU torch tensor of bytes (pinned or not)
+            if repr(data.dtype) != "torch.uint8" or not data.is_contiguous() or data.is_cuda:
+                raise ValueError("data must be a contiguous uint8 CPU tensor")
+            src, size = data, data.numel()
+        else:
+            src = _u8(data)
+            size = src.size
+        if hasattr(out, "data_ptr"):
+            ok = repr(out.dtype) == "torch.int32" and out.is_contiguous() and not out.is_cuda and out.numel() >= max(1, size)
+        else:
+            ok = out.dtype == np.int32 and out.flags["C_CONTIGUOUS"] and out.size >= max(1, size)
+        if not ok:
+            raise ValueError("out must be a contiguous int32 host array of at least max(1, len(data)) entries")
+        n = ctypes.c_int64(0)
+        st = self._lib.tt_encode(self._h, _ptr(src) if size else None, size, _ptr(out), ctypes.byref(n),
+                                 _stream(stream))
+        _lib.check(st, "tt_encode")
+        return n.value
+
     def encode_spans(self, data, stream=None):
         """``tt_encode_spans``: (IDs int32 [T], spans int32 [T, 4]) of one UTF-8 request; a span is
         (byte begin, byte end, char begin, char end)."""
