@@ -1,30 +1,36 @@
-"""Benchmark: exact tokenization of 1M-character requests on one MI355X.
+"""Benchmark: exact tokenization of 1,000,000-character requests on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3|4] [--no-cpu] [--calibrate-copy]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3|4] [--no-cpu] [--quick] [--calibrate-copy]
 
-A step is one full-request tokenization (pre-tokenization, BPE, compaction)
-of one distinct seeded 1,000,000-character sample whose bytes are already in
-HBM; the IDs stay in HBM.  W warm-up requests use other samples.  The K timed
-requests run back to back between two stream synchronisations:
-value = K * 1e6 chars / elapsed.  During the timed region the library records
-HIP events between its stages on the same stream; their average gives the
-duration of the dominant kernel (the tile kernel) for the roofline.
-Per-request latencies (enqueue to completion, input in HBM) give P50/P90/P99
-in a second pass; the host-to-host latency through ``tt_encode`` (PCIe copies
-included), a steady-state P50 (100 re-encodes of one sample), the P50 of the
-same requests with span export (IDs plus byte and character spans, device
-resident), the P50 of all timed samples joined into one request (many tiles
-per resident slot: the throughput with the chip full) and the host-to-host
-time of a 64 x 16,384-char document batch are reported separately, and so
-are the append latency of incremental-repair sessions at 100,000 and
-1,000,000 characters and the latency of the two front-end options
-(ignore_merges, added-token literals) and of the o200k-style and
-DeepSeek-style patterns.  The CPU oracle is timed on the same timed samples,
-one thread pinned to one core, and its IDs are compared with the GPU's.
+The headline follows the paper's sampled protocol for array delivery (Sec. 5.4:
+every request a fresh sample encoded once; the paper reports P50 over 20
+samples): W warm-up requests on other samples, then K distinct seeded
+1,000,000-character samples, each tokenized once through ``tt_encode``, host
+bytes in and host IDs out.  A step is one such call: stage-in (host copy into
+pinned staging, one DMA), the tile kernel (pre-tokenization, BPE, placement),
+stage-out (one DMA, one synchronisation, host copy into the caller's array).
+The caller's buffers are ordinary pageable numpy arrays, the output array
+reused from call to call:
 
-``--calibrate-copy`` first runs a plain int32 copy kernel of 64 MiB read +
-64 MiB written, so that a hardware-counter profile of this command can scale
-the tile kernel's FETCH_SIZE / WRITE_SIZE to bytes.
+    value = 1,000,000 chars / P50(host-to-host latency)
+
+p50/p90/p99 are host-to-host too.  Reported beside it, on the same samples:
+the same calls with pinned caller buffers, the Python binding's fresh-array
+``Tokenizer.encode``, the device-resident path (input already in HBM, IDs left
+in HBM), the multilingual configuration C4 with its own roofline, request
+sizes of 100,000, 2,000,000 and 4,400,000 characters, the 3,000,000-character
+stress request C5 and its 64-document batch, incremental repair, the
+front-end options and the o200k-style and DeepSeek-style patterns.
+
+During the headline's timed calls the library records HIP events around the
+tile kernel on the caller's stream; their mean is the kernel time of the
+roofline.  The CPU oracle is timed on a bounded sample of the same requests
+(one thread pinned to one core), and on C5's batch over all host cores.
+
+``--quick`` keeps the headline, C4 and the device-resident figures only (for
+profiler runs).  ``--calibrate-copy`` first runs a plain int32 copy of 64 MiB
+read + 64 MiB written, so that a hardware-counter profile of this command can
+scale the tile kernel's FETCH_SIZE / WRITE_SIZE to bytes.
 
 Prints one JSON line.
 """
@@ -41,6 +47,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tile_kernel_traffic.json")
+SHAPES_FILE = os.path.join(ROOT, "tests", "golden", "workload_shapes.json")
 CSRC = os.path.join(ROOT, "paper_2607_29678_amd", "csrc")
 
 
@@ -54,11 +61,16 @@ def percentile(xs, q):
     return xs[lo] + (xs[hi] - xs[lo]) * (k - lo)
 
 
+def pcts(xs, nd=4):
+    return {"p50_ms": round(percentile(xs, 50), nd), "p90_ms": round(percentile(xs, 90), nd),
+            "p99_ms": round(percentile(xs, 99), nd), "n": len(xs)}
+
+
 def kernel_source_sha():
     """SHA-256 over the library sources (the counters are void once these change)."""
     h = hashlib.sha256()
     for name in sorted(os.listdir(CSRC)):
-        if name.endswith((".hip", ".h", ".inc")):
+        if name.endswith((".hip", ".h", ".inc", ".cpp")):
             with open(os.path.join(CSRC, name), "rb") as f:
                 h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
@@ -76,7 +88,288 @@ def measured_traffic(config):
     return rec.get("traffic_bytes_per_launch")
 
 
-def incremental_repair(tok, k, sid, n_appends=24):
+def stored_shapes():
+    try:
+        with open(SHAPES_FILE) as f:
+            return json.load(f)
+    except (OSError, ValueError):
+        return {}
+
+
+class Ctx:
+    """Device, stream and the tokenizer handles of the run."""
+
+    def __init__(self):
+        import torch
+
+        from paper_2607_29678_amd import Tokenizer
+        from workloads.tables import load_table
+
+        self.torch = torch
+        self.dev = torch.device("cuda:0")
+        torch.cuda.set_device(self.dev)
+        self.stream = torch.cuda.current_stream(self.dev)
+        self.sid = self.stream.cuda_stream
+        self._tok = {}
+        self.Tokenizer = Tokenizer
+        self.load_table = load_table
+
+    def tok(self, table, pattern):
+        key = (table, pattern)
+        if key not in self._tok:
+            m, vb, vo = self.load_table(table)
+            self._tok[key] = self.Tokenizer(m, vb, vo, pattern)
+        return self._tok[key]
+
+
+def host_calls(ctx, tok, arrs, out, warmup, record_kernel=False):
+    """Host-to-host latency (ms) of tt_encode on each array once after `warmup`
+    calls; returns (latencies, token counts, tile-kernel ms per call or None)."""
+    for i in range(warmup):
+        tok.encode_into(arrs[i], out, ctx.sid)
+    timed = range(warmup, len(arrs))
+    if record_kernel:
+        tok.set_profiling(len(timed))
+    lat, counts = [], []
+    for i in timed:
+        a = time.perf_counter()
+        t = tok.encode_into(arrs[i], out, ctx.sid)
+        lat.append((time.perf_counter() - a) * 1e3)
+        counts.append(t)
+    kern = None
+    if record_kernel:
+        kern = [c["tile"] for c in tok.stage_times(ctx.sid)]
+        tok.set_profiling(0)
+    return lat, counts, kern
+
+
+def device_calls(ctx, tok, d_in, lens, d_out, d_len, reps=1):
+    """Device-resident latency (enqueue to completion, input in HBM) and tile-kernel ms."""
+    tok.set_profiling(len(d_in) * reps)
+    lat = []
+    for _ in range(reps):
+        for i in range(len(d_in)):
+            ctx.torch.cuda.synchronize()
+            a = time.perf_counter()
+            tok.encode_device(d_in[i], lens[i], d_out, d_len, ctx.sid)
+            ctx.stream.synchronize()
+            lat.append((time.perf_counter() - a) * 1e3)
+    kern = [c["tile"] for c in tok.stage_times(ctx.sid)]
+    tok.set_profiling(0)
+    return lat, kern
+
+
+def roofline_of(bytes_avg, tokens_avg, kernel_ms, traffic):
+    alg = bytes_avg + 4.0 * tokens_avg
+    achieved = alg / (kernel_ms * 1e-3) / 1e9
+    return {"kernel": "tile_kernel", "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6), "traffic": traffic,
+            "algorithmic_bytes": int(alg), "kernel_ms": round(kernel_ms, 4)}
+
+
+def config_block(ctx, k, steps, warmup, extras=True):
+    """Host-to-host protocol on configuration k's latency samples, with the
+    device-resident figures and the tile kernel's roofline."""
+    import numpy as np
+
+    from workloads import textgen
+
+    cfg = textgen.CONFIGS[k]
+    tok = ctx.tok(k, cfg["pattern"])
+    n_total = warmup + steps
+    texts = [textgen.latency_sample(k, s % 32) for s in range(n_total)]
+    raw = [t.encode("utf-8") for t in texts]
+    arrs = [np.frombuffer(b, dtype=np.uint8) for b in raw]
+    n_chars = [len(t) for t in texts]
+    cap = max(len(b) for b in raw)
+    out = np.zeros(cap, dtype=np.int32)  # touched once, reused like a serving loop's buffer
+    lat, counts, kern = host_calls(ctx, tok, arrs, out, warmup, record_kernel=True)
+    timed = list(range(warmup, n_total))
+    res = {"samples": steps, "warmup": warmup, "host_to_host_pageable": pcts(lat)}
+    res["_lat"] = lat
+    # pinned caller buffers (torch pin_memory), same samples
+    torch = ctx.torch
+    pin_in = [torch.from_numpy(a.copy()).pin_memory() for a in arrs]
+    pin_out = torch.zeros(cap, dtype=torch.int32).pin_memory()
+    plat, pcounts, _ = host_calls(ctx, tok, pin_in, pin_out, warmup)
+    res["host_to_host_pinned"] = pcts(plat)
+    # the binding's fresh-array call (allocates its output on every call)
+    blat = []
+    for i in timed:
+        a = time.perf_counter()
+        ids = tok.encode(raw[i], ctx.sid)
+        blat.append((time.perf_counter() - a) * 1e3)
+    res["python_binding_encode"] = pcts(blat)
+    # device-resident: input in HBM, IDs left in HBM
+    d_in = [torch.from_numpy(a.copy()).to(ctx.dev) for a in arrs]
+    d_out = torch.empty((n_total, cap), dtype=torch.int32, device=ctx.dev)
+    d_len = torch.zeros(n_total, dtype=torch.int64, device=ctx.dev)
+    for i in range(warmup):
+        tok.encode_device(d_in[i], len(raw[i]), d_out[i], d_len[i:i + 1], ctx.sid)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in timed:
+        tok.encode_device(d_in[i], len(raw[i]), d_out[i], d_len[i:i + 1], ctx.sid)
+    torch.cuda.synchronize()
+    b2b = time.perf_counter() - t0
+    lens = d_len.cpu().numpy()
+    if (lens[timed] <= 0).any():
+        raise SystemExit("tokenizer reported an error: %s" % lens[timed])
+    if [int(lens[i]) for i in timed] != counts or pcounts != counts:
+        raise SystemExit("host and device paths returned different token counts")
+    # the host path's IDs equal the device path's (last timed sample, all three host variants)
+    last = timed[-1]
+    dev_ids = d_out[last, : int(lens[last])].cpu().numpy()
+    if not (np.array_equal(out[: counts[-1]], dev_ids) and np.array_equal(pin_out[: counts[-1]].numpy(), dev_ids)
+            and np.array_equal(ids, dev_ids)):
+        raise SystemExit("host and device paths returned different IDs")
+    dlat, dkern = device_calls(ctx, tok, [d_in[i] for i in timed], [len(raw[i]) for i in timed], d_out[0],
+                               d_len[0:1])
+    res["device_resident"] = dict(pcts(dlat), back_to_back_chars_per_s=round(sum(n_chars[i] for i in timed) / b2b, 1),
+                                  tile_kernel_ms_mean=round(sum(dkern) / len(dkern), 4))
+    B_avg = sum(len(raw[i]) for i in timed) / len(timed)
+    T_avg = sum(counts) / len(counts)
+    kernel_ms = sum(kern) / len(kern)
+    res["workload"] = {"chars": n_chars[timed[0]], "bytes_avg": int(B_avg), "tokens_avg": int(T_avg)}
+    res["roofline"] = roofline_of(B_avg, T_avg, kernel_ms, measured_traffic(k))
+    res["roofline"]["kernel_ms_from"] = "HIP events around the tile kernel of the %d timed tt_encode calls" % steps
+    if extras:
+        # steady state: 100 re-encodes of one sample, input in HBM
+        st, _ = device_calls(ctx, tok, [d_in[timed[0]]] * 100, [len(raw[timed[0]])] * 100, d_out[0], d_len[0:1])
+        res["device_resident"]["steady_state_p50_ms"] = round(percentile(st, 50), 4)
+        # span export, device-resident
+        d_spans = torch.empty((cap, 4), dtype=torch.int32, device=ctx.dev)
+        d_sids = torch.empty(cap, dtype=torch.int32, device=ctx.dev)
+        d_slen = torch.zeros(1, dtype=torch.int64, device=ctx.dev)
+        span_lat = []
+        for i in timed:
+            torch.cuda.synchronize()
+            a = time.perf_counter()
+            tok.encode_spans_device(d_in[i], len(raw[i]), d_sids, d_spans, d_slen, ctx.sid)
+            ctx.stream.synchronize()
+            span_lat.append((time.perf_counter() - a) * 1e3)
+        res["device_resident"]["span_export_p50_ms"] = round(percentile(span_lat, 50), 4)
+        starts = tok.pretokenize(raw[timed[0]], ctx.sid)
+        res["workload"]["pieces_first_timed"] = len(starts)
+        res["workload"]["longest_piece_bytes_first_timed"] = int(
+            np.max(np.diff(np.append(starts, len(raw[timed[0]])))))
+    res["_texts"] = (raw, timed, counts, d_out, lens)
+    return res
+
+
+def sizes_block(ctx, k, warmup=2):
+    """Host-to-host P50 at the paper's other request sizes (Sec. 5.4: 100 K, 2 M and
+    4.4 M characters), on distinct seeded samples of configuration k."""
+    import numpy as np
+
+    from workloads import textgen
+
+    cfg = textgen.CONFIGS[k]
+    tok = ctx.tok(k, cfg["pattern"])
+    pool = [textgen.latency_sample(k, s) for s in range(3, 28)]
+    npool = len(pool)
+    # distinct requests: prefixes, and runs of consecutive samples (rotated)
+    shapes = {
+        100_000: [t[:100_000] for t in pool[:22]],
+        2_000_000: [pool[j] + pool[(j + 1) % npool] for j in range(12)],
+        4_400_000: ["".join(pool[(j + i) % npool] for i in range(4)) + pool[(j + 4) % npool][:400_000]
+                    for j in range(0, 24, 2)],
+    }
+    rows = []
+    for n_chars, texts in shapes.items():
+        arrs = [np.frombuffer(t.encode("utf-8"), dtype=np.uint8) for t in texts]
+        out = np.zeros(max(a.size for a in arrs), dtype=np.int32)
+        w = min(warmup, len(arrs) - 3)
+        lat, counts, kern = host_calls(ctx, tok, arrs, out, w, record_kernel=True)
+        rows.append({"chars": n_chars, "samples": len(lat), "host_to_host_p50_ms": round(percentile(lat, 50), 4),
+                     "host_to_host_p90_ms": round(percentile(lat, 90), 4),
+                     "chars_per_s": round(n_chars / (percentile(lat, 50) * 1e-3), 1),
+                     "tile_kernel_ms_mean": round(sum(kern) / len(kern), 4)})
+    return rows
+
+
+def stress_block(ctx):
+    """C5: the 3,000,000-character stress request and its 64-document batch."""
+    import numpy as np
+
+    from workloads import textgen
+
+    torch = ctx.torch
+    tok = ctx.tok(5, "cl100k")
+    text = textgen.config_text(5).encode("utf-8")
+    arr = np.frombuffer(text, dtype=np.uint8)
+    out = np.zeros(arr.size, dtype=np.int32)
+    tok.encode_into(arr, out, ctx.sid)
+    tok.set_profiling(8)
+    lat = []
+    for _ in range(8):
+        a = time.perf_counter()
+        T = tok.encode_into(arr, out, ctx.sid)
+        lat.append((time.perf_counter() - a) * 1e3)
+    kern = [c["tile"] for c in tok.stage_times(ctx.sid)]
+    tok.set_profiling(0)
+    d_in = torch.from_numpy(arr.copy()).to(ctx.dev)
+    d_out = torch.empty(arr.size, dtype=torch.int32, device=ctx.dev)
+    d_len = torch.zeros(1, dtype=torch.int64, device=ctx.dev)
+    dlat, dkern = device_calls(ctx, tok, [d_in] * 8, [arr.size] * 8, d_out, d_len)
+    if int(d_len.item()) != T or not np.array_equal(d_out[:T].cpu().numpy(), out[:T]):
+        raise SystemExit("C5: host and device paths differ")
+    starts = tok.pretokenize(text, ctx.sid)
+    req = {"chars": 3_000_000, "bytes": arr.size, "tokens": T, "pieces": len(starts),
+           "longest_piece_bytes": int(np.max(np.diff(np.append(starts, arr.size)))),
+           "host_to_host": pcts(lat), "host_to_host_note": "one request, encoded 8 times after a warm-up call",
+           "device_resident_p50_ms": round(percentile(dlat, 50), 4),
+           "tile_kernel_ms_mean": round(sum(dkern) / len(dkern), 4),
+           "chars_per_s_host_to_host": round(3_000_000 / (percentile(lat, 50) * 1e-3), 1)}
+    sh = stored_shapes().get("C5_request")
+    if sh:
+        req["max_rounds_per_piece"] = sh["max_rounds_per_piece"]
+        req["tokens_match_oracle_shape_file"] = sh["tokens"] == T
+    docs = [d.encode("utf-8") for d in textgen.batch_docs()]
+    tok.encode_batch(docs, ctx.sid)
+    blat = []
+    for _ in range(10):
+        a = time.perf_counter()
+        tok.encode_batch(docs, ctx.sid)
+        blat.append((time.perf_counter() - a) * 1e3)
+    bchars = sum(len(d.decode("utf-8")) for d in docs)
+    batch = {"docs": len(docs), "chars": bchars, "bytes": sum(len(d) for d in docs), "host_to_host": pcts(blat),
+             "chars_per_s": round(bchars / (percentile(blat, 50) * 1e-3), 1)}
+    sb = stored_shapes().get("C5_batch")
+    if sb:
+        batch["max_rounds_per_piece"] = sb["max_rounds_per_piece"]
+    return {"request": req, "batch_64x16k": batch}
+
+
+def large_request(ctx, k, raw, timed):
+    """All timed samples joined into one request: the throughput with the chip full."""
+    import numpy as np
+
+    torch = ctx.torch
+    tok = ctx.tok(k, "gpt2" if k == 3 else "cl100k")
+    big = b"".join(raw[i] for i in timed)
+    d_big = torch.from_numpy(np.frombuffer(big, dtype=np.uint8).copy()).to(ctx.dev)
+    d_bout = torch.empty(len(big), dtype=torch.int32, device=ctx.dev)
+    d_blen = torch.zeros(1, dtype=torch.int64, device=ctx.dev)
+    tok.encode_device(d_big, len(big), d_bout, d_blen, ctx.sid)
+    torch.cuda.synchronize()
+    lat = []
+    for _ in range(10):
+        a = time.perf_counter()
+        tok.encode_device(d_big, len(big), d_bout, d_blen, ctx.sid)
+        ctx.stream.synchronize()
+        lat.append((time.perf_counter() - a) * 1e3)
+    T = int(d_blen.item())
+    if T <= 0:
+        raise SystemExit("tokenizer reported an error on the joined request: %d" % T)
+    chars = len(big.decode("utf-8"))
+    ms = percentile(lat, 50)
+    return {"chars": chars, "bytes": len(big), "tokens": T, "device_resident_p50_ms": round(ms, 4),
+            "chars_per_s": round(chars / (ms * 1e-3), 1),
+            "hbm_frac": round((len(big) + 4.0 * T) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)}
+
+
+def incremental_repair(ctx, k, n_appends=24):
     """Append latency of a session (window re-tokenization and splice, host to
     host) against re-tokenizing the whole text through tt_encode, at two
     context sizes; appends are seeded lognormal sizes around 1,500 characters
@@ -88,6 +381,8 @@ def incremental_repair(tok, k, sid, n_appends=24):
     from paper_2607_29678_amd import Session
     from workloads import textgen
 
+    tok = ctx.tok(k, textgen.CONFIGS[k]["pattern"])
+    sid = ctx.sid
     feed = textgen.latency_sample(k, 30)
     rows = []
     for ctx_chars, ctx_seed in ((100_000, 28), (1_000_000, 29)):
@@ -123,30 +418,28 @@ def incremental_repair(tok, k, sid, n_appends=24):
             "context": {"paper_repair_p50_ms_1M": 1.23, "paper_hardware": "CPU session store (Qwen3 real text)"}}
 
 
-def front_end_options(sid, n=10):
+def front_end_options(ctx, n=10):
     """ignore_merges and added tokens (Sec. 4.2, Sec. 4.5) on 1,000,000-character
     requests.  ignore_merges: the multilingual samples with the cl100k-style
     table, device-resident P50 with and without the option.  Added tokens: the
     transcript samples with a chat-template literal before every turn (about
     one per 1,400 characters), host to host through tt_encode, against the same
-    text on a handle without literals."""
+    text on a handle without literals.  Then the o200k-style and DeepSeek-style
+    patterns against cl100k-style on the same samples and table."""
     import numpy as np
-    import torch
 
-    from paper_2607_29678_amd import Tokenizer
     from workloads import textgen
-    from workloads.tables import load_table
 
-    dev = torch.device("cuda:0")
-    stream = torch.cuda.current_stream(dev)
-    out = {}
-    m, vb, vo = load_table(4)
+    torch = ctx.torch
+    dev, sid, stream = ctx.dev, ctx.sid, ctx.stream
+    m, vb, vo = ctx.load_table(4)
     texts = [textgen.latency_sample(4, s).encode("utf-8") for s in range(n)]
     d_in = [torch.from_numpy(np.frombuffer(t, dtype=np.uint8).copy()).to(dev) for t in texts]
     d_out = torch.empty(max(len(t) for t in texts), dtype=torch.int32, device=dev)
     d_len = torch.zeros(1, dtype=torch.int64, device=dev)
+    res = {}
     for ignore in (False, True):
-        tok = Tokenizer(m, vb, vo, "cl100k", ignore_merges=ignore)
+        tok = ctx.Tokenizer(m, vb, vo, "cl100k", ignore_merges=ignore)
         lat = []
         for i in range(n + 2):
             j = i % n
@@ -156,12 +449,12 @@ def front_end_options(sid, n=10):
             stream.synchronize()
             if i >= 2:
                 lat.append((time.perf_counter() - a) * 1e3)
-        out["ignore_merges" if ignore else "plain"] = round(percentile(lat, 50), 4)
+        res["ignore_merges" if ignore else "plain"] = round(percentile(lat, 50), 4)
         tok.close()
-    ign = {"workload": "C4 samples (1,000,000 chars, cl100k-style, 100,000 merges)", "p50_ms_plain": out["plain"],
-           "p50_ms_ignore_merges": out["ignore_merges"]}
+    ign = {"workload": "C4 samples (1,000,000 chars, cl100k-style, 100,000 merges)",
+           "device_resident_p50_ms_plain": res["plain"], "device_resident_p50_ms_ignore_merges": res["ignore_merges"]}
 
-    m, vb, vo = load_table(3)
+    m, vb, vo = ctx.load_table(3)
     lits = [("<|im_start|>", 50300), ("<|im_end|>", 50301), ("<|endoftext|>", 50302)]
     texts = []
     for s in range(n):
@@ -172,25 +465,23 @@ def front_end_options(sid, n=10):
             pos += 1400
             k += 1
         texts.append("".join(parts).encode("utf-8"))
-    res = {}
+    out = np.zeros(max(len(t) for t in texts), dtype=np.int32)
+    lres = {}
     for name, added in (("no_literals", None), ("literals", lits)):
-        tok = Tokenizer(m, vb, vo, "gpt2", added=added)
-        tok.encode(texts[0], sid)
+        tok = ctx.Tokenizer(m, vb, vo, "gpt2", added=added)
+        tok.encode_into(texts[0], out, sid)
         lat = []
         for t in texts:
             a = time.perf_counter()
-            tok.encode(t, sid)
+            tok.encode_into(t, out, sid)
             lat.append((time.perf_counter() - a) * 1e3)
-        res[name] = round(percentile(lat, 50), 4)
+        lres[name] = round(percentile(lat, 50), 4)
         tok.close()
     lit = {"workload": "C3 samples with a literal before every 1,400 characters (%d literals, %d bytes)"
                        % (len(texts[0].split(b"<|im_")) - 1, len(texts[0])),
-           "host_to_host_p50_ms_literal_handle": res["literals"],
-           "host_to_host_p50_ms_same_text_plain_handle": res["no_literals"]}
-    # the o200k-style and DeepSeek-style patterns (no table of their own: the
-    # multilingual table serves them), against cl100k-style on the same
-    # samples and table
-    m, vb, vo = load_table(4)
+           "host_to_host_p50_ms_literal_handle": lres["literals"],
+           "host_to_host_p50_ms_same_text_plain_handle": lres["no_literals"]}
+    m, vb, vo = ctx.load_table(4)
     o2 = {}
     for k in (3, 4):
         texts = [textgen.latency_sample(k, s).encode("utf-8") for s in range(n)]
@@ -198,7 +489,7 @@ def front_end_options(sid, n=10):
         d_out = torch.empty(max(len(t) for t in texts), dtype=torch.int32, device=dev)
         row = {}
         for pat in ("cl100k", "o200k", "deepseek"):
-            tok = Tokenizer(m, vb, vo, pat)
+            tok = ctx.Tokenizer(m, vb, vo, pat)
             lat = []
             for i in range(n + 2):
                 j = i % n
@@ -208,11 +499,100 @@ def front_end_options(sid, n=10):
                 stream.synchronize()
                 if i >= 2:
                     lat.append((time.perf_counter() - a) * 1e3)
-            row["p50_ms_" + pat] = round(percentile(lat, 50), 4)
+            row["device_resident_p50_ms_" + pat] = round(percentile(lat, 50), 4)
             tok.close()
         o2["C%d_samples" % k] = row
     o2["table"] = "C4 (100,000 merges)"
     return {"ignore_merges": ign, "added_tokens": lit, "other_patterns": o2}
+
+
+_BATCH_TABLE = None  # set before the worker processes fork, so no task carries the table
+
+
+def _oracle_batch_worker(data):
+    from oracle.tokenizer import encode as oracle_encode
+
+    return len(oracle_encode(data, _BATCH_TABLE, "cl100k"))
+
+
+def oracle_pool():
+    """Worker processes for the oracle's batch leg, forked before the GPU is
+    initialised, with C5's merge table already built."""
+    import multiprocessing as mp
+
+    from oracle.bpe import MergeTable
+    from workloads.tables import load_table, vocab_list
+
+    global _BATCH_TABLE
+    m, vb, vo = load_table(5)
+    _BATCH_TABLE = MergeTable(m.tolist(), vocab_list(vb, vo))
+    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    return mp.get_context("fork").Pool(workers), workers
+
+
+def cpu_baseline(k, head, c4, pool, workers):
+    """The oracle as it stands, on the GPU machine's host: a bounded sample of the
+    headline's requests (one thread pinned to one core, the tokenize call only),
+    a sample of C4's, and C5's 64-document batch over all host cores (one
+    document per task).  The IDs of the timed samples are compared with the
+    GPU's."""
+    from oracle.bpe import MergeTable
+    from oracle.tokenizer import encode as oracle_encode
+    from workloads import textgen
+    from workloads.tables import load_table, vocab_list
+
+    def one_core(cfg_k, block, n_samples):
+        raw, timed, counts, d_out, lens = block["_texts"]
+        m, vb, vo = load_table(cfg_k)
+        table = MergeTable(m.tolist(), vocab_list(vb, vo))
+        pat = textgen.CONFIGS[cfg_k]["pattern"]
+        affinity = os.sched_getaffinity(0)
+        core = min(affinity)
+        os.sched_setaffinity(0, {core})
+        dt, chars, same = 0.0, 0, True
+        try:
+            for i in timed[:n_samples]:
+                a = time.perf_counter()
+                ids = oracle_encode(raw[i], table, pat)
+                dt += time.perf_counter() - a
+                chars += len(raw[i].decode("utf-8"))
+                same &= d_out[i, : int(lens[i])].cpu().numpy().tolist() == ids
+        finally:
+            os.sched_setaffinity(0, affinity)
+        return dt, chars, same, core
+
+    dt, chars, same, core = one_core(k, head, 10)
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
+    n_cores = len(os.sched_getaffinity(0))
+    out = {"value": round(chars / dt, 1), "unit": "chars/s", "cores": 1, "kind": "oracle",
+           "sample": "10 of the timed 1,000,000-char C%d samples, one after another, one thread pinned to core %d, "
+                     "pure Python" % (k, core),
+           "seconds": round(dt, 2), "ids_identical_to_gpu": bool(same),
+           "host": {"cpu_model": model, "cores_visible": n_cores, "python": sys.version.split()[0]}}
+    if c4 is not None:
+        dt4, chars4, same4, _ = one_core(4, c4, 4)
+        out["c4"] = {"value": round(chars4 / dt4, 1), "unit": "chars/s", "cores": 1,
+                     "sample": "4 of the timed 1,000,000-char C4 samples, one thread pinned to core %d" % core,
+                     "seconds": round(dt4, 2), "ids_identical_to_gpu": bool(same4)}
+    # C5's batch over all host cores (the pool was forked before the GPU was touched)
+    docs = [d.encode("utf-8") for d in textgen.batch_docs()]
+    warm = docs[0].decode("utf-8")[:64].encode("utf-8")
+    pool.map(_oracle_batch_worker, [warm] * workers, chunksize=1)  # every worker has started
+    a = time.perf_counter()
+    counts = pool.map(_oracle_batch_worker, docs, chunksize=1)
+    dtb = time.perf_counter() - a
+    bchars = sum(len(d.decode("utf-8")) for d in docs)
+    sb = stored_shapes().get("C5_batch", {})
+    out["c5_batch_all_cores"] = {"value": round(bchars / dtb, 1), "unit": "chars/s", "cores": workers,
+                                 "sample": "C5's 64 x 16,384-char documents, one document per task",
+                                 "seconds": round(dtb, 3), "tokens": int(sum(counts)),
+                                 "tokens_match_shape_file": sum(counts) == sb.get("tokens")}
+    return out
 
 
 def main():
@@ -222,213 +602,60 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=(3, 4))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--quick", action="store_true", help="headline, C4 and device-resident figures only")
     ap.add_argument("--calibrate-copy", action="store_true", help="run the counter-calibration copy kernel first")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: the tokenizer runs on a single MI355X "
-              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        print("bench.py measures one GPU only: the tokenizer runs on a single MI355X and this "
+              "benchmark has no multi-GPU mode (--gpus %d requested)" % args.gpus, file=sys.stderr)
         sys.exit(2)
+    if args.steps < 1 or args.warmup < 0:
+        raise SystemExit("--steps must be >= 1 and --warmup >= 0")
 
-    import numpy as np
-    import torch
-
-    from paper_2607_29678_amd import Tokenizer
     from workloads import textgen
-    from workloads.tables import load_table
 
-    k = args.config
-    cfg = textgen.CONFIGS[k]
-    merges, vb, vo = load_table(k)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    stream = torch.cuda.current_stream(dev)
-    sid = stream.cuda_stream
-    tok = Tokenizer(merges, vb, vo, cfg["pattern"])
-
+    pool = workers = None
+    if not args.no_cpu and not args.quick:
+        pool, workers = oracle_pool()
+    ctx = Ctx()
     if args.calibrate_copy:
-        src = torch.arange(16 << 20, dtype=torch.int32, device=dev)
+        torch = ctx.torch
+        src = torch.arange(16 << 20, dtype=torch.int32, device=ctx.dev)
         dst = torch.empty_like(src)
         torch.add(src, 0, out=dst)  # reads 64 MiB, writes 64 MiB
         torch.cuda.synchronize()
         del src, dst
 
-    # seeded samples: warm-up samples are distinct from the timed ones
-    n_total = args.warmup + args.steps
-    texts = [textgen.latency_sample(k, s % 32).encode("utf-8") for s in range(n_total)]
-    d_in = [torch.from_numpy(np.frombuffer(t, dtype=np.uint8).copy()).to(dev) for t in texts]
-    cap = max(len(t) for t in texts)
-    d_out = torch.empty((len(texts), cap), dtype=torch.int32, device=dev)
-    d_len = torch.zeros(len(texts), dtype=torch.int64, device=dev)
-    n_chars = [len(t.decode("utf-8")) for t in texts]
-    torch.cuda.synchronize()
+    k = args.config
+    cfg = textgen.CONFIGS[k]
+    head = config_block(ctx, k, args.steps, args.warmup, extras=not args.quick)
+    other_k = 4 if k == 3 else 3
+    other = config_block(ctx, other_k, args.steps, args.warmup, extras=False)
+    lat = head.pop("_lat")
+    other.pop("_lat")
+    p50 = percentile(lat, 50)
+    value = 1_000_000 / (p50 * 1e-3)
 
-    def run(i):
-        tok.encode_device(d_in[i], len(texts[i]), d_out[i], d_len[i:i + 1], sid)
+    extra = {}
+    if not args.quick:
+        raw, timed = head["_texts"][0], head["_texts"][1]
+        extra["request_sizes"] = {"config": "C%d text" % k, "rows": sizes_block(ctx, k)}
+        extra["stress_c5"] = stress_block(ctx)
+        extra["large_request_device_resident"] = large_request(ctx, k, raw, timed)
+        extra["incremental_repair"] = incremental_repair(ctx, k)
+        extra["front_end_options"] = front_end_options(ctx)
 
-    for i in range(args.warmup):
-        run(i)
-    torch.cuda.synchronize()
-
-    # --- timed region: K requests back to back, stage events recorded -------
-    timed = list(range(args.warmup, n_total))
-    tok.set_profiling(len(timed))
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in timed:
-        run(i)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    stage_calls = tok.stage_times(sid)
-    tok.set_profiling(0)
-    chars = sum(n_chars[i] for i in timed)
-    value = chars / elapsed
-    lens = d_len.cpu().numpy()
-    if (lens[timed] <= 0).any():
-        raise SystemExit("tokenizer reported an error: %s" % lens[timed])
-    stage_avg = {s: sum(c[s] for c in stage_calls) / len(stage_calls) for s in stage_calls[0]}
-
-    # --- per-request latency (enqueue to completion, input in HBM) -----------
-    lat = []
-    for i in timed:
-        torch.cuda.synchronize()
-        a = time.perf_counter()
-        run(i)
-        stream.synchronize()
-        lat.append((time.perf_counter() - a) * 1e3)
-
-    # --- host-to-host latency through tt_encode (PCIe copies included) --------
-    host_lat = []
-    for i in timed[: min(10, len(timed))]:
-        a = time.perf_counter()
-        tok.encode(texts[i], sid)
-        host_lat.append((time.perf_counter() - a) * 1e3)
-
-    # --- steady state: 100 re-encodes of one sample (input in HBM) --------------
-    steady = []
-    for _ in range(100):
-        torch.cuda.synchronize()
-        a = time.perf_counter()
-        run(timed[0])
-        stream.synchronize()
-        steady.append((time.perf_counter() - a) * 1e3)
-
-    # --- span export: IDs with byte and character spans (device-resident) -----
-    d_spans = torch.empty((cap, 4), dtype=torch.int32, device=dev)
-    d_sids = torch.empty(cap, dtype=torch.int32, device=dev)
-    d_slen = torch.zeros(1, dtype=torch.int64, device=dev)
-    span_lat = []
-    for i in timed:
-        torch.cuda.synchronize()
-        a = time.perf_counter()
-        tok.encode_spans_device(d_in[i], len(texts[i]), d_sids, d_spans, d_slen, sid)
-        stream.synchronize()
-        span_lat.append((time.perf_counter() - a) * 1e3)
-    if int(d_slen.item()) != int(lens[timed[-1]]):
-        raise SystemExit("span export returned a different token count")
-
-    # --- shape of the work: pieces of one sample (split-level export) ----------
-    starts = tok.pretokenize(texts[timed[0]], sid)
-    n_pieces = len(starts)
-    longest_piece = int(np.max(np.diff(np.append(starts, len(texts[timed[0]]))))) if n_pieces else 0
-
-    # --- throughput with the chip full: the timed samples as one request -------
-    # (a 1,000,000-char request fills about two thirds of the resident tile
-    # slots once, so its time is one tile's latency; a request of all timed
-    # samples runs many tiles per slot)
-    big = b"".join(texts[i] for i in timed)
-    d_big = torch.from_numpy(np.frombuffer(big, dtype=np.uint8).copy()).to(dev)
-    d_bout = torch.empty(len(big), dtype=torch.int32, device=dev)
-    d_blen = torch.zeros(1, dtype=torch.int64, device=dev)
-    tok.encode_device(d_big, len(big), d_bout, d_blen, sid)
-    torch.cuda.synchronize()
-    big_lat = []
-    for _ in range(10):
-        a = time.perf_counter()
-        tok.encode_device(d_big, len(big), d_bout, d_blen, sid)
-        stream.synchronize()
-        big_lat.append((time.perf_counter() - a) * 1e3)
-    big_T = int(d_blen.item())
-    if big_T <= 0:
-        raise SystemExit("tokenizer reported an error on the joined request: %d" % big_T)
-    big_chars = sum(n_chars[i] for i in timed)
-    big_ms = percentile(big_lat, 50)
-    large_request = {"chars": big_chars, "bytes": len(big), "tokens": big_T, "p50_ms": round(big_ms, 4),
-                     "chars_per_s": round(big_chars / (big_ms * 1e-3), 1),
-                     "hbm_frac": round((len(big) + 4.0 * big_T) / (big_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)}
-    del d_big, d_bout
-
-    # --- a batch of 64 independent 16,384-char documents (the stress config's
-    # batch, its own tokenizer), host to host through tt_encode_batch -----------
-    bmerges, bvb, bvo = load_table(5)
-    btok = Tokenizer(bmerges, bvb, bvo, textgen.CONFIGS[5]["pattern"])
-    docs = [d.encode("utf-8") for d in textgen.batch_docs()]
-    btok.encode_batch(docs, sid)
-    blat = []
-    for _ in range(10):
-        a = time.perf_counter()
-        btok.encode_batch(docs, sid)
-        blat.append((time.perf_counter() - a) * 1e3)
-    bchars = sum(len(d.decode("utf-8")) for d in docs)
-    batch = {"docs": len(docs), "chars": bchars, "bytes": sum(len(d) for d in docs),
-             "p50_ms_host_to_host": round(percentile(blat, 50), 4),
-             "chars_per_s": round(bchars / (percentile(blat, 50) * 1e-3), 1)}
-    btok.close()
-
-    # --- incremental repair: appends to a stored session (Sec. 3.2) ------------
-    repair = incremental_repair(tok, k, sid)
-
-    # --- front-end options: ignore_merges and added-token literals ----------------
-    options = front_end_options(sid)
-
-    # --- roofline of the dominant kernel -------------------------------------
-    # algorithmic bytes of one tile-kernel launch: the request's bytes are
-    # read once and its token IDs written once (merge-table probes are L2
-    # traffic, not HBM traffic, for tables of a few MB)
-    B_avg = sum(len(texts[i]) for i in timed) / len(timed)
-    T_avg = float(np.mean(lens[timed]))
-    tile_ms = stage_avg["tile"]
-    alg = B_avg + 4.0 * T_avg
-    achieved = alg / (tile_ms * 1e-3) / 1e9
-    roofline = {"kernel": "tile_kernel", "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
-                "traffic": measured_traffic(k), "algorithmic_bytes": int(alg),
-                "kernel_ms": round(tile_ms, 4)}
-
-    # --- CPU oracle baseline on the timed samples --------------------------------
     cpu = None
-    if not args.no_cpu:
-        from oracle.bpe import MergeTable
-        from oracle.tokenizer import encode as oracle_encode
-        from workloads.tables import vocab_list
-
-        table = MergeTable(merges.tolist(), vocab_list(vb, vo))
-        host_ids = d_out.cpu().numpy()
-        same = True
-        dt = 0.0
-        # one process pinned to one core, timing the tokenize call only
-        affinity = os.sched_getaffinity(0)
-        core = min(affinity)
-        os.sched_setaffinity(0, {core})
-        try:
-            for i in timed:
-                a = time.perf_counter()
-                ids = oracle_encode(texts[i], table, cfg["pattern"])
-                dt += time.perf_counter() - a
-                same &= host_ids[i, : int(lens[i])].tolist() == ids
-        finally:
-            os.sched_setaffinity(0, affinity)
-        model = ""
-        try:
-            with open("/proc/cpuinfo") as f:
-                model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
-        except OSError:
-            pass
-        cpu = {"value": round(sum(n_chars[i] for i in timed) / dt, 1), "unit": "chars/s", "cores": 1,
-               "kind": "oracle",
-               "sample": "the %d timed 1,000,000-char samples, one after another, one thread pinned to core %d, "
-                         "pure Python" % (len(timed), core),
-               "seconds": round(dt, 2), "ids_identical_to_gpu": bool(same),
-               "host": {"cpu_model": model, "cores_visible": len(affinity), "python": sys.version.split()[0]}}
+    if not args.no_cpu and not args.quick:
+        cpu = cpu_baseline(k, head, other if other_k == 4 else head, pool, workers)
+        pool.close()
+        pool.join()
+    head.pop("_texts")
+    other.pop("_texts")
+    shapes = stored_shapes()
+    sh = shapes.get("C%d_latency_sample_3" % k)
+    if sh and args.warmup == 3:
+        head["workload"]["first_timed_oracle_shape"] = sh
 
     out = {
         "metric": "exact-tokenization chars/sec and P50 latency for a 1M-char request, 1 MI355X",
@@ -437,31 +664,30 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(elapsed * 1e3 / len(timed), 4),
+        "ms_per_step": round(sum(lat) / len(lat), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int32",
         "data": "synthetic",
-        "config": {"workload": "C%d: 1,000,000-char seeded %s request, %s-style pattern, %d merges"
+        "config": {"workload": "C%d: 1,000,000-char seeded %s requests, %s-style pattern, %d merges; each of "
+                               "%d distinct samples tokenized once through tt_encode, host bytes in, host int32 IDs "
+                               "out (pageable caller buffers)"
                                % (k, "agent-transcript" if k == 3 else "multilingual agent-transcript",
-                                  cfg["pattern"], cfg["merges"]),
-                   "chars": 1_000_000, "bytes_avg": int(B_avg), "tokens_avg": int(T_avg), "samples": len(timed),
-                   "pieces_sample0": n_pieces, "longest_piece_bytes_sample0": longest_piece},
-        "p50_ms": round(percentile(lat, 50), 4),
+                                  cfg["pattern"], cfg["merges"], args.steps),
+                   "chars": 1_000_000, "bytes_avg": head["workload"]["bytes_avg"],
+                   "tokens_avg": head["workload"]["tokens_avg"], "samples": args.steps},
+        "p50_ms": round(p50, 4),
         "p90_ms": round(percentile(lat, 90), 4),
         "p99_ms": round(percentile(lat, 99), 4),
-        "host_to_host_p50_ms": round(percentile(host_lat, 50), 4),
-        "steady_state_p50_ms": round(percentile(steady, 50), 4),
-        "span_export_p50_ms": round(percentile(span_lat, 50), 4),
-        "large_request": large_request,
-        "batch_64x16k": batch,
-        "incremental_repair": repair,
-        "front_end_options": options,
-        "stage_ms": {s: round(v, 4) for s, v in stage_avg.items()},
-        "roofline": roofline,
+        "latency_scope": "host to host through tt_encode (stage-in, tile kernel, stage-out)",
+        "headline_detail": head,
+        "C%d" % other_k: other,
+        **extra,
+        "roofline": head["roofline"],
         "cpu_baseline": cpu,
-        "context": {"paper_p50_ms_1M_chars": 0.87, "paper_hardware": "RTX PRO 6000 Blackwell (Qwen3 real text)"},
+        "context": {"paper_p50_ms_1M_chars": 0.87, "paper_hardware": "RTX PRO 6000 Blackwell (Qwen3 real text, "
+                    "array delivery)", "paper_llama31_p50_ms_1M_chars": 0.80},
     }
     print(json.dumps(out))
 
