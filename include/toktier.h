@@ -187,6 +187,27 @@ int tt_encode(tt_tokenizer* h, const uint8_t* utf8, int64_t len, int32_t* out_id
 int tt_encode_device(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_t* d_out_ids,
                      int64_t* d_out_len, void* stream);
 
+/* tt_encode_device for callers that cannot allocate: code under stream
+ * capture, tight serving loops, and hosts that forbid allocation while
+ * serving.  The same arguments, layout, results and asynchrony as
+ * tt_encode_device, and the same kernels; the call allocates nothing.  Its
+ * workspace is one fixed array of device memory per GPU, reserved when the
+ * library is loaded on that GPU and held until the process ends (about 43 MB
+ * for TT_NOALLOC_MAX_BYTES); the call does no memory allocation, on the device
+ * or on the host.
+ *  - len > TT_NOALLOC_MAX_BYTES returns TT_ERR_TOO_LARGE (nothing is enqueued).
+ *  - Handles with added-token literals return TT_ERR_BAD_ARG.
+ *  - Every call on a GPU uses that GPU's one array: calls on one GPU whose
+ *    work overlaps (other streams, other host threads, other handles) race and
+ *    must be ordered by the caller.  Calls in stream order are independent:
+ *    each call takes a new call number on the host, so the array's words from
+ *    earlier calls are never mistaken for its own.  For the same reason a
+ *    captured call cannot be replayed.
+ *  - No stage events are recorded (tt_set_profiling does not apply). */
+#define TT_NOALLOC_MAX_BYTES ((int64_t)1 << 21)
+int tt_encode_device_noalloc(tt_tokenizer* h, const uint8_t* d_utf8, int64_t len, int32_t* d_out_ids,
+                             int64_t* d_out_len, void* stream);
+
 /* Tokenize a batch of independent documents in one call (Sec. 4.2: documents
  * are concatenated and runs are cut at document boundaries; no piece or token
  * crosses a document boundary).

@@ -9,7 +9,7 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libtoktier.so")
-SOURCES = ["tt_api.hip", "tt_tile.hip", "tt_batch.hip", "tt_spans.hip", "tt_session.hip", "tt_copy.cpp"]
+SOURCES = ["tt_api.hip", "tt_tile.hip", "tt_batch.hip", "tt_spans.hip", "tt_session.hip", "tt_copy.cpp", "tt_noalloc.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

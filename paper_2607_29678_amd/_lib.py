@@ -16,6 +16,7 @@ TT_PATTERN_CL100K = 1
 TT_PATTERN_O200K = 2
 TT_PATTERN_DEEPSEEK = 3
 TT_MAX_BYTES = 1 << 30
+TT_NOALLOC_MAX_BYTES = 1 << 21
 
 STATUS = {
     0: "TT_OK",
@@ -40,6 +41,7 @@ SIGNATURES = {
     "tt_destroy": (None, [_P]),
     "tt_encode": (ctypes.c_int, [_P, _P, _I64, _P, ctypes.POINTER(_I64), _P]),
     "tt_encode_device": (ctypes.c_int, [_P, _P, _I64, _P, _P, _P]),
+    "tt_encode_device_noalloc": (ctypes.c_int, [_P, _P, _I64, _P, _P, _P]),
     "tt_encode_batch": (ctypes.c_int, [_P, _P, _P, _I32, _P, _P, _P]),
     "tt_encode_spans": (ctypes.c_int, [_P, _P, _I64, _P, _P, ctypes.POINTER(_I64), _P]),
     "tt_encode_spans_device": (ctypes.c_int, [_P, _P, _I64, _P, _P, _P, _P]),

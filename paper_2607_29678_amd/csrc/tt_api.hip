@@ -380,10 +380,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_len = out_len;
   w.out_doc_off = out_docs;
   w.out_spans = out_spans;
-  DevTables tb{h->d_slots, h->nb,     h->d_pair0,  h->d_join,  h->d_ext,     h->n_ids,
-               h->d_dict,  h->dnb,    h->d_dict2,  h->dnb2,    h->d_toklen,  h->vmax,
-               h->d_vdict, h->vdnb,   h->d_vdict2, h->vdnb2,   h->d_vlong,   h->vlnb,
-               h->d_vblob};
+  const DevTables tb = handle_tables(h);
   const int ring = h->profile;
   if (ring != s->ring) {  // (re)size the event ring
     for (auto e : s->ev)
@@ -625,6 +622,14 @@ void added_documents(const AddedSet& added, const uint8_t* t, int64_t a, int64_t
 
 namespace tt {
 int handle_pattern(const tt_tokenizer* h) { return h->pattern; }
+int handle_device(const tt_tokenizer* h) { return h->device; }
+bool handle_ignore(const tt_tokenizer* h) { return h->ignore; }
+DevTables handle_tables(const tt_tokenizer* h) {
+  return DevTables{h->d_slots, h->nb,     h->d_pair0,  h->d_join,  h->d_ext,   h->n_ids,
+                   h->d_dict,  h->dnb,    h->d_dict2,  h->dnb2,    h->d_toklen, h->vmax,
+                   h->d_vdict, h->vdnb,   h->d_vdict2, h->vdnb2,   h->d_vlong, h->vlnb,
+                   h->d_vblob};
+}
 bool handle_has_added(const tt_tokenizer* h) { return !h->added.empty(); }
 uint32_t handle_max_token_bytes(const tt_tokenizer* h) { return h->max_tok_bytes; }
 

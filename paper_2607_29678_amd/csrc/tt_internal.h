@@ -279,8 +279,12 @@ hipError_t launch_doc_offsets(const Work& w, hipStream_t s);
 // span export, after the tile kernel: byte ends and character spans
 hipError_t launch_spans(const Work& w, hipStream_t s);
 
-// Facts of a handle for the host-side session code.
+// Facts of a handle for the host-side session code and the entry points
+// outside tt_api.hip.
 int handle_pattern(const tt_tokenizer* h);
+int handle_device(const tt_tokenizer* h);
+bool handle_ignore(const tt_tokenizer* h);  // ignore_merges
+DevTables handle_tables(const tt_tokenizer* h);
 bool handle_has_added(const tt_tokenizer* h);  // added-token literals (sessions do not take them)
 uint32_t handle_max_token_bytes(const tt_tokenizer* h);  // longest token, in bytes
 // span export of a small host request with one synchronisation (pinned buffers)

@@ -165,6 +165,14 @@ class Tokenizer:
                                         _stream(stream))
         _lib.check(st, "tt_encode_device")
 
+    def encode_device_noalloc(self, d_utf8, length, d_out_ids, d_out_len, stream=None):
+        """``tt_encode_device_noalloc``: as ``encode_device``, with the library's fixed per-GPU
+        workspace (no allocation; at most ``TT_NOALLOC_MAX_BYTES`` bytes; overlapping calls on one GPU
+        race)."""
+        st = self._lib.tt_encode_device_noalloc(self._h, _ptr(d_utf8), int(length), _ptr(d_out_ids),
+                                                _ptr(d_out_len), _stream(stream))
+        _lib.check(st, "tt_encode_device_noalloc")
+
     def encode_spans_device(self, d_utf8, length, d_out_ids, d_out_spans, d_out_len, stream=None):
         """``tt_encode_spans_device``: enqueue on ``stream``; d_out_spans holds 4 int32 per token."""
         st = self._lib.tt_encode_spans_device(self._h, _ptr(d_utf8), int(length), _ptr(d_out_ids),

@@ -21,7 +21,8 @@ def _declared():
 
 
 def test_header_declares_the_boundary():
-    assert _declared() == sorted(["tt_create", "tt_create_ex", "tt_destroy", "tt_encode", "tt_encode_device", "tt_encode_batch",
+    assert _declared() == sorted(["tt_create", "tt_create_ex", "tt_destroy", "tt_encode", "tt_encode_device",
+                                  "tt_encode_device_noalloc", "tt_encode_batch",
                                   "tt_encode_spans", "tt_encode_spans_device", "tt_pretokenize",
                                   "tt_status_string", "tt_info", "tt_set_profiling", "tt_stage_times",
                                   "tt_session_create", "tt_session_destroy", "tt_session_append",
