@@ -90,3 +90,39 @@ def test_o200k_table_equals_oracle_classes():
     bad = [cp for cp in range(0x110000) if not 0xD800 <= cp <= 0xDFFF
            and _four_bit(l1, l2, cp) != code.get(o200k_class(cp), 0)]
     assert bad == [], bad[:10]
+
+
+def _two_bit(l1, l2, cp):
+    return (l2[l1[cp >> 8] * 64 + ((cp & 255) >> 2)] >> ((cp & 3) * 2)) & 3
+
+
+def test_base_table_equals_oracle_classes():
+    """The GPT-2- and cl100k-style table (letters, numbers, whitespace, other)
+    against the oracle's classes for every scalar value: a skew between class
+    tables is exactly the failure the paper reports between Unicode versions."""
+    from oracle.classes import L, N, W, char_class
+
+    l1, l2 = _arrays("class_table.inc", "TT_CLS_L1", "TT_CLS_L2")
+    code = {L: 1, N: 2, W: 3}
+    bad = [cp for cp in range(0x110000) if not 0xD800 <= cp <= 0xDFFF
+           and _two_bit(l1, l2, cp) != code.get(char_class(cp), 0)]
+    assert bad == [], bad[:10]
+
+
+def test_base_ascii_formula_equals_oracle():
+    """The kernels classify ASCII by formula (char_code in tt_tile.hip), not by
+    the table: letters, digits, CR/LF and the other whitespace, else other."""
+    from oracle.classes import L, N, W, char_class
+
+    def formula(cp):
+        if 0 <= (cp | 32) - ord("a") < 26:
+            return L
+        if 0 <= cp - ord("0") < 10:
+            return N
+        if cp in (10, 13) or cp == 32 or 0 <= cp - 9 < 5:
+            return W
+        return None
+
+    for cp in range(128):
+        want = char_class(cp)
+        assert formula(cp) == (want if want in (L, N, W) else None), cp

@@ -246,3 +246,23 @@ def test_splice_plan_argument_errors():
         splice_plan(b"abc", 2, 0, [1], [(0, 1, 0, 1)], [1], [(0, 1, 0, 1)], 4)  # x must be > 0
     with pytest.raises(TokTierError):
         splice_plan(b"abc", 5, 1, [1], [(0, 1, 0, 1)], [1], [(0, 1, 0, 1)], 4)  # A longer than the text
+
+
+def test_deepseek_sync_boundaries_long_contexts():
+    """The DeepSeek-style set on longer strings (24 to 64 characters) than the
+    exhaustive and random checks above, so that every listed transition is met
+    with long runs on both sides (letter runs, punctuation runs absorbing CR/LF,
+    whitespace runs with and without CR/LF, number groups, CJK/kana stretches,
+    unmatched stretches of control characters)."""
+    rng = random.Random(0xD5EE)
+    runs = ["abc", "Zq", "été", "́", "...", "、。", "¿", "   ", "\t \t", "\r\n", "\n\n ",
+            "\x01\x02", "12345", "中文", "゙", "゛゛", "぀", "'s", " .", "-x"]
+    memo = {}
+    hits = 0
+    for _ in range(1000):
+        text = ""
+        target = rng.randint(24, 64)
+        while len(text) < target:
+            text += rng.choice(runs)
+        hits += _check_string(text, "deepseek", memo)
+    assert hits > 10000
