@@ -223,6 +223,7 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
   // words that carry epochs or the ticket come first: they are cleared once here
   size_t o_ctrl = take(sizeof(Ctrl));
   size_t o_tsum = take(8 * NT);
+  size_t o_tend = take(8 * NT);
   size_t o_tlast = take(8 * NT);
   size_t o_tagg = take(8 * NT);
   size_t o_tcagg = take(8 * NT);
@@ -251,6 +252,7 @@ int ws_reserve(Workspace* s, uint64_t need, hipStream_t st) {
   Work& w = s->w;
   w.ctrl = reinterpret_cast<Ctrl*>(b + o_ctrl);
   w.tile_sum = reinterpret_cast<uint64_t*>(b + o_tsum);
+  w.tile_end = reinterpret_cast<uint64_t*>(b + o_tend);
   w.tile_last = reinterpret_cast<uint64_t*>(b + o_tlast);
   w.tile_agg = reinterpret_cast<uint64_t*>(b + o_tagg);
   w.tile_cagg = reinterpret_cast<uint64_t*>(b + o_tcagg);

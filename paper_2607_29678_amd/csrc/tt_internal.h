@@ -239,7 +239,9 @@ struct Work {
   uint32_t epoch;           // this call's epoch
   uint32_t ticket_base;     // first tile ticket of this call
   uint32_t n_tiles;
-  uint64_t* tile_sum;       // [tiles] (epoch << 32) | trailing-run summary (cl100k carries)
+  uint64_t* tile_sum;       // [tiles] (epoch << 32) | trailing-run summary (cl100k carries), or the
+                            // start of the tile's last piece (walked patterns)
+  uint64_t* tile_end;       // [tiles] walked patterns: (epoch << 32) | end of the tile's last piece
   uint64_t* tile_last;      // [tiles] (epoch << 32) | last unit start in the tile, or NO_START
   uint64_t* tile_agg;       // [tiles] output counts for the placement look-back (epoch-tagged)
   uint64_t* tile_cagg;      // [tiles] span export: non-continuation byte counts, same protocol

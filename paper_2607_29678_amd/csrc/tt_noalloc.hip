@@ -22,12 +22,13 @@ namespace {
 constexpr uint64_t NA_MAX = TT_NOALLOC_MAX_BYTES;
 constexpr uint64_t NA_TILES = (NA_MAX + PT_OWN - 1) / PT_OWN + 1;
 constexpr uint64_t align256(uint64_t x) { return (x + 255) / 256 * 256; }
-// layout: control word, three arrays of epoch-tagged tile words (cleared at
+// layout: control word, four arrays of epoch-tagged tile words (cleared at
 // set-up), staging of incoming units (4 B per byte), rows of long units
 // (4 words per byte, then the selection masks)
 constexpr uint64_t NA_CTRL = 0;
 constexpr uint64_t NA_TSUM = NA_CTRL + align256(sizeof(Ctrl));
-constexpr uint64_t NA_TLAST = NA_TSUM + align256(8 * NA_TILES);
+constexpr uint64_t NA_TEND = NA_TSUM + align256(8 * NA_TILES);
+constexpr uint64_t NA_TLAST = NA_TEND + align256(8 * NA_TILES);
 constexpr uint64_t NA_TAGG = NA_TLAST + align256(8 * NA_TILES);
 constexpr uint64_t NA_CLEAR = NA_TAGG + align256(8 * NA_TILES);  // bytes cleared at set-up
 constexpr uint64_t NA_STAGE = NA_CLEAR;
@@ -102,6 +103,7 @@ extern "C" int tt_encode_device_noalloc(tt_tokenizer* h, const uint8_t* d_utf8, 
   w.ticket_base = ds.ticket_base;
   w.n_tiles = n_tiles_for((uint32_t)len);
   w.tile_sum = reinterpret_cast<uint64_t*>(b + NA_TSUM);
+  w.tile_end = reinterpret_cast<uint64_t*>(b + NA_TEND);
   w.tile_last = reinterpret_cast<uint64_t*>(b + NA_TLAST);
   w.tile_agg = reinterpret_cast<uint64_t*>(b + NA_TAGG);
   w.stage = reinterpret_cast<uint32_t*>(b + NA_STAGE);

@@ -64,6 +64,16 @@ __device__ __forceinline__ uint64_t ld_word(const uint64_t* p) {
 __device__ __forceinline__ void st_word(uint64_t* p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// One lane waits for a word tagged with the call's epoch in its high half,
+// sleeping between polls so that the wave does not flood the cache with loads.
+__device__ __forceinline__ uint64_t wait_word(const uint64_t* p, uint32_t epoch) {
+  uint64_t x = ld_word(p);
+  while ((uint32_t)(x >> 32) != epoch) {
+    __builtin_amdgcn_s_sleep(1);
+    x = ld_word(p);
+  }
+  return x;
+}
 
 constexpr int CLS_L1_BYTES = 4352, CLS_L2_BYTES = TT_CLS_NBLOCKS * 64;
 
@@ -370,6 +380,7 @@ struct PtShared {
   uint32_t carry_nlpre;       // cl100k: class before a CR/LF stretch entering the tile
   uint32_t cwave[PT_THREADS / 64];  // span export: per-wave sums
   int64_t o2_doc_after;          // walked patterns, batch: first document start after the window
+  int64_t o2_last_s, o2_last_e;  // walked patterns: the tile's last piece (window indices)
   uint32_t whole[PT_WIN / 32];  // ignore_merges: starts of pieces that are vocabulary entries
   uint32_t cbase;             // span export: non-continuation bytes before the tile
   uint32_t ctile;             // span export: non-continuation bytes the tile owns
@@ -935,10 +946,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       if (need && lane == 0) {
         uint32_t acc = 0, pre = C_NONE;
         for (int64_t j = (int64_t)t - 1; j >= 0; --j) {
-          uint64_t x;
-          do {
-            x = ld_word(&w.tile_sum[j]);
-          } while ((uint32_t)(x >> 32) != w.epoch);
+          const uint64_t x = wait_word(&w.tile_sum[j], w.epoch);
           const uint32_t v = (uint32_t)x;
           acc += (v >> 1) & 3u;
           if (!(v & SUM_RUNALL)) {
@@ -1032,19 +1040,33 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     // a wave runs as long as its busiest lane, not its longest segment of
     // every start
     // thread 0 first walks the segment that the tile's first bytes continue,
-    // from its start in the left context, else from the last piece start the
-    // previous tile published
+    // from its start in the left context, else from the end of the last piece
+    // of the previous tile (which holds the previous tile's last byte, so its
+    // end is at or after this tile's first byte).  When that piece also holds
+    // this tile's last byte, the tile has no piece start of its own and
+    // passes the piece on without walking: a long piece is walked once, by the
+    // tile it starts in, not again by every tile it covers.
+    // The last piece of the tile (the one that holds its last byte) is kept in
+    // last_s / last_e for the next tile.
+    if (tid == 0) {
+      sh.o2_last_s = PT_HALO;  // (kept only for invalid text, whose output is discarded)
+      sh.o2_last_e = own_end;
+    }
     int64_t first = -1;
     if (tid == 0 && !segbit(PT_HALO)) {
       for (int q = PT_HALO - 1; q >= 0 && first < 0; --q)
         if (segbit(q)) first = q;
       if (first < 0 && t == 0) first = PT_HALO;  // (invalid text: no character at the text start)
       if (first < 0) {
-        uint64_t x;
-        do {
-          x = ld_word(&w.tile_sum[t - 1]);
-        } while ((uint32_t)(x >> 32) != w.epoch);
-        first = (int64_t)(uint32_t)x - w0;
+        const uint64_t xs = wait_word(&w.tile_sum[t - 1], w.epoch);
+        const uint64_t xe = wait_word(&w.tile_end[t - 1], w.epoch);
+        const int64_t ps = (int64_t)(uint32_t)xs - w0, pe = (int64_t)(uint32_t)xe - w0;
+        if (pe >= own_end) {
+          sh.o2_last_s = ps;
+          sh.o2_last_e = pe;
+        } else {
+          first = pe < PT_HALO ? PT_HALO : pe;  // (pe < PT_HALO only for invalid text)
+        }
       }
     }
     uint32_t todo = 0;  // bit j: own position qb + j starts a segment to walk
@@ -1058,12 +1080,14 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       todo &= todo - 1u;
     }
     bool active = on_first || s != -1;
-    int64_t first_end = PT_HALO;  // the last start thread 0's first walk visits (stays so only for invalid text)
 #pragma unroll 1
     while (active) {
       if (s >= PT_HALO) sh.ph.a.o2piece[s] = 1;  // (s < own_end <= PT_WIN)
-      if (on_first) first_end = s;
       const int64_t e = DS ? ds_piece_end(v, s) : o2_piece_end(v, s);
+      if (e >= own_end) {  // the tile's last piece (one lane finds it)
+        sh.o2_last_s = s;
+        sh.o2_last_e = e;
+      }
       if (e < own_end && !segbit(e)) {
         s = e;
       } else if (todo) {
@@ -1077,21 +1101,11 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     __syncthreads();
     const uint32_t pw = *reinterpret_cast<const uint32_t*>(&sh.ph.a.o2piece[qb]);
     flags = (pw & 1u) | ((pw >> 7) & 2u) | ((pw >> 14) & 4u) | ((pw >> 21) & 8u);
-    // later tiles may start from this tile's last piece: the last start in
-    // its bytes, else the last one the first walk visited (before them)
-    {
-      const uint64_t any = __ballot(flags != 0u);
-      const int hi_lane = any ? 63 - __builtin_clzll(any) : -1;
-      if (lane == hi_lane) sh.wave_tot[wave] = (uint32_t)(qb + 31 - __builtin_clz(flags));
-      if (lane == 0 && !any) sh.wave_tot[wave] = 0xFFFFFFFFu;
-    }
-    __syncthreads();
+    // the next tile continues from this tile's last piece
     if (tid == 0) {
-      int64_t lastp = INT64_MIN;
-      for (int v2 = PT_THREADS / 64 - 1; v2 >= 0 && lastp == INT64_MIN; --v2)
-        if (sh.wave_tot[v2] != 0xFFFFFFFFu) lastp = sh.wave_tot[v2];
-      if (lastp == INT64_MIN) lastp = first_end;
-      st_word(&w.tile_sum[t], ((uint64_t)w.epoch << 32) | (uint32_t)(w0 + lastp));
+      const uint64_t ep = (uint64_t)w.epoch << 32;
+      st_word(&w.tile_end[t], ep | (uint32_t)(w0 + sh.o2_last_e));
+      st_word(&w.tile_sum[t], ep | (uint32_t)(w0 + sh.o2_last_s));
     }
   }
   uint32_t scan_st = s0;  // cl100k: scan state before position q
@@ -1284,10 +1298,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   if (has_inc && (uint32_t)tid == m_proc % (uint32_t)PT_THREADS) {
     uint32_t found = NO_START;
     for (int64_t j = (int64_t)t - 1; j >= 0; --j) {
-      uint64_t x;
-      do {
-        x = ld_word(&w.tile_last[j]);
-      } while ((uint32_t)(x >> 32) != w.epoch);
+      const uint64_t x = wait_word(&w.tile_last[j], w.epoch);
       if ((uint32_t)x != NO_START) {
         found = (uint32_t)x;
         break;
