@@ -232,7 +232,11 @@ def config_block(ctx, k, steps, warmup, extras=True):
     kernel_ms = sum(kern) / len(kern)
     res["workload"] = {"chars": n_chars[timed[0]], "bytes_avg": int(B_avg), "tokens_avg": int(T_avg)}
     res["roofline"] = roofline_of(B_avg, T_avg, kernel_ms, measured_traffic(k))
-    res["roofline"]["kernel_ms_from"] = "HIP events around the tile kernel of the %d timed tt_encode calls" % steps
+    res["roofline"]["kernel_ms_from"] = ("HIP events around the tile kernel of the %d timed tt_encode calls, which "
+                                         "read the request from pinned host memory over PCIe" % steps)
+    res["roofline_device_resident"] = roofline_of(B_avg, T_avg, sum(dkern) / len(dkern), None)
+    res["roofline_device_resident"]["kernel_ms_from"] = ("HIP events around the tile kernel of tt_encode_device "
+                                                         "on the same samples, request and IDs in HBM")
     if extras:
         # steady state: 100 re-encodes of one sample, input in HBM
         st, _ = device_calls(ctx, tok, [d_in[timed[0]]] * 100, [len(raw[timed[0]])] * 100, d_out[0], d_len[0:1])

@@ -163,9 +163,9 @@ void tt_destroy(tt_tokenizer* h);
  *  out_len        receives the number of IDs written.
  * Blocks until out_ids/out_len are valid, with one host synchronisation for
  * requests up to 256 MiB (Sec. 4.3: the single-request path keeps the host
- * out of the chain).  The request goes to the device in one copy, straight
- * from utf8 when it is pinned host memory, else through pinned staging; the
- * IDs come back in one copy started before their count is known, sized from
+ * out of the chain).  The device reads the request straight from utf8 when
+ * it is pinned host memory, else from a pinned copy; the IDs come back in one
+ * copy started before their count is known, sized from
  * the IDs-per-byte ratio of the stream's recent requests (a request with more
  * IDs takes a second copy of the rest), straight into out_ids when it is
  * pinned.  Staging copies of at least 256 KiB are split among the calling

@@ -415,8 +415,10 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
 constexpr uint64_t PINNED_MAX = 1ull << 28;
 
 // tt_encode through pinned staging, with one host synchronisation.
-//  - stage-in: one DMA, from the caller's buffer when it is pinned, else from a
-//    pinned copy;
+//  - stage-in: the tile kernel reads the request straight from pinned host
+//    memory (the caller's buffer when it is pinned, else a pinned copy): each
+//    tile fetches its window over the bus as it starts, so the transfer
+//    overlaps the tiles' work instead of preceding the launch;
 //  - the tile kernel places the IDs in device memory and its last tile writes
 //    the output length straight into pinned host memory;
 //  - stage-out: the IDs are copied back before their count is known, as many as
@@ -436,9 +438,8 @@ int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t le
   } else if (!pin_out) {
     host_copy_wake();  // for the copy of the IDs
   }
-  if (hipMemcpyAsync(s->d_in, src, (size_t)len, hipMemcpyHostToDevice, st) != hipSuccess) return TT_ERR_HIP;
   *s->h_len = 0;
-  rc = run_chain(h, s, s->d_in, (uint32_t)len, nullptr, 0, s->d_out, s->h_len, nullptr, st, 1);
+  rc = run_chain(h, s, src, (uint32_t)len, nullptr, 0, s->d_out, s->h_len, nullptr, st, 1);
   if (rc) return rc;
   int32_t* dst = pin_out ? out_ids : s->h_ids;
   const int64_t guess = std::min<int64_t>(len, (int64_t)(s->id_ratio * (double)len) + 1024);
