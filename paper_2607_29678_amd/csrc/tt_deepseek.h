@@ -68,6 +68,32 @@ __host__ __device__ inline uint32_t ds_ascii_class(uint32_t cp) {
   return DS_O;
 }
 
+// The DeepSeek-style bitmaps (run sets, tt_o200k.h): numbers; ASCII
+// letters; letters and marks of the rest; letters and marks of the CJK/kana
+// set; punctuation and symbols of the rest; those of the CJK/kana set;
+// whitespace; and CR/LF (single bytes: their bitmap serves runs and "last").
+// A set never mixes the groups, so a run stops at a group change.
+enum : int { DSB_N = 0, DSB_AL = 1, DSB_LM0 = 2, DSB_LM2 = 3, DSB_PS0 = 4, DSB_PS2 = 5, DSB_SP = 6, DSB_NL = 7 };
+constexpr uint32_t DSB_RUNS = (1u << DSB_N) | (1u << DSB_AL) | (1u << DSB_LM0) | (1u << DSB_LM2) | (1u << DSB_PS0) |
+                              (1u << DSB_PS2) | (1u << DSB_SP);
+__host__ __device__ inline uint32_t ds_bits_of(uint32_t c) {
+  switch (c) {
+    case DS_N: return 1u << DSB_N;
+    case DS_AL: return (1u << DSB_AL) | (1u << DSB_LM0);
+    case DS_L:
+    case DS_M: return 1u << DSB_LM0;
+    case DS_KL:
+    case DS_KM: return 1u << DSB_LM2;
+    case DS_AP:
+    case DS_PS: return 1u << DSB_PS0;
+    case DS_KP: return 1u << DSB_PS2;
+    case DS_SP:
+    case DS_WS: return 1u << DSB_SP;
+    case DS_NL: return (1u << DSB_SP) | (1u << DSB_NL);
+    default: return 0u;
+  }
+}
+
 template <class P>
 __host__ __device__ inline uint32_t ds_table_class(P l1, P l2, uint32_t cp) {
   const uint32_t blk = l1[cp >> 8];
@@ -138,63 +164,126 @@ __device__ inline uint32_t ds_view_cls(const O2View& v, int64_t q) {
 // Class of a character outside the window (rare: walks that run past it).
 __device__ __noinline__ uint32_t ds_cls_far(const O2View v, int64_t q) { return ds_view_cls(v, q); }
 
+// The classes of a group (bit c set when class c is in it): the rest, and
+// the CJK/kana set.
+constexpr uint32_t DSM_G0 = (1u << DS_O) | (1u << DS_AL) | (1u << DS_L) | (1u << DS_M) | (1u << DS_AP) |
+                            (1u << DS_PS) | (1u << DS_SP) | (1u << DS_WS) | (1u << DS_NL);
+constexpr uint32_t DSM_G2 = (1u << DS_KL) | (1u << DS_KM) | (1u << DS_KP) | (1u << DS_KO);
+
+// The part of a run scan past the window (rare): from q (a character start
+// after the piece's start), while the class is in `mask` (classes of one
+// group only); `last` becomes the start of the last character whose class
+// is in `track`.
+__device__ __noinline__ ScanEnd ds_scan_far(const O2View v, int64_t q, uint32_t mask, uint32_t track, int64_t last) {
+  while (!v.past(q)) {
+    const uint32_t c = ds_view_cls(v, q);
+    if (!((mask >> c) & 1u)) break;
+    if ((track >> c) & 1u) last = q;
+    q += v.clen(q);
+  }
+  return {q, last};
+}
+
 // End (window index) of the piece that starts at s.  Always > s.  A piece
 // of numbers is one to three of them (walks start at a number stretch's
 // head, so the chunks line up with it).  Otherwise the third splitter runs
 // inside the group stretch of s: its alternatives in order, and when none
 // matches at s, the unmatched stretch up to the next position where one does.
-__device__ __forceinline__ int64_t ds_piece_end(const O2View& v, int64_t s) {
-  auto cls = [&](int64_t q) -> uint32_t { return v.in_win(q) ? (uint32_t)(v.code[PT_PAD + q] & 15u) : ds_cls_far(v, q); };
-  const uint32_t c0 = cls(s);
+// The alternatives that match end with a run scan (one for letters, one for
+// whitespace, two for punctuation then CR/LF).  The view is one of those of
+// tt_o200k.h.
+template <class V, class P>
+__device__ __forceinline__ P ds_end(V& v, const P s) {
+  const uint32_t c0 = v.cls(s);
   const uint32_t g0 = ds_group(c0);
+  const uint32_t gm = g0 == 0u ? DSM_G0 : g0 == 2u ? DSM_G2 : 0u;
   // q is beyond the group stretch of s (the third splitter's end of text)
-  auto stop = [&](int64_t q) { return q > s && (v.past(q) || ds_group(cls(q)) != g0); };
-  auto in = [&](int64_t q, uint32_t mask) { return !stop(q) && ((mask >> cls(q)) & 1u) != 0u; };
-  auto scan = [&](int64_t q, uint32_t mask) -> int64_t {
-    while (in(q, mask)) q += v.clen(q);
-    return q;
-  };
-  const int64_t s1 = s + v.clen(s);
+  auto stop = [&](P q) { return q > s && (v.past(q) || ds_group(v.cls(q)) != g0); };
+  auto in = [&](P q, uint32_t mask) { return !stop(q) && ((mask >> v.cls(q)) & 1u) != 0u; };
+  const P s1 = s + (P)v.clen(s);
   if (c0 == DS_N) {  // S1
-    int64_t q = s1;
-    for (int k = 1; k < 3 && in(q, 1u << DS_N); ++k) q += v.clen(q);
+    P q = s1;
+    for (int k = 1; k < 3 && in(q, 1u << DS_N); ++k) q += (P)v.clen(q);
     return q;
   }
-  // D1: ASCII punctuation or symbol, then ASCII letters
-  if (c0 == DS_AP && in(s1, 1u << DS_AL)) return scan(s1, 1u << DS_AL);
-  // D2: the optional first character, then letters and marks
-  if ((DSM_PFX >> c0) & 1u) {
-    const int64_t e = scan(s1, DSM_LM);
-    if (e > s1) return e;
-  }
-  if ((DSM_LM >> c0) & 1u) return scan(s1, DSM_LM);
-  // D3: optional U+0020, punctuation and symbols, then CR/LF
-  const int64_t st = (c0 == DS_SP && in(s1, DSM_PS)) ? s1 : s;
-  if (in(st, DSM_PS)) return scan(scan(st, DSM_PS), 1u << DS_NL);
-  // D4-D6: whitespace
-  if ((DSM_SPACE >> c0) & 1u) {
-    int64_t q = s, last_nl = -1, last_start = s;
-    while (in(q, DSM_SPACE)) {
-      if (cls(q) == DS_NL) last_nl = q;
-      last_start = q;
-      q += v.clen(q);
+  // the closing run (run bitmaps hold the classes of one group, and the
+  // classes passed for the part past the window are those of the group of s)
+  int alt;
+  P q0 = s1, last = -1;
+  uint32_t mask, track = 0u;
+  int rb, tb = -1;
+  if (c0 == DS_AP && in(s1, 1u << DS_AL)) {
+    // D1: ASCII punctuation or symbol, then ASCII letters
+    alt = 1;
+    mask = 1u << DS_AL;
+    rb = DSB_AL;
+  } else if (((DSM_LM >> c0) & 1u) || (((DSM_PFX >> c0) & 1u) && in(s1, DSM_LM))) {
+    // D2: the optional first character, then letters and marks
+    alt = 1;
+    mask = DSM_LM;
+    rb = g0 == 2u ? DSB_LM2 : DSB_LM0;
+  } else {
+    // D3: optional U+0020, punctuation and symbols, then CR/LF
+    const P st = (c0 == DS_SP && in(s1, DSM_PS)) ? s1 : s;
+    if (in(st, DSM_PS)) {
+      alt = 3;
+      q0 = st + (P)v.clen(st);
+      mask = DSM_PS;
+      rb = g0 == 2u ? DSB_PS2 : DSB_PS0;
+    } else if ((DSM_SPACE >> c0) & 1u) {
+      // D4-D6: whitespace, with its last CR/LF
+      alt = 4;
+      mask = DSM_SPACE;
+      track = 1u << DS_NL;
+      rb = DSB_SP;
+      tb = DSB_NL;
+      if (c0 == DS_NL) last = s;
+    } else {
+      // no alternative matches at s: the unmatched stretch ends where one
+      // does, which is any character but one of none of the classes that no
+      // letter or mark follows
+      P q = s1;
+      while (!stop(q)) {
+        const uint32_t c = v.cls(q);
+        if (c != DS_O && c != DS_KO) break;
+        const P q1 = q + (P)v.clen(q);
+        if (in(q1, DSM_LM)) break;
+        q = q1;
+      }
+      return q;
     }
-    if (last_nl >= 0) return last_nl + 1;  // \s*[\r\n]+ (CR and LF are one byte)
-    if (stop(q)) return q;                  // \s+(?!\S) at the end of the stretch
-    return last_start > s ? last_start : q; // gives back the last character, else \s+
   }
-  // no alternative matches at s: the unmatched stretch ends where one does,
-  // which is any character but one of none of the classes that no letter or
-  // mark follows
-  int64_t q = s1;
-  while (!stop(q)) {
-    const uint32_t c = cls(q);
-    if (c != DS_O && c != DS_KO) break;
-    const int64_t q1 = q + v.clen(q);
-    if (in(q1, DSM_LM)) break;
-    q = q1;
+  P e;
+#pragma unroll 1
+  for (;;) {
+    e = v.scan(q0, mask & gm, track, last, rb, tb);
+    if (alt != 3 || g0 != 0u) break;
+    alt = 1;  // D3 in the rest: then CR/LF (in the CJK/kana set there is none)
+    q0 = e;
+    mask = 1u << DS_NL;
+    rb = DSB_NL;
   }
-  return q;
+  if (alt != 4) return e;
+  if (last >= 0) return last + 1;  // \s*[\r\n]+ (CR and LF are one byte)
+  if (stop(e)) return e;           // \s+(?!\S) at the end of the stretch
+  // \s+(?!\S) gives back the last character, if there are two or more
+  for (P r = e - 1; r > s && r >= e - 4; --r)
+    if ((v.byte(r) & 0xC0u) != 0x80u) return r;
+  return e;  // else \s+
+}
+
+// The piece's end with the full view (rare: pieces at the window's end).
+__device__ __noinline__ int64_t ds_end_full(const O2View v, int64_t s) {
+  FullView<ds_cls_far, ds_scan_far> f{v};
+  return ds_end(f, s);
+}
+
+// End (window index) of the piece that starts at s (0 <= s < PT_WIN).
+__device__ __forceinline__ int64_t ds_piece_end(const O2View& v, int64_t s) {
+  WinView f{v.buf, v.code, v.bits, (int32_t)(v.n - v.w0 < PT_WIN ? v.n - v.w0 : PT_WIN)};
+  const int32_t e = ds_end(f, (int32_t)s);
+  if (!f.out && e + WIN_MARGIN <= PT_WIN) return e;
+  return ds_end_full(v, s);
 }
 
 }  // namespace tt

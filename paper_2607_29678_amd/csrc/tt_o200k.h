@@ -95,7 +95,60 @@ __host__ __device__ inline uint32_t o2_lead_len(uint32_t b) {
 // The request as seen from one tile: window bytes and codes in LDS, the rest
 // in global memory.  Positions are window indices (the window starts at text
 // position w0); they may lie outside the window.
-typedef __attribute__((address_space(3))) const uint8_t lds_u8;  // a byte in LDS
+typedef __attribute__((address_space(3))) const uint8_t lds_u8;    // a byte in LDS
+typedef __attribute__((address_space(3))) const uint32_t lds_u32;  // a word in LDS
+
+// Class-set bitmaps of a tile's window: bit q of bitmap k (word q / 32 of
+// its PT_WIN / 32 words) tells whether window index q belongs to set k.  In a
+// "run" set the continuation bytes of the text are members too, so that a run
+// scan can step byte by byte.  In a "last" set only the characters of the
+// set are members (their first bytes): such a set finds the last character of
+// a class inside a run.  Document starts and positions outside the text are
+// in no set (a run stops there).
+constexpr int WALK_BITMAPS = 8;
+constexpr int WIN_WORDS = PT_WIN / 32;
+
+// First window index p >= q (0 <= q < PT_WIN) whose bit in bitmap b is 0, or
+// PT_WIN when every bit from q to the window end is 1.
+__device__ __forceinline__ int64_t win_next_zero(lds_u32* b, int64_t q) {
+  uint32_t wi = (uint32_t)q >> 5;
+  uint32_t x = ~b[wi] & (0xFFFFFFFFu << ((uint32_t)q & 31u));
+  while (x == 0u) {
+    if (++wi >= (uint32_t)WIN_WORDS) return PT_WIN;
+    x = ~b[wi];
+  }
+  return (int64_t)(wi * 32u + (uint32_t)__builtin_ctz(x));
+}
+
+// Last window index in [a, e) whose bit in bitmap b is 1, or -1
+// (0 <= a, e <= PT_WIN).
+__device__ __forceinline__ int64_t win_last_one(lds_u32* b, int64_t a, int64_t e) {
+  if (e <= a) return -1;
+  const int32_t wa = (int32_t)(a >> 5);
+  int32_t wi = (int32_t)((e - 1) >> 5);
+  uint32_t x = b[wi] & (0xFFFFFFFFu >> (31u - ((uint32_t)(e - 1) & 31u)));
+  for (;;) {
+    if (wi == wa) x &= 0xFFFFFFFFu << ((uint32_t)a & 31u);
+    if (x) return (int64_t)wi * 32 + 31 - __builtin_clz(x);
+    if (--wi < wa) return -1;
+    x = b[wi];
+  }
+}
+
+// The o200k-style bitmaps: runs of [Lu Lt Lm Lo M], of [Ll Lm Lo M], of
+// [^\s\p{L}\p{N}] and of \s; the last Lm/Lo letter or mark, and the last CR/LF.
+enum : int { O2B_UB = 0, O2B_LB = 1, O2B_OS = 2, O2B_SP = 3, O2B_BM = 4, O2B_NL = 5 };
+constexpr uint32_t O2B_RUNS = (1u << O2B_UB) | (1u << O2B_LB) | (1u << O2B_OS) | (1u << O2B_SP);
+__host__ __device__ inline uint32_t o2_bits_of(uint32_t c) {
+  uint32_t m = 0;
+  if (c == O2_UP || c == O2_BO || c == O2_MK) m |= 1u << O2B_UB;
+  if (c == O2_LO || c == O2_BO || c == O2_MK) m |= 1u << O2B_LB;
+  if (c == O2_O || c == O2_MK) m |= 1u << O2B_OS;
+  if (c == O2_WS || c == O2_NL) m |= 1u << O2B_SP;
+  if (c == O2_BO || c == O2_MK) m |= 1u << O2B_BM;
+  if (c == O2_NL) m |= 1u << O2B_NL;
+  return m;
+}
 
 struct O2View {
   lds_u8* buf;          // window bytes at PT_PAD + q, q in [-PT_PAD, PT_WIN + 16)
@@ -105,6 +158,7 @@ struct O2View {
   const uint8_t* text;  // the request
   int64_t w0, n;
   int64_t doc_after;    // first document start at or after w0 + PT_WIN (n if none)
+  lds_u32* bits;        // the window's class-set bitmaps, WIN_WORDS words each
 
   __device__ bool in_win(int64_t q) const { return q >= 0 && q < PT_WIN; }
   __device__ uint32_t byte(int64_t q) const {
@@ -143,46 +197,161 @@ constexpr uint32_t M_OS = (1u << O2_O) | (1u << O2_MK);                    // [^
 constexpr uint32_t M_SP = (1u << O2_WS) | (1u << O2_NL);                   // \s
 constexpr uint32_t M_PF = (1u << O2_O) | (1u << O2_MK) | (1u << O2_WS);    // [^\r\n\p{L}\p{N}]
 
-// End (window index) of the piece that starts at s, by the pattern's
-// alternatives in order.  Always > s.  Every alternative is evaluated with the
-// same few scans ("advance while the character's class is in a set"), and the
-// first one that matches is taken: the lanes of a wave, each on its own
-// piece, then run the same instructions.
-__device__ __forceinline__ int64_t o2_piece_end(const O2View& v, int64_t s) {
-  auto stop = [&](int64_t q) { return q > s && v.past(q); };
-  auto cls = [&](int64_t q) -> uint32_t { return v.in_win(q) ? (uint32_t)(v.code[PT_PAD + q] & 15u) : o2_cls_far(v, q); };
-  // advance from q while the class is in `mask`; `last` receives the start
-  // of the last character whose class is in `track` (or keeps its value)
-  auto scan = [&](int64_t q, uint32_t mask, uint32_t track, int64_t& last) -> int64_t {
-    for (;;) {
-      if (stop(q)) return q;
-      const uint32_t c = cls(q);
-      if (!((mask >> c) & 1u)) return q;
-      if ((track >> c) & 1u) last = q;
-      q += v.clen(q);
+// The part of a run scan past the window (rare): from q (a character start
+// after the piece's start), while the class is in `mask`; `last` becomes the
+// start of the last character whose class is in `track`.
+struct ScanEnd {
+  int64_t q, last;
+};
+__device__ __noinline__ ScanEnd o2_scan_far(const O2View v, int64_t q, uint32_t mask, uint32_t track, int64_t last) {
+  while (!v.past(q)) {
+    const uint32_t c = v.cls(q);
+    if (!((mask >> c) & 1u)) break;
+    if ((track >> c) & 1u) last = q;
+    q += v.clen(q);
+  }
+  return {q, last};
+}
+
+// Two ways to read a walk's positions (P is the position type).  The piece
+// rules below take either.
+//
+// WinView: the window in LDS only, with 32-bit positions and no branch to
+// global memory; every position at or past the window's end reads as past
+// the text.  Its answer is the piece's end when no run scan reached the
+// window's end (`out`) and the end lies at least WIN_MARGIN bytes before it:
+// a rule reads at most WIN_MARGIN - 1 bytes past the end it returns.  Else
+// the piece is taken again with the full view.
+constexpr int WIN_MARGIN = 5;
+struct WinView {
+  lds_u8* buf;
+  lds_u8* code;
+  lds_u32* bits;
+  int32_t qn;        // window index of the text end, at most PT_WIN
+  bool out = false;  // a run scan reached the window's end
+
+  __device__ uint32_t byte(int32_t q) const { return buf[PT_PAD + q]; }
+  __device__ uint32_t clen(int32_t q) const { return o2_lead_len(byte(q)); }
+  __device__ uint32_t cls(int32_t q) const { return code[PT_PAD + q] & 15u; }
+  __device__ bool past(int32_t q) const { return q >= qn || (code[PT_PAD + q] & 0x80u) != 0u; }
+  // advance from q (> the piece start, a character start) while the class
+  // is in run bitmap rb; `last` receives the start of the last character
+  // in bitmap tb (-1 for none), or keeps its value
+  __device__ int32_t scan(int32_t q, uint32_t, uint32_t, int32_t& last, int rb, int tb) {
+    if (q >= PT_WIN) {
+      out = true;
+      return q;
     }
-  };
-  const uint32_t c0 = cls(s);
-  const int64_t l0 = v.clen(s);
-  const bool pfx = ((M_PF >> c0) & 1u) != 0u && !stop(s + l0);
-  int64_t unused = -1;
-  // the letter bodies after the prefix (a) and from s (b): the run of the
-  // upper-case set, its last "both" character, and the class after it
-  const int64_t ba = s + l0;
-  int64_t lba = -1, lbb = -1;
-  const int64_t qa = pfx ? scan(ba, M_UB, M_BM, lba) : ba;
-  const int64_t qb = scan(s, M_UB, M_BM, lbb);
-  const bool loa = pfx && !stop(qa) && cls(qa) == O2_LO;
-  const bool lob = !stop(qb) && cls(qb) == O2_LO;
+    const int32_t p = (int32_t)win_next_zero(bits + rb * WIN_WORDS, q);
+    if (tb >= 0) {
+      const int32_t t = (int32_t)win_last_one(bits + tb * WIN_WORDS, q, p);
+      if (t >= 0) last = t;
+    }
+    out = out || p >= PT_WIN;
+    return p;
+  }
+};
+
+// FullView: any position of the request (outside the window from the text
+// and the class table, through the out-of-line helpers of the pattern).
+template <uint32_t (*FAR_CLS)(const O2View, int64_t), ScanEnd (*FAR_SCAN)(const O2View, int64_t, uint32_t, uint32_t, int64_t)>
+struct FullView {
+  const O2View& v;
+  __device__ uint32_t byte(int64_t q) const { return v.byte(q); }
+  __device__ uint32_t clen(int64_t q) const { return v.clen(q); }
+  __device__ uint32_t cls(int64_t q) const { return v.in_win(q) ? (uint32_t)(v.code[PT_PAD + q] & 15u) : FAR_CLS(v, q); }
+  __device__ bool past(int64_t q) const { return v.past(q); }
+  // as WinView::scan, with `mask` the classes of the run for the part past
+  // the window
+  __device__ int64_t scan(int64_t q, uint32_t mask, uint32_t track, int64_t& last, int rb, int tb) const {
+    if (q < PT_WIN) {
+      const int64_t p = win_next_zero(v.bits + rb * WIN_WORDS, q);
+      if (tb >= 0) {
+        const int64_t t = win_last_one(v.bits + tb * WIN_WORDS, q, p);
+        if (t >= 0) last = t;
+      }
+      if (p < PT_WIN) return p;
+      int64_t r = PT_WIN - 1;  // the run reaches the window's end: go on from its last character
+      while (r > q && (v.byte(r) & 0xC0u) == 0x80u) --r;
+      q = r + v.clen(r);
+    }
+    const ScanEnd f = FAR_SCAN(v, q, mask, track, last);
+    last = f.last;
+    return f.q;
+  }
+};
+
+// End (window index) of the piece that starts at s, by the pattern's
+// alternatives in order.  Always > s.  Every alternative is evaluated with
+// two run scans ("advance while the character's class is in a set"): the
+// upper-case letter body after the first character, then the run the chosen
+// alternative ends with; the first alternative that matches is taken.
+template <class V, class P>
+__device__ __forceinline__ P o2_end(V& v, const P s) {
+  auto stop = [&](P q) { return q > s && v.past(q); };
+  const uint32_t c0 = v.cls(s);
+  const P s1 = s + (P)v.clen(s);
+  const bool pfx = ((M_PF >> c0) & 1u) != 0u && !stop(s1);
+  const bool ub0 = ((M_UB >> c0) & 1u) != 0u;
+  // the letter bodies after the prefix (a) and from s (b), both runs of the
+  // upper-case set from s1 (a character at s in that set cannot be a prefix
+  // but a mark, which is both): where each ends and its last "both"
+  // character
+  P qu = s1, lu = -1;
+  if (pfx || ub0) qu = v.scan(s1, M_UB, M_BM, lu, O2B_UB, O2B_BM);
+  const P qa = qu, lba = lu;
+  const P qb = ub0 ? qu : s;
+  const P lbb = lu >= 0 ? (ub0 ? lu : (P)-1) : ((M_BM >> c0) & 1u) ? s : (P)-1;
+  const bool loa = pfx && !stop(qa) && v.cls(qa) == O2_LO;
+  const bool lob = !stop(qb) && v.cls(qb) == O2_LO;
   // P1 with the prefix, P1 without, P2 with, P2 without: where the
-  // lower-case set starts
-  int64_t from = -1;
+  // lower-case set starts (in the first two cases the character at `from`
+  // is in that set; in the last two, P2 with an empty lower-case part, it
+  // is not)
+  P from = -1;
+  bool from_in = true;
   if (pfx && (loa || lba >= 0)) from = loa ? qa : lba;
   else if (lob || lbb >= 0) from = lob ? qb : lbb;
-  else if (pfx && qa > ba) from = qa;
-  else if (qb > s) from = qb;
+  else if (pfx && qa > s1) from = qa, from_in = false;
+  else if (qb > s) from = qb, from_in = false;
+  // P3: one to three numbers
+  if (from < 0 && c0 == O2_N) {
+    P q = s1;
+    for (int k = 1; k < 3 && !stop(q) && v.cls(q) == O2_N; ++k) q += (P)v.clen(q);
+    return q;
+  }
+  // the closing run: the lower-case set (P1, P2); symbols and marks after an
+  // optional U+0020 (P4); whitespace, with its last CR/LF (P5-P7)
+  int alt;
+  P q0, last = -1;
+  uint32_t mask, track = 0u;
+  int rb, tb = -1;
   if (from >= 0) {
-    const int64_t e = scan(from, M_LB, 0u, unused);
+    alt = 1;  // (from > s unless the character at s is in the lower-case set)
+    q0 = from_in ? from + (P)v.clen(from) : from;
+    mask = M_LB;
+    rb = O2B_LB;
+  } else {
+    const P st = (v.byte(s) == 0x20u && !stop(s1) && ((M_OS >> v.cls(s1)) & 1u)) ? s1 : s;
+    if ((M_OS >> v.cls(st)) & 1u) {
+      alt = 4;
+      q0 = st + (P)v.clen(st);
+      mask = M_OS;
+      rb = O2B_OS;
+    } else if ((M_SP >> c0) & 1u) {
+      alt = 5;
+      q0 = s1;
+      mask = M_SP;
+      track = 1u << O2_NL;
+      rb = O2B_SP;
+      tb = O2B_NL;
+      if (c0 == O2_NL) last = s;
+    } else {
+      return s1;  // only invalid text gets here
+    }
+  }
+  const P e = v.scan(q0, mask, track, last, rb, tb);
+  if (alt == 1) {
     // the optional case-insensitive contraction
     if (stop(e) || v.byte(e) != 0x27u || stop(e + 1)) return e;
     const uint32_t b1 = v.byte(e + 1);
@@ -195,34 +364,31 @@ __device__ __forceinline__ int64_t o2_piece_end(const O2View& v, int64_t s) {
     }
     return e;
   }
-  // P3: one to three numbers
-  if (c0 == O2_N) {
-    int64_t q = s + l0;
-    for (int k = 1; k < 3 && !stop(q) && cls(q) == O2_N; ++k) q += v.clen(q);
-    return q;
-  }
-  // P4: optional U+0020, symbols and marks, then CR/LF and "/"
-  const int64_t st = (v.byte(s) == 0x20u && !stop(s + 1) && ((M_OS >> cls(s + 1)) & 1u)) ? s + 1 : s;
-  if ((M_OS >> cls(st)) & 1u) {
-    int64_t q = scan(st, M_OS, 0u, unused);
+  if (alt == 4) {  // then CR/LF and "/"
+    P q = e;
     while (!stop(q) && (v.byte(q) == 0x0Au || v.byte(q) == 0x0Du || v.byte(q) == 0x2Fu)) ++q;
     return q;
   }
-  // P5-P7: whitespace
-  if ((M_SP >> c0) & 1u) {
-    int64_t last_nl = -1, last_start = s;
-    const int64_t q = scan(s, M_SP, 1u << O2_NL, last_nl);
-    if (last_nl >= 0) return last_nl + 1;  // \s*[\r\n]+
-    if (stop(q)) return q;                  // \s+(?!\S) at the end of the text
-    // \s+(?!\S) gives back the last character, if there are two or more
-    for (int64_t r = q - 1; r > s && r >= q - 4; --r)
-      if ((v.byte(r) & 0xC0u) != 0x80u) {
-        last_start = r;
-        break;
-      }
-    return last_start > s ? last_start : q;  // else \s+
-  }
-  return s + l0;  // only invalid text gets here
+  if (last >= 0) return last + 1;  // \s*[\r\n]+
+  if (stop(e)) return e;           // \s+(?!\S) at the end of the text
+  // \s+(?!\S) gives back the last character, if there are two or more
+  for (P r = e - 1; r > s && r >= e - 4; --r)
+    if ((v.byte(r) & 0xC0u) != 0x80u) return r;
+  return e;  // else \s+
+}
+
+// The piece's end with the full view (rare: pieces at the window's end).
+__device__ __noinline__ int64_t o2_end_full(const O2View v, int64_t s) {
+  FullView<o2_cls_far, o2_scan_far> f{v};
+  return o2_end(f, s);
+}
+
+// End (window index) of the piece that starts at s (0 <= s < PT_WIN).
+__device__ __forceinline__ int64_t o2_piece_end(const O2View& v, int64_t s) {
+  WinView f{v.buf, v.code, v.bits, (int32_t)(v.n - v.w0 < PT_WIN ? v.n - v.w0 : PT_WIN)};
+  const int32_t e = o2_end(f, (int32_t)s);
+  if (!f.out && e + WIN_MARGIN <= PT_WIN) return e;
+  return o2_end_full(v, s);
 }
 
 }  // namespace tt

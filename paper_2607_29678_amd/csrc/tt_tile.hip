@@ -336,7 +336,10 @@ union PhaseMem {
     uint8_t code[PT_PAD + PT_WIN + 16] __attribute__((aligned(16)));  // class/identity/doc-start codes
     union {
       int16_t run_end[PT_WIN];  // cl100k: window index of the head after a run's head
-      uint8_t o2piece[PT_WIN];  // walked patterns: 1 at the piece starts the walks find
+      struct {
+        uint8_t o2piece[PT_WIN];  // walked patterns: 1 at the piece starts the walks find
+        uint32_t o2bits[WALK_BITMAPS * WIN_WORDS];  // walked patterns: class-set bitmaps of the window
+      };
     };
     uint32_t o2seg[PT_WIN / 32];    // walked patterns: segment starts (synchronizing positions, document starts)
     uint32_t nocut[PT_WIN / 32];    // ignore_merges: window positions no junction cut may split
@@ -526,6 +529,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   constexpr bool DS = PAT == TT_PATTERN_DEEPSEEK;
   constexpr bool WALK = PAT == TT_PATTERN_O200K || DS;
   if (WALK && tid < PT_WIN / 32) sh.ph.a.o2seg[tid] = 0;
+  static_assert(WALK_BITMAPS * WIN_WORDS == PT_THREADS, "one bitmap word per thread to clear");
+  if (WALK) sh.ph.a.o2bits[tid] = 0;
   // the ticket's round trip (tickets are handed out one at a time) overlaps
   // the staging of the tables, which do not depend on the tile
   uint32_t ticket = 0;
@@ -1030,9 +1035,30 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       if (st) seg |= 1u << j;
     }
     if (seg) atomicOr(&sh.ph.a.o2seg[qb >> 5], seg << (qb & 31));
+    // the class-set bitmaps of the thread's four positions (tt_o200k.h): the
+    // sets of a character at its first byte, the run sets at its continuation
+    // bytes, nothing at document starts and outside the text
+    {
+      uint32_t nib[WALK_BITMAPS];
+#pragma unroll
+      for (int k = 0; k < WALK_BITMAPS; ++k) nib[k] = 0;
+#pragma unroll
+      for (int j = 0; j < PT_BPT; ++j) {
+        const uint32_t c = cr(j);
+        const uint32_t cl = c & 15u;
+        uint32_t m = 0;
+        if (inside(qb + j) && !(c & CODE_DOCSTART))
+          m = cl == O2_NONE ? (DS ? DSB_RUNS : O2B_RUNS) : (DS ? ds_bits_of(cl) : o2_bits_of(cl));
+#pragma unroll
+        for (int k = 0; k < WALK_BITMAPS; ++k) nib[k] |= ((m >> k) & 1u) << j;
+      }
+#pragma unroll
+      for (int k = 0; k < WALK_BITMAPS; ++k)
+        if (nib[k]) atomicOr(&sh.ph.a.o2bits[k * WIN_WORDS + (qb >> 5)], nib[k] << (qb & 31));
+    }
     __syncthreads();
     const O2View v{(lds_u8*)sh.buf, (lds_u8*)sh.ph.a.code, (lds_u8*)sh.ph.a.o2.l1, (lds_u8*)sh.ph.a.o2.l2,
-                   w.text, w0, n, BATCH ? sh.o2_doc_after : n};
+                   w.text, w0, n, BATCH ? sh.o2_doc_after : n, (lds_u32*)sh.ph.a.o2bits};
     const int64_t own_end = n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN;
     auto segbit = [&](int64_t q) -> bool { return q >= 0 && q < PT_WIN && ((sh.ph.a.o2seg[q >> 5] >> (q & 31)) & 1u); };
     // one loop per lane, one piece per step: the lane's walk starts in order
