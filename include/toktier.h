@@ -164,11 +164,10 @@ void tt_destroy(tt_tokenizer* h);
  * Blocks until out_ids/out_len are valid, with one host synchronisation for
  * requests up to 256 MiB (Sec. 4.3: the single-request path keeps the host
  * out of the chain).  The device reads the request straight from utf8 when
- * it is pinned host memory, else from a pinned copy; the IDs come back in one
- * copy started before their count is known, sized from
- * the IDs-per-byte ratio of the stream's recent requests (a request with more
- * IDs takes a second copy of the rest), straight into out_ids when it is
- * pinned.  Staging copies of at least 256 KiB are split among the calling
+ * it is pinned host memory, else from a pinned copy, and writes the IDs
+ * straight into out_ids when it is pinned host memory, else into pinned
+ * staging that is then copied into out_ids.  Staging copies of at least
+ * 256 KiB are split among the calling
  * thread and up to three worker threads of the library, which spin for 2 ms
  * after a copy, then sleep.  Longer requests take the length and the IDs back
  * in two copies.  NUL bytes are ordinary characters; no byte-order mark is

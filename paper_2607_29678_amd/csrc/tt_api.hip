@@ -46,8 +46,7 @@ struct Workspace {
   // tt_encode: pinned staging, sized with the capacity
   uint64_t pin_cap = 0;        // bytes of request it holds
   uint8_t* h_in = nullptr;     // request bytes for the DMA (pageable callers)
-  int32_t* h_ids = nullptr;    // IDs back from the device (pageable callers)
-  double id_ratio = 1.0;       // IDs per byte to copy back before the length is known
+  int32_t* h_ids = nullptr;    // IDs from the device (pageable callers)
   // profiling: stage boundaries of the most recent calls, a ring of
   // `ring` calls with N_STAGES + 1 events each
   std::vector<hipEvent_t> ev;
@@ -419,12 +418,12 @@ constexpr uint64_t PINNED_MAX = 1ull << 28;
 //    memory (the caller's buffer when it is pinned, else a pinned copy): each
 //    tile fetches its window over the bus as it starts, so the transfer
 //    overlaps the tiles' work instead of preceding the launch;
-//  - the tile kernel places the IDs in device memory and its last tile writes
-//    the output length straight into pinned host memory;
-//  - stage-out: the IDs are copied back before their count is known, as many as
-//    the recent IDs-per-byte ratio of this workspace predicts (plus a margin);
-//    the rare request with more IDs takes a second copy of the rest.  The copy
-//    goes straight into the caller's buffer when it is pinned.
+//  - stage-out: the tile kernel places the IDs straight into pinned host
+//    memory (the caller's array when it is pinned, else pinned staging that
+//    the copy threads then copy into the caller's array), and its last tile
+//    writes the output length there too: no copy engine transfer at all.
+//    Each wave of a tile writes its IDs as one contiguous range (whole lines
+//    over the bus).
 int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t len, int32_t* out_ids,
                   int64_t* out_len, hipStream_t st) {
   int rc = reserve_pinned(s, (uint64_t)len);
@@ -439,26 +438,14 @@ int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t le
     host_copy_wake();  // for the copy of the IDs
   }
   *s->h_len = 0;
-  rc = run_chain(h, s, src, (uint32_t)len, nullptr, 0, s->d_out, s->h_len, nullptr, st, 1);
-  if (rc) return rc;
+  // the tile kernel writes the IDs at their places in pinned host memory
   int32_t* dst = pin_out ? out_ids : s->h_ids;
-  const int64_t guess = std::min<int64_t>(len, (int64_t)(s->id_ratio * (double)len) + 1024);
-  if (hipMemcpyAsync(dst, s->d_out, 4 * (size_t)guess, hipMemcpyDeviceToHost, st) != hipSuccess ||
-      hipStreamSynchronize(st) != hipSuccess)
-    return TT_ERR_HIP;
+  rc = run_chain(h, s, src, (uint32_t)len, nullptr, 0, dst, s->h_len, nullptr, st, 1);
+  if (rc) return rc;
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
   const int64_t T = *s->h_len;
   if (T < 0) return (int)T;
   if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
-  if (T > guess) {
-    if (hipMemcpyAsync(dst + guess, s->d_out + guess, 4 * (size_t)(T - guess), hipMemcpyDeviceToHost, st) !=
-            hipSuccess ||
-        hipStreamSynchronize(st) != hipSuccess)
-      return TT_ERR_HIP;
-  }
-  // the next guess: 5% above this request's ratio, falling slowly after text
-  // with many IDs per byte
-  const double r = 1.05 * (double)T / (double)len;
-  s->id_ratio = std::min(1.0, std::max(r, 0.9 * s->id_ratio));
   if (!pin_out && T > 0) host_copy(out_ids, s->h_ids, 4 * (size_t)T);
   *out_len = T;
   return TT_OK;

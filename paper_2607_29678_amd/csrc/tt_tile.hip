@@ -1606,21 +1606,60 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   for (uint32_t i = (uint32_t)tid; i < inc_cnt; i += PT_THREADS)
     if (prefix + i < lim) out[prefix + i] = ext_of(w.stage[s_prev + i]);
   const uint32_t obase = prefix + inc_cnt;
+  // Token o of unit k sits at position ustart[k] + o, so the tokens of a
+  // wave's positions go to one contiguous range of the output, in position
+  // order.  Without span export (which reads tok[] again) each wave first
+  // packs its tokens at the front of its own part of tok[] and then writes
+  // the range with consecutive lanes on consecutive words: whole lines, which
+  // matters most when the output is pinned host memory.
   uint32_t before = texcl;  // unit starts at or before position q
-#pragma unroll 1
+  int32_t val[PT_BPT];
+  uint32_t at_of[PT_BPT];
+  uint32_t has = 0;
+#pragma unroll
   for (int j = 0; j < PT_BPT; ++j) {
     const int q = qb + j;
     const bool st = (flags >> j) & 1u;
     before += st ? 1u : 0u;
+    val[j] = 0;
+    at_of[j] = 0;
     if (before == 0u || before - 1u >= m_proc) continue;
     const uint32_t k = before - 1u;
     const uint32_t o = (uint32_t)q - sh.ustart[k];
     const uint32_t at = obase + sh.ph.b.uoff[k] + o;
-    if (o < sh.ucnt[k] && at < lim) out[at] = ext_of(sh.ph.b.tok[q]);
+    if (o < sh.ucnt[k] && at < lim) {
+      val[j] = ext_of(sh.ph.b.tok[q]);
+      at_of[j] = at;
+      has |= 1u << j;
+    }
     if (BATCH && st && sh.dstart[PT_PAD + q]) {
       w.unit_tile[w0 + q] = t;
       w.unit_pos[w0 + q] = inc_cnt + sh.ph.b.uoff[k];
     }
+  }
+  if (SPANS) {
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j)
+      if ((has >> j) & 1u) out[at_of[j]] = val[j];
+  } else {
+    const uint32_t mine = (uint32_t)__builtin_popcount(has);
+    const uint32_t incl = wave_incl_sum(mine);
+    const uint32_t n_wave = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+    const uint64_t holders = __ballot(mine != 0u);
+    // the wave's first output index (the lowest lane holding a token, its
+    // lowest position with one)
+    const uint32_t first = (has & 1u) ? at_of[0] : (has & 2u) ? at_of[1] : (has & 4u) ? at_of[2] : at_of[3];
+    const uint32_t base = holders ? (uint32_t)__builtin_amdgcn_readlane((int)first, (int)__builtin_ctzll(holders)) : 0u;
+    uint32_t* pack = &sh.ph.b.tok[wave * 64 * PT_BPT];
+    __syncthreads();  // every read of tok[] above is done
+    uint32_t r = incl - mine;
+#pragma unroll
+    for (int j = 0; j < PT_BPT; ++j)
+      if ((has >> j) & 1u) pack[r++] = (uint32_t)val[j];
+    __syncthreads();
+    // (valid text: the wave's indices are exactly base .. base + n_wave - 1)
+    for (uint32_t i = (uint32_t)lane; i < n_wave; i += 64)
+      if (base + i < lim) out[base + i] = (int32_t)pack[i];
   }
   if (BATCH && tid == 0 && has_inc) {
     w.unit_tile[s_prev] = t;

@@ -1,13 +1,12 @@
 """History independence and the comparator itself.
 
 A call's output must not depend on what the handle or its stream's workspace
-did before: the workspace keeps epoch-tagged words, a grown capacity and the
-IDs-per-byte ratio that sizes the early copy of the IDs.  Requests of
-different sizes and ratios go through one handle and one stream in turn (the
-text with many IDs per byte after text with few takes the second copy of the
-rest), through the host entry point with pageable and pinned caller buffers
-and through the device entry point; each result is compared with the oracle
-and with a fresh handle's.
+did before: the workspace keeps epoch-tagged words, a grown capacity and
+pinned staging that holds the previous request's bytes and IDs.  Requests of
+different sizes and IDs-per-byte ratios go through one handle and one stream
+in turn, through the host entry point with pageable and pinned caller
+buffers and through the device entry point; each result is compared with the
+oracle and with a fresh handle's.
 
 The comparator of the parity tests is checked too: a mutated ID or a moved
 piece boundary in a real GPU result must be reported, at its position.
