@@ -7,8 +7,9 @@ every request a fresh sample encoded once; the paper reports P50 over 20
 samples): W warm-up requests on other samples, then K distinct seeded
 1,000,000-character samples, each tokenized once through ``tt_encode``, host
 bytes in and host IDs out.  A step is one such call: stage-in (host copy into
-pinned staging, one DMA), the tile kernel (pre-tokenization, BPE, placement),
-stage-out (one DMA, one synchronisation, host copy into the caller's array).
+pinned staging, which the tile kernel reads over the bus), the tile kernel
+(pre-tokenization, BPE, placement of the IDs into pinned staging), one
+synchronisation, stage-out (host copy into the caller's array).
 The caller's buffers are ordinary pageable numpy arrays, the output array
 reused from call to call:
 
@@ -20,7 +21,8 @@ the same calls with pinned caller buffers, the Python binding's fresh-array
 in HBM), the multilingual configuration C4 with its own roofline, request
 sizes of 100,000, 2,000,000 and 4,400,000 characters, the 3,000,000-character
 stress request C5 and its 64-document batch, incremental repair, the
-front-end options and the o200k-style and DeepSeek-style patterns.
+front-end options and the o200k-style and DeepSeek-style patterns, and the
+headline calls again under 28 competing CPU-bound processes.
 
 During the headline's timed calls the library records HIP events around the
 tile kernel on the caller's stream; their mean is the kernel time of the
@@ -513,6 +515,91 @@ def front_end_options(ctx, n=10):
 _BATCH_TABLE = None  # set before the worker processes fork, so no task carries the table
 
 
+def _burn(flag, rank):
+    # a competing CPU-bound process: spins while flag > rank, idles otherwise,
+    # exits when flag is -1
+    x = 0
+    while True:
+        f = flag.value
+        if f < 0:
+            return
+        if f <= rank:
+            time.sleep(0.005)
+            continue
+        for _ in range(20000):
+            x += 1
+
+
+def load_procs(n):
+    """n CPU-bound processes for the contention figures, forked before the GPU is
+    initialised; process r spins while the flag is above r."""
+    import multiprocessing as mp
+
+    ctxm = mp.get_context("fork")
+    flag = ctxm.Value("i", 0, lock=False)
+    procs = [ctxm.Process(target=_burn, args=(flag, r), daemon=True) for r in range(n)]
+    for p in procs:
+        p.start()
+    return flag, procs
+
+
+def contention_block(ctx, k, flag, n_procs, steps=20, warmup=3, rounds=10):
+    """Host-to-host latency of the same samples without and with competing
+    CPU-bound processes (Sec. 5.4 measures the tail of a 50,000-character
+    request under 28 competing processes).  One eager launch and one
+    synchronisation per request, no graph.  The competing processes are
+    raised in two steps: as many as leave two of the available CPUs free,
+    then all n_procs."""
+    import numpy as np
+
+    from workloads import textgen
+
+    cfg = textgen.CONFIGS[k]
+    tok = ctx.tok(k, cfg["pattern"])
+    torch = ctx.torch
+    try:
+        share = len(os.sched_getaffinity(0))
+    except AttributeError:
+        share = os.cpu_count()
+    steps_load = [0, max(0, min(n_procs, share - 2)), n_procs]
+    texts = [textgen.latency_sample(k, s % 32) for s in range(warmup + steps)]
+    res = {"competing_processes": steps_load[1:], "cpus_available": share, "calls_per_figure": rounds * steps,
+           "sizes": {}}
+    for chars in (50_000, 1_000_000):
+        raw = [t[:chars].encode("utf-8") for t in texts]
+        arrs = [np.frombuffer(b, dtype=np.uint8) for b in raw]
+        cap = max(len(b) for b in raw)
+        out = np.zeros(cap, dtype=np.int32)
+        pin_in = [torch.from_numpy(a.copy()).pin_memory() for a in arrs]
+        pin_out = torch.zeros(cap, dtype=torch.int32).pin_memory()
+        d_in = [torch.from_numpy(a.copy()).to(ctx.dev) for a in arrs]
+        d_out = torch.empty(cap, dtype=torch.int32, device=ctx.dev)
+        d_len = torch.zeros(1, dtype=torch.int64, device=ctx.dev)
+
+        def measure():
+            r = {"pageable": [], "pinned": [], "device_resident": []}
+            for _ in range(rounds):
+                r["pageable"] += host_calls(ctx, tok, arrs, out, warmup)[0]
+                r["pinned"] += host_calls(ctx, tok, pin_in, pin_out, warmup)[0]
+                for i in range(warmup, len(arrs)):
+                    a = time.perf_counter()
+                    tok.encode_device(d_in[i], len(raw[i]), d_out, d_len, ctx.sid)
+                    ctx.stream.synchronize()
+                    r["device_resident"].append((time.perf_counter() - a) * 1e3)
+            return {key: pcts(v) for key, v in r.items()}
+
+        rows = {}
+        for n in steps_load:
+            flag.value = n
+            time.sleep(0.3)
+            try:
+                rows["idle" if n == 0 else "%d_processes" % n] = measure()
+            finally:
+                flag.value = 0
+        res["sizes"]["%d_chars" % chars] = rows
+    return res
+
+
 def _oracle_batch_worker(data):
     from oracle.tokenizer import encode as oracle_encode
 
@@ -621,6 +708,9 @@ def main():
     pool = workers = None
     if not args.no_cpu and not args.quick:
         pool, workers = oracle_pool()
+    load = None
+    if not args.quick:
+        load = load_procs(28)
     ctx = Ctx()
     if args.calibrate_copy:
         torch = ctx.torch
@@ -648,6 +738,10 @@ def main():
         extra["large_request_device_resident"] = large_request(ctx, k, raw, timed)
         extra["incremental_repair"] = incremental_repair(ctx, k)
         extra["front_end_options"] = front_end_options(ctx)
+        extra["host_contention"] = contention_block(ctx, k, load[0], len(load[1]))
+        load[0].value = -1
+        for p in load[1]:
+            p.join()
 
     cpu = None
     if not args.no_cpu and not args.quick:

@@ -430,12 +430,11 @@ int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t le
   if (rc) return rc;
   const uint8_t* src = utf8;
   const bool pin_out = host_pinned(out_ids, 4 * len);
-  if (!host_pinned(utf8, len)) {
-    host_copy_wake();
+  const bool pin_in = host_pinned(utf8, len);
+  if (!pin_out || !pin_in) host_copy_wake((size_t)len);  // (the IDs take about as many bytes)
+  if (!pin_in) {
     host_copy(s->h_in, utf8, (size_t)len);
     src = s->h_in;
-  } else if (!pin_out) {
-    host_copy_wake();  // for the copy of the IDs
   }
   *s->h_len = 0;
   // the tile kernel writes the IDs at their places in pinned host memory

@@ -150,7 +150,9 @@ CopyPool& pool() {
 
 }  // namespace
 
-void host_copy_wake() { pool().wake(); }
+void host_copy_wake(size_t n) {
+  if (n >= PAR_MIN) pool().wake();
+}
 
 void host_copy(void* dst, const void* src, size_t n) { pool().copy(dst, src, n); }
 

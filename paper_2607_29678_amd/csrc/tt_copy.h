@@ -12,8 +12,8 @@ namespace tt {
 // copies while another thread's copy is running, are a plain memcpy.
 void host_copy(void* dst, const void* src, size_t n);
 
-// Let sleeping workers start spinning ahead of a copy (cheap when they are
-// awake).
-void host_copy_wake();
+// Let sleeping workers start spinning ahead of a copy of n bytes (cheap when
+// they are awake; nothing for copies too small to be split).
+void host_copy_wake(size_t n);
 
 }  // namespace tt

@@ -18,7 +18,7 @@ static int run(int id, int iters) {
     const size_t n = (it % 3 == 0) ? (size_t)(rng() % 4096) : (size_t)(rng() % (2 << 20));
     const size_t so = rng() % 4096, doff = rng() % 4096;
     std::memset(dst.data(), 0xA5, dst.size());
-    if (it % 7 == 0) tt::host_copy_wake();
+    if (it % 7 == 0) tt::host_copy_wake(n);
     tt::host_copy(dst.data() + doff, src.data() + so, n);
     if (std::memcmp(dst.data() + doff, src.data() + so, n) != 0) {
       std::printf("caller %d iteration %d: copy of %zu bytes differs\n", id, it, n);
