@@ -166,50 +166,6 @@ __device__ __forceinline__ uint32_t char_code(const ClassLds& ct, uint32_t cp) {
   return cls | (id << 3);
 }
 
-// Expected sequence length of a lead byte (0 for bytes that cannot lead).
-__device__ __forceinline__ int lead_len(uint32_t b) {
-  if (b < 0x80u) return 1;
-  if (b < 0xC2u) return 0;
-  if (b < 0xE0u) return 2;
-  if (b < 0xF0u) return 3;
-  if (b < 0xF5u) return 4;
-  return 0;
-}
-
-// Strict UTF-8 decode of the sequence starting at s[0]; `avail` bytes may be
-// read (bounded by the text end and the next document start).  Returns the
-// length, or 0 if the sequence is invalid.
-__device__ __forceinline__ int decode(const uint8_t* s, int avail, uint32_t& cp) {
-  uint32_t b0 = s[0];
-  int len = lead_len(b0);
-  if (len == 0 || len > avail) return 0;
-  if (len == 1) {
-    cp = b0;
-    return 1;
-  }
-  uint32_t b1 = s[1];
-  uint32_t lo = 0x80u, hi = 0xBFu;
-  if (b0 == 0xE0u) lo = 0xA0u;
-  else if (b0 == 0xEDu) hi = 0x9Fu;
-  else if (b0 == 0xF0u) lo = 0x90u;
-  else if (b0 == 0xF4u) hi = 0x8Fu;
-  if (b1 < lo || b1 > hi) return 0;
-  if (len == 2) {
-    cp = ((b0 & 0x1Fu) << 6) | (b1 & 0x3Fu);
-    return 2;
-  }
-  uint32_t b2 = s[2];
-  if ((b2 & 0xC0u) != 0x80u) return 0;
-  if (len == 3) {
-    cp = ((b0 & 0x0Fu) << 12) | ((b1 & 0x3Fu) << 6) | (b2 & 0x3Fu);
-    return 3;
-  }
-  uint32_t b3 = s[3];
-  if ((b3 & 0xC0u) != 0x80u) return 0;
-  cp = ((b0 & 0x07u) << 18) | ((b1 & 0x3Fu) << 12) | ((b2 & 0x3Fu) << 6) | (b3 & 0x3Fu);
-  return 4;
-}
-
 // Strict UTF-8 decode from bytes in registers, with selects only: the length
 // of the sequence that starts with b0 (0 if it is invalid or longer than
 // `avail`) and its code point.
@@ -389,6 +345,9 @@ struct PtShared {
   uint32_t ctile;             // span export: non-continuation bytes the tile owns
   int64_t doc_lo_idx;         // batch: first document start index touching the window
   int last_own;               // cl100k: window index of the tile's last own character
+  // cl100k: a whitespace stretch after CR/LF that reaches the window's end
+  int32_t ws_pend;            // its window index, or -1
+  uint32_t ws_res;            // 1 when it is the last stretch of its run (read on past the window)
 };
 
 }  // namespace
@@ -574,6 +533,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     sh.med_next = 0;
     sh.n_big = 0;
     sh.inc_cnt = 0;
+    sh.ws_pend = -1;
   }
   __syncthreads();
   const uint32_t t = wave_uniform(sh.tile);
@@ -967,40 +927,14 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   }
 
   // rule 2 of cl100k: is the whitespace stretch starting at q (after CR/LF)
-  // the last stretch of its whitespace run?
-  auto ws_stretch_is_last = [&](int q) -> bool {
+  // the last stretch of its whitespace run?  1 yes, 0 no, -1 when the stretch
+  // reaches the window's end and the answer lies in the text after it (the
+  // block reads on there together, below)
+  auto ws_stretch_is_last = [&](int q) -> int {
     int e = sh.ph.a.run_end[q];
-    if (e >= 0) return (code_at(e) & CODE_DOCSTART) || cls(e) != C_NL;
-    if (w0 + PT_WIN >= n) return true;  // the run reaches the end of the text
-    // the stretch continues past the window: read on in global memory
-    int64_t pos = w0 + PT_WIN;
-    int64_t lim = n;
-    if (BATCH) {
-      int lo = 0, hi = w.n_docs;
-      while (lo < hi) {
-        int mid = (lo + hi) >> 1;
-        if (w.doc_off[mid] < pos) lo = mid + 1;
-        else hi = mid;
-      }
-      if (lo < w.n_docs && w.doc_off[lo] < lim) lim = w.doc_off[lo];
-    }
-    while (pos < lim && (w.text[pos] & 0xC0u) == 0x80u) ++pos;
-    while (pos < lim) {
-      uint8_t tmp[4] = {0, 0, 0, 0};
-      int avail = 0;
-      while (avail < 4 && pos + avail < lim) {
-        tmp[avail] = w.text[pos + avail];
-        ++avail;
-      }
-      uint32_t cp = 0;
-      int len = decode(tmp, avail, cp);
-      if (len == 0) return true;  // invalid input; reported elsewhere
-      uint32_t c = code_cls(char_code<PAT>(sh.ph.a.cls, cp));
-      if (c == C_NL) return false;
-      if (c != C_WS) return true;
-      pos += len;
-    }
-    return true;
+    if (e >= 0) return ((code_at(e) & CODE_DOCSTART) || cls(e) != C_NL) ? 1 : 0;
+    if (w0 + PT_WIN >= n) return 1;  // the run reaches the end of the text
+    return -1;
   };
 
   // ---- piece-start predicate ----------------------------------------------
@@ -1170,7 +1104,13 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
           } else {
             pre = sh.carry_nlpre;
           }
-          start = (pre == C_O) || ws_stretch_is_last(q);
+          if (pre == C_O) {
+            start = true;
+          } else {
+            const int r = ws_stretch_is_last(q);
+            start = r > 0;
+            if (r < 0) sh.ws_pend = q;  // (one stretch at most reaches the window's end)
+          }
         }
       } else if (c0 == C_N) {
         const uint32_t off = seg_cnt(ex) + (seg_has(ex) ? 0u : sh.carry_n);
@@ -1194,6 +1134,69 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     }
     if (d1 == 0u) start = true;
     if (start) flags |= 1u << j;
+  }
+  if (PAT == TT_PATTERN_CL100K) {
+    // the whitespace stretch after CR/LF that reaches the window's end, if
+    // any: the block reads on past the window
+    __syncthreads();
+    const int pend = sh.ws_pend;
+    if (pend >= 0) {
+      // Wave 0 reads on, 16 bytes per lane per step, to the first byte that is
+      // not plain ASCII whitespace (space, tab, VT, FF) and decodes the
+      // character there (CR/LF: not the run's last stretch; other whitespace:
+      // read on after it; anything else, or the end of the text or document:
+      // the last).  Every lane holds the same position and answer; offsets
+      // are from the window's end.
+      if (wave == 0) {
+        const uint8_t* base = w.text + (w0 + PT_WIN);
+        int64_t lim = n;
+        if (BATCH) {
+          int lo = 0, hi = w.n_docs;
+          while (lo < hi) {
+            int mid = (lo + hi) >> 1;
+            if (w.doc_off[mid] < w0 + PT_WIN) lo = mid + 1;
+            else hi = mid;
+          }
+          if (lo < w.n_docs && w.doc_off[lo] < lim) lim = w.doc_off[lo];
+        }
+        const uint32_t end = (uint32_t)(lim - (w0 + PT_WIN));
+        uint32_t pos = 0, res = 2u;
+        while (pos < end && (base[pos] & 0xC0u) == 0x80u) ++pos;
+#pragma unroll 1
+        while (res == 2u) {
+          uint32_t first = 16u;
+#pragma unroll 4
+          for (int k = 15; k >= 0; --k) {
+            const uint32_t p = pos + 16u * (uint32_t)lane + (uint32_t)k;
+            const uint32_t b = p < end ? (uint32_t)base[p] : 0u;  // (the end counts as a stop)
+            if (b != 0x20u && b != 0x09u && b != 0x0Bu && b != 0x0Cu) first = (uint32_t)k;
+          }
+          const uint64_t m = __ballot(first < 16u);
+          if (m == 0ull) {
+            pos += 16u * 64u;
+            continue;
+          }
+          const int src = __builtin_ctzll(m);
+          const uint32_t p = pos + 16u * (uint32_t)src + (uint32_t)__builtin_amdgcn_readlane((int)first, src);
+          if (p >= end) {
+            res = 1u;
+            break;
+          }
+          const uint32_t avail = end - p < 4u ? end - p : 4u;
+          auto at = [&](uint32_t k) -> uint32_t { return k < avail ? (uint32_t)base[p + k] : 0u; };
+          uint32_t cp = 0;
+          const uint32_t len = decode_sel(at(0), at(1), at(2), at(3), avail, cp);
+          const uint32_t c = len == 0u ? (uint32_t)C_O : code_cls(char_code_sel<PAT>(sh.ph.a.cls, cp));
+          if (len == 0u) res = 1u;  // invalid input; reported elsewhere
+          else if (c == C_NL) res = 0u;
+          else if (c != C_WS) res = 1u;
+          else pos = p + len;
+        }
+        if (lane == 0) sh.ws_res = res;
+      }
+      __syncthreads();
+      if (sh.ws_res == 1u && tid == pend / PT_BPT) flags |= 1u << (pend % PT_BPT);
+    }
   }
   const bool last = t == n_tiles - 1;
   if (IGN) {
