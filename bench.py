@@ -30,7 +30,8 @@ roofline.  The CPU oracle is timed on a bounded sample of the same requests
 (one thread pinned to one core), and on C5's batch over all host cores.
 
 ``--quick`` keeps the headline, C4 and the device-resident figures only (for
-profiler runs).  ``--calibrate-copy`` first runs a plain int32 copy of 64 MiB
+profiler runs); ``--no-contention`` leaves out the contention figures and
+forks no competing processes.  ``--calibrate-copy`` first runs a plain int32 copy of 64 MiB
 read + 64 MiB written, so that a hardware-counter profile of this command can
 scale the tile kernel's FETCH_SIZE / WRITE_SIZE to bytes.
 
@@ -695,6 +696,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--quick", action="store_true", help="headline, C4 and device-resident figures only")
     ap.add_argument("--calibrate-copy", action="store_true", help="run the counter-calibration copy kernel first")
+    ap.add_argument("--no-contention", action="store_true",
+                    help="skip the figures under competing CPU processes (no processes are forked)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the tokenizer runs on a single MI355X and this "
@@ -709,7 +712,7 @@ def main():
     if not args.no_cpu and not args.quick:
         pool, workers = oracle_pool()
     load = None
-    if not args.quick:
+    if not args.quick and not args.no_contention:
         load = load_procs(28)
     ctx = Ctx()
     if args.calibrate_copy:
@@ -738,10 +741,11 @@ def main():
         extra["large_request_device_resident"] = large_request(ctx, k, raw, timed)
         extra["incremental_repair"] = incremental_repair(ctx, k)
         extra["front_end_options"] = front_end_options(ctx)
-        extra["host_contention"] = contention_block(ctx, k, load[0], len(load[1]))
-        load[0].value = -1
-        for p in load[1]:
-            p.join()
+        if load is not None:
+            extra["host_contention"] = contention_block(ctx, k, load[0], len(load[1]))
+            load[0].value = -1
+            for p in load[1]:
+                p.join()
 
     cpu = None
     if not args.no_cpu and not args.quick:
