@@ -655,9 +655,17 @@ def cpu_baseline(k, head, c4, pool, workers):
 
     dt, chars, same, core = one_core(k, head, 10)
     model = ""
+    cpu = {}
     try:
         with open("/proc/cpuinfo") as f:
-            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+            for ln in f:
+                if not ln.strip():
+                    break  # the first processor's block
+                key, _, val = ln.partition(":")
+                key = key.strip()
+                if key in ("model name", "vendor_id", "cpu family", "model", "stepping", "cpu MHz", "cache size"):
+                    cpu[key.replace(" ", "_")] = val.strip()
+        model = cpu.get("model_name", "")
     except OSError:
         pass
     n_cores = len(os.sched_getaffinity(0))
@@ -665,7 +673,8 @@ def cpu_baseline(k, head, c4, pool, workers):
            "sample": "10 of the timed 1,000,000-char C%d samples, one after another, one thread pinned to core %d, "
                      "pure Python" % (k, core),
            "seconds": round(dt, 2), "ids_identical_to_gpu": bool(same),
-           "host": {"cpu_model": model, "cores_visible": n_cores, "python": sys.version.split()[0]}}
+           "host": {"cpu_model": model, "cpuinfo": cpu, "cores_visible": n_cores, "cpus_online": os.cpu_count(),
+                    "python": sys.version.split()[0]}}
     if c4 is not None:
         dt4, chars4, same4, _ = one_core(4, c4, 4)
         out["c4"] = {"value": round(chars4 / dt4, 1), "unit": "chars/s", "cores": 1,
