@@ -12,6 +12,7 @@
 // (Sec. 4.2 dispatches by piece length):
 //   bpe_thread  <= 16 bytes: one thread, the unit in registers;
 //   bpe_wave    <= 64 bytes: one wave64, one token per lane;
+//   bpe_pair32  two units of <= 32 bytes: one wave64, one unit per half;
 //   bpe_rows    longer:      NW waves over rows of 64 tokens in LDS or global
 //                            memory.
 // IDs are internal: byte b is b, the result of merge r is 256 + r.
@@ -170,6 +171,72 @@ __device__ __forceinline__ uint32_t bpe_wave(uint32_t L, ByteF byte, const DevTa
   }
   if ((uint32_t)lane < n) out(lane, id);
   return n;
+}
+
+// ---------------------------------------------------------------------------
+// Two units of at most 32 bytes on one wave64: lanes 0..31 hold the tokens of
+// unit A, lanes 32..63 those of unit B, and each half runs the rounds of
+// bpe_wave on its own unit (its own minimum, occurrences and compaction) until
+// both are done; a half whose unit is done keeps its lanes in place.  The pair
+// (lane 31, lane 32) is never a pair: the rank at lane 31 is always RANK_INF.
+// byte(h, j) and out(h, j, id) take the half (0: A, 1: B) and the position in
+// it.  Returns count(A) | count(B) << 16.  Every lane of the wave calls it
+// with the same arguments.
+// ---------------------------------------------------------------------------
+// Minimum over the calling lane's half (32 lanes) of a wave: complete in
+// lanes 31 and 63 (the row steps of wave_min_u32, then one row broadcast
+// into rows 1 and 3).
+__device__ __forceinline__ uint32_t half_min_u32(uint32_t v) {
+  int x = (int)v;
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));  // row_mirror
+  x = (int)min((uint32_t)x, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x142, 0xA, 0xF, false));  // row_bcast15 into rows 1, 3
+  return (uint32_t)x;
+}
+
+template <class ByteF, class OutF>
+__device__ __forceinline__ uint32_t bpe_pair32(uint32_t LA, uint32_t LB, ByteF byte, const DevTables& tb, OutF out) {
+  const int lane = (int)(threadIdx.x & 63u);
+  const uint32_t h = (uint32_t)lane >> 5;  // 0: unit A, 1: unit B
+  const uint32_t j = (uint32_t)lane & 31u;  // position in the half
+  const uint64_t half = h ? 0xFFFFFFFF00000000ull : 0x00000000FFFFFFFFull;
+  uint32_t n = h ? LB : LA;  // tokens of this half's unit (<= 32)
+  uint32_t id = j < n ? byte(h, j) : 0u;
+  uint32_t idn = (uint32_t)__shfl_down((int)id, 1, 64);
+  uint32_t rk = j + 1u < n ? tb.pair0[(id << 8) | idn] : RANK_INF;
+  for (;;) {
+    const uint32_t mh = half_min_u32(rk);
+    const uint32_t mA = (uint32_t)__builtin_amdgcn_readlane((int)mh, 31);
+    const uint32_t mB = (uint32_t)__builtin_amdgcn_readlane((int)mh, 63);
+    if (mA == RANK_INF && mB == RANK_INF) break;
+    const uint32_t m = h ? mB : mA;
+    const bool active = m != RANK_INF;  // this half merges this round
+    const uint64_t sel = leftmost_nonoverlapping(__ballot(active && rk == m));
+    const uint64_t keep = __ballot(j < n) & ~(sel << 1);
+    const bool me_sel = (sel >> lane) & 1ull;
+    const bool nx_sel = j < 31u && ((sel >> (lane + 1)) & 1ull);
+    const uint32_t nid = me_sel ? 256u + m : id;
+    const uint32_t r = (me_sel || nx_sel) ? RANK_DIRTY : rk;
+    // a half that merged at least one pair has a free last lane for the
+    // lanes that do not survive; a half that merged none stays in place
+    const bool kept = (keep >> lane) & 1ull;
+    const int dest = kept ? (int)(32u * h + bits_below(keep & half)) : active ? (int)(32u * h + 31u) : lane;
+    id = (uint32_t)__builtin_amdgcn_ds_permute(dest << 2, (int)nid);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_ds_permute(dest << 2, (int)r);
+    n = (uint32_t)__popcll(keep & half);
+    idn = (uint32_t)__shfl_down((int)id, 1, 64);
+    rk = RANK_INF;
+    if (j < n) {
+      rk = r2;
+      if (r2 == RANK_DIRTY) rk = j + 1u < n ? probe_rank(tb.slots, tb.nb, id, idn) : RANK_INF;
+    }
+  }
+  if (j < n) out(h, j, id);
+  const uint32_t cA = (uint32_t)__builtin_amdgcn_readlane((int)n, 0);
+  const uint32_t cB = (uint32_t)__builtin_amdgcn_readlane((int)n, 32);
+  return cA | (cB << 16);
 }
 
 // ---------------------------------------------------------------------------

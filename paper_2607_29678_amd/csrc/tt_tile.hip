@@ -1506,6 +1506,35 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       const bool inc_u = u == U_INCOMING;
       const uint32_t a = inc_u ? 0u : sh.ustart[u];
       const uint32_t L = inc_u ? L_inc : sh.ustart[u + 1] - a;
+      if (!(IGN && SPANS) && L <= 32u) {
+        // the queue is in 8-byte length classes, longest first, and 32 bytes
+        // end a class, so every unit left has at most 32 bytes too: take the
+        // next one as well, one unit per half wave (not in the rarely used
+        // ignore_merges span export, which it would push into spills)
+        const uint32_t i2 = wave_uniform(atomicAdd(&sh.med_next, 1u)) / 64u;
+        if (i2 < n_med) {
+          const uint32_t u2 = wave_uniform(sh.med[i2]);
+          const bool inc2 = u2 == U_INCOMING;
+          const uint32_t a2 = inc2 ? 0u : sh.ustart[u2];
+          const uint32_t L2 = inc2 ? L_inc : sh.ustart[u2 + 1] - a2;
+          auto by2 = [&](uint32_t hf, uint32_t j) -> uint32_t {
+            const bool in = hf ? inc2 : inc_u;
+            return in ? inc_byte(j) : (uint32_t)sh.buf[PT_PAD + (hf ? a2 : a) + j];
+          };
+          auto ot2 = [&](uint32_t hf, uint32_t j, uint32_t id) {
+            if (hf ? inc2 : inc_u) inc_out(j, id);
+            else sh.ph.b.tok[(hf ? a2 : a) + j] = id;
+          };
+          const uint32_t c2 = bpe_pair32(L, L2, by2, tb, ot2);
+          if (lane == 0) {
+            if (inc_u) sh.inc_cnt = c2 & 0xFFFFu;
+            else sh.ucnt[u] = (uint16_t)(c2 & 0xFFFFu);
+            if (inc2) sh.inc_cnt = c2 >> 16;
+            else sh.ucnt[u2] = (uint16_t)(c2 >> 16);
+          }
+          continue;
+        }
+      }
       auto by = [&](int j) -> uint32_t {
         return inc_u ? inc_byte((uint32_t)j) : (uint32_t)sh.buf[PT_PAD + a + (uint32_t)j];
       };
