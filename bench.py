@@ -345,7 +345,14 @@ def stress_block(ctx):
     sb = stored_shapes().get("C5_batch")
     if sb:
         batch["max_rounds_per_piece"] = sb["max_rounds_per_piece"]
-    return {"request": req, "batch_64x16k": batch}
+    # the same request under the walked patterns (its 65,550-byte letter run and its
+    # long whitespace and digit runs are single long pieces there too)
+    walked = {}
+    for pat in ("cl100k", "o200k", "deepseek"):
+        wt = ctx.tok(5, pat)
+        wl, _ = device_calls(ctx, wt, [d_in] * 5, [arr.size] * 5, d_out, d_len)
+        walked["device_resident_p50_ms_" + pat] = round(percentile(wl, 50), 4)
+    return {"request": req, "batch_64x16k": batch, "patterns_on_the_request": walked}
 
 
 def large_request(ctx, k, raw, timed):

@@ -170,18 +170,25 @@ constexpr uint32_t DSM_G0 = (1u << DS_O) | (1u << DS_AL) | (1u << DS_L) | (1u <<
                             (1u << DS_PS) | (1u << DS_SP) | (1u << DS_WS) | (1u << DS_NL);
 constexpr uint32_t DSM_G2 = (1u << DS_KL) | (1u << DS_KM) | (1u << DS_KP) | (1u << DS_KO);
 
-// The part of a run scan past the window (rare): from q (a character start
-// after the piece's start), while the class is in `mask` (classes of one
-// group only); `last` becomes the start of the last character whose class
-// is in `track`.
+// The class set of run bitmap k (its classes of one group), and the classes
+// whose last character the scans of that set track.
+__host__ __device__ inline uint32_t ds_run_mask(int k) {
+  return k == DSB_N ? 1u << DS_N : k == DSB_AL ? 1u << DS_AL : k == DSB_LM0 ? DSM_LM & DSM_G0
+         : k == DSB_LM2 ? DSM_LM & DSM_G2 : k == DSB_PS0 ? DSM_PS & DSM_G0 : k == DSB_PS2 ? DSM_PS & DSM_G2
+         : k == DSB_SP ? DSM_SPACE : k == DSB_NL ? 1u << DS_NL : 0u;
+}
+__host__ __device__ inline uint32_t ds_run_track(int k) { return k == DSB_SP ? 1u << DS_NL : 0u; }
+
+// The part of a run scan past the window (rare), as scan_far in tt_o200k.h,
+// with `mask` holding classes of one group only.
 __device__ __noinline__ ScanEnd ds_scan_far(const O2View v, int64_t q, uint32_t mask, uint32_t track, int64_t last) {
-  while (!v.past(q)) {
-    const uint32_t c = ds_view_cls(v, q);
-    if (!((mask >> c) & 1u)) break;
-    if ((track >> c) & 1u) last = q;
-    q += v.clen(q);
-  }
-  return {q, last};
+  return scan_far(v, q, mask, track, last, [&](uint32_t cp) { return ds_table_class(v.l1, v.l2, cp); });
+}
+
+// far_run_wave for the DeepSeek-style classes, out of line.
+__device__ __noinline__ FarRun ds_far_run_wave(const O2View v, int64_t pos, int64_t last, int64_t lim, uint32_t mask,
+                                               uint32_t track) {
+  return far_run_wave(v, pos, last, lim, mask, track, [&](uint32_t cp) { return ds_table_class(v.l1, v.l2, cp); });
 }
 
 // End (window index) of the piece that starts at s.  Always > s.  A piece

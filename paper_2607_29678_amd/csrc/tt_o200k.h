@@ -97,6 +97,7 @@ __host__ __device__ inline uint32_t o2_lead_len(uint32_t b) {
 // position w0); they may lie outside the window.
 typedef __attribute__((address_space(3))) const uint8_t lds_u8;    // a byte in LDS
 typedef __attribute__((address_space(3))) const uint32_t lds_u32;  // a word in LDS
+typedef __attribute__((address_space(3))) const int32_t lds_i32;   // a signed word in LDS
 
 // Class-set bitmaps of a tile's window: bit q of bitmap k (word q / 32 of
 // its PT_WIN / 32 words) tells whether window index q belongs to set k.  In a
@@ -105,7 +106,8 @@ typedef __attribute__((address_space(3))) const uint32_t lds_u32;  // a word in 
 // set are members (their first bytes): such a set finds the last character of
 // a class inside a run.  Document starts and positions outside the text are
 // in no set (a run stops there).
-constexpr int WALK_BITMAPS = 8;
+constexpr int WALK_BITMAPS = 9;
+constexpr int WB_DIGITS = 8;  // both patterns: ASCII digits (a run of them is cut in threes from its head)
 constexpr int WIN_WORDS = PT_WIN / 32;
 
 // First window index p >= q (0 <= q < PT_WIN) whose bit in bitmap b is 0, or
@@ -159,6 +161,9 @@ struct O2View {
   int64_t w0, n;
   int64_t doc_after;    // first document start at or after w0 + PT_WIN (n if none)
   lds_u32* bits;        // the window's class-set bitmaps, WIN_WORDS words each
+  lds_u8* asc;          // the pattern's class of every ASCII character
+  lds_i32* far_end;     // per run bitmap: where its run through the window's end ends (see far_runs)
+  lds_i32* far_last;    //   and the last tracked character past the window (-1 if none)
 
   __device__ bool in_win(int64_t q) const { return q >= 0 && q < PT_WIN; }
   __device__ uint32_t byte(int64_t q) const {
@@ -197,20 +202,191 @@ constexpr uint32_t M_OS = (1u << O2_O) | (1u << O2_MK);                    // [^
 constexpr uint32_t M_SP = (1u << O2_WS) | (1u << O2_NL);                   // \s
 constexpr uint32_t M_PF = (1u << O2_O) | (1u << O2_MK) | (1u << O2_WS);    // [^\r\n\p{L}\p{N}]
 
+// The class set of run bitmap k (0 for a bitmap that is not a run set), and
+// the classes whose last character the scans of that set track.
+__host__ __device__ inline uint32_t o2_run_mask(int k) {
+  return k == O2B_UB ? M_UB : k == O2B_LB ? M_LB : k == O2B_OS ? M_OS : k == O2B_SP ? M_SP : 0u;
+}
+__host__ __device__ inline uint32_t o2_run_track(int k) { return k == O2B_UB ? M_BM : k == O2B_SP ? 1u << O2_NL : 0u; }
+
 // The part of a run scan past the window (rare): from q (a character start
-// after the piece's start), while the class is in `mask`; `last` becomes the
-// start of the last character whose class is in `track`.
+// past the window), while the class is in `mask`; `last` becomes the start of
+// the last character whose class is in `track`.  The text is read 16 bytes a
+// step (all loads of a step in flight together), and the characters that lie
+// whole in those bytes are decoded and classed from registers (ASCII from the
+// ASCII table, others from the class table with tcls), so that a run of tens
+// of thousands of characters costs thousands of load round trips, not tens of
+// thousands.
 struct ScanEnd {
   int64_t q, last;
 };
-__device__ __noinline__ ScanEnd o2_scan_far(const O2View v, int64_t q, uint32_t mask, uint32_t track, int64_t last) {
-  while (!v.past(q)) {
-    const uint32_t c = v.cls(q);
-    if (!((mask >> c) & 1u)) break;
-    if ((track >> c) & 1u) last = q;
-    q += v.clen(q);
+template <class TClsF>
+__device__ __forceinline__ ScanEnd scan_far(const O2View& v, int64_t q, uint32_t mask, uint32_t track, int64_t last,
+                                            TClsF tcls) {
+  const int64_t lim = (v.doc_after < v.n ? v.doc_after : v.n) - v.w0;  // where the document ends
+#pragma unroll 1
+  while (q < lim) {
+    const uint8_t* src = v.text + (v.w0 + q);
+    const int64_t avail = lim - q;  // bytes before the end (> 0)
+    uint32_t B[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) B[i] = i < avail ? (uint32_t)src[i] : 0u;
+    uint32_t o = 0;      // start of the next character in the step's bytes
+    bool stop = false;   // a character did not fit, or the run ended
+    bool end = false;    // the run ended at o
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (!stop && (uint32_t)i == o) {
+        const uint32_t b0 = B[i];
+        const uint32_t L = o2_lead_len(b0);  // (1 for bytes that cannot lead)
+        if ((int64_t)i + (int64_t)L > (avail < 16 ? avail : 16)) {
+          stop = true;  // not whole in this step: the next step starts with it
+        } else {
+          uint32_t c;
+          if (b0 < 0x80u) {
+            c = v.asc[b0];
+          } else if (L == 1u) {
+            c = O2_NONE;  // a stray continuation byte: invalid text
+          } else {
+            uint32_t cp = b0 & (0x7Fu >> L);
+#pragma unroll
+            for (int k = 1; k < 4; ++k)
+              if ((uint32_t)k < L && i + k < 16) cp = (cp << 6) | (B[i + k] & 0x3Fu);
+            c = cp < 0x110000u ? tcls(cp) : O2_NONE;
+          }
+          if (!((mask >> c) & 1u)) {
+            stop = true;
+            end = true;
+          } else {
+            if ((track >> c) & 1u) last = q + i;
+            o = (uint32_t)i + L;
+          }
+        }
+      }
+    }
+    q += o;
+    if (end || o == 0u) break;  // (o == 0: a character cut by the end of the text)
   }
   return {q, last};
+}
+
+// Where the runs that hold the window's last character end past the window.
+// Every walk's scan that reaches the window's end continues the same run past
+// it: from the end of the window's last character, while the class is in the
+// run set.  So a tile finds that continuation once per run set before its
+// walks: first over the 16 bytes staged past the window (one thread per set),
+// then, for a run that goes on beyond them, with one wave over the text,
+// 16 bytes per lane per step (far_run_wave).
+struct FarRun {
+  int64_t end, last;
+  bool open;  // the run goes on past the staged bytes
+};
+template <class TClsF>
+__device__ __forceinline__ FarRun far_run_staged(const O2View& v, int64_t q, int64_t lim, uint32_t mask, uint32_t track,
+                                                 TClsF tcls) {
+  int64_t last = -1;
+#pragma unroll 1
+  for (;;) {
+    if (q >= lim) return {q, last, false};          // the document ends
+    if (q + 4 > PT_WIN + 16) return {q, last, true};  // (the next character may not be staged whole)
+    const uint32_t b0 = v.buf[PT_PAD + q];
+    const uint32_t L = o2_lead_len(b0);
+    if (q + (int64_t)L > lim) return {q, last, false};  // cut by the end: not in any set
+    uint32_t c;
+    if (b0 < 0x80u) {
+      c = v.asc[b0];
+    } else if (L == 1u) {
+      c = O2_NONE;
+    } else {
+      uint32_t cp = b0 & (0x7Fu >> L);
+      for (uint32_t k = 1; k < L; ++k) cp = (cp << 6) | (v.buf[PT_PAD + q + k] & 0x3Fu);
+      c = cp < 0x110000u ? tcls(cp) : O2_NONE;
+    }
+    if (!((mask >> c) & 1u)) return {q, last, false};
+    if ((track >> c) & 1u) last = q;
+    q += L;
+  }
+}
+
+// The same past the staged bytes, on one wave: lane i takes the characters
+// that start in [pos + 16i, pos + 16i + 16), decoded from 19 bytes in
+// registers; the first lane that finds the run's end gives it, and the last
+// tracked character is the latest one before that end.  Every lane of the
+// wave calls it with the same arguments.
+template <class TClsF>
+__device__ __forceinline__ FarRun far_run_wave(const O2View& v, int64_t pos, int64_t last, int64_t lim, uint32_t mask,
+                                               uint32_t track, TClsF tcls) {
+  const uint32_t lane = threadIdx.x & 63u;
+  constexpr uint32_t NONE = 0xFFFFFFFFu;
+#pragma unroll 1
+  for (;;) {
+    const int64_t a = pos + 16 * (int64_t)lane;
+    const int64_t avail = lim - a;  // bytes of the lane's reach before the end (may be <= 0)
+    uint32_t B[19];
+#pragma unroll
+    for (int i = 0; i < 19; ++i) B[i] = i < avail ? (uint32_t)v.text[v.w0 + a + i] : 0u;
+    // a character that starts before a belongs to the lane before
+    uint32_t o = (B[0] & 0xC0u) == 0x80u ? ((B[1] & 0xC0u) == 0x80u ? ((B[2] & 0xC0u) == 0x80u ? 3u : 2u) : 1u) : 0u;
+    uint32_t stop = NONE;    // offset of the run's end in the lane's part
+    uint32_t mylast = NONE;  // offset of the lane's last tracked character
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (stop == NONE && (uint32_t)i == o) {
+        if ((int64_t)i >= avail) {
+          stop = (uint32_t)i;  // the document ends
+        } else {
+          const uint32_t b0 = B[i];
+          const uint32_t L = o2_lead_len(b0);
+          uint32_t c;
+          if ((int64_t)i + (int64_t)L > avail) {
+            c = O2_NONE;  // cut by the end
+          } else if (b0 < 0x80u) {
+            c = v.asc[b0];
+          } else if (L == 1u) {
+            c = O2_NONE;
+          } else {
+            uint32_t cp = b0 & (0x7Fu >> L);
+#pragma unroll
+            for (int k = 1; k < 4; ++k)
+              if ((uint32_t)k < L) cp = (cp << 6) | (B[i + k] & 0x3Fu);
+            c = cp < 0x110000u ? tcls(cp) : O2_NONE;
+          }
+          if (!((mask >> c) & 1u)) {
+            stop = (uint32_t)i;
+          } else {
+            if ((track >> c) & 1u) mylast = (uint32_t)i;
+            o = (uint32_t)i + L;
+          }
+        }
+      }
+    }
+    const uint64_t ends = __ballot(stop != NONE);
+    const uint32_t first = ends ? (uint32_t)__builtin_ctzll(ends) : 64u;  // lane with the run's end
+    // latest tracked character in the lanes up to that one (offsets from pos, + 1; 0 for none)
+    uint32_t t = (lane <= first && mylast != NONE) ? 16u * lane + mylast + 1u : 0u;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t u = (uint32_t)__shfl_xor((int)t, d, 64);
+      t = u > t ? u : t;
+    }
+    if (t != 0u) last = pos + (int64_t)(t - 1u);
+    if (ends) {
+      const uint32_t st = (uint32_t)__builtin_amdgcn_readlane((int)stop, (int)first);
+      return {pos + 16 * (int64_t)first + st, last, false};
+    }
+    pos += 16 * 64;
+  }
+}
+
+// far_run_wave for the o200k-style classes, out of line (it runs for few
+// tiles, and its registers would otherwise weigh on the whole kernel).
+__device__ __noinline__ FarRun o2_far_run_wave(const O2View v, int64_t pos, int64_t last, int64_t lim, uint32_t mask,
+                                               uint32_t track) {
+  return far_run_wave(v, pos, last, lim, mask, track, [&](uint32_t cp) { return o2_table_class(v.l1, v.l2, cp); });
+}
+
+__device__ __noinline__ ScanEnd o2_scan_far(const O2View v, int64_t q, uint32_t mask, uint32_t track, int64_t last) {
+  return scan_far(v, q, mask, track, last, [&](uint32_t cp) { return o2_table_class(v.l1, v.l2, cp); });
 }
 
 // Two ways to read a walk's positions (P is the position type).  The piece
@@ -271,9 +447,10 @@ struct FullView {
         if (t >= 0) last = t;
       }
       if (p < PT_WIN) return p;
-      int64_t r = PT_WIN - 1;  // the run reaches the window's end: go on from its last character
-      while (r > q && (v.byte(r) & 0xC0u) == 0x80u) --r;
-      q = r + v.clen(r);
+      // the run holds the window's last character: where it ends past the
+      // window was found for the tile before the walks
+      if (tb >= 0 && v.far_last[rb] >= 0) last = v.far_last[rb];
+      return v.far_end[rb];
     }
     const ScanEnd f = FAR_SCAN(v, q, mask, track, last);
     last = f.last;

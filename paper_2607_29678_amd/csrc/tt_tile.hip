@@ -345,6 +345,10 @@ struct PtShared {
   uint32_t ctile;             // span export: non-continuation bytes the tile owns
   int64_t doc_lo_idx;         // batch: first document start index touching the window
   int last_own;               // cl100k: window index of the tile's last own character
+  // walked patterns: where the run of each run set through the window's end
+  // ends past it, and its last tracked character there (window indices)
+  int32_t far_end[WALK_BITMAPS], far_last[WALK_BITMAPS];
+  uint32_t far_open;          // sets whose run goes on past the staged bytes
   // cl100k: a whitespace stretch after CR/LF that reaches the window's end
   int32_t ws_pend;            // its window index, or -1
   uint32_t ws_res;            // 1 when it is the last stretch of its run (read on past the window)
@@ -488,8 +492,11 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   constexpr bool DS = PAT == TT_PATTERN_DEEPSEEK;
   constexpr bool WALK = PAT == TT_PATTERN_O200K || DS;
   if (WALK && tid < PT_WIN / 32) sh.ph.a.o2seg[tid] = 0;
-  static_assert(WALK_BITMAPS * WIN_WORDS == PT_THREADS, "one bitmap word per thread to clear");
-  if (WALK) sh.ph.a.o2bits[tid] = 0;
+  static_assert(WALK_BITMAPS * WIN_WORDS <= 2 * PT_THREADS, "two bitmap words per thread to clear");
+  if (WALK) {
+    sh.ph.a.o2bits[tid] = 0;
+    if (tid + PT_THREADS < WALK_BITMAPS * WIN_WORDS) sh.ph.a.o2bits[tid + PT_THREADS] = 0;
+  }
   // the ticket's round trip (tickets are handed out one at a time) overlaps
   // the staging of the tables, which do not depend on the tile
   uint32_t ticket = 0;
@@ -534,6 +541,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     sh.n_big = 0;
     sh.inc_cnt = 0;
     sh.ws_pend = -1;
+    sh.far_open = 0;
   }
   __syncthreads();
   const uint32_t t = wave_uniform(sh.tile);
@@ -981,8 +989,11 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         const uint32_t c = cr(j);
         const uint32_t cl = c & 15u;
         uint32_t m = 0;
-        if (inside(qb + j) && !(c & CODE_DOCSTART))
+        if (inside(qb + j) && !(c & CODE_DOCSTART)) {
           m = cl == O2_NONE ? (DS ? DSB_RUNS : O2B_RUNS) : (DS ? ds_bits_of(cl) : o2_bits_of(cl));
+          const uint32_t b = sh.buf[PT_PAD + qb + j];
+          if (b - (uint32_t)'0' < 10u) m |= 1u << WB_DIGITS;
+        }
 #pragma unroll
         for (int k = 0; k < WALK_BITMAPS; ++k) nib[k] |= ((m >> k) & 1u) << j;
       }
@@ -992,7 +1003,51 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     }
     __syncthreads();
     const O2View v{(lds_u8*)sh.buf, (lds_u8*)sh.ph.a.code, (lds_u8*)sh.ph.a.o2.l1, (lds_u8*)sh.ph.a.o2.l2,
-                   w.text, w0, n, BATCH ? sh.o2_doc_after : n, (lds_u32*)sh.ph.a.o2bits};
+                   w.text, w0, n, BATCH ? sh.o2_doc_after : n, (lds_u32*)sh.ph.a.o2bits,
+                   (lds_u8*)sh.ph.a.o2.asc, (lds_i32*)sh.far_end, (lds_i32*)sh.far_last};
+    // the runs through the window's end: how far the run of each run set that
+    // holds the window's last character goes on past the window, for the
+    // walks' scans that reach the end (tt_o200k.h, far_run_staged and
+    // far_run_wave)
+    {
+      int r0 = PT_WIN - 1;  // the window's last character
+      while (r0 > PT_WIN - 4 && (sh.buf[PT_PAD + r0] & 0xC0u) == 0x80u) --r0;
+      const uint32_t c_last = sh.ph.a.code[PT_PAD + r0] & 15u;
+      const int64_t start = r0 + (int64_t)o2_lead_len(sh.buf[PT_PAD + r0]);
+      const int64_t doc_end = BATCH && sh.o2_doc_after < n ? sh.o2_doc_after : n;
+      const int64_t lim = doc_end - w0;
+      auto tcls = [&](uint32_t cp) -> uint32_t {
+        return DS ? ds_table_class(v.l1, v.l2, cp) : o2_table_class(v.l1, v.l2, cp);
+      };
+      if (tid < WALK_BITMAPS) {
+        const uint32_t mk = DS ? ds_run_mask(tid) : o2_run_mask(tid);
+        const uint32_t tk = DS ? ds_run_track(tid) : o2_run_track(tid);
+        FarRun f{start, -1, false};
+        if (mk != 0u && ((mk >> c_last) & 1u)) f = far_run_staged(v, start, lim, mk, tk, tcls);
+        sh.far_end[tid] = (int32_t)f.end;
+        sh.far_last[tid] = (int32_t)f.last;
+        if (f.open) atomicOr(&sh.far_open, 1u << tid);
+      }
+      __syncthreads();
+      const uint32_t open = sh.far_open;
+      if (open != 0u) {
+        if (wave == 0) {
+#pragma unroll 1
+          for (int k = 0; k < WALK_BITMAPS; ++k) {
+            if (!((open >> k) & 1u)) continue;
+            const uint32_t mk = DS ? ds_run_mask(k) : o2_run_mask(k);
+            const uint32_t tk = DS ? ds_run_track(k) : o2_run_track(k);
+            const FarRun f = DS ? ds_far_run_wave(v, sh.far_end[k], sh.far_last[k], lim, mk, tk)
+                                : o2_far_run_wave(v, sh.far_end[k], sh.far_last[k], lim, mk, tk);
+            if (lane == 0) {
+              sh.far_end[k] = (int32_t)f.end;
+              sh.far_last[k] = (int32_t)f.last;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
     const int64_t own_end = n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN;
     auto segbit = [&](int64_t q) -> bool { return q >= 0 && q < PT_WIN && ((sh.ph.a.o2seg[q >> 5] >> (q & 31)) & 1u); };
     // one loop per lane, one piece per step: the lane's walk starts in order
@@ -1043,9 +1098,25 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
 #pragma unroll 1
     while (active) {
       if (s >= PT_HALO) sh.ph.a.o2piece[s] = 1;  // (s < own_end <= PT_WIN)
-      const int64_t e = DS ? ds_piece_end(v, s) : o2_piece_end(v, s);
+      // A run of numbers is cut in threes from its head whatever surrounds it
+      // (no other alternative takes a number), so from a piece start inside a
+      // run of ASCII digits every third byte starts a piece: the full chunks
+      // that end by own_end are marked in one step (a run of thousands of
+      // digits is one short loop, not a piece per step).
+      const int64_t dig = win_next_zero(v.bits + WB_DIGITS * WIN_WORDS, s) - s;  // ASCII digits from s
+      const int64_t full = (dig < own_end - s ? dig : own_end - s) / 3;
+      int64_t ps = s, e;
+      if (full >= 1) {
+#pragma unroll 1
+        for (int64_t k = 1; k < full; ++k)
+          if (s + 3 * k >= PT_HALO) sh.ph.a.o2piece[s + 3 * k] = 1;
+        ps = s + 3 * (full - 1);
+        e = s + 3 * full;
+      } else {
+        e = DS ? ds_piece_end(v, s) : o2_piece_end(v, s);
+      }
       if (e >= own_end) {  // the tile's last piece (one lane finds it)
-        sh.o2_last_s = s;
+        sh.o2_last_s = ps;
         sh.o2_last_e = e;
       }
       if (e < own_end && !segbit(e)) {

@@ -1,9 +1,9 @@
 """GPU parity for long BPE units and tile-boundary placements.
 
 The library encodes a unit (a piece, or a part of a piece that no merge can
-join across) with one thread up to 16 bytes, one wave up to 64 bytes, the
-whole block over rows in LDS up to a tile window, and over rows in global
-memory beyond that; a unit that starts in one tile and ends in a later one is
+join across) with one thread up to 16 bytes, half a wave up to 32 bytes (two
+such units share a wave), one wave up to 64 bytes, the whole block over rows in
+LDS up to a tile window, and over rows in global memory beyond that; a unit that starts in one tile and ends in a later one is
 encoded by the later tile.  These cases build units of chosen lengths from
 bytes whose every adjacent pair is the junction of some merge (so nothing cuts
 them), put them at chosen offsets from the tile edges, and compare the IDs with
@@ -100,3 +100,41 @@ def test_lengths_around_tile_edges(gpu, k):
             got = tok.encode(data).tolist()
             want = oracle_ids(data, oracle_table(k), pattern_of(k), memo)
             assert got == want, "length %d" % n
+
+
+def _paired_texts(k, seed):
+    """Many units of 17-32 bytes (two share a wave, one per half), mixed with
+    longer ones that go first in the queue, odd and even counts per tile, and
+    such units at tile edges, where one of a pair is the tile's incoming unit."""
+    rng = random.Random(seed)
+    letters = _clique(k, b"etaoinsrhldcumfpgwybvkxjqz")
+    texts = []
+
+    def unit(n):
+        return bytes(rng.choice(letters) for _ in range(n))
+
+    for count in (1, 2, 3, 7, 8, 9, 40, 41, 150):
+        parts = [unit(rng.choice((17, 18, 24, 25, 31, 32))) for _ in range(count)]
+        parts += [unit(rng.choice((33, 48, 64, 65, 100))) for _ in range(count // 3)]
+        rng.shuffle(parts)
+        texts.append(b" ".join(parts))
+    for edge in (1, 2):
+        for off in (-20, -17, -1, 0, 3):
+            pre = edge * TILE_OWN + off
+            filler = b" ".join(unit(rng.choice((17, 20, 32))) for _ in range(max(1, pre // 22)))[: max(0, pre)]
+            texts.append(filler + unit(rng.choice((17, 23, 32))) + b" " + unit(19) + b" z")
+    return texts
+
+
+@pytest.mark.parametrize("k", [1, 4])
+def test_paired_wave_units(gpu, k):
+    tok = lib_tokenizer(k)
+    memo = {}
+    texts = _paired_texts(k, 91 + k)
+    for i, data in enumerate(texts):
+        got = tok.encode(data).tolist()
+        want = oracle_ids(data, oracle_table(k), pattern_of(k), memo)
+        assert got == want, "case %d: %d bytes" % (i, len(data))
+    got = tok.encode_batch(texts)
+    for j, d in enumerate(texts):
+        assert got[j].tolist() == oracle_ids(d, oracle_table(k), pattern_of(k), memo), "document %d" % j
