@@ -185,10 +185,9 @@ __device__ __noinline__ ScanEnd ds_scan_far(const O2View v, int64_t q, uint32_t 
   return scan_far(v, q, mask, track, last, [&](uint32_t cp) { return ds_table_class(v.l1, v.l2, cp); });
 }
 
-// far_run_wave for the DeepSeek-style classes, out of line.
-__device__ __noinline__ FarRun ds_far_run_wave(const O2View v, int64_t pos, int64_t last, int64_t lim, uint32_t mask,
-                                               uint32_t track) {
-  return far_run_wave(v, pos, last, lim, mask, track, [&](uint32_t cp) { return ds_table_class(v.l1, v.l2, cp); });
+// far_serve for the DeepSeek-style pattern, out of line.
+__device__ __noinline__ void ds_far_serve(const O2View v, uint32_t sets) {
+  far_serve(v, sets, ds_run_mask, ds_run_track, [&](uint32_t cp) { return ds_table_class(v.l1, v.l2, cp); });
 }
 
 // End (window index) of the piece that starts at s.  Always > s.  A piece
@@ -279,13 +278,16 @@ __device__ __forceinline__ P ds_end(V& v, const P s) {
   return e;  // else \s+
 }
 
-// The piece's end with the full view (rare: pieces at the window's end).
+// The piece's end with the full view (rare: pieces at the window's end), or
+// -1 - k when the run through the window's end of bitmap k is needed first.
 __device__ __noinline__ int64_t ds_end_full(const O2View v, int64_t s) {
   FullView<ds_cls_far, ds_scan_far> f{v};
-  return ds_end(f, s);
+  const int64_t e = ds_end(f, s);
+  return f.need >= 0 ? -1 - (int64_t)f.need : e;
 }
 
-// End (window index) of the piece that starts at s (0 <= s < PT_WIN).
+// End (window index) of the piece that starts at s (0 <= s < PT_WIN), or
+// -1 - k as ds_end_full.
 __device__ __forceinline__ int64_t ds_piece_end(const O2View& v, int64_t s) {
   WinView f{v.buf, v.code, v.bits, (int32_t)(v.n - v.w0 < PT_WIN ? v.n - v.w0 : PT_WIN)};
   const int32_t e = ds_end(f, (int32_t)s);

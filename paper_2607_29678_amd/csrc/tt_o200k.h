@@ -137,6 +137,28 @@ __device__ __forceinline__ int64_t win_last_one(lds_u32* b, int64_t a, int64_t e
   }
 }
 
+// Position of the set bit of rank r (counted from bit 0) of m; r < popcount(m).
+__host__ __device__ inline uint32_t select_bit64(uint64_t m, uint32_t r) {
+  uint32_t p = 0;
+  uint32_t x = (uint32_t)m;
+  uint32_t c = (uint32_t)__builtin_popcount(x);
+  if (r >= c) {
+    r -= c;
+    p = 32;
+    x = (uint32_t)(m >> 32);
+  }
+#pragma unroll
+  for (int w = 16; w >= 1; w >>= 1) {
+    c = (uint32_t)__builtin_popcount(x & ((1u << w) - 1u));
+    if (r >= c) {
+      r -= c;
+      p += (uint32_t)w;
+      x >>= w;
+    }
+  }
+  return p;
+}
+
 // The o200k-style bitmaps: runs of [Lu Lt Lm Lo M], of [Ll Lm Lo M], of
 // [^\s\p{L}\p{N}] and of \s; the last Lm/Lo letter or mark, and the last CR/LF.
 enum : int { O2B_UB = 0, O2B_LB = 1, O2B_OS = 2, O2B_SP = 3, O2B_BM = 4, O2B_NL = 5 };
@@ -152,6 +174,17 @@ __host__ __device__ inline uint32_t o2_bits_of(uint32_t c) {
   return m;
 }
 
+// The runs through the window's end (far_serve): per run bitmap, where its
+// run through the window's end ends and the last tracked character past the
+// window (-1 if none), both window indices, and their state (FAR_NONE, then
+// FAR_BUSY while a wave finds them, FAR_READY once they hold their values).
+enum : uint32_t { FAR_NONE = 0, FAR_BUSY = 1, FAR_READY = 2 };
+struct FarRuns {
+  int32_t end[WALK_BITMAPS], last[WALK_BITMAPS];
+  uint32_t state[WALK_BITMAPS];
+};
+typedef __attribute__((address_space(3))) FarRuns lds_far;
+
 struct O2View {
   lds_u8* buf;          // window bytes at PT_PAD + q, q in [-PT_PAD, PT_WIN + 16)
   lds_u8* code;         // window codes at PT_PAD + q: class | CODE_DOCSTART
@@ -162,8 +195,7 @@ struct O2View {
   int64_t doc_after;    // first document start at or after w0 + PT_WIN (n if none)
   lds_u32* bits;        // the window's class-set bitmaps, WIN_WORDS words each
   lds_u8* asc;          // the pattern's class of every ASCII character
-  lds_i32* far_end;     // per run bitmap: where its run through the window's end ends (see far_runs)
-  lds_i32* far_last;    //   and the last tracked character past the window (-1 if none)
+  lds_far* far;         // the runs through the window's end (see far_serve)
 
   __device__ bool in_win(int64_t q) const { return q >= 0 && q < PT_WIN; }
   __device__ uint32_t byte(int64_t q) const {
@@ -273,10 +305,10 @@ __device__ __forceinline__ ScanEnd scan_far(const O2View& v, int64_t q, uint32_t
 // Where the runs that hold the window's last character end past the window.
 // Every walk's scan that reaches the window's end continues the same run past
 // it: from the end of the window's last character, while the class is in the
-// run set.  So a tile finds that continuation once per run set before its
-// walks: first over the 16 bytes staged past the window (one thread per set),
-// then, for a run that goes on beyond them, with one wave over the text,
-// 16 bytes per lane per step (far_run_wave).
+// run set.  So a tile finds that continuation once per run set, when a walk
+// first needs it, on one wave: first over the 16 bytes staged past the window
+// (one lane), then, for a run that goes on beyond them, over the text with
+// the whole wave, 16 bytes per lane per step (far_run_wave).
 struct FarRun {
   int64_t end, last;
   bool open;  // the run goes on past the staged bytes
@@ -378,11 +410,62 @@ __device__ __forceinline__ FarRun far_run_wave(const O2View& v, int64_t pos, int
   }
 }
 
-// far_run_wave for the o200k-style classes, out of line (it runs for few
-// tiles, and its registers would otherwise weigh on the whole kernel).
-__device__ __noinline__ FarRun o2_far_run_wave(const O2View v, int64_t pos, int64_t last, int64_t lim, uint32_t mask,
-                                               uint32_t track) {
-  return far_run_wave(v, pos, last, lim, mask, track, [&](uint32_t cp) { return o2_table_class(v.l1, v.l2, cp); });
+// Finds, on one wave, the runs through the window's end of the run bitmaps
+// in `sets` (bit k: bitmap k) that are not found yet: lane 0 takes the staged
+// bytes, then the whole wave reads on if the run goes further.  A set that
+// another wave is finding is waited for (that wave waits for nothing).  The
+// walks ask for a set only when a scan of theirs reaches the window's end
+// (FullView), so most tiles find none.  mask_of / track_of give a bitmap's
+// class set and tracked classes, tcls the class of a non-ASCII code point.
+// Every lane of the wave calls it with the same `sets`.
+template <class MaskF, class TrackF, class TClsF>
+__device__ __forceinline__ void far_serve(const O2View& v, uint32_t sets, MaskF mask_of, TrackF track_of, TClsF tcls) {
+  const uint32_t lane = threadIdx.x & 63u;
+  const int64_t lim = (v.doc_after < v.n ? v.doc_after : v.n) - v.w0;  // where the document ends
+  uint32_t* state = (uint32_t*)v.far->state;
+#pragma unroll 1
+  for (int k = 0; k < WALK_BITMAPS; ++k) {
+    if (!((sets >> k) & 1u)) continue;
+    uint32_t mine = 0;
+    if (lane == 0u) mine = atomicCAS(&state[k], FAR_NONE, FAR_BUSY) == FAR_NONE;
+    mine = (uint32_t)__builtin_amdgcn_readfirstlane((int)mine);
+    if (!mine) {
+      while (__hip_atomic_load(&state[k], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != FAR_READY)
+        __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    const uint32_t mk = mask_of(k), tk = track_of(k);
+    int32_t fe = 0, fl = -1, fo = 0;
+    if (lane == 0u) {
+      int r0 = PT_WIN - 1;  // the window's last character
+      while (r0 > PT_WIN - 4 && (v.buf[PT_PAD + r0] & 0xC0u) == 0x80u) --r0;
+      const uint32_t c_last = v.code[PT_PAD + r0] & 15u;
+      const int64_t start = r0 + (int64_t)o2_lead_len(v.buf[PT_PAD + r0]);
+      FarRun f{start, -1, false};
+      if (mk != 0u && ((mk >> c_last) & 1u)) f = far_run_staged(v, start, lim, mk, tk, tcls);
+      fe = (int32_t)f.end;
+      fl = (int32_t)f.last;
+      fo = f.open;
+    }
+    fe = __builtin_amdgcn_readfirstlane(fe);
+    fl = __builtin_amdgcn_readfirstlane(fl);
+    if (__builtin_amdgcn_readfirstlane(fo)) {
+      const FarRun f = far_run_wave(v, fe, fl, lim, mk, tk, tcls);
+      fe = (int32_t)f.end;
+      fl = (int32_t)f.last;
+    }
+    if (lane == 0u) {
+      v.far->end[k] = fe;
+      v.far->last[k] = fl;
+      __hip_atomic_store(&state[k], FAR_READY, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+  }
+}
+
+// far_serve for the o200k-style pattern, out of line (rare, and its
+// registers would otherwise weigh on the whole kernel).
+__device__ __noinline__ void o2_far_serve(const O2View v, uint32_t sets) {
+  far_serve(v, sets, o2_run_mask, o2_run_track, [&](uint32_t cp) { return o2_table_class(v.l1, v.l2, cp); });
 }
 
 __device__ __noinline__ ScanEnd o2_scan_far(const O2View v, int64_t q, uint32_t mask, uint32_t track, int64_t last) {
@@ -433,13 +516,20 @@ struct WinView {
 template <uint32_t (*FAR_CLS)(const O2View, int64_t), ScanEnd (*FAR_SCAN)(const O2View, int64_t, uint32_t, uint32_t, int64_t)>
 struct FullView {
   const O2View& v;
+  int need = -1;  // a run bitmap whose run through the window's end is not found yet (see scan)
   __device__ uint32_t byte(int64_t q) const { return v.byte(q); }
   __device__ uint32_t clen(int64_t q) const { return v.clen(q); }
   __device__ uint32_t cls(int64_t q) const { return v.in_win(q) ? (uint32_t)(v.code[PT_PAD + q] & 15u) : FAR_CLS(v, q); }
-  __device__ bool past(int64_t q) const { return v.past(q); }
+  __device__ bool past(int64_t q) const { return need >= 0 || v.past(q); }
   // as WinView::scan, with `mask` the classes of the run for the part past
-  // the window
-  __device__ int64_t scan(int64_t q, uint32_t mask, uint32_t track, int64_t& last, int rb, int tb) const {
+  // the window.  A run that holds the window's last character ends where the
+  // tile's run of that bitmap through the window's end ends (far_serve); when
+  // that is not found yet, the scan sets `need`, and from then on every scan
+  // returns at once and every position reads as past the text (the piece's
+  // end is then of no use: the walk asks for the run and takes the piece
+  // again).
+  __device__ int64_t scan(int64_t q, uint32_t mask, uint32_t track, int64_t& last, int rb, int tb) {
+    if (need >= 0) return q;
     if (q < PT_WIN) {
       const int64_t p = win_next_zero(v.bits + rb * WIN_WORDS, q);
       if (tb >= 0) {
@@ -447,10 +537,12 @@ struct FullView {
         if (t >= 0) last = t;
       }
       if (p < PT_WIN) return p;
-      // the run holds the window's last character: where it ends past the
-      // window was found for the tile before the walks
-      if (tb >= 0 && v.far_last[rb] >= 0) last = v.far_last[rb];
-      return v.far_end[rb];
+      if (__hip_atomic_load((const uint32_t*)&v.far->state[rb], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != FAR_READY) {
+        need = rb;
+        return PT_WIN;
+      }
+      if (tb >= 0 && v.far->last[rb] >= 0) last = v.far->last[rb];
+      return v.far->end[rb];
     }
     const ScanEnd f = FAR_SCAN(v, q, mask, track, last);
     last = f.last;
@@ -554,13 +646,16 @@ __device__ __forceinline__ P o2_end(V& v, const P s) {
   return e;  // else \s+
 }
 
-// The piece's end with the full view (rare: pieces at the window's end).
+// The piece's end with the full view (rare: pieces at the window's end), or
+// -1 - k when the run through the window's end of bitmap k is needed first.
 __device__ __noinline__ int64_t o2_end_full(const O2View v, int64_t s) {
   FullView<o2_cls_far, o2_scan_far> f{v};
-  return o2_end(f, s);
+  const int64_t e = o2_end(f, s);
+  return f.need >= 0 ? -1 - (int64_t)f.need : e;
 }
 
-// End (window index) of the piece that starts at s (0 <= s < PT_WIN).
+// End (window index) of the piece that starts at s (0 <= s < PT_WIN), or
+// -1 - k as o2_end_full.
 __device__ __forceinline__ int64_t o2_piece_end(const O2View& v, int64_t s) {
   WinView f{v.buf, v.code, v.bits, (int32_t)(v.n - v.w0 < PT_WIN ? v.n - v.w0 : PT_WIN)};
   const int32_t e = o2_end(f, (int32_t)s);

@@ -346,9 +346,9 @@ struct PtShared {
   int64_t doc_lo_idx;         // batch: first document start index touching the window
   int last_own;               // cl100k: window index of the tile's last own character
   // walked patterns: where the run of each run set through the window's end
-  // ends past it, and its last tracked character there (window indices)
-  int32_t far_end[WALK_BITMAPS], far_last[WALK_BITMAPS];
-  uint32_t far_open;          // sets whose run goes on past the staged bytes
+  // ends past it, its last tracked character there, and whether wave 0 has
+  // published them
+  FarRuns far;
   // cl100k: a whitespace stretch after CR/LF that reaches the window's end
   int32_t ws_pend;            // its window index, or -1
   uint32_t ws_res;            // 1 when it is the last stretch of its run (read on past the window)
@@ -541,8 +541,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     sh.n_big = 0;
     sh.inc_cnt = 0;
     sh.ws_pend = -1;
-    sh.far_open = 0;
   }
+  if (tid < WALK_BITMAPS) sh.far.state[tid] = FAR_NONE;
   __syncthreads();
   const uint32_t t = wave_uniform(sh.tile);
   const uint32_t n_tiles = w.n_tiles;
@@ -952,10 +952,17 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // back), whitespace after CR/LF and a letter after a lone symbol branch.
   uint32_t flags = 0;
   if (WALK) {
-    // o200k- and DeepSeek-style: segment starts are document starts and
+    // o200k- and DeepSeek-style: segment starts are document starts,
     // synchronizing positions (their two neighbouring characters form a
-    // transition of o2_sync or ds_sync); the pieces of a segment come from
-    // running the pattern's alternatives from its start, one thread per segment
+    // transition of o2_sync or ds_sync) and two whitespace cases that start a
+    // piece for every left context given the text to their right (below);
+    // the pieces of a segment come from running the pattern's alternatives
+    // from its start, one lane per segment
+    auto walk_ws = [&](uint32_t cl) -> bool { return DS ? (cl == DS_SP || cl == DS_WS) : cl == O2_WS; };
+    auto walk_solid = [&](uint32_t cl) -> bool {  // not whitespace (DeepSeek-style: and of the rest group)
+      return DS ? (cl != DS_SP && cl != DS_WS && cl != DS_NL && ds_group(cl) == 0u)
+                : (cl != O2_WS && cl != O2_NL && cl != O2_NONE);
+    };
     uint32_t seg = 0;
 #pragma unroll
     for (int j = 0; j < PT_BPT; ++j) {
@@ -973,6 +980,17 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
           st = DS ? ds_sync(cr(j - k) & 15u, c & 15u)
                   : o2_sync(cr(j - k) & 15u, c & 15u, k == 1 ? bx : 0x80u, sh.buf[PT_PAD + q]);
         }
+      }
+      if (!st && walk_ws(c & 15u)) {
+        // one-byte whitespace before a character that is not whitespace, in
+        // the same document (and, DeepSeek-style, the same group stretch):
+        // no piece holds whitespace past its first character unless the
+        // piece ends with whitespace or CR/LF (the alternatives that take
+        // whitespace runs), and those cannot end before a character that is
+        // not whitespace inside the stretch, so a piece starts here whatever
+        // the left context
+        const uint32_t c2 = cr(j + 1);
+        st = inside(q + 1) && !(c2 & CODE_DOCSTART) && walk_solid(c2 & 15u);
       }
       if (st) seg |= 1u << j;
     }
@@ -1001,55 +1019,40 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       for (int k = 0; k < WALK_BITMAPS; ++k)
         if (nib[k]) atomicOr(&sh.ph.a.o2bits[k * WIN_WORDS + (qb >> 5)], nib[k] << (qb & 31));
     }
+    if (tid == 0) {  // the tile's last piece, until a walk finds it (kept only for invalid text)
+      sh.o2_last_s = PT_HALO;
+      sh.o2_last_e = n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN;
+    }
     __syncthreads();
     const O2View v{(lds_u8*)sh.buf, (lds_u8*)sh.ph.a.code, (lds_u8*)sh.ph.a.o2.l1, (lds_u8*)sh.ph.a.o2.l2,
                    w.text, w0, n, BATCH ? sh.o2_doc_after : n, (lds_u32*)sh.ph.a.o2bits,
-                   (lds_u8*)sh.ph.a.o2.asc, (lds_i32*)sh.far_end, (lds_i32*)sh.far_last};
-    // the runs through the window's end: how far the run of each run set that
-    // holds the window's last character goes on past the window, for the
-    // walks' scans that reach the end (tt_o200k.h, far_run_staged and
-    // far_run_wave)
-    {
-      int r0 = PT_WIN - 1;  // the window's last character
-      while (r0 > PT_WIN - 4 && (sh.buf[PT_PAD + r0] & 0xC0u) == 0x80u) --r0;
-      const uint32_t c_last = sh.ph.a.code[PT_PAD + r0] & 15u;
-      const int64_t start = r0 + (int64_t)o2_lead_len(sh.buf[PT_PAD + r0]);
-      const int64_t doc_end = BATCH && sh.o2_doc_after < n ? sh.o2_doc_after : n;
-      const int64_t lim = doc_end - w0;
-      auto tcls = [&](uint32_t cp) -> uint32_t {
-        return DS ? ds_table_class(v.l1, v.l2, cp) : o2_table_class(v.l1, v.l2, cp);
-      };
-      if (tid < WALK_BITMAPS) {
-        const uint32_t mk = DS ? ds_run_mask(tid) : o2_run_mask(tid);
-        const uint32_t tk = DS ? ds_run_track(tid) : o2_run_track(tid);
-        FarRun f{start, -1, false};
-        if (mk != 0u && ((mk >> c_last) & 1u)) f = far_run_staged(v, start, lim, mk, tk, tcls);
-        sh.far_end[tid] = (int32_t)f.end;
-        sh.far_last[tid] = (int32_t)f.last;
-        if (f.open) atomicOr(&sh.far_open, 1u << tid);
-      }
-      __syncthreads();
-      const uint32_t open = sh.far_open;
-      if (open != 0u) {
-        if (wave == 0) {
-#pragma unroll 1
-          for (int k = 0; k < WALK_BITMAPS; ++k) {
-            if (!((open >> k) & 1u)) continue;
-            const uint32_t mk = DS ? ds_run_mask(k) : o2_run_mask(k);
-            const uint32_t tk = DS ? ds_run_track(k) : o2_run_track(k);
-            const FarRun f = DS ? ds_far_run_wave(v, sh.far_end[k], sh.far_last[k], lim, mk, tk)
-                                : o2_far_run_wave(v, sh.far_end[k], sh.far_last[k], lim, mk, tk);
-            if (lane == 0) {
-              sh.far_end[k] = (int32_t)f.end;
-              sh.far_last[k] = (int32_t)f.last;
-            }
-          }
-        }
-        __syncthreads();
-      }
-    }
+                   (lds_u8*)sh.ph.a.o2.asc, (lds_far*)&sh.far};
     const int64_t own_end = n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN;
     auto segbit = [&](int64_t q) -> bool { return q >= 0 && q < PT_WIN && ((sh.ph.a.o2seg[q >> 5] >> (q & 31)) & 1u); };
+    {
+      // Whitespace right after CR/LF whose whitespace run holds no further
+      // CR/LF starts a piece whatever the left context: the CR/LF ends a
+      // symbol piece's CR/LF tail or a piece of the CR/LF alternative, which
+      // runs to the last CR/LF of its whitespace run.  The run is read from
+      // the bitmaps, so these marks come after the barrier; a walk of another
+      // wave that does not see one yet walks on through it, to the same
+      // pieces.
+      uint32_t add = 0;
+#pragma unroll
+      for (int j = 0; j < PT_BPT; ++j) {
+        const int q = qb + j;
+        const uint32_t c = cr(j);
+        if (((seg >> j) & 1u) || q < 1 || !inside(q) || !inside(q - 1) || (c & CODE_DOCSTART) || !walk_ws(c & 15u) ||
+            (cr(j - 1) & 15u) != (DS ? (uint32_t)DS_NL : (uint32_t)O2_NL))
+          continue;
+        const int64_t r = win_next_zero(v.bits + (DS ? DSB_SP : O2B_SP) * WIN_WORDS, q);
+        if (r < PT_WIN && win_last_one(v.bits + (DS ? DSB_NL : O2B_NL) * WIN_WORDS, q, r) < 0) add |= 1u << j;
+      }
+      if (add) {
+        seg |= add;
+        atomicOr(&sh.ph.a.o2seg[qb >> 5], add << (qb & 31));
+      }
+    }
     // one loop per lane, one piece per step: the lane's walk starts in order
     // (thread 0's continued segment first, then its own segment starts), so
     // a wave runs as long as its busiest lane, not its longest segment of
@@ -1062,11 +1065,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     // passes the piece on without walking: a long piece is walked once, by the
     // tile it starts in, not again by every tile it covers.
     // The last piece of the tile (the one that holds its last byte) is kept in
-    // last_s / last_e for the next tile.
-    if (tid == 0) {
-      sh.o2_last_s = PT_HALO;  // (kept only for invalid text, whose output is discarded)
-      sh.o2_last_e = own_end;
-    }
+    // last_s / last_e for the next tile (their defaults were set before the
+    // barrier above, so that no walk's write can come before them).
     int64_t first = -1;
     if (tid == 0 && !segbit(PT_HALO)) {
       for (int q = PT_HALO - 1; q >= 0 && first < 0; --q)
@@ -1088,46 +1088,85 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
 #pragma unroll
     for (int j = 0; j < PT_BPT; ++j)
       if (((seg >> j) & 1u) && qb + j >= PT_HALO && qb + j < own_end) todo |= 1u << j;
+    // The wave's segment starts are dealt to its lanes in turn (a lane whose
+    // four bytes hold several starts does not walk them all): rank r counts
+    // the starts at byte j = 0 of every lane first, then j = 1, and so on;
+    // lane l walks ranks l, l + 64, ...
+    const uint64_t sb0 = __ballot(todo & 1u), sb1 = __ballot(todo & 2u), sb2 = __ballot(todo & 4u),
+                   sb3 = __ballot(todo & 8u);
+    const uint32_t sn0 = (uint32_t)__builtin_popcountll(sb0), sn1 = (uint32_t)__builtin_popcountll(sb1),
+                   sn2 = (uint32_t)__builtin_popcountll(sb2);
+    const uint32_t n_seg = sn0 + sn1 + sn2 + (uint32_t)__builtin_popcountll(sb3);
+    auto seg_at = [&](uint32_t r) -> int64_t {  // window index of the start of rank r (< n_seg)
+      uint64_t m = sb0;
+      int j = 0;
+      if (r >= sn0) { r -= sn0; m = sb1; j = 1; }
+      if (j == 1 && r >= sn1) { r -= sn1; m = sb2; j = 2; }
+      if (j == 2 && r >= sn2) { r -= sn2; m = sb3; j = 3; }
+      return (int64_t)((wave * 64 + (int)select_bit64(m, r)) * PT_BPT + j);
+    };
+    uint32_t rank = lane;
     int64_t s = first;
     bool on_first = first != -1;
-    if (!on_first && todo) {
-      s = qb + __builtin_ctz(todo);
-      todo &= todo - 1u;
+    if (!on_first && rank < n_seg) {
+      s = seg_at(rank);
+      rank += 64;
     }
     bool active = on_first || s != -1;
+    // A walk whose piece needs a run through the window's end (rare) stops
+    // at that piece; when every lane of the wave has stopped or finished,
+    // the wave finds the runs asked for and those walks go on.
+    int need = -1;
 #pragma unroll 1
-    while (active) {
-      if (s >= PT_HALO) sh.ph.a.o2piece[s] = 1;  // (s < own_end <= PT_WIN)
-      // A run of numbers is cut in threes from its head whatever surrounds it
-      // (no other alternative takes a number), so from a piece start inside a
-      // run of ASCII digits every third byte starts a piece: the full chunks
-      // that end by own_end are marked in one step (a run of thousands of
-      // digits is one short loop, not a piece per step).
-      const int64_t dig = win_next_zero(v.bits + WB_DIGITS * WIN_WORDS, s) - s;  // ASCII digits from s
-      const int64_t full = (dig < own_end - s ? dig : own_end - s) / 3;
-      int64_t ps = s, e;
-      if (full >= 1) {
+    for (;;) {
 #pragma unroll 1
-        for (int64_t k = 1; k < full; ++k)
-          if (s + 3 * k >= PT_HALO) sh.ph.a.o2piece[s + 3 * k] = 1;
-        ps = s + 3 * (full - 1);
-        e = s + 3 * full;
-      } else {
-        e = DS ? ds_piece_end(v, s) : o2_piece_end(v, s);
+      while (active) {
+        if (s >= PT_HALO) sh.ph.a.o2piece[s] = 1;  // (s < own_end <= PT_WIN)
+        // A run of numbers is cut in threes from its head whatever surrounds it
+        // (no other alternative takes a number), so from a piece start inside a
+        // run of ASCII digits every third byte starts a piece: the full chunks
+        // that end by own_end are marked in one step (a run of thousands of
+        // digits is one short loop, not a piece per step).
+        int64_t full = 0;  // full chunks of three ASCII digits from s
+        if ((uint32_t)sh.buf[PT_PAD + s] - (uint32_t)'0' < 10u) {
+          const int64_t dig = win_next_zero(v.bits + WB_DIGITS * WIN_WORDS, s) - s;
+          full = (dig < own_end - s ? dig : own_end - s) / 3;
+        }
+        int64_t ps = s, e;
+        if (full >= 1) {
+#pragma unroll 1
+          for (int64_t k = 1; k < full; ++k)
+            if (s + 3 * k >= PT_HALO) sh.ph.a.o2piece[s + 3 * k] = 1;
+          ps = s + 3 * (full - 1);
+          e = s + 3 * full;
+        } else {
+          e = DS ? ds_piece_end(v, s) : o2_piece_end(v, s);
+          if (e < 0) {  // the piece needs the run through the window's end of bitmap -1 - e
+            need = (int)(-1 - e);
+            break;
+          }
+        }
+        if (e >= own_end) {  // the tile's last piece (one lane finds it)
+          sh.o2_last_s = ps;
+          sh.o2_last_e = e;
+        }
+        if (e < own_end && !segbit(e)) {
+          s = e;
+        } else if (rank < n_seg) {
+          on_first = false;
+          s = seg_at(rank);
+          rank += 64;
+        } else {
+          active = false;
+        }
       }
-      if (e >= own_end) {  // the tile's last piece (one lane finds it)
-        sh.o2_last_s = ps;
-        sh.o2_last_e = e;
-      }
-      if (e < own_end && !segbit(e)) {
-        s = e;
-      } else if (todo) {
-        on_first = false;
-        s = qb + __builtin_ctz(todo);
-        todo &= todo - 1u;
-      } else {
-        active = false;
-      }
+      uint32_t sets = need >= 0 ? 1u << need : 0u;  // the bitmaps the wave's walks ask for
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) sets |= (uint32_t)__shfl_xor((int)sets, d, 64);
+      if (sets == 0u) break;
+      if (DS) ds_far_serve(v, sets);
+      else o2_far_serve(v, sets);
+      need = -1;
     }
     __syncthreads();
     const uint32_t pw = *reinterpret_cast<const uint32_t*>(&sh.ph.a.o2piece[qb]);
