@@ -340,6 +340,7 @@ struct PtShared {
   uint32_t cwave[PT_THREADS / 64];  // span export: per-wave sums
   int64_t o2_doc_after;          // walked patterns, batch: first document start after the window
   int64_t o2_last_s, o2_last_e;  // walked patterns: the tile's last piece (window indices)
+  uint32_t o2_pub;               //   and whether it is published yet
   uint32_t whole[PT_WIN / 32];  // ignore_merges: starts of pieces that are vocabulary entries
   uint32_t cbase;             // span export: non-continuation bytes before the tile
   uint32_t ctile;             // span export: non-continuation bytes the tile owns
@@ -1022,6 +1023,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (tid == 0) {  // the tile's last piece, until a walk finds it (kept only for invalid text)
       sh.o2_last_s = PT_HALO;
       sh.o2_last_e = n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN;
+      sh.o2_pub = 0;
     }
     __syncthreads();
     const O2View v{(lds_u8*)sh.buf, (lds_u8*)sh.ph.a.code, (lds_u8*)sh.ph.a.o2.l1, (lds_u8*)sh.ph.a.o2.l2,
@@ -1065,8 +1067,16 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     // passes the piece on without walking: a long piece is walked once, by the
     // tile it starts in, not again by every tile it covers.
     // The last piece of the tile (the one that holds its last byte) is kept in
-    // last_s / last_e for the next tile (their defaults were set before the
-    // barrier above, so that no walk's write can come before them).
+    // last_s / last_e (their defaults were set before the barrier above, so
+    // that no walk's write can come before them), and the next tile continues
+    // from it: the lane that finds it publishes it at once (the next tile may
+    // be waiting for it), not after the tile's other walks.
+    auto publish_last = [&](int64_t ps, int64_t pe) {
+      const uint64_t ep = (uint64_t)w.epoch << 32;
+      st_word(&w.tile_end[t], ep | (uint32_t)(w0 + pe));
+      st_word(&w.tile_sum[t], ep | (uint32_t)(w0 + ps));
+      sh.o2_pub = 1u;
+    };
     int64_t first = -1;
     if (tid == 0 && !segbit(PT_HALO)) {
       for (int q = PT_HALO - 1; q >= 0 && first < 0; --q)
@@ -1079,6 +1089,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         if (pe >= own_end) {
           sh.o2_last_s = ps;
           sh.o2_last_e = pe;
+          publish_last(ps, pe);
         } else {
           first = pe < PT_HALO ? PT_HALO : pe;  // (pe < PT_HALO only for invalid text)
         }
@@ -1149,6 +1160,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         if (e >= own_end) {  // the tile's last piece (one lane finds it)
           sh.o2_last_s = ps;
           sh.o2_last_e = e;
+          publish_last(ps, e);
         }
         if (e < own_end && !segbit(e)) {
           s = e;
@@ -1171,12 +1183,8 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     __syncthreads();
     const uint32_t pw = *reinterpret_cast<const uint32_t*>(&sh.ph.a.o2piece[qb]);
     flags = (pw & 1u) | ((pw >> 7) & 2u) | ((pw >> 14) & 4u) | ((pw >> 21) & 8u);
-    // the next tile continues from this tile's last piece
-    if (tid == 0) {
-      const uint64_t ep = (uint64_t)w.epoch << 32;
-      st_word(&w.tile_end[t], ep | (uint32_t)(w0 + sh.o2_last_e));
-      st_word(&w.tile_sum[t], ep | (uint32_t)(w0 + sh.o2_last_s));
-    }
+    // (no walk found the last piece only in invalid text)
+    if (tid == 0 && sh.o2_pub == 0u) publish_last(sh.o2_last_s, sh.o2_last_e);
   }
   uint32_t scan_st = s0;  // cl100k: scan state before position q
 #pragma unroll
