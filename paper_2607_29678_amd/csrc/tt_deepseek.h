@@ -52,7 +52,7 @@ constexpr uint32_t DSM_PFX =
     (1u << DS_O) | (1u << DS_M) | (1u << DS_N) | (1u << DS_SP) | (1u << DS_WS) | (1u << DS_KM) | (1u << DS_KO);
 
 // Group of a class: 0 the rest, 1 numbers, 2 the CJK/kana set, 3 none.
-__host__ __device__ inline uint32_t ds_group(uint32_t c) {
+__host__ __device__ constexpr uint32_t ds_group(uint32_t c) {
   return c == DS_N ? 1u : (c >= DS_KL && c <= DS_KO) ? 2u : c == DS_NONE ? 3u : 0u;
 }
 
@@ -76,7 +76,7 @@ __host__ __device__ inline uint32_t ds_ascii_class(uint32_t cp) {
 enum : int { DSB_N = 0, DSB_AL = 1, DSB_LM0 = 2, DSB_LM2 = 3, DSB_PS0 = 4, DSB_PS2 = 5, DSB_SP = 6, DSB_NL = 7 };
 constexpr uint32_t DSB_RUNS = (1u << DSB_N) | (1u << DSB_AL) | (1u << DSB_LM0) | (1u << DSB_LM2) | (1u << DSB_PS0) |
                               (1u << DSB_PS2) | (1u << DSB_SP);
-__host__ __device__ inline uint32_t ds_bits_of(uint32_t c) {
+__host__ __device__ constexpr uint32_t ds_bits_of(uint32_t c) {
   switch (c) {
     case DS_N: return 1u << DSB_N;
     case DS_AL: return (1u << DSB_AL) | (1u << DSB_LM0);
@@ -122,7 +122,7 @@ __host__ __device__ inline uint32_t ds_table_class(P l1, P l2, uint32_t cp) {
 // (D3 does not take letters, marks or unassigned code points); before an
 // unassigned code point, after anything but another one (which may be D2's
 // first character before letters).
-__host__ __device__ inline bool ds_sync(uint32_t x, uint32_t y) {
+__host__ __device__ constexpr bool ds_sync(uint32_t x, uint32_t y) {
   if (x == DS_NONE || y == DS_NONE) return false;
   if (ds_group(x) != ds_group(y)) return true;
   const uint32_t bx = 1u << x;
@@ -143,6 +143,29 @@ __host__ __device__ inline bool ds_sync(uint32_t x, uint32_t y) {
     case DS_KO: return x != DS_KO;
     default: return false;
   }
+}
+
+// Branch-free forms of ds_sync and ds_bits_of for the tile kernel, as bit
+// tables built from the functions themselves: ds_sync in four 64-bit tables
+// (table y / 4, bit 16 (y % 4) + x), and per bitmap the classes in it.
+constexpr uint64_t ds_sync_table(uint32_t yq) {
+  uint64_t t = 0;
+  for (uint32_t y = 4 * yq; y < 4 * yq + 4; ++y)
+    for (uint32_t x = 0; x < 16; ++x)
+      if (ds_sync(x, y)) t |= 1ull << (16 * (y - 4 * yq) + x);
+  return t;
+}
+__device__ __forceinline__ bool ds_sync_bits(uint32_t x, uint32_t y) {
+  constexpr uint64_t T0 = ds_sync_table(0), T1 = ds_sync_table(1), T2 = ds_sync_table(2), T3 = ds_sync_table(3);
+  const uint32_t yq = y >> 2;
+  const uint64_t t = yq == 0u ? T0 : yq == 1u ? T1 : yq == 2u ? T2 : T3;
+  return ((t >> (16u * (y & 3u) + (x & 15u))) & 1u) != 0u;
+}
+constexpr uint32_t ds_bitmap_classes(int k) {
+  uint32_t m = ((DSB_RUNS >> k) & 1u) << DS_NONE;
+  for (uint32_t c = 0; c < 15; ++c)
+    if ((ds_bits_of(c) >> k) & 1u) m |= 1u << c;
+  return m;
 }
 
 // DeepSeek-style class of the character at window index q of a tile's view

@@ -34,7 +34,7 @@ enum : uint32_t {
   O2_NONE = 15 // continuation byte, or outside the text
 };
 
-__host__ __device__ inline bool o2_letter(uint32_t c) { return c == O2_UP || c == O2_LO || c == O2_BO; }
+__host__ __device__ constexpr bool o2_letter(uint32_t c) { return c == O2_UP || c == O2_LO || c == O2_BO; }
 __host__ __device__ inline bool o2_ub(uint32_t c) { return c == O2_UP || c == O2_BO || c == O2_MK; }
 __host__ __device__ inline bool o2_lb(uint32_t c) { return c == O2_LO || c == O2_BO || c == O2_MK; }
 __host__ __device__ inline bool o2_oset(uint32_t c) { return c == O2_O || c == O2_MK; }
@@ -71,7 +71,7 @@ __host__ __device__ inline uint32_t o2_table_class(P l1, P l2, uint32_t cp) {
 //     symbol piece absorbs CR/LF and "/" after it), and after whitespace other
 //     than U+0020 (which would join it);
 //   - marks are never safe: they can extend a letter run and a symbol run.
-__host__ __device__ inline bool o2_sync(uint32_t x, uint32_t y, uint32_t cx, uint32_t cy) {
+__host__ __device__ constexpr bool o2_sync(uint32_t x, uint32_t y, uint32_t cx, uint32_t cy) {
   switch (y) {
     case O2_N: return x != O2_N && x != O2_NONE;
     case O2_UP: return x == O2_N || x == O2_NL || x == O2_LO;
@@ -163,7 +163,7 @@ __host__ __device__ inline uint32_t select_bit64(uint64_t m, uint32_t r) {
 // [^\s\p{L}\p{N}] and of \s; the last Lm/Lo letter or mark, and the last CR/LF.
 enum : int { O2B_UB = 0, O2B_LB = 1, O2B_OS = 2, O2B_SP = 3, O2B_BM = 4, O2B_NL = 5 };
 constexpr uint32_t O2B_RUNS = (1u << O2B_UB) | (1u << O2B_LB) | (1u << O2B_OS) | (1u << O2B_SP);
-__host__ __device__ inline uint32_t o2_bits_of(uint32_t c) {
+__host__ __device__ constexpr uint32_t o2_bits_of(uint32_t c) {
   uint32_t m = 0;
   if (c == O2_UP || c == O2_BO || c == O2_MK) m |= 1u << O2B_UB;
   if (c == O2_LO || c == O2_BO || c == O2_MK) m |= 1u << O2B_LB;
@@ -171,6 +171,34 @@ __host__ __device__ inline uint32_t o2_bits_of(uint32_t c) {
   if (c == O2_WS || c == O2_NL) m |= 1u << O2B_SP;
   if (c == O2_BO || c == O2_MK) m |= 1u << O2B_BM;
   if (c == O2_NL) m |= 1u << O2B_NL;
+  return m;
+}
+
+// Branch-free forms of o2_sync and o2_bits_of for the tile kernel (a switch
+// over classes becomes a tree of divergent branches on the GPU), as bit tables
+// built from the functions themselves.  o2_sync depends on the two code
+// points only through "cy is an apostrophe", "cy is a slash" and "cx is
+// U+0020": one 64-bit table per case, bit 8y + x.
+constexpr uint64_t o2_sync_table(uint32_t cx, uint32_t cy) {
+  uint64_t t = 0;
+  for (uint32_t y = 0; y < 8; ++y)
+    for (uint32_t x = 0; x < 8; ++x)
+      if (o2_sync(x, y, cx, cy)) t |= 1ull << (8 * y + x);
+  return t;
+}
+__device__ __forceinline__ bool o2_sync_bits(uint32_t x, uint32_t y, uint32_t cx, uint32_t cy) {
+  constexpr uint64_t T0 = o2_sync_table(0x80, 0x80), T1 = o2_sync_table(0x80, 0x27), T2 = o2_sync_table(0x80, 0x2F);
+  constexpr uint64_t T3 = o2_sync_table(0x20, 0x80), T4 = o2_sync_table(0x20, 0x27), T5 = o2_sync_table(0x20, 0x2F);
+  const bool sp = cx == 0x20u;
+  const uint64_t t = cy == 0x27u ? (sp ? T4 : T1) : cy == 0x2Fu ? (sp ? T5 : T2) : (sp ? T3 : T0);
+  return x < 8u && y < 8u && ((t >> (8u * y + x)) & 1u) != 0u;
+}
+// The classes (bit c) whose characters are in bitmap k, continuation bytes
+// (class O2_NONE) in every run set.
+constexpr uint32_t o2_bitmap_classes(int k) {
+  uint32_t m = ((O2B_RUNS >> k) & 1u) << O2_NONE;
+  for (uint32_t c = 0; c < 15; ++c)
+    if ((o2_bits_of(c) >> k) & 1u) m |= 1u << c;
   return m;
 }
 

@@ -469,6 +469,30 @@ __device__ uint32_t place_tile(const Work& w, Sh& sh, uint32_t t, uint32_t count
   return sh.prefix;
 }
 
+// Phase stamps (a diagnostic build of the library, compiled with
+// TT_PHASE_STAMPS; the product build has none of this): thread 0 of every tile
+// writes the 100 MHz wall clock at each phase boundary into tt_phase_buf, slot
+// k of the tile's TT_PHASE_SLOTS, and tt_phase_stamps copies them to the host.
+// Slots: 0 entry, 1 ticket and tables, 2 window staged, 3 classified, 4 cl100k
+// scan done, 5 predicate done, 6 dispatch done, 7 thread and wave engines
+// done, 8 block engine done, 9 placement look-back done, 10 tokens written;
+// inside the dispatch 11 unit scan done, 12 unit starts listed, 13 incoming
+// unit found and dictionaries probed, 14 length lists built; inside the
+// walked patterns' predicate 16 bitmaps built, 17 extra starts and the first
+// wait done, 18 walks done, 19 flags done; 23 the block index.
+#ifdef TT_PHASE_STAMPS
+constexpr int TT_PHASE_SLOTS = 24, TT_PHASE_TILES = 8192;
+__device__ unsigned long long tt_phase_buf[TT_PHASE_TILES * TT_PHASE_SLOTS];
+#define TT_PHASE(k)                                                                            \
+  do {                                                                                         \
+    if (tid == 0 && t < (uint32_t)TT_PHASE_TILES) tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + (k)] = wall_clock64(); \
+  } while (0)
+#else
+#define TT_PHASE(k) \
+  do {              \
+  } while (0)
+#endif
+
 // MODE 0: split-level export; the outputs are the byte offsets of the pieces.
 // MODE 1: encoding; the outputs are the (internal) IDs of the units' tokens.
 // MODE 2: encoding with span export: also the byte start of every token and the
@@ -482,6 +506,9 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int64_t n = w.n;
+#ifdef TT_PHASE_STAMPS
+  const unsigned long long phase_s0 = wall_clock64();
+#endif
 
   if (tid <= SMALL_MAX) sh.hist[tid] = 0;
   if (tid >= 64 && tid < 64 + MED_CLASSES) sh.hmed[tid - 64] = 0;
@@ -492,12 +519,6 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // the patterns whose pieces are walked between synchronizing positions
   constexpr bool DS = PAT == TT_PATTERN_DEEPSEEK;
   constexpr bool WALK = PAT == TT_PATTERN_O200K || DS;
-  if (WALK && tid < PT_WIN / 32) sh.ph.a.o2seg[tid] = 0;
-  static_assert(WALK_BITMAPS * WIN_WORDS <= 2 * PT_THREADS, "two bitmap words per thread to clear");
-  if (WALK) {
-    sh.ph.a.o2bits[tid] = 0;
-    if (tid + PT_THREADS < WALK_BITMAPS * WIN_WORDS) sh.ph.a.o2bits[tid + PT_THREADS] = 0;
-  }
   // the ticket's round trip (tickets are handed out one at a time) overlaps
   // the staging of the tables, which do not depend on the tile
   uint32_t ticket = 0;
@@ -548,6 +569,13 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   const uint32_t t = wave_uniform(sh.tile);
   const uint32_t n_tiles = w.n_tiles;
   if (t >= n_tiles) return;
+#ifdef TT_PHASE_STAMPS
+  if (tid == 0 && t < (uint32_t)TT_PHASE_TILES) {
+    tt_phase_buf[(size_t)t * TT_PHASE_SLOTS] = phase_s0;
+    tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + 23] = blockIdx.x;
+  }
+#endif
+  TT_PHASE(1);
   const int64_t t0 = (int64_t)t * PT_OWN;
   const int64_t w0 = t0 - PT_HALO;
 
@@ -622,6 +650,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     __syncthreads();
   }
 
+  TT_PHASE(2);
   // ---- decode, validate, classify ------------------------------------------
   // A thread's four positions are one aligned word of the window.  It reads
   // its word and the words on either side (bytes and document-start flags) and
@@ -727,6 +756,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     st_word(&w.tile_cagg[t], ((uint64_t)w.epoch << PL_EPOCH_SHIFT) | c_tile);
   }
 
+  TT_PHASE(3);
   // ---- neighbour helpers (window indices; -1 = none) ----------------------
   auto code_at = [&](int q) -> uint32_t { return sh.ph.a.code[PT_PAD + q]; };
   auto cls = [&](int q) -> uint32_t { return code_cls(code_at(q)); };
@@ -946,6 +976,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     return -1;
   };
 
+  TT_PHASE(4);
   // ---- piece-start predicate ----------------------------------------------
   // The run-local rules, from the codes of the position, of the characters
   // before and after it (register window) and, for cl100k, the run scan.  The
@@ -964,68 +995,81 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       return DS ? (cl != DS_SP && cl != DS_WS && cl != DS_NL && ds_group(cl) == 0u)
                 : (cl != O2_WS && cl != O2_NL && cl != O2_NONE);
     };
+    // Everything here is selects over the register window and table bits
+    // (o2_sync_bits, ds_sync_bits, the bitmap class masks): a switch over
+    // classes would be a tree of divergent branches.
+    // the window bytes qb - 4 .. qb + 3: the character before a position
+    // starts at most four bytes back
+    const uint32_t bwlo = *reinterpret_cast<const uint32_t*>(&sh.buf[PT_PAD + qb - 4]);
+    const uint32_t bwhi = *reinterpret_cast<const uint32_t*>(&sh.buf[PT_PAD + qb]);
+    auto wbyte = [&](int r) -> uint32_t {  // r in [-4, 4)
+      return ((r < 0 ? bwlo : bwhi) >> (8 * (r & 3))) & 255u;
+    };
     uint32_t seg = 0;
+    uint32_t nib[WALK_BITMAPS];  // the class-set bitmaps' bits of the thread's four positions
+#pragma unroll
+    for (int k = 0; k < WALK_BITMAPS; ++k) nib[k] = 0;
 #pragma unroll
     for (int j = 0; j < PT_BPT; ++j) {
       const int q = qb + j;
       const uint32_t c = cr(j);
-      if (!inside(q) || (c & 15u) == O2_NONE) continue;
-      bool st = (c & CODE_DOCSTART) != 0u;
-      if (!st) {
-        int k = 0;  // the character before q starts at most four bytes back
+      const uint32_t cl = c & 15u;
+      const bool in_q = inside(q);
+      const bool dstart = (c & CODE_DOCSTART) != 0u;
+      // the character before q: its distance, class and (one-byte) byte
+      int k = 0;
+      uint32_t xc = O2_NONE, xb = 0x80u;
 #pragma unroll
-        for (int d = 4; d >= 1; --d)
-          if ((cr(j - d) & 15u) != O2_NONE) k = d;
-        if (k > 0 && q - k >= 0) {
-          const uint32_t bx = sh.buf[PT_PAD + q - k];
-          st = DS ? ds_sync(cr(j - k) & 15u, c & 15u)
-                  : o2_sync(cr(j - k) & 15u, c & 15u, k == 1 ? bx : 0x80u, sh.buf[PT_PAD + q]);
-        }
+      for (int d = 4; d >= 1; --d) {
+        const bool lead = (cr(j - d) & 15u) != O2_NONE;
+        k = lead ? d : k;
+        xc = lead ? (cr(j - d) & 15u) : xc;
+        xb = lead ? (d == 1 ? wbyte(j - 1) : 0x80u) : xb;
       }
-      if (!st && walk_ws(c & 15u)) {
-        // one-byte whitespace before a character that is not whitespace, in
-        // the same document (and, DeepSeek-style, the same group stretch):
-        // no piece holds whitespace past its first character unless the
-        // piece ends with whitespace or CR/LF (the alternatives that take
-        // whitespace runs), and those cannot end before a character that is
-        // not whitespace inside the stretch, so a piece starts here whatever
-        // the left context
-        const uint32_t c2 = cr(j + 1);
-        st = inside(q + 1) && !(c2 & CODE_DOCSTART) && walk_solid(c2 & 15u);
+      const bool pair = (k > 0) & (q - k >= 0) &
+                        (DS ? ds_sync_bits(xc, cl) : o2_sync_bits(xc, cl, xb, wbyte(j)));
+      // one-byte whitespace before a character that is not whitespace, in
+      // the same document (and, DeepSeek-style, the same group stretch): no
+      // piece holds whitespace past its first character unless the piece
+      // ends with whitespace or CR/LF (the alternatives that take whitespace
+      // runs), and those cannot end before a character that is not
+      // whitespace inside the stretch, so a piece starts here whatever the
+      // left context
+      const uint32_t c2 = cr(j + 1);
+      const bool ws_solid = walk_ws(cl) & inside(q + 1) & ((c2 & CODE_DOCSTART) == 0u) & walk_solid(c2 & 15u);
+      seg |= (uint32_t)(in_q & (cl != O2_NONE) & (dstart | pair | ws_solid)) << j;
+      // the class-set bitmaps (tt_o200k.h): the sets of a character at its
+      // first byte, the run sets at its continuation bytes, nothing at
+      // document starts and outside the text; and the ASCII digits
+      const bool in_b = in_q & !dstart;
+#pragma unroll
+      for (int kb = 0; kb < WALK_BITMAPS; ++kb) {
+        const uint32_t cls_k = DS ? ds_bitmap_classes(kb) : o2_bitmap_classes(kb);
+        const bool bit = kb == WB_DIGITS ? wbyte(j) - (uint32_t)'0' < 10u : ((cls_k >> cl) & 1u) != 0u;
+        nib[kb] |= (uint32_t)(in_b & bit) << j;
       }
-      if (st) seg |= 1u << j;
     }
-    if (seg) atomicOr(&sh.ph.a.o2seg[qb >> 5], seg << (qb & 31));
-    // the class-set bitmaps of the thread's four positions (tt_o200k.h): the
-    // sets of a character at its first byte, the run sets at its continuation
-    // bytes, nothing at document starts and outside the text
-    {
-      uint32_t nib[WALK_BITMAPS];
+    // A bitmap word holds the four positions of eight consecutive lanes: the
+    // last lane of the eight stores the word, ORed together over DPP row
+    // shifts (no atomics, and no clearing beforehand).
+    static_assert(PT_BPT == 4 && PT_THREADS * PT_BPT == PT_WIN, "eight lanes per bitmap word");
+    auto store_word = [&](uint32_t* words, uint32_t nib4) {
+      int x = (int)(nib4 << (qb & 31));
+      x |= __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);  // row_shr:1
+      x |= __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);  // row_shr:2
+      x |= __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);  // row_shr:4
+      if ((lane & 7) == 7) words[qb >> 5] = (uint32_t)x;
+    };
+    store_word(sh.ph.a.o2seg, seg);
 #pragma unroll
-      for (int k = 0; k < WALK_BITMAPS; ++k) nib[k] = 0;
-#pragma unroll
-      for (int j = 0; j < PT_BPT; ++j) {
-        const uint32_t c = cr(j);
-        const uint32_t cl = c & 15u;
-        uint32_t m = 0;
-        if (inside(qb + j) && !(c & CODE_DOCSTART)) {
-          m = cl == O2_NONE ? (DS ? DSB_RUNS : O2B_RUNS) : (DS ? ds_bits_of(cl) : o2_bits_of(cl));
-          const uint32_t b = sh.buf[PT_PAD + qb + j];
-          if (b - (uint32_t)'0' < 10u) m |= 1u << WB_DIGITS;
-        }
-#pragma unroll
-        for (int k = 0; k < WALK_BITMAPS; ++k) nib[k] |= ((m >> k) & 1u) << j;
-      }
-#pragma unroll
-      for (int k = 0; k < WALK_BITMAPS; ++k)
-        if (nib[k]) atomicOr(&sh.ph.a.o2bits[k * WIN_WORDS + (qb >> 5)], nib[k] << (qb & 31));
-    }
+    for (int kb = 0; kb < WALK_BITMAPS; ++kb) store_word(&sh.ph.a.o2bits[kb * WIN_WORDS], nib[kb]);
     if (tid == 0) {  // the tile's last piece, until a walk finds it (kept only for invalid text)
       sh.o2_last_s = PT_HALO;
       sh.o2_last_e = n - w0 < PT_HALO + PT_OWN ? n - w0 : PT_HALO + PT_OWN;
       sh.o2_pub = 0;
     }
     __syncthreads();
+    TT_PHASE(16);
     const O2View v{(lds_u8*)sh.buf, (lds_u8*)sh.ph.a.code, (lds_u8*)sh.ph.a.o2.l1, (lds_u8*)sh.ph.a.o2.l2,
                    w.text, w0, n, BATCH ? sh.o2_doc_after : n, (lds_u32*)sh.ph.a.o2bits,
                    (lds_u8*)sh.ph.a.o2.asc, (lds_far*)&sh.far};
@@ -1095,6 +1139,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
         }
       }
     }
+    TT_PHASE(17);
     uint32_t todo = 0;  // bit j: own position qb + j starts a segment to walk
 #pragma unroll
     for (int j = 0; j < PT_BPT; ++j)
@@ -1181,11 +1226,13 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       need = -1;
     }
     __syncthreads();
+    TT_PHASE(18);
     const uint32_t pw = *reinterpret_cast<const uint32_t*>(&sh.ph.a.o2piece[qb]);
     flags = (pw & 1u) | ((pw >> 7) & 2u) | ((pw >> 14) & 4u) | ((pw >> 21) & 8u);
     // (no walk found the last piece only in invalid text)
     if (tid == 0 && sh.o2_pub == 0u) publish_last(sh.o2_last_s, sh.o2_last_e);
   }
+  if (WALK) TT_PHASE(19);
   uint32_t scan_st = s0;  // cl100k: scan state before position q
 #pragma unroll
   for (int j = 0; j < (WALK ? 0 : PT_BPT); ++j) {
@@ -1386,6 +1433,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     }
   }
 
+  TT_PHASE(5);
   // ---- units: block scan of the start flags --------------------------------
   const uint32_t cnt = __popc(flags);
   const uint32_t inc = wave_incl_sum(cnt);
@@ -1411,6 +1459,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     return;
   }
 
+  TT_PHASE(11);
   // the tile's last unit start, published before this block waits on anything
   if (m == 0) {
     if (tid == 0) st_word(&w.tile_last[t], ((uint64_t)w.epoch << 32) | NO_START);
@@ -1441,6 +1490,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // dispatches it waits for that word; the others dispatch their own units
   // meanwhile.  (Only invalid input, whose text starts with a continuation
   // byte, leaves no unit start before the tile; its output is discarded.)
+  TT_PHASE(12);
   uint32_t sp_own = 0;
   if (has_inc && (uint32_t)tid == m_proc % (uint32_t)PT_THREADS) {
     uint32_t found = NO_START;
@@ -1557,6 +1607,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   const uint32_t L_inc = has_inc ? e_inc - s_prev : 0u;
   auto inc_byte = [&](uint32_t j) -> uint32_t { return byte_abs(s_prev + j); };
   auto inc_out = [&](uint32_t j, uint32_t id) { w.stage[s_prev + j] = id; };
+  TT_PHASE(13);
   // where each length (class) starts: a wave scan over the counts (wave 0 for
   // the thread units, wave 1 for the wave units)
   if (wave == 0) {
@@ -1583,8 +1634,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     else sh.med[sh.hmed[med_class(L)] + pos] = e;
   }
   __syncthreads();
+  TT_PHASE(14);
   const uint32_t n_small = wave_uniform(sh.n_small), n_med = wave_uniform(sh.n_med);
 
+  TT_PHASE(6);
   // thread per unit, on the first TH_THREADS threads
   if (tid < TH_THREADS) {
     uint32_t* rk = &sh.ph.b.rk[0][tid];
@@ -1670,6 +1723,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   }
   __syncthreads();
 
+  TT_PHASE(7);
   // ---- BPE, whole block per longer unit ------------------------------------
   // (rare in text: rows in LDS up to ROWS_LDS bytes, else in global scratch
   // at the unit's byte offset; there the selection masks of a unit of L > 64
@@ -1716,6 +1770,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     __syncthreads();
   }
 
+  TT_PHASE(8);
   // ---- output: the tile's tokens, in order, at their place --------------------
   uint32_t csum = 0;
 #pragma unroll 1
@@ -1746,6 +1801,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   // (place_tile ends with a barrier, which also publishes uoff to the block)
   const uint32_t prefix = place_tile(w, sh, t, inc_cnt + ctot, tile_bad, tid, lane, wave,
                                      SPANS ? w.tile_cagg : nullptr, SPANS ? sh.ctile : 0u);
+  TT_PHASE(9);
   // Valid input gives every tile a disjoint byte range and at most one output
   // per byte, so every output index is below n.  Invalid input (whose output
   // is discarded) can break that; the bound keeps it inside the buffer.
@@ -1895,6 +1951,10 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (q0 >= PT_HALO && q0 < PT_HALO + PT_OWN && p0 < n) w.ccount[p0 >> 2] = sh.cbase + c_excl;
     if (last && tid == 0 && (n & 3) == 0) w.ccount[n >> 2] = sh.cbase + sh.ctile;
   }
+#ifdef TT_PHASE_STAMPS
+  __syncthreads();
+  TT_PHASE(10);
+#endif
 }
 
 namespace {
@@ -1933,3 +1993,16 @@ hipError_t launch_tile(const Work& w, const DevTables& tb, int pattern, int mode
 }
 
 }  // namespace tt
+
+#ifdef TT_PHASE_STAMPS
+// The phase stamps of the first n_tiles tiles of the last call (n_tiles *
+// TT_PHASE_SLOTS words, tile-major) into out (host memory).  Diagnostic build
+// only; returns TT_OK, TT_ERR_BAD_ARG or TT_ERR_HIP.
+extern "C" int tt_phase_stamps(unsigned long long* out, int n_tiles) {
+  if (!out || n_tiles < 0 || n_tiles > tt::TT_PHASE_TILES) return TT_ERR_BAD_ARG;
+  const hipError_t e = hipMemcpyFromSymbol(out, HIP_SYMBOL(tt::tt_phase_buf),
+                                           (size_t)n_tiles * tt::TT_PHASE_SLOTS * sizeof(unsigned long long), 0,
+                                           hipMemcpyDeviceToHost);
+  return e == hipSuccess ? TT_OK : TT_ERR_HIP;
+}
+#endif
