@@ -479,19 +479,21 @@ __device__ uint32_t place_tile(const Work& w, Sh& sh, uint32_t t, uint32_t count
 // inside the dispatch 11 unit scan done, 12 unit starts listed, 13 incoming
 // unit found and dictionaries probed, 14 length lists built; inside the
 // walked patterns' predicate 16 bitmaps built, 17 extra starts and the first
-// wait done, 18 walks done, 19 flags done; 23 the block index.
+// wait done, 18 walks done, 19 flags done; 20 the incoming unit's start known
+// (by the thread that dispatches it); 23 the block index.
 #ifdef TT_PHASE_STAMPS
 constexpr int TT_PHASE_SLOTS = 24, TT_PHASE_TILES = 8192;
 __device__ unsigned long long tt_phase_buf[TT_PHASE_TILES * TT_PHASE_SLOTS];
-#define TT_PHASE(k)                                                                            \
+#define TT_PHASE_BY(k, who)                                                                    \
   do {                                                                                         \
-    if (tid == 0 && t < (uint32_t)TT_PHASE_TILES) tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + (k)] = wall_clock64(); \
+    if ((who) && t < (uint32_t)TT_PHASE_TILES) tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + (k)] = wall_clock64(); \
   } while (0)
 #else
-#define TT_PHASE(k) \
-  do {              \
+#define TT_PHASE_BY(k, who) \
+  do {                      \
   } while (0)
 #endif
+#define TT_PHASE(k) TT_PHASE_BY(k, tid == 0)
 
 // MODE 0: split-level export; the outputs are the byte offsets of the pieces.
 // MODE 1: encoding; the outputs are the (internal) IDs of the units' tokens.
@@ -572,6 +574,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
 #ifdef TT_PHASE_STAMPS
   if (tid == 0 && t < (uint32_t)TT_PHASE_TILES) {
     tt_phase_buf[(size_t)t * TT_PHASE_SLOTS] = phase_s0;
+    tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + 20] = 0;  // (written later only by a tile with an incoming unit)
     tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + 23] = blockIdx.x;
   }
 #endif
@@ -1503,6 +1506,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     }
     sh.s_prev = found;
     sp_own = found != NO_START ? found : 0u;
+    TT_PHASE_BY(20, true);
   }
   auto inc_byte_own = [&](uint32_t j) -> uint32_t { return byte_abs(sp_own + j); };
   auto inc_out_own = [&](uint32_t j, uint32_t id) { w.stage[sp_own + j] = id; };

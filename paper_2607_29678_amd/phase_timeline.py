@@ -28,7 +28,8 @@ from . import _build, _lib
 SLOTS, MAX_TILES, PT_OWN = 24, 8192, 1984
 PHASES = ["ticket and tables", "window staging", "decode and classify", "cl100k scan and carries", "predicate",
           "units and dispatch", "thread and wave engines", "block engine", "placement look-back", "writing tokens"]
-DISPATCH = ["unit scan", "unit starts listed", "incoming unit and dictionaries", "length lists", "to the engines"]
+DISPATCH = ["unit scan", "unit starts listed", "incoming unit and dictionaries", "length lists", "to the engines",
+            "incoming unit's start known (after the listing)"]
 WALK = ["bitmaps", "extra starts and first wait", "walks", "flags"]
 
 
@@ -75,8 +76,9 @@ def timeline(workload, pattern, table, samples=8, reps=2):
             a = buf[: nt * SLOTS].reshape(nt, SLOTS).astype(np.int64)
             rel = (a - a[:, 0].min()) * 0.01  # 100 MHz ticks -> microseconds
             phases.append(np.diff(rel[:, :11], axis=1))
+            inc = np.where(a[:, 20] > 0, rel[:, 20] - rel[:, 12], 0.0)  # (0: no incoming unit)
             disp.append(np.stack([rel[:, 11] - rel[:, 5], rel[:, 12] - rel[:, 11], rel[:, 13] - rel[:, 12],
-                                  rel[:, 14] - rel[:, 13], rel[:, 6] - rel[:, 14]], axis=1))
+                                  rel[:, 14] - rel[:, 13], rel[:, 6] - rel[:, 14], inc], axis=1))
             if pattern in ("o200k", "deepseek"):
                 walk.append(np.stack([rel[:, 16] - rel[:, 4], rel[:, 17] - rel[:, 16], rel[:, 18] - rel[:, 17],
                                       rel[:, 19] - rel[:, 18]], axis=1))

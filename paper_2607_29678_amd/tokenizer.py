@@ -40,6 +40,13 @@ def _stream(s):
     return None if s is None else ctypes.c_void_p(int(s))
 
 
+def _shrunk(a, n):
+    """``a`` (a fresh array this module owns) cut to its first n rows in place:
+    the allocation shrinks without a copy of the rows kept."""
+    a.resize((n,) + a.shape[1:], refcheck=False)
+    return a
+
+
 def _u8(data):
     if isinstance(data, np.ndarray):
         return np.ascontiguousarray(data, dtype=np.uint8)
@@ -102,7 +109,7 @@ class Tokenizer:
         st = self._lib.tt_encode(self._h, _ptr(src) if src.size else None, src.size, _ptr(out), ctypes.byref(n),
                                  _stream(stream))
         _lib.check(st, "tt_encode")
-        return out[: n.value].copy()
+        return _shrunk(out, n.value)
 
     def encode_into(self, data, out, stream=None) -> int:
         """``tt_encode`` into a caller-provided int32 array ``out`` (numpy or a CPU torch tensor, at
@@ -137,7 +144,7 @@ class Tokenizer:
         st = self._lib.tt_encode_spans(self._h, _ptr(src) if src.size else None, src.size, _ptr(ids), _ptr(spans),
                                        ctypes.byref(n), _stream(stream))
         _lib.check(st, "tt_encode_spans")
-        return ids[: n.value].copy(), spans[: n.value].copy()
+        return _shrunk(ids, n.value), _shrunk(spans, n.value)
 
     def encode_batch(self, docs, stream=None):
         """``tt_encode_batch``: list of int32 ID arrays, one per document."""
@@ -160,7 +167,7 @@ class Tokenizer:
         st = self._lib.tt_pretokenize(self._h, _ptr(src) if src.size else None, src.size, _ptr(out),
                                       ctypes.byref(n), _stream(stream))
         _lib.check(st, "tt_pretokenize")
-        return out[: n.value].copy()
+        return _shrunk(out, n.value)
 
     # -- device entry point ------------------------------------------------
     def encode_device(self, d_utf8, length, d_out_ids, d_out_len, stream=None):
@@ -253,7 +260,7 @@ class Session:
         spans = np.empty((max(1, count), 4), dtype=np.int32)
         _lib.check(self._lib.tt_session_tokens(self._s, int(start), int(count), _ptr(ids), _ptr(spans)),
                    "tt_session_tokens")
-        return ids[:count].copy(), spans[:count].copy()
+        return _shrunk(ids, count), _shrunk(spans, count)
 
     def ids(self) -> np.ndarray:
         return self.tokens()[0]
@@ -267,7 +274,7 @@ def sync_boundaries(data, pattern="gpt2") -> np.ndarray:
     out = np.zeros(max(1, src.size), dtype=np.uint8)
     _lib.check(lib.tt_sync_boundaries(pat, _ptr(src) if src.size else None, src.size, _ptr(out)),
                "tt_sync_boundaries")
-    return out[: src.size].copy()
+    return _shrunk(out, src.size)
 
 
 def splice_plan(text, a_len, x, c_ids, c_spans, f_ids, f_spans, max_token_chars, pattern="gpt2"):

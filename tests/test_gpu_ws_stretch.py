@@ -66,3 +66,19 @@ def test_long_stretch_to_document_end_in_batch(gpu):
     got = tok.encode_batch(docs)
     for j, d in enumerate(docs):
         assert got[j].tolist() == oracle_ids(d, table, "cl100k"), "document %d" % j
+
+
+@pytest.mark.parametrize("tail", ["\r\nxy", "xy"])
+def test_long_stretch_deep_in_a_large_request(gpu, tail):
+    """A 150,000-byte stretch after CR/LF that starts 300,000 bytes into a
+    pageable request of more than 256 KB (staged through pinned memory by the
+    copy threads), so that the read past the window starts far from the
+    request's first tiles."""
+    tok = lib_tokenizer(K)
+    table = oracle_table(K)
+    text = ("Word, " * 50_000) + "ab\n" + " " * 150_000 + tail + " more words" * 1000
+    data = text.encode("utf-8")
+    assert len(data) > 256 * 1024
+    ids = tok.encode(data).tolist()
+    assert ids == oracle_ids(data, table, "cl100k")
+    assert tok.pretokenize(data).tolist() == piece_byte_starts(text, "cl100k")
