@@ -480,9 +480,12 @@ __device__ uint32_t place_tile(const Work& w, Sh& sh, uint32_t t, uint32_t count
 // unit found and dictionaries probed, 14 length lists built; inside the
 // walked patterns' predicate 16 bitmaps built, 17 extra starts and the first
 // wait done, 18 walks done, 19 flags done; 20 the incoming unit's start known
-// (by the thread that dispatches it); 23 the block index.
+// (by the thread that dispatches it); 21 the predicate's per-position rules
+// done (thread 0), 22 the cl100k read past the window and the vocabulary
+// probes of ignore_merges done; 23 the block index; 24 + w: wave w done with
+// the predicate (the same point as 5, per wave).
 #ifdef TT_PHASE_STAMPS
-constexpr int TT_PHASE_SLOTS = 24, TT_PHASE_TILES = 8192;
+constexpr int TT_PHASE_SLOTS = 32, TT_PHASE_TILES = 8192;
 __device__ unsigned long long tt_phase_buf[TT_PHASE_TILES * TT_PHASE_SLOTS];
 #define TT_PHASE_BY(k, who)                                                                    \
   do {                                                                                         \
@@ -1303,6 +1306,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (d1 == 0u) start = true;
     if (start) flags |= 1u << j;
   }
+  TT_PHASE(21);
   if (PAT == TT_PATTERN_CL100K) {
     // the whitespace stretch after CR/LF that reaches the window's end, if
     // any: the block reads on past the window
@@ -1418,6 +1422,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (mask) atomicOr(&sh.ph.a.nocut[qb >> 5], mask << (qb & 31));
     __syncthreads();
   }
+  TT_PHASE(22);
   if (SEG) {
     // BPE segments: add the byte positions inside pieces that no merge spans
     // (q is not a piece start, so q - 1 lies in the same piece)
@@ -1437,6 +1442,7 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   }
 
   TT_PHASE(5);
+  TT_PHASE_BY(24 + wave, lane == 0);
   // ---- units: block scan of the start flags --------------------------------
   const uint32_t cnt = __popc(flags);
   const uint32_t inc = wave_incl_sum(cnt);

@@ -25,12 +25,14 @@ import numpy as np
 
 from . import _build, _lib
 
-SLOTS, MAX_TILES, PT_OWN = 24, 8192, 1984
+SLOTS, MAX_TILES, PT_OWN = 32, 8192, 1984
 PHASES = ["ticket and tables", "window staging", "decode and classify", "cl100k scan and carries", "predicate",
           "units and dispatch", "thread and wave engines", "block engine", "placement look-back", "writing tokens"]
 DISPATCH = ["unit scan", "unit starts listed", "incoming unit and dictionaries", "length lists", "to the engines",
             "incoming unit's start known (after the listing)"]
 WALK = ["bitmaps", "extra starts and first wait", "walks", "flags"]
+PRED = ["per-position rules (wave 0)", "read past the window, vocabulary probes", "junction cuts (wave 0)",
+        "predicate, slowest wave"]
 
 
 def _summary(rows, names):
@@ -64,7 +66,7 @@ def timeline(workload, pattern, table, samples=8, reps=2):
         tok.encode_device(d_in[i], len(texts[i]), d_out, d_len, stream.cuda_stream)
     torch.cuda.synchronize()
     buf = np.zeros(MAX_TILES * SLOTS, dtype=np.uint64)
-    phases, disp, walk, crit, spans = [], [], [], [], []
+    phases, disp, walk, pred, crit, spans = [], [], [], [], [], []
     tok.set_profiling(samples * reps)
     for _ in range(reps):
         for i, t in enumerate(texts):
@@ -79,6 +81,8 @@ def timeline(workload, pattern, table, samples=8, reps=2):
             inc = np.where(a[:, 20] > 0, rel[:, 20] - rel[:, 12], 0.0)  # (0: no incoming unit)
             disp.append(np.stack([rel[:, 11] - rel[:, 5], rel[:, 12] - rel[:, 11], rel[:, 13] - rel[:, 12],
                                   rel[:, 14] - rel[:, 13], rel[:, 6] - rel[:, 14], inc], axis=1))
+            pred.append(np.stack([rel[:, 21] - rel[:, 4], rel[:, 22] - rel[:, 21], rel[:, 5] - rel[:, 22],
+                                  rel[:, 24:32].max(axis=1) - rel[:, 4]], axis=1))
             if pattern in ("o200k", "deepseek"):
                 walk.append(np.stack([rel[:, 16] - rel[:, 4], rel[:, 17] - rel[:, 16], rel[:, 18] - rel[:, 17],
                                       rel[:, 19] - rel[:, 18]], axis=1))
@@ -92,6 +96,7 @@ def timeline(workload, pattern, table, samples=8, reps=2):
            "kernel_us_p50_hip_events": round(float(np.median(kernel_us)), 2),
            "stamp_span_us_p50": round(float(np.median(spans)), 2),
            "phases": _summary(phases, PHASES), "dispatch": _summary(disp, DISPATCH),
+           "predicate_split": _summary(pred, PRED),
            "critical_tiles": crit[:4]}
     if walk:
         out["walked_predicate"] = _summary(walk, WALK)

@@ -36,6 +36,13 @@ def test_library_exports_every_declared_symbol():
     assert set(_lib.SIGNATURES) == set(_declared())
 
 
+def test_product_library_has_no_phase_stamps():
+    # the per-phase clock stamps exist only in the diagnostic build
+    # (phase_timeline.py, TT_PHASE_STAMPS); the product library exports none
+    lib = _lib.load()
+    assert not hasattr(lib, "tt_phase_stamps")
+
+
 def test_status_strings():
     lib = _lib.load()
     for code in _lib.STATUS:
