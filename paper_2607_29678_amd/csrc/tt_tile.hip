@@ -483,7 +483,8 @@ __device__ uint32_t place_tile(const Work& w, Sh& sh, uint32_t t, uint32_t count
 // (by the thread that dispatches it); 21 the predicate's per-position rules
 // done (thread 0), 22 the cl100k read past the window and the vocabulary
 // probes of ignore_merges done; 23 the block index; 24 + w: wave w done with
-// the predicate (the same point as 5, per wave).
+// the predicate (the same point as 5, per wave); 15 where the block runs (XCD
+// in the high word, the hardware ID register in the low word).
 #ifdef TT_PHASE_STAMPS
 constexpr int TT_PHASE_SLOTS = 32, TT_PHASE_TILES = 8192;
 __device__ unsigned long long tt_phase_buf[TT_PHASE_TILES * TT_PHASE_SLOTS];
@@ -579,6 +580,11 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     tt_phase_buf[(size_t)t * TT_PHASE_SLOTS] = phase_s0;
     tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + 20] = 0;  // (written later only by a tile with an incoming unit)
     tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + 23] = blockIdx.x;
+    // where the block runs: the XCD (XCC_ID register) and the hardware ID
+    // register (compute unit, shader array and engine in bits 8-15)
+    const uint32_t xcc = (uint32_t)__builtin_amdgcn_s_getreg((3 << 11) | 20) & 15u;
+    const uint32_t hw = (uint32_t)__builtin_amdgcn_s_getreg((31 << 11) | 4);
+    tt_phase_buf[(size_t)t * TT_PHASE_SLOTS + 15] = ((unsigned long long)xcc << 32) | hw;
   }
 #endif
   TT_PHASE(1);

@@ -7,8 +7,11 @@ boundary of the tile kernel (the slots are listed in ``csrc/tt_tile.hip``).
 This script encodes seeded device-resident requests through that build and
 prints, per workload, one JSON line: the mean and maximum time of every phase
 over the tiles, the phases of the critical tiles (the last to finish their
-placement look-back), the split of the dispatch phase and, for the walked
-patterns, of the predicate phase.  Times are in microseconds; the kernel time
+placement look-back) and of the tiles that publish their token count last
+(which every later tile's placement waits for), when tiles start and publish
+their counts (also by the number of tiles on the tile's compute unit), the
+split of the dispatch phase and, for the walked patterns, of the predicate
+phase.  Times are in microseconds; the kernel time
 from HIP events is printed beside the stamps' span.
 
     python -m paper_2607_29678_amd.phase_timeline --build
@@ -41,6 +44,12 @@ def _summary(rows, names):
             "max": {k: round(float(a[:, j].max()), 2) for j, k in enumerate(names)}}
 
 
+def _spread(rows):
+    a = np.concatenate(rows)
+    return {"p50": round(float(np.percentile(a, 50)), 2), "p90": round(float(np.percentile(a, 90)), 2),
+            "max": round(float(a.max()), 2)}
+
+
 def timeline(workload, pattern, table, samples=8, reps=2):
     import torch
     from workloads import textgen
@@ -66,7 +75,8 @@ def timeline(workload, pattern, table, samples=8, reps=2):
         tok.encode_device(d_in[i], len(texts[i]), d_out, d_len, stream.cuda_stream)
     torch.cuda.synchronize()
     buf = np.zeros(MAX_TILES * SLOTS, dtype=np.uint64)
-    phases, disp, walk, pred, crit, spans = [], [], [], [], [], []
+    phases, disp, walk, pred, crit, spans, late, starts, counts = [], [], [], [], [], [], [], [], []
+    by_cu = {}  # tiles on a compute unit -> times at which such tiles publish their counts
     tok.set_profiling(samples * reps)
     for _ in range(reps):
         for i, t in enumerate(texts):
@@ -88,6 +98,22 @@ def timeline(workload, pattern, table, samples=8, reps=2):
                                       rel[:, 19] - rel[:, 18]], axis=1))
             c = int(np.argmax(rel[:, 9]))
             crit.append({"tile": c, "of": nt, "phases": [round(float(x), 2) for x in phases[-1][c]]})
+            # the tile whose count is published last (the end of its engines):
+            # every later tile's placement waits for it
+            # the compute unit of each tile (XCD, then bits 8-15 of the hardware
+            # ID: unit, shader array, engine) and how many tiles it holds
+            cu = (a[:, 15] >> 32) * 256 + ((a[:, 15] >> 8) & 255)
+            _, inv, per = np.unique(cu, return_inverse=True, return_counts=True)
+            on_cu = per[inv]
+            for k in np.unique(on_cu):
+                by_cu.setdefault(int(k), []).append(rel[on_cu == k, 8])
+            b = int(np.argmax(rel[:, 8]))
+            late.append({"tile": b, "of": nt, "starts_at": round(float(rel[b, 0]), 2),
+                         "count_at": round(float(rel[b, 8]), 2),
+                         "phases": [round(float(x), 2) for x in phases[-1][b]],
+                         "incoming_start_wait": round(float(inc[b]), 2), "tiles_on_its_unit": int(on_cu[b])})
+            starts.append(rel[:, 0])
+            counts.append(rel[:, 8])
             spans.append(float(rel[:, 10].max()))
     kernel_us = [x["tile"] * 1e3 for x in tok.stage_times(stream.cuda_stream)]
     tok.set_profiling(0)
@@ -97,7 +123,11 @@ def timeline(workload, pattern, table, samples=8, reps=2):
            "stamp_span_us_p50": round(float(np.median(spans)), 2),
            "phases": _summary(phases, PHASES), "dispatch": _summary(disp, DISPATCH),
            "predicate_split": _summary(pred, PRED),
-           "critical_tiles": crit[:4]}
+           "critical_tiles": crit[:4],
+           "tile_start_us": _spread(starts), "count_published_us": _spread(counts),
+           "last_count_tiles": late[:4],
+           "count_published_us_by_tiles_on_unit": {str(k): dict(_spread(v), tiles=int(sum(len(x) for x in v)))
+                                                   for k, v in sorted(by_cu.items())}}
     if walk:
         out["walked_predicate"] = _summary(walk, WALK)
     return out
