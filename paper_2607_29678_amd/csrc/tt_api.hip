@@ -162,6 +162,7 @@ struct tt_tokenizer {
   int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
   uint32_t* d_toklen = nullptr;  // [256 + M] byte length of every internal ID
   uint32_t n_ids = 0;
+  bool ext16 = false;          // every caller ID is in [0, 65536): staged IDs cross the bus as 16 bits
   uint32_t max_tok_bytes = 1;  // byte length of the longest token (incremental repair)
   bool ignore = false;         // ignore_merges: whole pieces probed in the vocabulary first
   uint32_t vmax = 0;           // longest vocabulary string (bytes) of the probes
@@ -362,7 +363,7 @@ bool host_pinned(const void* p, int64_t len) {
 // mode 2: encode with span export into out_spans ([n][4], single requests).
 int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, const int64_t* d_docs,
               int32_t n_docs, int32_t* out_ids, int64_t* out_len, int64_t* out_docs, hipStream_t st, int mode,
-              int32_t* out_spans = nullptr) {
+              int32_t* out_spans = nullptr, uint16_t* out16 = nullptr) {
   if (s->epoch + 1 >= EPOCH_LIMIT) {
     // epochs wrapped: clear the words that carry them and start again
     if (hipMemsetAsync(s->dmem, 0, s->ctl_bytes, st) != hipSuccess) return TT_ERR_HIP;
@@ -381,6 +382,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_len = out_len;
   w.out_doc_off = out_docs;
   w.out_spans = out_spans;
+  w.out16 = mode == 1 ? out16 : nullptr;
   const DevTables tb = handle_tables(h);
   const int ring = h->profile;
   if (ring != s->ring) {  // (re)size the event ring
@@ -423,7 +425,9 @@ constexpr uint64_t PINNED_MAX = 1ull << 28;
 //    the copy threads then copy into the caller's array), and its last tile
 //    writes the output length there too: no copy engine transfer at all.
 //    Each wave of a tile writes its IDs as one contiguous range (whole lines
-//    over the bus).
+//    over the bus).  Staged IDs of a handle whose caller IDs all fit in 16
+//    bits cross the bus as 16-bit values (half the bytes), and the copy
+//    threads widen them into the caller's array.
 int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t len, int32_t* out_ids,
                   int64_t* out_len, hipStream_t st) {
   int rc = reserve_pinned(s, (uint64_t)len);
@@ -439,13 +443,18 @@ int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t le
   *s->h_len = 0;
   // the tile kernel writes the IDs at their places in pinned host memory
   int32_t* dst = pin_out ? out_ids : s->h_ids;
-  rc = run_chain(h, s, src, (uint32_t)len, nullptr, 0, dst, s->h_len, nullptr, st, 1);
+  const bool narrow = !pin_out && h->ext16;
+  rc = run_chain(h, s, src, (uint32_t)len, nullptr, 0, dst, s->h_len, nullptr, st, 1, nullptr,
+                 narrow ? reinterpret_cast<uint16_t*>(s->h_ids) : nullptr);
   if (rc) return rc;
   if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
   const int64_t T = *s->h_len;
   if (T < 0) return (int)T;
   if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
-  if (!pin_out && T > 0) host_copy(out_ids, s->h_ids, 4 * (size_t)T);
+  if (!pin_out && T > 0) {
+    if (narrow) host_widen16(out_ids, reinterpret_cast<const uint16_t*>(s->h_ids), (size_t)T);
+    else host_copy(out_ids, s->h_ids, 4 * (size_t)T);
+  }
   *out_len = T;
   return TT_OK;
 }
@@ -961,6 +970,7 @@ int tt_create_ex(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_
   h->dnb = dnb;
   h->dnb2 = dnb2;
   h->n_ids = n_ids;
+  h->ext16 = std::all_of(ext.begin(), ext.end(), [](int32_t v) { return v >= 0 && v < 65536; });
   h->max_tok_bytes = *std::max_element(toklen.begin(), toklen.end());
   if (hipGetDevice(&h->device) != hipSuccess) {
     delete h;

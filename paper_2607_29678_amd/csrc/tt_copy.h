@@ -4,6 +4,7 @@
 #pragma once
 
 #include <cstddef>
+#include <cstdint>
 
 namespace tt {
 
@@ -11,6 +12,10 @@ namespace tt {
 // split among the calling thread and the pool's workers; smaller ones, and
 // copies while another thread's copy is running, are a plain memcpy.
 void host_copy(void* dst, const void* src, size_t n);
+
+// dst[i] = src[i] for i < count (16-bit values widened to int32), split the
+// same way as host_copy (by output bytes).
+void host_widen16(int32_t* dst, const uint16_t* src, size_t count);
 
 // Let sleeping workers start spinning ahead of a copy of n bytes (cheap when
 // they are awake; nothing for copies too small to be split).

@@ -1825,8 +1825,13 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   int32_t* __restrict__ out = w.out_ids;
   const int32_t* __restrict__ ext = tb.ext_id;
   auto ext_of = [&](uint32_t v) -> int32_t { return v < tb.n_ids ? ext[v] : -1; };
-  for (uint32_t i = (uint32_t)tid; i < inc_cnt; i += PT_THREADS)
-    if (prefix + i < lim) out[prefix + i] = ext_of(w.stage[s_prev + i]);
+  uint16_t* __restrict__ out16 = SPANS ? nullptr : w.out16;
+  for (uint32_t i = (uint32_t)tid; i < inc_cnt; i += PT_THREADS) {
+    if (prefix + i >= lim) continue;
+    const int32_t v = ext_of(w.stage[s_prev + i]);
+    if (out16) out16[prefix + i] = (uint16_t)v;
+    else out[prefix + i] = v;
+  }
   const uint32_t obase = prefix + inc_cnt;
   // Token o of unit k sits at position ustart[k] + o, so the tokens of a
   // wave's positions go to one contiguous range of the output, in position
@@ -1880,8 +1885,13 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
       if ((has >> j) & 1u) pack[r++] = (uint32_t)val[j];
     __syncthreads();
     // (valid text: the wave's indices are exactly base .. base + n_wave - 1)
-    for (uint32_t i = (uint32_t)lane; i < n_wave; i += 64)
-      if (base + i < lim) out[base + i] = (int32_t)pack[i];
+    if (out16) {
+      for (uint32_t i = (uint32_t)lane; i < n_wave; i += 64)
+        if (base + i < lim) out16[base + i] = (uint16_t)pack[i];
+    } else {
+      for (uint32_t i = (uint32_t)lane; i < n_wave; i += 64)
+        if (base + i < lim) out[base + i] = (int32_t)pack[i];
+    }
   }
   if (BATCH && tid == 0 && has_inc) {
     w.unit_tile[s_prev] = t;

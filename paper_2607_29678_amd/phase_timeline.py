@@ -4,8 +4,9 @@ A diagnostic build of the library (``python -m paper_2607_29678_amd._build
 --phases``, or ``--build`` here; compile it on the build host, not on the GPU
 host) has thread 0 of every tile write the 100 MHz wall clock at each phase
 boundary of the tile kernel (the slots are listed in ``csrc/tt_tile.hip``).
-This script encodes seeded device-resident requests through that build and
-prints, per workload, one JSON line: the mean and maximum time of every phase
+This script encodes seeded device-resident requests (``--host``: requests in
+pageable host arrays through ``tt_encode``) through that build and prints, per
+workload, one JSON line: the mean and maximum time of every phase
 over the tiles, the phases of the critical tiles (the last to finish their
 placement look-back) and of the tiles that publish their token count last
 (which every later tile's placement waits for), when tiles start and publish
@@ -50,7 +51,7 @@ def _spread(rows):
             "max": round(float(a.max()), 2)}
 
 
-def timeline(workload, pattern, table, samples=8, reps=2):
+def timeline(workload, pattern, table, samples=8, reps=2, host=False):
     import torch
     from workloads import textgen
     from workloads.tables import load_table
@@ -71,8 +72,19 @@ def timeline(workload, pattern, table, samples=8, reps=2):
     d_in = [torch.from_numpy(np.frombuffer(t, dtype=np.uint8).copy()).to(dev) for t in texts]
     d_out = torch.empty(max(len(t) for t in texts), dtype=torch.int32, device=dev)
     d_len = torch.zeros(1, dtype=torch.int64, device=dev)
+    # host delivery: tt_encode from pageable arrays (the kernel reads the request
+    # from pinned staging and writes the IDs into pinned memory over the bus)
+    h_in = [np.frombuffer(t, dtype=np.uint8).copy() for t in texts]
+    h_out = np.empty(max(len(t) for t in texts), dtype=np.int32)
+
+    def call(i):
+        if host:
+            tok.encode_into(h_in[i], h_out, stream.cuda_stream)
+        else:
+            tok.encode_device(d_in[i], len(texts[i]), d_out, d_len, stream.cuda_stream)
+
     for i in range(2):
-        tok.encode_device(d_in[i], len(texts[i]), d_out, d_len, stream.cuda_stream)
+        call(i)
     torch.cuda.synchronize()
     buf = np.zeros(MAX_TILES * SLOTS, dtype=np.uint64)
     phases, disp, walk, pred, crit, spans, late, starts, counts = [], [], [], [], [], [], [], [], []
@@ -82,7 +94,7 @@ def timeline(workload, pattern, table, samples=8, reps=2):
         for i, t in enumerate(texts):
             nt = (len(t) + PT_OWN - 1) // PT_OWN
             assert nt <= MAX_TILES
-            tok.encode_device(d_in[i], len(t), d_out, d_len, stream.cuda_stream)
+            call(i)
             stream.synchronize()
             _lib.check(lib.tt_phase_stamps(buf.ctypes.data, nt), "tt_phase_stamps")
             a = buf[: nt * SLOTS].reshape(nt, SLOTS).astype(np.int64)
@@ -119,6 +131,7 @@ def timeline(workload, pattern, table, samples=8, reps=2):
     tok.set_profiling(0)
     tok.close()
     out = {"workload": workload, "pattern": pattern, "table": table, "calls": samples * reps,
+           "delivery": "tt_encode from pageable host arrays" if host else "device-resident (tt_encode_device)",
            "kernel_us_p50_hip_events": round(float(np.median(kernel_us)), 2),
            "stamp_span_us_p50": round(float(np.median(spans)), 2),
            "phases": _summary(phases, PHASES), "dispatch": _summary(disp, DISPATCH),
@@ -139,6 +152,7 @@ def main(argv=None):
     ap.add_argument("--runs", default="C3:gpt2:3,C4:cl100k:4",
                     help="comma-separated WORKLOAD:PATTERN:TABLE (tables as in workloads.tables)")
     ap.add_argument("--samples", type=int, default=8)
+    ap.add_argument("--host", action="store_true", help="time tt_encode from host arrays instead of device-resident calls")
     args = ap.parse_args(argv)
     if args.build:
         print(_build.build(verbose=True, phases=True))
@@ -148,7 +162,7 @@ def main(argv=None):
     _lib.LIB_PATH = _build.PHASES_LIB  # this process loads the diagnostic build instead of the product
     for run in args.runs.split(","):
         w, p, t = run.split(":")
-        print(json.dumps(timeline(w, p, int(t), samples=args.samples)), flush=True)
+        print(json.dumps(timeline(w, p, int(t), samples=args.samples, host=args.host)), flush=True)
     return 0
 
 

@@ -82,6 +82,7 @@ class Tokenizer:
         self._h = h
         self.pattern = pat
         self.n_merges = len(m)
+        self.vocab_size = len(vo) - 1  # caller IDs lie in [0, vocab_size)
 
     def close(self):
         if getattr(self, "_h", None):

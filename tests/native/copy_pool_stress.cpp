@@ -1,6 +1,8 @@
 // Stress test of the staging copy pool: many sizes, offsets and concurrent
-// callers; every copy is checked byte by byte.  Built with g++ (optionally
-// with ThreadSanitizer) by tests/test_copy_pool.py.
+// callers, plain and widening (16-bit values into int32) copies; every copy is
+// checked value by value, and the bytes around the destination must stay
+// untouched.  Built with g++ (optionally with ThreadSanitizer) by
+// tests/test_copy_pool.py.
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
@@ -19,17 +21,32 @@ static int run(int id, int iters) {
     const size_t so = rng() % 4096, doff = rng() % 4096;
     std::memset(dst.data(), 0xA5, dst.size());
     if (it % 7 == 0) tt::host_copy_wake(n);
-    tt::host_copy(dst.data() + doff, src.data() + so, n);
-    if (std::memcmp(dst.data() + doff, src.data() + so, n) != 0) {
-      std::printf("caller %d iteration %d: copy of %zu bytes differs\n", id, it, n);
-      return 1;
+    const bool wide = it % 3 == 1;  // a widening copy of n / 4 16-bit values into n bytes of int32
+    size_t n_out = n;
+    if (wide) {
+      n_out = n & ~(size_t)3;
+      const uint16_t* s16 = reinterpret_cast<const uint16_t*>(src.data() + (so & ~(size_t)1));
+      int32_t* d32 = reinterpret_cast<int32_t*>(dst.data() + (doff & ~(size_t)3));
+      tt::host_widen16(d32, s16, n_out / 4);
+      for (size_t i = 0; i < n_out / 4; ++i)
+        if (d32[i] != (int32_t)s16[i]) {
+          std::printf("caller %d iteration %d: widened value %zu of %zu differs\n", id, it, i, n_out / 4);
+          return 1;
+        }
+    } else {
+      tt::host_copy(dst.data() + doff, src.data() + so, n);
+      if (std::memcmp(dst.data() + doff, src.data() + so, n) != 0) {
+        std::printf("caller %d iteration %d: copy of %zu bytes differs\n", id, it, n);
+        return 1;
+      }
     }
-    for (size_t k = 0; k < doff; ++k)
+    const size_t d0 = wide ? (doff & ~(size_t)3) : doff;
+    for (size_t k = 0; k < d0; ++k)
       if (dst[k] != 0xA5) {
         std::printf("caller %d iteration %d: write before the destination\n", id, it);
         return 1;
       }
-    for (size_t k = doff + n; k < dst.size(); ++k)
+    for (size_t k = d0 + n_out; k < dst.size(); ++k)
       if (dst[k] != 0xA5) {
         std::printf("caller %d iteration %d: write after the destination\n", id, it);
         return 1;
