@@ -163,8 +163,9 @@ def device_calls(ctx, tok, d_in, lens, d_out, d_len, reps=1):
 
 
 def roofline_of(bytes_avg, tokens_avg, kernel_ms, traffic, id_bytes=4):
-    """The request's bytes read plus the IDs written (``id_bytes`` each: 2 when
-    tt_encode stages the IDs of a handle whose caller IDs fit in 16 bits)."""
+    """The request's bytes read plus the IDs written (``id_bytes`` each: 2 or 3
+    when tt_encode stages the IDs of a handle whose caller IDs fit in 16 or 24
+    bits)."""
     alg = bytes_avg + float(id_bytes) * tokens_avg
     achieved = alg / (kernel_ms * 1e-3) / 1e9
     return {"kernel": "tile_kernel", "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
@@ -237,8 +238,9 @@ def config_block(ctx, k, steps, warmup, extras=True):
     kernel_ms = sum(kern) / len(kern)
     res["workload"] = {"chars": n_chars[timed[0]], "bytes_avg": int(B_avg), "tokens_avg": int(T_avg)}
     # the timed calls deliver into a pageable array: the kernel writes staged
-    # IDs, 16-bit when every caller ID of the handle fits
-    id_bytes = 2 if tok.vocab_size <= 65536 else 4
+    # IDs in 2 bytes when every caller ID of the handle fits in 16 bits, in 3
+    # when they fit in 24
+    id_bytes = 2 if tok.vocab_size <= (1 << 16) else 3 if tok.vocab_size <= (1 << 24) else 4
     res["roofline"] = roofline_of(B_avg, T_avg, kernel_ms, measured_traffic(k), id_bytes)
     res["roofline"]["kernel_ms_from"] = ("HIP events around the tile kernel of the %d timed tt_encode calls, which "
                                          "read the request from pinned host memory over PCIe and write %d-byte IDs "

@@ -167,8 +167,9 @@ void tt_destroy(tt_tokenizer* h);
  * it is pinned host memory, else from a pinned copy, and writes the IDs
  * straight into out_ids when it is pinned host memory, else into pinned
  * staging that is then copied into out_ids.  When every ID of the handle's
- * vocabulary is below 65,536, the staged IDs cross the bus as 16-bit values
- * and the copy into out_ids widens them (out_ids still receives int32).
+ * vocabulary is below 65,536 (2^24), the staged IDs cross the bus in 2 (3)
+ * bytes each and the copy into out_ids widens them (out_ids still receives
+ * int32).
  * Staging copies of at least 256 KiB are split among the calling thread and
  * up to three worker threads of the library, which spin for 2 ms after a
  * copy, then sleep.  Longer requests take the length and the IDs back

@@ -162,7 +162,7 @@ struct tt_tokenizer {
   int32_t* d_ext = nullptr;    // [256 + M] caller's ID of every internal ID
   uint32_t* d_toklen = nullptr;  // [256 + M] byte length of every internal ID
   uint32_t n_ids = 0;
-  bool ext16 = false;          // every caller ID is in [0, 65536): staged IDs cross the bus as 16 bits
+  int id_bits = 32;            // 16 or 24 when every caller ID fits: staged IDs cross the bus in that many bits
   uint32_t max_tok_bytes = 1;  // byte length of the longest token (incremental repair)
   bool ignore = false;         // ignore_merges: whole pieces probed in the vocabulary first
   uint32_t vmax = 0;           // longest vocabulary string (bytes) of the probes
@@ -363,7 +363,7 @@ bool host_pinned(const void* p, int64_t len) {
 // mode 2: encode with span export into out_spans ([n][4], single requests).
 int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, const int64_t* d_docs,
               int32_t n_docs, int32_t* out_ids, int64_t* out_len, int64_t* out_docs, hipStream_t st, int mode,
-              int32_t* out_spans = nullptr, uint16_t* out16 = nullptr) {
+              int32_t* out_spans = nullptr, uint16_t* out16 = nullptr, uint8_t* out_hi = nullptr) {
   if (s->epoch + 1 >= EPOCH_LIMIT) {
     // epochs wrapped: clear the words that carry them and start again
     if (hipMemsetAsync(s->dmem, 0, s->ctl_bytes, st) != hipSuccess) return TT_ERR_HIP;
@@ -383,6 +383,7 @@ int run_chain(tt_tokenizer* h, Workspace* s, const uint8_t* text, uint32_t n, co
   w.out_doc_off = out_docs;
   w.out_spans = out_spans;
   w.out16 = mode == 1 ? out16 : nullptr;
+  w.out_hi = mode == 1 && out16 ? out_hi : nullptr;
   const DevTables tb = handle_tables(h);
   const int ring = h->profile;
   if (ring != s->ring) {  // (re)size the event ring
@@ -426,8 +427,9 @@ constexpr uint64_t PINNED_MAX = 1ull << 28;
 //    writes the output length there too: no copy engine transfer at all.
 //    Each wave of a tile writes its IDs as one contiguous range (whole lines
 //    over the bus).  Staged IDs of a handle whose caller IDs all fit in 16
-//    bits cross the bus as 16-bit values (half the bytes), and the copy
-//    threads widen them into the caller's array.
+//    bits cross the bus as 16-bit values (half the bytes), in 24 bits as a
+//    16-bit array and an array of their third bytes (three quarters), and
+//    the copy threads widen them into the caller's array.
 int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t len, int32_t* out_ids,
                   int64_t* out_len, hipStream_t st) {
   int rc = reserve_pinned(s, (uint64_t)len);
@@ -443,16 +445,20 @@ int encode_staged(tt_tokenizer* h, Workspace* s, const uint8_t* utf8, int64_t le
   *s->h_len = 0;
   // the tile kernel writes the IDs at their places in pinned host memory
   int32_t* dst = pin_out ? out_ids : s->h_ids;
-  const bool narrow = !pin_out && h->ext16;
+  // narrow staging: the low 16 bits at the start of h_ids, the third bytes
+  // after 2 * len bytes (3 * len <= the 4 * capacity bytes of h_ids)
+  const bool narrow = !pin_out && h->id_bits < 32;
+  uint16_t* lo16 = reinterpret_cast<uint16_t*>(s->h_ids);
+  uint8_t* hi8 = narrow && h->id_bits == 24 ? reinterpret_cast<uint8_t*>(s->h_ids) + 2 * (size_t)len : nullptr;
   rc = run_chain(h, s, src, (uint32_t)len, nullptr, 0, dst, s->h_len, nullptr, st, 1, nullptr,
-                 narrow ? reinterpret_cast<uint16_t*>(s->h_ids) : nullptr);
+                 narrow ? lo16 : nullptr, hi8);
   if (rc) return rc;
   if (hipStreamSynchronize(st) != hipSuccess) return TT_ERR_HIP;
   const int64_t T = *s->h_len;
   if (T < 0) return (int)T;
   if (T > len) return TT_ERR_HIP;  // cannot happen: at most one ID per byte
   if (!pin_out && T > 0) {
-    if (narrow) host_widen16(out_ids, reinterpret_cast<const uint16_t*>(s->h_ids), (size_t)T);
+    if (narrow) host_widen(out_ids, lo16, hi8, (size_t)T);
     else host_copy(out_ids, s->h_ids, 4 * (size_t)T);
   }
   *out_len = T;
@@ -970,7 +976,9 @@ int tt_create_ex(const tt_merge* merges, int32_t n_merges, const uint8_t* vocab_
   h->dnb = dnb;
   h->dnb2 = dnb2;
   h->n_ids = n_ids;
-  h->ext16 = std::all_of(ext.begin(), ext.end(), [](int32_t v) { return v >= 0 && v < 65536; });
+  const int32_t ext_max = *std::max_element(ext.begin(), ext.end());
+  const bool ext_nonneg = *std::min_element(ext.begin(), ext.end()) >= 0;
+  h->id_bits = !ext_nonneg ? 32 : ext_max < (1 << 16) ? 16 : ext_max < (1 << 24) ? 24 : 32;
   h->max_tok_bytes = *std::max_element(toklen.begin(), toklen.end());
   if (hipGetDevice(&h->device) != hipSuccess) {
     delete h;

@@ -55,10 +55,11 @@ class CopyPool {
     cv_.notify_all();
   }
 
-  // wide: src holds n / 4 16-bit values that dst receives as int32 (n bytes)
-  void copy(void* dst, const void* src, size_t n, bool wide = false) {
+  // wide: src holds n / 4 16-bit values that dst receives as int32 (n bytes),
+  // with bits 16..23 from hi when hi is set
+  void copy(void* dst, const void* src, size_t n, bool wide = false, const uint8_t* hi = nullptr) {
     if (n < PAR_MIN || threads_.empty() || !job_mu_.try_lock()) {
-      run_chunk(static_cast<uint8_t*>(dst), static_cast<const uint8_t*>(src), 0, n, wide);
+      run_chunk(static_cast<uint8_t*>(dst), static_cast<const uint8_t*>(src), hi, 0, n, wide);
       return;
     }
     const uint64_t seq = seq_.load(std::memory_order_relaxed) + 1;
@@ -70,6 +71,7 @@ class CopyPool {
     src_.store(static_cast<const uint8_t*>(src), std::memory_order_relaxed);
     n_.store(n, std::memory_order_relaxed);
     wide_.store(wide, std::memory_order_relaxed);
+    hi_.store(hi, std::memory_order_relaxed);
     n_chunks_.store((uint32_t)((n + CHUNK - 1) / CHUNK), std::memory_order_relaxed);
     done_.store(0, std::memory_order_relaxed);
     next_.store(seq << 32, std::memory_order_release);
@@ -96,22 +98,26 @@ class CopyPool {
       } while (!next_.compare_exchange_weak(v, v + 1, std::memory_order_acq_rel));
       const size_t n = n_.load(std::memory_order_relaxed);
       const size_t a = (size_t)i * CHUNK, b = std::min(n, a + CHUNK);
-      run_chunk(dst_.load(std::memory_order_relaxed), src_.load(std::memory_order_relaxed), a, b,
-                wide_.load(std::memory_order_relaxed));
+      run_chunk(dst_.load(std::memory_order_relaxed), src_.load(std::memory_order_relaxed),
+                hi_.load(std::memory_order_relaxed), a, b, wide_.load(std::memory_order_relaxed));
       done_.fetch_add(1, std::memory_order_acq_rel);
     }
   }
 
   // Output bytes [a, b) of a copy (for a widening copy a and b are multiples
   // of 4: CHUNK is, and so is n).
-  static void run_chunk(uint8_t* dst, const uint8_t* src, size_t a, size_t b, bool wide) {
+  static void run_chunk(uint8_t* dst, const uint8_t* src, const uint8_t* hi, size_t a, size_t b, bool wide) {
     if (!wide) {
       std::memcpy(dst + a, src + a, b - a);
       return;
     }
     int32_t* d = reinterpret_cast<int32_t*>(dst);
     const uint16_t* s = reinterpret_cast<const uint16_t*>(src);
-    for (size_t i = a / 4; i < b / 4; ++i) d[i] = (int32_t)s[i];
+    if (hi == nullptr) {
+      for (size_t i = a / 4; i < b / 4; ++i) d[i] = (int32_t)s[i];
+    } else {
+      for (size_t i = a / 4; i < b / 4; ++i) d[i] = (int32_t)((uint32_t)s[i] | ((uint32_t)hi[i] << 16));
+    }
   }
 
   void run() {
@@ -156,6 +162,7 @@ class CopyPool {
   std::atomic<const uint8_t*> src_{nullptr};
   std::atomic<size_t> n_{0};
   std::atomic<bool> wide_{false};
+  std::atomic<const uint8_t*> hi_{nullptr};
   std::atomic<uint32_t> n_chunks_{0};
 };
 
@@ -172,6 +179,8 @@ void host_copy_wake(size_t n) {
 
 void host_copy(void* dst, const void* src, size_t n) { pool().copy(dst, src, n); }
 
-void host_widen16(int32_t* dst, const uint16_t* src, size_t count) { pool().copy(dst, src, 4 * count, true); }
+void host_widen(int32_t* dst, const uint16_t* lo, const uint8_t* hi, size_t count) {
+  pool().copy(dst, lo, 4 * count, true, hi);
+}
 
 }  // namespace tt

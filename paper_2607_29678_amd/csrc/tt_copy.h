@@ -13,9 +13,10 @@ namespace tt {
 // copies while another thread's copy is running, are a plain memcpy.
 void host_copy(void* dst, const void* src, size_t n);
 
-// dst[i] = src[i] for i < count (16-bit values widened to int32), split the
-// same way as host_copy (by output bytes).
-void host_widen16(int32_t* dst, const uint16_t* src, size_t count);
+// dst[i] = lo[i] | hi[i] << 16 for i < count (hi == nullptr: dst[i] = lo[i]),
+// IDs staged as 16 or 24 bits widened to int32, split the same way as
+// host_copy (by output bytes).
+void host_widen(int32_t* dst, const uint16_t* lo, const uint8_t* hi, size_t count);
 
 // Let sleeping workers start spinning ahead of a copy of n bytes (cheap when
 // they are awake; nothing for copies too small to be split).

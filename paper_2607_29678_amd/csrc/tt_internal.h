@@ -254,7 +254,8 @@ struct Work {
   int32_t* out_spans;       // span export: [T][4] byte begin, byte end, char begin, char end
   int32_t* out_ids;         // output (caller IDs, or piece offsets for the split export)
   uint16_t* out16;          // encode without span export: when set, the IDs go here as 16-bit
-                            // values instead (every caller ID of the handle is below 65,536)
+                            // values instead (their low 16 bits when out_hi is set too)
+  uint8_t* out_hi;          // with out16: bits 16..23 of every ID (every caller ID is below 2^24)
   int64_t* out_len;         // output length, or -error
   int64_t* out_doc_off;     // batch: n_docs+1 output offsets (device)
 };

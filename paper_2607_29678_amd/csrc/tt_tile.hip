@@ -1825,12 +1825,18 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
   int32_t* __restrict__ out = w.out_ids;
   const int32_t* __restrict__ ext = tb.ext_id;
   auto ext_of = [&](uint32_t v) -> int32_t { return v < tb.n_ids ? ext[v] : -1; };
-  uint16_t* __restrict__ out16 = SPANS ? nullptr : w.out16;
+  // (narrow IDs: single requests of tt_encode only)
+  uint16_t* __restrict__ out16 = (SPANS || BATCH) ? nullptr : w.out16;
+  uint8_t* __restrict__ out_hi = (SPANS || BATCH) ? nullptr : w.out_hi;
   for (uint32_t i = (uint32_t)tid; i < inc_cnt; i += PT_THREADS) {
     if (prefix + i >= lim) continue;
     const int32_t v = ext_of(w.stage[s_prev + i]);
-    if (out16) out16[prefix + i] = (uint16_t)v;
-    else out[prefix + i] = v;
+    if (out16) {
+      out16[prefix + i] = (uint16_t)v;
+      if (out_hi) out_hi[prefix + i] = (uint8_t)((uint32_t)v >> 16);
+    } else {
+      out[prefix + i] = v;
+    }
   }
   const uint32_t obase = prefix + inc_cnt;
   // Token o of unit k sits at position ustart[k] + o, so the tokens of a
@@ -1888,6 +1894,9 @@ __global__ __launch_bounds__(PT_THREADS) __attribute__((amdgpu_waves_per_eu(6)))
     if (out16) {
       for (uint32_t i = (uint32_t)lane; i < n_wave; i += 64)
         if (base + i < lim) out16[base + i] = (uint16_t)pack[i];
+      if (out_hi)
+        for (uint32_t i = (uint32_t)lane; i < n_wave; i += 64)
+          if (base + i < lim) out_hi[base + i] = (uint8_t)(pack[i] >> 16);
     } else {
       for (uint32_t i = (uint32_t)lane; i < n_wave; i += 64)
         if (base + i < lim) out[base + i] = (int32_t)pack[i];

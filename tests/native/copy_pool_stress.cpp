@@ -1,7 +1,7 @@
 // Stress test of the staging copy pool: many sizes, offsets and concurrent
-// callers, plain and widening (16-bit values into int32) copies; every copy is
-// checked value by value, and the bytes around the destination must stay
-// untouched.  Built with g++ (optionally with ThreadSanitizer) by
+// callers, plain and widening (16- or 24-bit values into int32) copies; every
+// copy is checked value by value, and the bytes around the destination must
+// stay untouched.  Built with g++ (optionally with ThreadSanitizer) by
 // tests/test_copy_pool.py.
 #include <cstdint>
 #include <cstdio>
@@ -26,10 +26,12 @@ static int run(int id, int iters) {
     if (wide) {
       n_out = n & ~(size_t)3;
       const uint16_t* s16 = reinterpret_cast<const uint16_t*>(src.data() + (so & ~(size_t)1));
+      // every second widening copy also takes bits 16..23 from a byte array
+      const uint8_t* hi = (it / 3) % 2 ? src.data() + (2 << 20) + (so % 777) : nullptr;
       int32_t* d32 = reinterpret_cast<int32_t*>(dst.data() + (doff & ~(size_t)3));
-      tt::host_widen16(d32, s16, n_out / 4);
+      tt::host_widen(d32, s16, hi, n_out / 4);
       for (size_t i = 0; i < n_out / 4; ++i)
-        if (d32[i] != (int32_t)s16[i]) {
+        if (d32[i] != (int32_t)((uint32_t)s16[i] | (hi ? (uint32_t)hi[i] << 16 : 0u))) {
           std::printf("caller %d iteration %d: widened value %zu of %zu differs\n", id, it, i, n_out / 4);
           return 1;
         }

@@ -1,7 +1,7 @@
 """The staging copy pool of the host path (``csrc/tt_copy.cpp``), built on its
 own with g++ and run on the CPU: concurrent callers, sizes from 0 bytes to 2 MB
 around the chunk size, unaligned offsets, workers that fall asleep between
-copies, plain copies and the widening copies of 16-bit IDs into int32.  Every
+copies, plain copies and the widening copies of 16- and 24-bit IDs into int32.  Every
 copy is compared value by value, and the bytes around the destination must
 stay untouched.  A second build runs under ThreadSanitizer."""
 

@@ -2,11 +2,13 @@
 
 A request in pageable host memory is encoded through pinned staging: when every
 caller ID of the handle is below 65,536 the tile kernel writes the staged IDs
-as 16-bit values and the copy threads widen them into the caller's int32 array;
-otherwise it writes them as int32.  Pinned caller buffers receive int32 IDs
-directly.  All three must give the oracle's IDs (Sec. 4.3 delivers one request
-from host memory to host memory), at the full size of the 1,000,000-character
-GPT-2-style configuration and at a size below the copy threads' split.
+as 16-bit values, when below 2^24 as 16-bit values and their third bytes, and
+the copy threads widen them into the caller's int32 array.  Pinned caller
+buffers receive int32 IDs directly (the kernel's int32 stores, which staging
+uses too for larger IDs).  All must give the oracle's IDs (Sec. 4.3 delivers
+one request from host memory to host memory), at the full size of the
+1,000,000-character GPT-2-style configuration and at a size below the copy
+threads' split.
 """
 
 import numpy as np
@@ -17,7 +19,7 @@ from conftest import config_bytes, lib_tokenizer, oracle_config_ids, oracle_ids,
 pytestmark = pytest.mark.gpu
 
 K = 3        # GPT-2-style configuration: 50,000 merges, every ID below 65,536
-SHIFT = 70_000  # moves every ID of the same table above 65,535
+SHIFT = 70_000  # moves every ID of the same table above 65,535 (24-bit staging)
 
 
 def _shifted_handle():
@@ -68,12 +70,12 @@ def test_staged_ids_all_paths(gpu, size):
     got = _encode(tok, pin_in, pin_out)
     assert np.array_equal(got, want), "pinned caller buffers"
 
-    # the same table with IDs above 65,535: int32 staging
+    # the same table with IDs above 65,535: 24-bit staging
     tok2 = _shifted_handle()
     try:
         out2 = np.full(len(data), -7, dtype=np.int32)
         got2 = _encode(tok2, arr, out2)
-        assert np.array_equal(got2 - SHIFT, want), "pageable (32-bit staging)"
+        assert np.array_equal(got2 - SHIFT, want), "pageable (24-bit staging)"
         # and the 16-bit handle again after it (the staging is per handle and stream)
         got = _encode(tok, arr, out)
         assert np.array_equal(got, want), "pageable (16-bit staging), second call"
