@@ -16,8 +16,8 @@ reused from call to call:
     value = 1,000,000 chars / P50(host-to-host latency)
 
 p50/p90/p99 are host-to-host too.  Reported beside it, on the same samples:
-the same calls with pinned caller buffers, the Python binding's fresh-array
-``Tokenizer.encode``, the device-resident path (input already in HBM, IDs left
+the same calls with pinned caller buffers, the Python binding's
+``Tokenizer.encode`` (a new result array per call), the device-resident path (input already in HBM, IDs left
 in HBM), the multilingual configuration C4 with its own roofline, request
 sizes of 100,000, 2,000,000 and 4,400,000 characters, the 3,000,000-character
 stress request C5 and its 64-document batch, incremental repair, the
@@ -199,7 +199,8 @@ def config_block(ctx, k, steps, warmup, extras=True):
     pin_out = torch.zeros(cap, dtype=torch.int32).pin_memory()
     plat, pcounts, _ = host_calls(ctx, tok, pin_in, pin_out, warmup)
     res["host_to_host_pinned"] = pcts(plat)
-    # the binding's fresh-array call (allocates its output on every call)
+    # the binding's call that returns a new result array (kept until the next
+    # call, as a caller holding the last result would)
     blat = []
     for i in timed:
         a = time.perf_counter()

@@ -8,6 +8,8 @@ Device-memory entry points take raw device addresses (ints) or objects with a
 """
 
 import ctypes
+import sys
+import threading
 
 import numpy as np
 
@@ -47,6 +49,40 @@ def _shrunk(a, n):
     return a
 
 
+class _ResultBuffers:
+    """Output arrays of ``Tokenizer.encode``, reused once nothing refers to them.
+
+    A fresh array's pages are mapped on first touch, while the library copies
+    the IDs into it, and those faults cost more than the copy.  ``encode``
+    returns a view of a buffer kept here; a later call takes the buffer again
+    only when no array refers to it any more (every view of it holds a
+    reference), so a result stays valid for as long as the caller keeps it.
+    """
+
+    KEEP = 4                # buffers kept
+    MAX_ENTRIES = 1 << 24   # larger results get an array of their own
+
+    def __init__(self):
+        self._bufs = []
+        self._lock = threading.Lock()
+
+    def take(self, n):
+        """An int32 array of at least n entries that nothing else refers to,
+        and whether it is one of the kept buffers."""
+        if n > self.MAX_ENTRIES:
+            return np.empty(n, dtype=np.int32), False
+        with self._lock:
+            for b in self._bufs:
+                # references: the list, the loop variable and the call's argument
+                if b.size >= n and sys.getrefcount(b) == 3:
+                    return b, True
+            b = np.empty(n, dtype=np.int32)
+            if len(self._bufs) < self.KEEP:
+                self._bufs.append(b)
+                return b, True
+            return b, False
+
+
 def _u8(data):
     if isinstance(data, np.ndarray):
         return np.ascontiguousarray(data, dtype=np.uint8)
@@ -83,6 +119,7 @@ class Tokenizer:
         self.pattern = pat
         self.n_merges = len(m)
         self.vocab_size = len(vo) - 1  # caller IDs lie in [0, vocab_size)
+        self._results = _ResultBuffers()
 
     def close(self):
         if getattr(self, "_h", None):
@@ -103,14 +140,16 @@ class Tokenizer:
 
     # -- host entry points -------------------------------------------------
     def encode(self, data, stream=None) -> np.ndarray:
-        """``tt_encode``: token IDs (int32) of one UTF-8 request."""
+        """``tt_encode``: token IDs (int32) of one UTF-8 request.  The result may
+        be a view of a larger buffer that a later call reuses once no array
+        refers to it."""
         src = _u8(data)
-        out = np.empty(max(1, src.size), dtype=np.int32)
+        out, kept = self._results.take(max(1, src.size))
         n = ctypes.c_int64(0)
         st = self._lib.tt_encode(self._h, _ptr(src) if src.size else None, src.size, _ptr(out), ctypes.byref(n),
                                  _stream(stream))
         _lib.check(st, "tt_encode")
-        return _shrunk(out, n.value)
+        return out[: n.value] if kept else _shrunk(out, n.value)
 
     def encode_into(self, data, out, stream=None) -> int:
         """``tt_encode`` into a caller-provided int32 array ``out`` (numpy or a CPU torch tensor, at
