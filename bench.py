@@ -387,9 +387,22 @@ def large_request(ctx, k, raw, timed):
         raise SystemExit("tokenizer reported an error on the joined request: %d" % T)
     chars = len(big.decode("utf-8"))
     ms = percentile(lat, 50)
+    # the split export alone (pre-tokenization, piece offsets out) on the same
+    # request: its tile kernel reads the request from HBM and writes 8 bytes
+    # per piece
+    tok.set_profiling(8)
+    for _ in range(8):
+        starts = tok.pretokenize(big, ctx.sid)
+    split_ms = percentile([c["tile"] for c in tok.stage_times(ctx.sid)], 50)
+    tok.set_profiling(0)
+    split_bytes = len(big) + 8.0 * len(starts)
     return {"chars": chars, "bytes": len(big), "tokens": T, "device_resident_p50_ms": round(ms, 4),
             "chars_per_s": round(chars / (ms * 1e-3), 1),
-            "hbm_frac": round((len(big) + 4.0 * T) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)}
+            "hbm_frac": round((len(big) + 4.0 * T) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6),
+            "split_export": {"pieces": len(starts), "tile_kernel_ms_p50": round(split_ms, 4),
+                             "kernel_from": "HIP events around the tile kernel of tt_pretokenize (request in HBM)",
+                             "gb_per_s": round(split_bytes / (split_ms * 1e-3) / 1e9, 1),
+                             "hbm_frac": round(split_bytes / (split_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)}}
 
 
 def incremental_repair(ctx, k, n_appends=24):
