@@ -200,7 +200,10 @@ def config_block(ctx, k, steps, warmup, extras=True):
     plat, pcounts, _ = host_calls(ctx, tok, pin_in, pin_out, warmup)
     res["host_to_host_pinned"] = pcts(plat)
     # the binding's call that returns a new result array (kept until the next
-    # call, as a caller holding the last result would)
+    # call, as a caller holding the last result would), after the same warm-up
+    # calls as the other paths
+    for i in range(warmup):
+        ids = tok.encode(raw[i], ctx.sid)
     blat = []
     for i in timed:
         a = time.perf_counter()

@@ -72,13 +72,22 @@ class _ResultBuffers:
         if n > self.MAX_ENTRIES:
             return np.empty(n, dtype=np.int32), False
         with self._lock:
-            for b in self._bufs:
-                # references: the list, the loop variable and the call's argument
-                if b.size >= n and sys.getrefcount(b) == 3:
-                    return b, True
-            b = np.empty(n, dtype=np.int32)
+            free = []
+            for i in range(len(self._bufs)):
+                b = self._bufs[i]
+                # references: the list, b and the call's argument
+                if sys.getrefcount(b) == 3:
+                    if b.size >= n:
+                        return b, True
+                    free.append(i)
+            # a new buffer, with room for requests a little longer than this one,
+            # kept in place of the smallest free one when the pool is full
+            b = np.empty(min(n + n // 4, max(n, self.MAX_ENTRIES)), dtype=np.int32)
             if len(self._bufs) < self.KEEP:
                 self._bufs.append(b)
+                return b, True
+            if free:
+                self._bufs[min(free, key=lambda i: self._bufs[i].size)] = b
                 return b, True
             return b, False
 
